@@ -1,0 +1,244 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Each ``pin_*`` function takes the oracle variant to check (``mutant`` 0 is the
+real oracle; k > 0 builds it with a planted mistake) and raises AssertionError
+on a mismatch.  ``test_oracle_pins.py`` runs them on the real oracle and
+``test_oracle_mutants.py`` shows that every planted mistake trips at least one.
+
+Sources of truth used here:
+  * hand-worked traces of Sec. VI-B (Alg. 1 / Alg. 2) under the stated readings
+    (``tests/golden/hand_*.json``);
+  * ``torch.nn.functional.embedding_bag(mode="sum")`` in float64 on the CPU
+    (the textbook pooled lookup, Sec. II);
+  * the published first outputs of SplitMix64 seeded with 0;
+  * closed forms that hold for special cases: an LRU cache keeps the Cap rows
+    with the most recent events (global history), an unbounded cache keeps
+    everything it was offered, a zero-capacity cache never hits, and with
+    eviction_speed 0 the priority policy reduces to ranking by row id;
+  * invariants: hits + misses = distinct rows, |R| <= Cap, resident-count
+    conservation, digest = sum of SplitMix64 mixes over the resident dump.
+"""
+import numpy as np
+import torch
+
+import oracle
+import tracegen as tg
+from _helpers import golden_table, load_golden, splitmix64_mix_py
+
+GOLDEN_FILES = ("hand_lru.json", "hand_priority_es4.json", "hand_priority_es1.json", "hand_priority_es0.json")
+
+
+# ----------------------------------------------------------------------------- drivers
+
+def run_oracle(w, mutant=0, nbatches=None, want64=True):
+    """Drive the oracle through ``w``: placement(P_b, bits_{b-1}) then forward(I_b)."""
+    T = w.num_tables
+    tabs = [w.table_values(t) for t in range(T)]
+    o = oracle.for_workload(w, tabs, mutant=mutant)
+    recs = []
+    for b in range(nbatches or w.batches):
+        P, poff = w.prefetch_list(b)
+        bits = w.cache_bits(b - 1) if b > 0 else None
+        assert o.placement(P, poff, bits) == 0
+        place = [o.stats(t) for t in range(T)]
+        res = [o.resident(t) for t in range(T)]
+        idx, off = w.batch(b)
+        st, out32, out64 = o.forward(idx, off, w.bags, want64=want64)
+        assert st == 0
+        fwd = [o.stats(t) for t in range(T)]
+        recs.append(dict(place=place, resident=res, fwd=fwd, out32=out32, out64=out64, P=P, poff=poff,
+                         idx=idx, off=off))
+    o.close()
+    return tabs, recs
+
+
+def segments(w, off):
+    return [w.table_segment(off, t) for t in range(w.num_tables)]
+
+
+# ----------------------------------------------------------------------------- pins
+
+def pin_hand_examples(mutant=0):
+    for name in GOLDEN_FILES:
+        g = load_golden(name)
+        tab = golden_table(g)
+        o = oracle.Oracle([tab], ["f32"], [g["cap"]], policy=g["policy"], eviction_speed=g["eviction_speed"],
+                          mutant=mutant)
+        for b, step in enumerate(g["steps"]):
+            P = np.array(step["prefetch"], np.int32)
+            bits = None if step["bits"] is None else np.array(step["bits"], np.uint8)
+            assert o.placement(P, np.array([0, P.size], np.int64), bits) == 0
+            s = o.stats(0)
+            for k, v in step["expect_placement"].items():
+                assert s[k] == v, f"{name} placement {b}: {k} = {s[k]}, hand-worked {v}"
+            assert list(o.resident(0)) == step["resident"], f"{name} placement {b}: resident {list(o.resident(0))}"
+            idx = np.array(step["indices"], np.int32)
+            off = np.array(step["offsets"], np.int64)
+            st, out32, _ = o.forward(idx, off, off.size - 1)
+            assert st == 0
+            s = o.stats(0)
+            for k, v in step["expect_forward"].items():
+                assert s[k] == v, f"{name} forward {b}: {k} = {s[k]}, hand-worked {v}"
+            want = np.array(step["out"], np.float32).reshape(-1)
+            assert np.array_equal(out32, want), f"{name} forward {b}: out {out32} != {want}"
+        o.close()
+
+
+def pin_embedding_bag(mutant=0):
+    """Pooled sums against torch's embedding_bag(mode='sum') in float64."""
+    cases = [tg.random_tiny(s, max_rows=40, max_dim=9, batches=3, bags=5, integer_values=(s % 2 == 0))
+             for s in range(12)]
+    cases.append(tg.scaled_config(1, row_scale=0.01, batches=2, bags=64))
+    for w in cases:
+        tabs, recs = run_oracle(w, mutant=mutant)
+        f64 = [tg.storage_to_f64(a, tb.dtype) for a, tb in zip(tabs, w.tables)]
+        for r in recs:
+            ref = []
+            for t in range(w.num_tables):
+                s, e = w.table_segment(r["off"], t)
+                o_t = torch.from_numpy(r["off"][t * w.bags:(t + 1) * w.bags + 1] - s)
+                ref.append(torch.nn.functional.embedding_bag(
+                    torch.from_numpy(r["idx"][s:e].astype(np.int64)), torch.from_numpy(f64[t]), o_t,
+                    mode="sum", include_last_offset=True).numpy().reshape(-1))
+            ref = np.concatenate(ref) if ref else np.zeros(0)
+            if w.integer_values:
+                assert np.array_equal(r["out64"], ref), "integer-valued pooled sums must be exact"
+                assert np.array_equal(r["out32"], ref.astype(np.float32))
+            else:
+                assert np.allclose(r["out64"], ref, rtol=1e-12, atol=1e-12)
+                assert np.array_equal(r["out32"], r["out64"].astype(np.float32)), "one rounding of the fp64 sum"
+
+
+def pin_splitmix(mutant=0):
+    """Published first outputs of SplitMix64 seeded with 0: mix(k * golden gamma)."""
+    gamma = 0x9E3779B97F4A7C15
+    published = (0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F, 0xF88BB8A8724C81EC)
+    for k, want in enumerate(published, start=1):
+        z = (k * gamma) & ((1 << 64) - 1)
+        assert oracle.splitmix64_mix(z, mutant) == want
+        assert splitmix64_mix_py(z) == want
+
+
+def pin_lru_history(mutant=0, seeds=range(40)):
+    """LRU_BATCH keeps the Cap rows whose most recent event (access in forward f
+    -> f, prefetch before forward p -> p) is latest, ties to the higher id."""
+    for s in seeds:
+        w = tg.random_tiny(s, policy="lru", batches=6)
+        _, recs = run_oracle(w, mutant=mutant, want64=False)
+        T = w.num_tables
+        last = [dict() for _ in range(T)]
+        R = [set() for _ in range(T)]
+        pf_live = [dict() for _ in range(T)]
+        for b, r in enumerate(recs):
+            dig_t = []
+            for t in range(T):
+                P = set(r["P"][r["poff"][t]:r["poff"][t + 1]].tolist())
+                for p in P:
+                    last[t][p] = max(last[t].get(p, -1), b)
+                ranked = sorted(last[t], key=lambda x: (last[t][x], x), reverse=True)
+                newR = set(ranked[: w.tables[t].cap])
+                for x in newR - R[t]:
+                    pf_live[t][x] = x in P
+                for x in R[t] - newR:
+                    pf_live[t].pop(x, None)
+                R[t] = newR
+                assert sorted(newR) == r["resident"][t].tolist(), f"seed {s} batch {b} table {t}"
+                assert r["place"][t]["resident"] == len(newR)
+                dig_t.append(sum(splitmix64_mix_py((t << 40) | x) for x in newR) & ((1 << 64) - 1))
+                assert r["place"][t]["digest"] == dig_t[-1], f"seed {s} batch {b} table {t}: digest"
+            for t, (a, e) in enumerate(segments(w, r["off"])):
+                U = set(r["idx"][a:e].tolist())
+                assert r["fwd"][t]["misses"] == len(U - R[t])
+                assert r["fwd"][t]["hits"] == len(U & R[t])
+                assert r["fwd"][t]["hits_prefetch"] == sum(1 for x in U & R[t] if pf_live[t].get(x))
+                for x in U:
+                    last[t][x] = b
+                    if x in R[t]:
+                        pf_live[t][x] = False
+
+
+def pin_unbounded_cache(mutant=0, seeds=range(20)):
+    """Cap >= N: nothing is ever evicted; the cache holds every row accessed or
+    prefetched so far, and the misses of a batch are its never-seen rows."""
+    for s in seeds:
+        w = tg.random_tiny(s, batches=5)
+        for tb in w.tables:
+            tb.cap = tb.rows
+        _, recs = run_oracle(w, mutant=mutant, want64=False)
+        seen = [set() for _ in w.tables]
+        for b, r in enumerate(recs):
+            for t in range(w.num_tables):
+                seen[t] |= set(r["P"][r["poff"][t]:r["poff"][t + 1]].tolist())
+                assert r["resident"][t].tolist() == sorted(seen[t])
+                assert r["place"][t]["evicted"] == 0
+            for t, (a, e) in enumerate(segments(w, r["off"])):
+                U = set(r["idx"][a:e].tolist())
+                assert r["fwd"][t]["misses"] == len(U - seen[t])
+                seen[t] |= U
+
+
+def pin_zero_capacity(mutant=0, seeds=range(10)):
+    for s in seeds:
+        w = tg.random_tiny(s, batches=4)
+        for tb in w.tables:
+            tb.cap = 0
+        _, recs = run_oracle(w, mutant=mutant, want64=False)
+        for r in recs:
+            for t, (a, e) in enumerate(segments(w, r["off"])):
+                U = np.unique(r["idx"][a:e])
+                assert r["fwd"][t]["hits"] == 0 and r["fwd"][t]["misses"] == U.size
+                assert r["place"][t]["resident"] == 0
+                assert r["place"][t]["prefetch_dropped"] == np.unique(r["P"][r["poff"][t]:r["poff"][t + 1]]).size
+
+
+def pin_priority_es0(mutant=0, seeds=range(30)):
+    """eviction_speed 0.  Bits all 0: every score stays 0, so the cache keeps
+    the Cap highest ids of R ∪ U_{b-1} ∪ P_b.  Bits all 1: rows touched by the
+    last batch score 1 and everything else has aged to 0."""
+    for s in seeds:
+        for allbits in (0, 1):
+            w = tg.random_tiny(s, policy="priority", batches=6)
+            w.eviction_speed = 0
+            w.cache_bits = (lambda b, _w=w, _v=allbits: np.full(_w.batch(b)[0].size, _v, np.uint8))
+            _, recs = run_oracle(w, mutant=mutant, want64=False)
+            T = w.num_tables
+            R = [set() for _ in range(T)]
+            U_prev = [set() for _ in range(T)]
+            for b, r in enumerate(recs):
+                for t in range(T):
+                    P = set(r["P"][r["poff"][t]:r["poff"][t + 1]].tolist())
+                    cap = w.tables[t].cap
+                    if allbits:
+                        order = sorted(U_prev[t], reverse=True) + sorted((R[t] | P) - U_prev[t], reverse=True)
+                    else:
+                        order = sorted(R[t] | U_prev[t] | P, reverse=True)
+                    R[t] = set(order[:cap])
+                    assert r["resident"][t].tolist() == sorted(R[t]), f"seed {s} bits {allbits} batch {b} table {t}"
+                for t, (a, e) in enumerate(segments(w, r["off"])):
+                    U_prev[t] = set(r["idx"][a:e].tolist())
+
+
+def pin_invariants(mutant=0, seeds=range(40)):
+    for s in seeds:
+        w = tg.random_tiny(s, batches=6)
+        _, recs = run_oracle(w, mutant=mutant, want64=False)
+        prev = [0] * w.num_tables
+        for r in recs:
+            for t, (a, e) in enumerate(segments(w, r["off"])):
+                f, p = r["fwd"][t], r["place"][t]
+                assert f["lookups"] == e - a
+                assert f["unique"] == np.unique(r["idx"][a:e]).size
+                assert f["hits"] + f["misses"] == f["unique"]
+                assert 0 <= f["hits_prefetch"] <= f["hits"]
+                cap = w.tables[t].cap
+                assert p["resident"] <= cap and p["resident"] == r["resident"][t].size
+                assert p["resident"] == prev[t] - p["evicted"] + p["admitted_miss"] + p["prefetch_fill"]
+                assert p["prefetch_bytes"] == p["prefetch_fill"] * w.tables[t].row_bytes
+                assert f["ondemand_bytes"] == f["misses"] * w.tables[t].row_bytes
+                dig = sum(splitmix64_mix_py((t << 40) | int(x)) for x in r["resident"][t]) & ((1 << 64) - 1)
+                assert p["digest"] == dig
+                prev[t] = p["resident"]
+
+
+ALL_PINS = (pin_hand_examples, pin_embedding_bag, pin_splitmix, pin_lru_history, pin_unbounded_cache,
+            pin_zero_capacity, pin_priority_es0, pin_invariants)

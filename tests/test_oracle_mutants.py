@@ -1,0 +1,30 @@
+"""Every planted mistake in the oracle (built on the CPU with ORACLE_MUTANT=k)
+must trip at least one pin; otherwise the pins would not guard that part."""
+import pytest
+
+import oracle
+import oracle_pins as op
+
+MUTANTS = {
+    1: "ties evict the higher row id",
+    2: "no aging under PRIORITY",
+    3: "prefetch overwrites a larger score",
+    4: "last caching bit wins instead of OR",
+    5: "last index of every bag dropped",
+    6: "prefetch flag survives an access",
+    7: "LRU prefetch scored like a touch",
+    8: "digest forgets the table id",
+    9: "aging does not saturate at 0",
+}
+
+
+@pytest.mark.parametrize("k", sorted(MUTANTS), ids=lambda k: f"mutant{k}")
+def test_mutant_is_caught(k, tmp_path):
+    oracle.build(mutant=k)
+    caught = []
+    for pin in op.ALL_PINS:
+        try:
+            pin(k)
+        except AssertionError:
+            caught.append(pin.__name__)
+    assert caught, f"mutant {k} ({MUTANTS[k]}) passed every pin"
