@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""Throughput of the tiered pooled-embedding lookup on one MI355X.
+
+One step = one placement (prefetch list + caching bits applied to the HBM
+cache) followed by one pooled lookup of a batch, i.e. every row of the hot
+path.  Default workload: configuration 2 -- 8 fp32 tables x 1,000,000 rows x
+128 dims in pinned host memory, a 50,000-row HBM cache per table, 2,048 bags per
+table with Poisson(40) pooling clipped to [1, 200], Zipf(1.1) rows through a
+per-table permutation, prefetch list = the next batch's exact distinct rows,
+LRU-by-batch ranking.  Inputs are synthetic (tracegen) and resident in HBM
+before the timed region.
+
+Prints one JSON line: pooled lookups/s (value), the pooled kernel's achieved
+HBM bandwidth against the 8 TB/s peak (roofline), host-link traffic, on-demand
+fetches per batch, and the CPU oracle timed on the host (cpu_baseline).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+PCIE5_X16_GBS = 64.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, help="configuration id (1..5)")
+    ap.add_argument("--row-scale", type=float, default=1.0, help="<1 shrinks rows and caches (debug only)")
+    ap.add_argument("--miss-mode", default="zero_copy", choices=["zero_copy", "staged"])
+    ap.add_argument("--cpu-seconds", type=float, default=20.0, help="time budget of the CPU oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-link-peak", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only: the tables of a configuration are one "
+                                   "GPU's share; --gpus must be 1"}), flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import tracegen as tg
+    from paper_2511_08568_amd import TieredEmbeddingCache
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda", 0)
+    if args.row_scale < 1.0:
+        w = tg.scaled_config(args.config, row_scale=args.row_scale)
+    else:
+        w = tg.make_config(args.config)
+    W, K = args.warmup, args.steps
+    nb = W + K
+    T = w.num_tables
+
+    # -- tables in pinned host memory -------------------------------------------------------------
+    t0 = time.time()
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.uint16}
+    host = [torch.empty((tb.rows, tb.dim), dtype=tdt[tb.dtype], pin_memory=True) for tb in w.tables]
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(lambda t: w.table_values(t, out=host[t].numpy()), range(T)))
+    log(f"tables ready ({sum(h.numel() * h.element_size() for h in host) / 1e9:.2f} GB pinned) "
+        f"in {time.time() - t0:.1f}s")
+
+    # -- traces, staged into HBM before timing ----------------------------------------------------
+    t0 = time.time()
+    batches, prefetch, bits = [], [], []
+    for b in range(nb):
+        idx, off = w.batch(b)
+        P, poff = w.prefetch_list(b)
+        cb = w.cache_bits(b - 1) if b > 0 else None
+        batches.append((idx, off))
+        prefetch.append((P, poff))
+        bits.append(cb)
+    d_batches = [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in batches]
+    d_prefetch = [(torch.from_numpy(P).to(dev) if P.size else None, torch.from_numpy(po).to(dev))
+                  for P, po in prefetch]
+    d_bits = [None if cb is None else torch.from_numpy(cb).to(dev) for cb in bits]
+    max_idx = max(i.size for i, _ in batches)
+    max_pf = max(max(P.size for P, _ in prefetch), 1)
+    outs = [torch.empty(w.bags * sum(tb.dim for tb in w.tables), dtype=torch.float32, device=dev) for _ in range(2)]
+    torch.cuda.synchronize()
+    log(f"{nb} batches staged in {time.time() - t0:.1f}s (max {max_idx} indices)")
+
+    cache = TieredEmbeddingCache(host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables], policy=w.policy,
+                                 eviction_speed=w.eviction_speed, miss_mode=args.miss_mode,
+                                 max_bags_per_table=w.bags, max_indices=max_idx, max_prefetch=max_pf, timing=True)
+    log(f"cache ready: workspace {cache.workspace_bytes / 1e9:.2f} GB")
+
+    def step(b):
+        P, po = d_prefetch[b]
+        cache.placement(P, po, d_bits[b])
+        i, o = d_batches[b]
+        cache.forward(i, o, w.bags, out=outs[b & 1])
+
+    for b in range(W):
+        step(b)
+    torch.cuda.synchronize()
+    _, tot0 = cache.stats()
+    cache.stage_times(reset=True)
+
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for b in range(W, nb):
+        step(b)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    elapsed_ms = ev0.elapsed_time(ev1)
+    stages = cache.stage_times(reset=True)
+    _, tot1 = cache.stats()
+    log(f"timed {K} steps: {elapsed_ms:.3f} ms; stages {json.dumps({k: round(v[0], 3) for k, v in stages.items()})}")
+
+    # -- metrics ---------------------------------------------------------------------------------
+    lookups = sum(int(batches[b][0].size) for b in range(W, nb))
+    delta = {k: sum(tot1[t][k] - tot0[t][k] for t in range(T)) for k in tot1[0] if k != "digest"}
+    pool_ms, pool_calls = stages["fwd_pool"]
+    # algorithmic bytes of one pooled launch: per lookup row + 4-byte index, per bag 8-byte offset + fp32 output
+    alg_bytes = 0
+    for b in range(W, nb):
+        idx, off = batches[b]
+        for t, tb in enumerate(w.tables):
+            s, e = w.table_segment(off, t)
+            alg_bytes += (e - s) * (tb.row_bytes + 4) + w.bags * (8 + 4 * tb.dim)
+    bytes_per_launch = alg_bytes / K
+    pool_s = pool_ms / max(pool_calls, 1) / 1e3
+    achieved = bytes_per_launch / pool_s / 1e9 if pool_s > 0 else 0.0
+    link_bytes = delta["ondemand_bytes"] + delta["prefetch_bytes"]
+    link_ms = stages["fwd_fetch"][0] + stages["plc_fill"][0]
+    link_gbs = link_bytes / (link_ms / 1e3) / 1e9 if link_ms > 0 else 0.0
+
+    link_peak = None
+    if not args.no_link_peak:
+        buf = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
+        dbuf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        best = 0.0
+        for _ in range(5):
+            a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            dbuf.copy_(buf, non_blocking=True)
+            z.record()
+            torch.cuda.synchronize()
+            best = max(best, (1 << 30) / (a.elapsed_time(z) / 1e3) / 1e9)
+        link_peak = best
+        del buf, dbuf
+
+    result = {
+        "metric": "pooled lookups/s",
+        "value": lookups / (elapsed_ms / 1e3),
+        "unit": "lookups/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": elapsed_ms / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.tables[0].dtype,
+        "data": "synthetic (seeded Zipf traces standing in for the paper's Meta embedding-lookup traces)",
+        "config": {
+            "workload": f"configuration {args.config}: {T} {w.tables[0].dtype} tables x {w.tables[0].rows:,} rows "
+                        f"x dim {w.tables[0].dim}, HBM cache {w.tables[0].cap:,} rows/table, {w.bags} bags/table, "
+                        f"pooling {w.tables[0].pooling}, Zipf {w.tables[0].alpha}, prefetch {w.prefetch}, "
+                        f"policy {w.policy}",
+            "batches": f"{W} warmup + {K} timed, each placement + forward",
+            "miss_mode": args.miss_mode,
+            "row_scale": args.row_scale,
+        },
+        "roofline": {
+            "kernel": "k_pool (pooled gather + sum)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None,
+            "alg_bytes_per_launch": bytes_per_launch,
+            "avg_launch_us": pool_s * 1e6,
+        },
+        "ondemand_fetches_per_batch": delta["misses"] / K,
+        "prefetch_fills_per_batch": delta["prefetch_fill"] / K,
+        "host_link": {"bytes_per_batch": link_bytes / K, "achieved_GBs": link_gbs,
+                      "measured_h2d_peak_GBs": link_peak, "pcie5_x16_GBs": PCIE5_X16_GBS,
+                      "frac_of_measured_peak": (link_gbs / link_peak) if link_peak else None},
+        "hit_rate": delta["hits"] / max(delta["unique"], 1),
+        "stage_ms_per_step": {k: v[0] / K for k, v in stages.items()},
+    }
+
+    cache.close()
+
+    if not args.no_cpu_baseline:
+        import oracle
+        cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+        nth = max(1, min(cores, T))
+        tabs_np = [h.numpy() for h in host]
+        o = oracle.for_workload(w, tabs_np, nthreads=nth)
+        done, n_lookups, t_start = 0, 0, time.time()
+        for b in range(nb):
+            P, poff = prefetch[b]
+            assert o.placement(P, poff, bits[b]) == 0
+            idx, off = batches[b]
+            st, _, _ = o.forward(idx, off, w.bags)
+            assert st == 0
+            n_lookups += idx.size
+            done += 1
+            if time.time() - t_start > args.cpu_seconds:
+                break
+        secs = time.time() - t_start
+        o.close()
+        result["cpu_baseline"] = {
+            "value": n_lookups / secs,
+            "unit": "lookups/s",
+            "cores": nth,
+            "kind": "oracle",
+            "sample": f"batches 0..{done - 1} of the same workload (placement + forward each), {secs:.1f}s, "
+                      f"{nth} threads (one per table)",
+        }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

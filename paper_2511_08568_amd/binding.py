@@ -1,0 +1,272 @@
+"""ctypes binding of librecmg.so (include/recmg.h).
+
+The module-level functions carry the C entry points' names and only marshal
+arguments.  ``TieredEmbeddingCache`` adds the plumbing PyTorch is used for:
+device workspace, pinned host staging and streams.  Nothing here computes any
+part of the lookup; if the HIP library is missing, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "librecmg.so")
+
+RECMG_OK, RECMG_E_INVALID, RECMG_E_RANGE, RECMG_E_STATE, RECMG_E_HIP, RECMG_E_NOMEM = range(6)
+RECMG_F32, RECMG_F16, RECMG_BF16 = range(3)
+RECMG_LRU_BATCH, RECMG_PRIORITY = range(2)
+RECMG_ZERO_COPY, RECMG_STAGED = range(2)
+RECMG_MAX_TABLES = 256
+
+DTYPE_CODES = {"f32": RECMG_F32, "f16": RECMG_F16, "bf16": RECMG_BF16}
+POLICY_CODES = {"lru": RECMG_LRU_BATCH, "priority": RECMG_PRIORITY}
+MISS_CODES = {"zero_copy": RECMG_ZERO_COPY, "staged": RECMG_STAGED}
+
+STAT_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand_bytes", "evicted",
+               "admitted_miss", "prefetch_fill", "prefetch_resident", "prefetch_dropped", "miss_dropped",
+               "resident", "prefetch_bytes")
+
+EXPORTED = ("recmg_query_workspace", "recmg_cache_init", "recmg_apply_placement", "recmg_embbag_forward",
+            "recmg_stats", "recmg_stage_times", "recmg_cache_destroy", "recmg_last_error")
+STAGES = ("fwd_dedup", "fwd_fetch", "fwd_pool", "plc_classify", "plc_rank", "plc_apply", "plc_fill")
+
+
+class recmg_config_t(ctypes.Structure):
+    _fields_ = [
+        ("num_tables", ctypes.c_int32),
+        ("rows", ctypes.POINTER(ctypes.c_int64)),
+        ("dims", ctypes.POINTER(ctypes.c_int32)),
+        ("dtypes", ctypes.POINTER(ctypes.c_int32)),
+        ("host_tables", ctypes.POINTER(ctypes.c_void_p)),
+        ("cache_rows", ctypes.POINTER(ctypes.c_int64)),
+        ("policy", ctypes.c_int32),
+        ("eviction_speed", ctypes.c_int32),
+        ("miss_mode", ctypes.c_int32),
+        ("validate", ctypes.c_int32),
+        ("max_bags_per_table", ctypes.c_int32),
+        ("max_indices", ctypes.c_int64),
+        ("max_prefetch", ctypes.c_int64),
+        ("device_workspace", ctypes.c_void_p),
+        ("device_workspace_bytes", ctypes.c_size_t),
+        ("host_staging", ctypes.c_void_p),
+        ("host_staging_bytes", ctypes.c_size_t),
+        ("copy_stream", ctypes.c_void_p),
+        ("timing", ctypes.c_int32),
+    ]
+
+
+class recmg_table_stats_t(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_int64) for f in STAT_FIELDS] + [("digest", ctypes.c_uint64)]
+
+
+class RecmgError(RuntimeError):
+    def __init__(self, code: int, where: str, msg: str):
+        super().__init__(f"{where} failed with status {code}: {msg}")
+        self.code = code
+
+
+_LIB: Optional[ctypes.CDLL] = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load librecmg.so; raises if it has not been built (no fallback path exists)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2511_08568_amd/build.py "
+                           "(or __graft_entry__.build()); there is no non-HIP implementation")
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    lib.recmg_query_workspace.argtypes = [ctypes.POINTER(recmg_config_t), ctypes.POINTER(ctypes.c_size_t),
+                                          ctypes.POINTER(ctypes.c_size_t)]
+    lib.recmg_cache_init.argtypes = [ctypes.POINTER(recmg_config_t), ctypes.POINTER(P)]
+    lib.recmg_apply_placement.argtypes = [P, P, P, ctypes.c_int64, P, P]
+    lib.recmg_embbag_forward.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32, P, P]
+    lib.recmg_stats.argtypes = [P, ctypes.POINTER(recmg_table_stats_t), ctypes.POINTER(recmg_table_stats_t), P,
+                                ctypes.c_int64, P]
+    lib.recmg_stage_times.argtypes = [P, P, P, ctypes.c_int32]
+    lib.recmg_cache_destroy.argtypes = [P]
+    for name in EXPORTED[:-1]:
+        getattr(lib, name).restype = ctypes.c_int32
+    lib.recmg_last_error.restype = ctypes.c_char_p
+    lib.recmg_last_error.argtypes = []
+    _LIB = lib
+    return lib
+
+
+def recmg_last_error() -> str:
+    return load_library().recmg_last_error().decode()
+
+
+def _check(code: int, where: str):
+    if code != RECMG_OK:
+        raise RecmgError(code, where, recmg_last_error())
+
+
+def recmg_query_workspace(cfg: recmg_config_t):
+    dev, host = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    _check(load_library().recmg_query_workspace(ctypes.byref(cfg), ctypes.byref(dev), ctypes.byref(host)),
+           "recmg_query_workspace")
+    return int(dev.value), int(host.value)
+
+
+def recmg_cache_init(cfg: recmg_config_t) -> int:
+    h = ctypes.c_void_p(0)
+    _check(load_library().recmg_cache_init(ctypes.byref(cfg), ctypes.byref(h)), "recmg_cache_init")
+    return int(h.value)
+
+
+def recmg_apply_placement(handle: int, prefetch_rows: int, prefetch_offsets: int, num_prefetch: int,
+                          cache_bits: int, stream: int) -> int:
+    return int(load_library().recmg_apply_placement(handle, prefetch_rows or None, prefetch_offsets or None,
+                                                    int(num_prefetch), cache_bits or None, stream or None))
+
+
+def recmg_embbag_forward(handle: int, indices: int, offsets: int, num_indices: int, bags_per_table: int, out: int,
+                         stream: int) -> int:
+    return int(load_library().recmg_embbag_forward(handle, indices or None, offsets or None, int(num_indices),
+                                                   int(bags_per_table), out or None, stream or None))
+
+
+def recmg_stats(handle: int, last, total, resident_dump: int, dump_capacity: int, resident_counts: int) -> int:
+    return int(load_library().recmg_stats(handle, last, total, resident_dump or None, int(dump_capacity),
+                                          resident_counts or None))
+
+
+def recmg_stage_times(handle: int, ms: int, calls: int, reset: int) -> int:
+    return int(load_library().recmg_stage_times(handle, ms or None, calls or None, int(reset)))
+
+
+def recmg_cache_destroy(handle: int) -> int:
+    return int(load_library().recmg_cache_destroy(handle or None))
+
+
+# ---------------------------------------------------------------------------- convenience wrapper
+
+def _stream_ptr(stream) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+class TieredEmbeddingCache:
+    """One handle over a set of pinned host tables.
+
+    host_tables: CPU tensors in pinned memory, [rows, dim], float32 / float16 /
+    bfloat16 (or uint16 holding bfloat16 bits).  They must outlive the cache."""
+
+    def __init__(self, host_tables: Sequence, dtypes: Sequence[str], cache_rows: Sequence[int], *,
+                 policy: str = "lru", eviction_speed: int = 4, miss_mode: str = "zero_copy",
+                 max_bags_per_table: int, max_indices: int, max_prefetch: int, validate: bool = False,
+                 timing: bool = False, device: int = 0):
+        import torch
+        self.torch = torch
+        self.device = torch.device("cuda", device)
+        self.T = len(host_tables)
+        for t in host_tables:
+            if not t.is_pinned():
+                raise ValueError("host tables must be pinned (pin_memory=True)")
+        self._host = list(host_tables)
+        self.dims = [int(t.shape[1]) for t in host_tables]
+        self._rows = (ctypes.c_int64 * self.T)(*[int(t.shape[0]) for t in host_tables])
+        self._dims = (ctypes.c_int32 * self.T)(*self.dims)
+        self._dtypes = (ctypes.c_int32 * self.T)(*[DTYPE_CODES[d] for d in dtypes])
+        self._ptrs = (ctypes.c_void_p * self.T)(*[t.data_ptr() for t in host_tables])
+        self._caps = (ctypes.c_int64 * self.T)(*[int(c) for c in cache_rows])
+        cfg = recmg_config_t()
+        cfg.num_tables = self.T
+        cfg.rows = self._rows
+        cfg.dims = self._dims
+        cfg.dtypes = self._dtypes
+        cfg.host_tables = self._ptrs
+        cfg.cache_rows = self._caps
+        cfg.policy = POLICY_CODES[policy]
+        cfg.eviction_speed = int(eviction_speed)
+        cfg.miss_mode = MISS_CODES[miss_mode]
+        cfg.validate = int(bool(validate))
+        cfg.timing = int(bool(timing))
+        cfg.max_bags_per_table = int(max_bags_per_table)
+        cfg.max_indices = int(max_indices)
+        cfg.max_prefetch = int(max_prefetch)
+        dev_bytes, host_bytes = recmg_query_workspace(cfg)
+        with torch.cuda.device(self.device):
+            self.workspace = torch.empty(dev_bytes, dtype=torch.uint8, device=self.device)
+            self.copy_stream = torch.cuda.Stream(device=self.device) if miss_mode == "staged" else None
+        self.staging = torch.empty(host_bytes, dtype=torch.uint8, pin_memory=True) if host_bytes else None
+        cfg.device_workspace = self.workspace.data_ptr()
+        cfg.device_workspace_bytes = dev_bytes
+        if self.staging is not None:
+            cfg.host_staging = self.staging.data_ptr()
+            cfg.host_staging_bytes = host_bytes
+        if self.copy_stream is not None:
+            cfg.copy_stream = int(self.copy_stream.cuda_stream)
+        self.cfg = cfg
+        self.workspace_bytes = dev_bytes
+        with torch.cuda.device(self.device):
+            self.handle = recmg_cache_init(cfg)
+
+    def placement(self, prefetch_rows, prefetch_offsets, cache_bits=None, stream=None):
+        """prefetch_rows: cuda int32 [P]; prefetch_offsets: cuda int64 [T+1];
+        cache_bits: cuda uint8, one per index of the last forward, or None."""
+        n = int(prefetch_rows.numel()) if prefetch_rows is not None else 0
+        code = recmg_apply_placement(self.handle, prefetch_rows.data_ptr() if n else 0, prefetch_offsets.data_ptr(),
+                                     n, cache_bits.data_ptr() if cache_bits is not None else 0, _stream_ptr(stream))
+        _check(code, "recmg_apply_placement")
+
+    def forward(self, indices, offsets, bags_per_table: int, out=None, stream=None):
+        """indices: cuda int32 [L]; offsets: cuda int64 [T*B+1]. Returns cuda float32 [sum_t B*D_t]."""
+        torch = self.torch
+        if out is None:
+            out = torch.empty(bags_per_table * sum(self.dims), dtype=torch.float32, device=self.device)
+        n = int(indices.numel())
+        code = recmg_embbag_forward(self.handle, indices.data_ptr() if n else 0, offsets.data_ptr(), n,
+                                    int(bags_per_table), out.data_ptr() if out.numel() else 0, _stream_ptr(stream))
+        _check(code, "recmg_embbag_forward")
+        return out
+
+    def stats(self, dump: bool = False, strict: bool = True):
+        """(last, total[, resident rows per table]) as lists of dicts; synchronises."""
+        import numpy as np
+        last = (recmg_table_stats_t * self.T)()
+        total = (recmg_table_stats_t * self.T)()
+        counts = np.zeros(self.T, np.int64)
+        buf = None
+        if dump:
+            cap = int(sum(self._caps[t] for t in range(self.T)))
+            buf = np.zeros(max(cap, 1), np.int32)
+        code = recmg_stats(self.handle, last, total, buf.ctypes.data if dump else 0, buf.size if dump else 0,
+                           counts.ctypes.data if dump else 0)
+        if strict:
+            _check(code, "recmg_stats")
+        conv = lambda s: {**{f: int(getattr(s, f)) for f in STAT_FIELDS}, "digest": int(s.digest)}
+        L = [conv(last[t]) for t in range(self.T)]
+        Tt = [conv(total[t]) for t in range(self.T)]
+        if not dump:
+            return (L, Tt, code) if not strict else (L, Tt)
+        res, at = [], 0
+        for t in range(self.T):
+            res.append(buf[at:at + counts[t]].copy())
+            at += int(counts[t])
+        return (L, Tt, res, code) if not strict else (L, Tt, res)
+
+    def stage_times(self, reset: bool = True):
+        """{stage: (milliseconds, launches)} summed since the last reset (timing=True only)."""
+        import numpy as np
+        ms = np.zeros(len(STAGES), np.float64)
+        calls = np.zeros(len(STAGES), np.int64)
+        _check(recmg_stage_times(self.handle, ms.ctypes.data, calls.ctypes.data, int(reset)), "recmg_stage_times")
+        return {k: (float(ms[i]), int(calls[i])) for i, k in enumerate(STAGES)}
+
+    def close(self):
+        if getattr(self, "handle", 0):
+            _check(recmg_cache_destroy(self.handle), "recmg_cache_destroy")
+            self.handle = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

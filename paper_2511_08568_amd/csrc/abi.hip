@@ -1,0 +1,694 @@
+// C ABI of include/recmg.h: configuration checks, workspace carving, launch
+// order, the STAGED miss path and counter readback.  All arithmetic of the
+// lookup runs in the kernels of dedup.hip, forward.hip and placement.hip.
+#include <algorithm>
+#include <cstddef>
+#include <cstring>
+#include <memory>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "launch.h"
+
+using namespace recmg;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int32_t fail(int32_t code, const std::string &msg) {
+    g_last_error = msg;
+    return code;
+}
+
+#define HIP_TRY(expr)                                                                              \
+    do {                                                                                           \
+        hipError_t e_ = (expr);                                                                    \
+        if (e_ != hipSuccess) return fail(RECMG_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+    } while (0)
+
+constexpr uint32_t kMagic = 0x52434d47u;  // "RCMG"
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+int bitlen(uint64_t x) {
+    int b = 0;
+    while (x) {
+        ++b;
+        x >>= 1;
+    }
+    return b;
+}
+
+int64_t pow2ceil(int64_t x) {
+    int64_t p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+struct Geom {
+    int64_t rows = 0;
+    int32_t dim = 0, dtype = 0, esz = 0, row_bytes = 0, cap = 0;
+    int64_t map_cap = 0, bm_words = 0;
+    int32_t bm_nblk = 0, gsz = 0, nchunk = 0, vec = 0, bpb = 0, copy_unit = 0;
+};
+
+struct Layout {
+    size_t total = 0, host_total = 0;
+    std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, free_stack, map, bitmap, rank;
+    size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
+    size_t src = 0, inv = 0, U = 0, slotU = 0, M = 0, mflags = 0, mscore = 0, mslot = 0;
+    size_t NP = 0, ptag = 0, npslot = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, staging = 0;
+    int64_t stage_stride = 0, sum_cap = 0;
+    int32_t total_bm_blocks = 0;
+};
+
+int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
+    if (!cfg) return fail(RECMG_E_INVALID, "config is NULL");
+    const int T = cfg->num_tables;
+    if (T < 1 || T > RECMG_MAX_TABLES) return fail(RECMG_E_INVALID, "num_tables out of [1, RECMG_MAX_TABLES]");
+    if (!cfg->rows || !cfg->dims || !cfg->dtypes || !cfg->host_tables || !cfg->cache_rows)
+        return fail(RECMG_E_INVALID, "a per-table array is NULL");
+    if (cfg->policy != RECMG_LRU_BATCH && cfg->policy != RECMG_PRIORITY) return fail(RECMG_E_INVALID, "bad policy");
+    if (cfg->eviction_speed < 0 || cfg->eviction_speed > (1 << 20))
+        return fail(RECMG_E_INVALID, "eviction_speed out of [0, 2^20]");
+    if (cfg->miss_mode != RECMG_ZERO_COPY && cfg->miss_mode != RECMG_STAGED) return fail(RECMG_E_INVALID, "bad miss_mode");
+    if (cfg->max_bags_per_table < 0 || cfg->max_indices < 0 || cfg->max_indices >= (int64_t(1) << 31) ||
+        cfg->max_prefetch < 0 || cfg->max_prefetch >= (int64_t(1) << 31))
+        return fail(RECMG_E_INVALID, "max_* sizes out of range");
+    if ((int64_t)T * cfg->max_bags_per_table >= (int64_t(1) << 31)) return fail(RECMG_E_INVALID, "too many bags");
+    geo->assign(T, Geom());
+    for (int t = 0; t < T; ++t) {
+        Geom &g = (*geo)[t];
+        g.rows = cfg->rows[t];
+        g.dim = cfg->dims[t];
+        g.dtype = cfg->dtypes[t];
+        if (g.rows < 1 || g.rows >= (int64_t(1) << 31)) return fail(RECMG_E_INVALID, "rows out of [1, 2^31)");
+        if (g.dim < 1 || g.dim > (1 << 16)) return fail(RECMG_E_INVALID, "dim out of [1, 65536]");
+        if (g.dtype != RECMG_F32 && g.dtype != RECMG_F16 && g.dtype != RECMG_BF16) return fail(RECMG_E_INVALID, "bad dtype");
+        if (cfg->cache_rows[t] < 0) return fail(RECMG_E_INVALID, "negative cache_rows");
+        if (!cfg->host_tables[t]) return fail(RECMG_E_INVALID, "host table is NULL");
+        g.esz = g.dtype == RECMG_F32 ? 4 : 2;
+        g.row_bytes = g.dim * g.esz;
+        g.cap = (int32_t)std::min<int64_t>(cfg->cache_rows[t], g.rows);
+        g.map_cap = pow2ceil(std::max<int64_t>(64, 2 * (int64_t)g.cap));
+        const int64_t words = (g.rows + 31) / 32;
+        g.bm_nblk = (int32_t)((words + kWordsPerBlock - 1) / kWordsPerBlock);
+        g.bm_words = (int64_t)g.bm_nblk * kWordsPerBlock;
+        g.vec = g.row_bytes % 16 == 0;
+        if (g.vec && (reinterpret_cast<uintptr_t>(cfg->host_tables[t]) & 15))
+            return fail(RECMG_E_INVALID, "host table not 16-byte aligned");
+        const int ve = g.vec ? 16 / g.esz : 1;
+        const int lanes = (g.dim + ve - 1) / ve;
+        g.gsz = (int32_t)std::min<int64_t>(64, std::max<int64_t>(4, pow2ceil(lanes)));
+        g.nchunk = (lanes + g.gsz - 1) / g.gsz;
+        g.bpb = (kBlock / 64) * (64 / g.gsz);
+        g.copy_unit = g.row_bytes % 16 == 0 ? 16 : (g.row_bytes % 4 == 0 ? 4 : 2);
+    }
+    return RECMG_OK;
+}
+
+void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout *L) {
+    const int T = (int)geo.size();
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = align256(off + std::max<size_t>(bytes, 1));
+        return at;
+    };
+    int32_t maxrb = 0;
+    for (const Geom &g : geo) maxrb = std::max(maxrb, g.row_bytes);
+    L->stage_stride = ((int64_t)maxrb + 15) / 16 * 16;
+    for (int t = 0; t < T; ++t) {
+        const Geom &g = geo[t];
+        L->pool.push_back(take((size_t)g.cap * g.row_bytes));
+        L->slot_row.push_back(take((size_t)g.cap * 4));
+        L->slot_score.push_back(take((size_t)g.cap * 4));
+        L->slot_flags.push_back(take((size_t)g.cap * 4));
+        L->slot_touch.push_back(take((size_t)g.cap * 4));
+        L->free_stack.push_back(take((size_t)g.cap * 4));
+        L->map.push_back(take((size_t)g.map_cap * 8));
+        L->bitmap.push_back(take((size_t)g.bm_words * 4));
+        L->rank.push_back(take((size_t)g.bm_words * 8));
+        L->total_bm_blocks += g.bm_nblk;
+        L->sum_cap += g.cap;
+    }
+    const size_t mi = (size_t)cfg->max_indices, mp = (size_t)cfg->max_prefetch;
+    L->tabs = take(sizeof(DTable) * T);
+    L->st = take(sizeof(TState) * T);
+    L->err = take(4);
+    L->bm_block_start = take(4 * (T + 1));
+    L->blocksum = take(4 * (size_t)L->total_bm_blocks);
+    L->blockoff = take(4 * (size_t)L->total_bm_blocks);
+    L->tstart = take(8 * (T + 1));
+    L->pstart = take(8 * (T + 1));
+    L->src = take(4 * mi);
+    L->inv = take(4 * mi);
+    L->U = take(4 * mi);
+    L->slotU = take(4 * mi);
+    L->M = take(4 * mi);
+    L->mflags = take(4 * mi);
+    L->mscore = take(4 * mi);
+    L->mslot = take(4 * mi);
+    L->NP = take(4 * mp);
+    L->ptag = take(4 * mp);
+    L->npslot = take(4 * mp);
+    L->hist = take(4 * (size_t)kRadix * T);
+    L->dump = take(4 * (size_t)L->sum_cap);
+    L->dump_count = take(4 * T);
+    L->pool_bstart = take(4 * (T + 1));
+    L->staging = take(mi * (size_t)L->stage_stride);
+    L->total = off;
+    L->host_total = cfg->miss_mode == RECMG_STAGED ? align256(4 * std::max<size_t>(mi, 1)) + mi * (size_t)L->stage_stride : 0;
+}
+
+}  // namespace
+
+struct recmg_cache {
+    uint32_t magic = kMagic;
+    int device = 0;
+    int T = 0;
+    recmg_config_t cfg{};
+    std::vector<Geom> geo;
+    Layout L;
+    DGlobal g{};
+    std::vector<const char *> host;  // host tables (host pointers)
+    int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1;
+    int64_t max_rows = 0;
+    int64_t placements = 0, forwards = 0, last_n = 0;
+    bool have_fwd = false;
+    hipStream_t last_stream = nullptr;
+    int32_t pool_B = -1;
+    int64_t pool_blocks = 0;
+    std::vector<int32_t> pool_bstart;
+    // STAGED
+    hipStream_t copy_stream = nullptr;
+    hipEvent_t ev_ready = nullptr, ev_copied = nullptr;
+    int32_t *h_mrows = nullptr;
+    char *h_rows = nullptr;
+    std::vector<TState> h_st;
+    std::vector<int64_t> h_tstart;
+    // stage timing
+    struct Mark {
+        int stage;
+        hipEvent_t a, b;
+    };
+    std::vector<hipEvent_t> ev_free;
+    std::vector<Mark> marks;
+    double stage_ms[RECMG_NUM_STAGES] = {0};
+    int64_t stage_calls[RECMG_NUM_STAGES] = {0};
+};
+
+namespace {
+
+// Stage timing: an event pair per stage per call, resolved in recmg_stage_times.
+struct StageTimer {
+    recmg_cache_t *c;
+    int stage;
+    hipStream_t s;
+    hipEvent_t a = nullptr;
+    StageTimer(recmg_cache_t *c_, int stage_, hipStream_t s_) : c(c_), stage(stage_), s(s_) {
+        if (!c->cfg.timing) return;
+        a = take();
+        if (a) (void)hipEventRecord(a, s);
+    }
+    hipEvent_t take() {
+        if (c->ev_free.empty()) {
+            hipEvent_t e = nullptr;
+            if (hipEventCreate(&e) != hipSuccess) return nullptr;
+            return e;
+        }
+        hipEvent_t e = c->ev_free.back();
+        c->ev_free.pop_back();
+        return e;
+    }
+    ~StageTimer() {
+        if (!a) return;
+        hipEvent_t b = take();
+        if (!b) {
+            c->ev_free.push_back(a);
+            return;
+        }
+        (void)hipEventRecord(b, s);
+        c->marks.push_back({stage, a, b});
+    }
+};
+
+int32_t check_handle(recmg_cache_t *c) {
+    if (!c) return fail(RECMG_E_INVALID, "handle is NULL");
+    if (c->magic != kMagic) return fail(RECMG_E_STATE, "handle is not live");
+    return RECMG_OK;
+}
+
+int32_t set_device(recmg_cache_t *c) {
+    int cur = -1;
+    HIP_TRY(hipGetDevice(&cur));
+    if (cur != c->device) HIP_TRY(hipSetDevice(c->device));
+    return RECMG_OK;
+}
+
+// STAGED miss path: miss ids to the host, host gather into pinned staging,
+// one copy per table on the copy stream, compute stream waits for it.
+int32_t staged_fetch(recmg_cache_t *c, hipStream_t s) {
+    const int T = c->T;
+    HIP_TRY(hipMemcpyAsync(c->h_st.data(), c->g.st, sizeof(TState) * T, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(c->h_tstart.data(), c->g.tstart, 8 * (T + 1), hipMemcpyDeviceToHost, s));
+    int32_t err = 0;
+    HIP_TRY(hipMemcpyAsync(&err, c->g.err, 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (err) return RECMG_OK;  // the device flag already disables the rest
+    int64_t total = 0;
+    for (int t = 0; t < T; ++t) {
+        const int32_t nm = c->h_st[t].mcount;
+        if (nm)
+            HIP_TRY(hipMemcpyAsync(c->h_mrows + c->h_tstart[t], c->g.M + c->h_tstart[t], 4 * (size_t)nm,
+                                   hipMemcpyDeviceToHost, s));
+        total += nm;
+    }
+    if (total == 0) return RECMG_OK;
+    HIP_TRY(hipStreamSynchronize(s));
+    const int64_t stride = c->L.stage_stride;
+    auto gather = [&](int64_t lo, int64_t hi) {
+        int64_t k = 0;
+        for (int t = 0; t < T && k < hi; ++t) {
+            const int64_t nm = c->h_st[t].mcount, ts = c->h_tstart[t];
+            const int64_t rb = c->geo[t].row_bytes;
+            for (int64_t m = std::max<int64_t>(0, lo - k); m < nm && k + m < hi; ++m) {
+                const int64_t row = c->h_mrows[ts + m];
+                std::memcpy(c->h_rows + (ts + m) * stride, c->host[t] + row * rb, (size_t)rb);
+            }
+            k += nm;
+        }
+    };
+    const unsigned hw = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+    const unsigned nth = (unsigned)std::min<int64_t>(hw, std::max<int64_t>(1, total / 2048));
+    if (nth <= 1) {
+        gather(0, total);
+    } else {
+        std::vector<std::thread> th;
+        for (unsigned k = 0; k < nth; ++k)
+            th.emplace_back(gather, total * k / nth, total * (k + 1) / nth);
+        for (auto &x : th) x.join();
+    }
+    hipStream_t cs = c->copy_stream ? c->copy_stream : s;
+    if (cs != s) {
+        HIP_TRY(hipEventRecord(c->ev_ready, s));
+        HIP_TRY(hipStreamWaitEvent(cs, c->ev_ready, 0));
+    }
+    for (int t = 0; t < T; ++t) {
+        const int64_t nm = c->h_st[t].mcount, ts = c->h_tstart[t];
+        if (nm)
+            HIP_TRY(hipMemcpyAsync(c->g.staging + ts * stride, c->h_rows + ts * stride, (size_t)(nm * stride),
+                                   hipMemcpyHostToDevice, cs));
+    }
+    if (cs != s) {
+        HIP_TRY(hipEventRecord(c->ev_copied, cs));
+        HIP_TRY(hipStreamWaitEvent(s, c->ev_copied, 0));
+    }
+    return RECMG_OK;
+}
+
+int32_t host_check_ids(const int32_t *dev_ids, const int64_t *dev_off, int64_t n_off, int64_t stride_off,
+                       int64_t n_ids, const std::vector<Geom> &geo, hipStream_t s) {
+    std::vector<int64_t> off(n_off);
+    std::vector<int32_t> ids(std::max<int64_t>(n_ids, 1));
+    HIP_TRY(hipMemcpyAsync(off.data(), dev_off, 8 * n_off, hipMemcpyDeviceToHost, s));
+    if (n_ids > 0) HIP_TRY(hipMemcpyAsync(ids.data(), dev_ids, 4 * n_ids, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (off[0] != 0 || off[n_off - 1] != n_ids) return fail(RECMG_E_RANGE, "offsets do not span the ids");
+    for (int64_t i = 0; i + 1 < n_off; ++i)
+        if (off[i] > off[i + 1]) return fail(RECMG_E_RANGE, "offsets decrease");
+    for (size_t t = 0; t < geo.size(); ++t)
+        for (int64_t i = off[t * stride_off]; i < off[(t + 1) * stride_off]; ++i)
+            if (ids[i] < 0 || ids[i] >= geo[t].rows) return fail(RECMG_E_RANGE, "row id out of range");
+    return RECMG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *recmg_last_error(void) { return g_last_error.c_str(); }
+
+int32_t recmg_query_workspace(const recmg_config_t *cfg, size_t *device_bytes, size_t *host_staging_bytes) {
+    std::vector<Geom> geo;
+    int32_t rc = check_config(cfg, &geo);
+    if (rc) return rc;
+    Layout L;
+    make_layout(cfg, geo, &L);
+    if (device_bytes) *device_bytes = L.total;
+    if (host_staging_bytes) *host_staging_bytes = L.host_total;
+    return RECMG_OK;
+}
+
+int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
+    if (!out) return fail(RECMG_E_INVALID, "out is NULL");
+    std::vector<Geom> geo;
+    int32_t rc = check_config(cfg, &geo);
+    if (rc) return rc;
+    Layout L;
+    make_layout(cfg, geo, &L);
+    if (!cfg->device_workspace || cfg->device_workspace_bytes < L.total)
+        return fail(RECMG_E_NOMEM, "device workspace smaller than recmg_query_workspace");
+    if (reinterpret_cast<uintptr_t>(cfg->device_workspace) & 255)
+        return fail(RECMG_E_INVALID, "device workspace not 256-byte aligned");
+    if (cfg->miss_mode == RECMG_STAGED && (!cfg->host_staging || cfg->host_staging_bytes < L.host_total))
+        return fail(RECMG_E_NOMEM, "host staging smaller than recmg_query_workspace");
+    const int T = cfg->num_tables;
+
+    std::unique_ptr<recmg_cache> c(new recmg_cache());
+    HIP_TRY(hipGetDevice(&c->device));
+    c->T = T;
+    c->cfg = *cfg;
+    c->geo = geo;
+    c->L = L;
+    // host tables: must be pinned memory visible to the device
+    std::vector<const char *> dev_host(T);
+    for (int t = 0; t < T; ++t) {
+        void *dp = nullptr;
+        if (hipHostGetDevicePointer(&dp, const_cast<void *>(cfg->host_tables[t]), 0) != hipSuccess || !dp) {
+            (void)hipGetLastError();
+            return fail(RECMG_E_INVALID, "host table " + std::to_string(t) + " is not pinned host memory");
+        }
+        dev_host[t] = static_cast<const char *>(dp);
+        c->host.push_back(static_cast<const char *>(cfg->host_tables[t]));
+    }
+    char *ws = static_cast<char *>(cfg->device_workspace);
+    DGlobal &g = c->g;
+    g.tabs = reinterpret_cast<DTable *>(ws + L.tabs);
+    g.st = reinterpret_cast<TState *>(ws + L.st);
+    g.err = reinterpret_cast<int32_t *>(ws + L.err);
+    g.bm_block_start = reinterpret_cast<int32_t *>(ws + L.bm_block_start);
+    g.blocksum = reinterpret_cast<int32_t *>(ws + L.blocksum);
+    g.blockoff = reinterpret_cast<int32_t *>(ws + L.blockoff);
+    g.tstart = reinterpret_cast<int64_t *>(ws + L.tstart);
+    g.pstart = reinterpret_cast<int64_t *>(ws + L.pstart);
+    g.src = reinterpret_cast<int32_t *>(ws + L.src);
+    g.inv = reinterpret_cast<int32_t *>(ws + L.inv);
+    g.U = reinterpret_cast<int32_t *>(ws + L.U);
+    g.slotU = reinterpret_cast<int32_t *>(ws + L.slotU);
+    g.M = reinterpret_cast<int32_t *>(ws + L.M);
+    g.mflags = reinterpret_cast<uint32_t *>(ws + L.mflags);
+    g.mscore = reinterpret_cast<int32_t *>(ws + L.mscore);
+    g.mslot = reinterpret_cast<int32_t *>(ws + L.mslot);
+    g.NP = reinterpret_cast<int32_t *>(ws + L.NP);
+    g.ptag = reinterpret_cast<int32_t *>(ws + L.ptag);
+    g.npslot = reinterpret_cast<int32_t *>(ws + L.npslot);
+    g.hist = reinterpret_cast<int32_t *>(ws + L.hist);
+    g.dump = reinterpret_cast<int32_t *>(ws + L.dump);
+    g.dump_count = reinterpret_cast<int32_t *>(ws + L.dump_count);
+    g.staging = ws + L.staging;
+    g.stage_stride = L.stage_stride;
+    g.T = T;
+    g.total_bm_blocks = L.total_bm_blocks;
+
+    std::vector<DTable> tabs(T);
+    std::vector<int32_t> bstart(T + 1, 0);
+    int64_t out_off = 0, cap_off = 0;
+    for (int t = 0; t < T; ++t) {
+        const Geom &ge = geo[t];
+        DTable &d = tabs[t];
+        std::memset(&d, 0, sizeof(d));
+        d.host = dev_host[t];
+        d.pool = ws + L.pool[t];
+        d.slot_row = reinterpret_cast<int32_t *>(ws + L.slot_row[t]);
+        d.slot_score = reinterpret_cast<int32_t *>(ws + L.slot_score[t]);
+        d.slot_flags = reinterpret_cast<uint32_t *>(ws + L.slot_flags[t]);
+        d.slot_touch = reinterpret_cast<int32_t *>(ws + L.slot_touch[t]);
+        d.free_stack = reinterpret_cast<int32_t *>(ws + L.free_stack[t]);
+        d.map = reinterpret_cast<int2 *>(ws + L.map[t]);
+        d.bitmap = reinterpret_cast<uint32_t *>(ws + L.bitmap[t]);
+        d.rank = reinterpret_cast<uint2 *>(ws + L.rank[t]);
+        d.rows = ge.rows;
+        d.out_elem_off = out_off;
+        d.cap_off = cap_off;
+        d.dim = ge.dim;
+        d.dtype = ge.dtype;
+        d.row_bytes = ge.row_bytes;
+        d.cap = ge.cap;
+        d.map_mask = (int32_t)(ge.map_cap - 1);
+        d.bm_words = (int32_t)ge.bm_words;
+        d.bm_block0 = bstart[t];
+        d.bm_nblk = ge.bm_nblk;
+        d.gsz = ge.gsz;
+        d.nchunk = ge.nchunk;
+        d.vec = ge.vec;
+        d.bags_per_block = ge.bpb;
+        d.copy_unit = ge.copy_unit;
+        bstart[t + 1] = bstart[t] + ge.bm_nblk;
+        out_off += ge.dim;
+        cap_off += ge.cap;
+        c->max_cap = std::max(c->max_cap, ge.cap);
+        c->max_map = (int32_t)std::max<int64_t>(c->max_map, ge.map_cap);
+        c->max_units = std::max(c->max_units, ge.row_bytes / ge.copy_unit);
+        c->max_rows = std::max(c->max_rows, ge.rows);
+    }
+    c->rowbits = std::max(1, bitlen((uint64_t)(c->max_rows - 1)));
+
+    // clear the metadata (not the slot pool or staging), set "free" markers
+    hipStream_t s0 = nullptr;
+    for (int t = 0; t < T; ++t) {
+        const Geom &ge = geo[t];
+        HIP_TRY(hipMemsetAsync(ws + L.slot_row[t], 0xff, (size_t)ge.cap * 4, s0));
+        HIP_TRY(hipMemsetAsync(ws + L.slot_score[t], 0, (size_t)ge.cap * 4, s0));
+        HIP_TRY(hipMemsetAsync(ws + L.slot_flags[t], 0, (size_t)ge.cap * 4, s0));
+        HIP_TRY(hipMemsetAsync(ws + L.slot_touch[t], 0xff, (size_t)ge.cap * 4, s0));
+        HIP_TRY(hipMemsetAsync(ws + L.map[t], 0xff, (size_t)ge.map_cap * 8, s0));
+        HIP_TRY(hipMemsetAsync(ws + L.bitmap[t], 0, (size_t)ge.bm_words * 4, s0));
+    }
+    HIP_TRY(hipMemsetAsync(ws + L.st, 0, sizeof(TState) * T, s0));
+    HIP_TRY(hipMemsetAsync(ws + L.err, 0, 4, s0));
+    HIP_TRY(hipMemsetAsync(ws + L.hist, 0, 4 * (size_t)kRadix * T, s0));
+    HIP_TRY(hipMemcpy(ws + L.tabs, tabs.data(), sizeof(DTable) * T, hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(ws + L.bm_block_start, bstart.data(), 4 * (T + 1), hipMemcpyHostToDevice));
+    launch_init_state(g, c->max_cap, s0);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipDeviceSynchronize());
+
+    if (cfg->miss_mode == RECMG_STAGED) {
+        c->h_mrows = static_cast<int32_t *>(cfg->host_staging);
+        c->h_rows = static_cast<char *>(cfg->host_staging) + align256(4 * std::max<size_t>((size_t)cfg->max_indices, 1));
+        c->copy_stream = static_cast<hipStream_t>(cfg->copy_stream);
+        HIP_TRY(hipEventCreateWithFlags(&c->ev_ready, hipEventDisableTiming));
+        HIP_TRY(hipEventCreateWithFlags(&c->ev_copied, hipEventDisableTiming));
+    }
+    c->h_st.resize(T);
+    c->h_tstart.resize(T + 1);
+    *out = c.release();
+    g_last_error.clear();
+    return RECMG_OK;
+}
+
+int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, const int64_t *prefetch_offsets,
+                              int64_t num_prefetch, const uint8_t *cache_bits, void *stream) {
+    int32_t rc = check_handle(c);
+    if (rc) return rc;
+    if (!prefetch_offsets) return fail(RECMG_E_INVALID, "prefetch_offsets is NULL");
+    if (num_prefetch < 0 || num_prefetch > c->cfg.max_prefetch)
+        return fail(RECMG_E_INVALID, "num_prefetch out of [0, max_prefetch]");
+    if (num_prefetch > 0 && !prefetch_rows) return fail(RECMG_E_INVALID, "prefetch_rows is NULL");
+    if ((rc = set_device(c))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (c->cfg.validate && (rc = host_check_ids(prefetch_rows, prefetch_offsets, c->T + 1, 1, num_prefetch, c->geo, s)))
+        return rc;
+    const DGlobal &g = c->g;
+    const int64_t b = c->placements;
+    if (b + 2 >= (int64_t(1) << 31)) return fail(RECMG_E_STATE, "placement count exhausted");
+    PlcParams p{};
+    p.prio = c->cfg.policy == RECMG_PRIORITY;
+    p.es = c->cfg.eviction_speed;
+    p.lru_touch = (int32_t)b;
+    p.pscore = p.prio ? p.es : (int32_t)(b + 1);
+    p.have_fwd = c->have_fwd ? 1 : 0;
+    p.last_stamp = c->have_fwd ? (int32_t)(c->forwards - 1) : -2;
+    p.rowbits = c->rowbits;
+    const int64_t maxscore = p.prio ? (int64_t)p.es + 1 : b + 1;
+    p.total_bits = bitlen((uint64_t)maxscore) + p.rowbits;
+    if (p.total_bits < 1) p.total_bits = 1;
+    p.passes = (p.total_bits + kRadixBits - 1) / kRadixBits;
+
+    {
+        StageTimer tm(c, RECMG_STAGE_PLC_CLASSIFY, s);
+        launch_plc_prep(g, prefetch_offsets, num_prefetch, s);
+        if (p.prio && cache_bits && c->have_fwd) launch_plc_bits(g, cache_bits, c->last_n, s);
+        if (num_prefetch > 0) {
+            launch_mark(g, prefetch_rows, g.pstart, num_prefetch, s);
+            launch_dedup(g, 1, reinterpret_cast<int32_t *>(reinterpret_cast<char *>(g.st) + offsetof(TState, pcount)),
+                         (int)(sizeof(TState) / 4), 0, p.have_fwd, s);
+        }
+    }
+    const int64_t cand = (c->have_fwd ? c->last_n : 0) + num_prefetch;
+    const int64_t per_table = c->max_cap + (cand + c->T - 1) / c->T;
+    const int64_t cand_grid = std::min<int64_t>(std::max<int64_t>(cand / c->T, 1024), cand + 1);
+    {
+        StageTimer tm(c, RECMG_STAGE_PLC_RANK, s);
+        launch_plc_rank(g, p, per_table, s);
+    }
+    {
+        StageTimer tm(c, RECMG_STAGE_PLC_APPLY, s);
+        launch_plc_apply(g, p, c->max_cap, c->max_map, cand_grid, s);
+    }
+    {
+        StageTimer tm(c, RECMG_STAGE_PLC_FILL, s);
+        launch_plc_fill(g, p, cand_grid, c->max_units, s);
+    }
+    launch_plc_finalize(g, s);
+    HIP_TRY(hipGetLastError());
+    c->placements++;
+    c->have_fwd = false;
+    c->last_stream = s;
+    return RECMG_OK;
+}
+
+int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int64_t *offsets, int64_t num_indices,
+                             int32_t bags_per_table, float *out, void *stream) {
+    int32_t rc = check_handle(c);
+    if (rc) return rc;
+    const int64_t B = bags_per_table, n = num_indices;
+    if (B < 0 || B > c->cfg.max_bags_per_table) return fail(RECMG_E_INVALID, "bags_per_table out of [0, max]");
+    if (n < 0 || n > c->cfg.max_indices) return fail(RECMG_E_INVALID, "num_indices out of [0, max_indices]");
+    if (!offsets) return fail(RECMG_E_INVALID, "offsets is NULL");
+    if (n > 0 && !indices) return fail(RECMG_E_INVALID, "indices is NULL");
+    if (B > 0 && !out) return fail(RECMG_E_INVALID, "out is NULL");
+    if ((rc = set_device(c))) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (c->cfg.validate && (rc = host_check_ids(indices, offsets, (int64_t)c->T * B + 1, B, n, c->geo, s))) return rc;
+    const DGlobal &g = c->g;
+    if (c->pool_B != (int32_t)B) {
+        c->pool_bstart.assign(c->T + 1, 0);
+        for (int t = 0; t < c->T; ++t)
+            c->pool_bstart[t + 1] = c->pool_bstart[t] + (int32_t)((B + c->geo[t].bpb - 1) / c->geo[t].bpb);
+        HIP_TRY(hipMemcpyAsync(static_cast<char *>(c->cfg.device_workspace) + c->L.pool_bstart, c->pool_bstart.data(),
+                               4 * (c->T + 1), hipMemcpyHostToDevice, s));
+        HIP_TRY(hipStreamSynchronize(s));
+        c->pool_B = (int32_t)B;
+        c->pool_blocks = c->pool_bstart[c->T];
+    }
+    if (c->forwards + 1 >= (int64_t(1) << 31)) return fail(RECMG_E_STATE, "forward count exhausted");
+    const int32_t stamp = (int32_t)c->forwards;
+    {
+        StageTimer tm(c, RECMG_STAGE_FWD_DEDUP, s);
+        launch_fwd_prep(g, offsets, (int32_t)B, n, s);
+        if (n > 0) {
+            launch_mark(g, indices, g.tstart, n, s);
+            launch_dedup(g, 0, reinterpret_cast<int32_t *>(reinterpret_cast<char *>(g.st) + offsetof(TState, ucount)),
+                         (int)(sizeof(TState) / 4), stamp, 0, s);
+            launch_fwd_src(g, indices, n, s);
+        }
+    }
+    if (n > 0) {
+        StageTimer tm(c, RECMG_STAGE_FWD_FETCH, s);
+        if (c->cfg.miss_mode == RECMG_ZERO_COPY) {
+            launch_fetch(g, s);
+        } else if ((rc = staged_fetch(c, s))) {
+            return rc;
+        }
+    }
+    {
+        StageTimer tm(c, RECMG_STAGE_FWD_POOL, s);
+        launch_pool(g, offsets, (int32_t)B, out, c->pool_blocks,
+                    reinterpret_cast<const int32_t *>(static_cast<char *>(c->cfg.device_workspace) + c->L.pool_bstart),
+                    s);
+    }
+    launch_fwd_finalize(g, s);
+    HIP_TRY(hipGetLastError());
+    c->forwards++;
+    c->have_fwd = true;
+    c->last_n = n;
+    c->last_stream = s;
+    return RECMG_OK;
+}
+
+int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_stats_t *total, int32_t *resident_dump,
+                    int64_t dump_capacity, int64_t *resident_counts) {
+    int32_t rc = check_handle(c);
+    if (rc) return rc;
+    if ((rc = set_device(c))) return rc;
+    hipStream_t s = c->last_stream;
+    HIP_TRY(hipStreamSynchronize(s));
+    const int T = c->T;
+    std::vector<TState> st(T);
+    int32_t err = 0;
+    HIP_TRY(hipMemcpy(st.data(), c->g.st, sizeof(TState) * T, hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(&err, c->g.err, 4, hipMemcpyDeviceToHost));
+    for (int t = 0; t < T; ++t) {
+        for (int which = 0; which < 2; ++which) {
+            recmg_table_stats_t *o = which == 0 ? last : total;
+            if (!o) continue;
+            const int64_t *v = which == 0 ? st[t].last : st[t].total;
+            int64_t *dst = &o[t].lookups;
+            for (int k = 0; k < 14; ++k) dst[k] = v[k];
+            o[t].digest = st[t].digest;
+        }
+    }
+    if (err & ERR_INTERNAL) return fail(RECMG_E_STATE, "device error flag: slot accounting invariant failed");
+    if (err) return fail(RECMG_E_RANGE, "device error flag set (row id out of range or malformed offsets)");
+    if (resident_dump || resident_counts) {
+        int64_t need = 0;
+        for (int t = 0; t < T; ++t) need += st[t].n_res;
+        if (resident_dump && dump_capacity < need) return fail(RECMG_E_INVALID, "dump_capacity too small");
+        launch_mark_resident(c->g, c->max_cap, s);
+        launch_dedup(c->g, 2, c->g.dump_count, 1, 0, 0, s);
+        HIP_TRY(hipGetLastError());
+        std::vector<int32_t> cnt(T);
+        HIP_TRY(hipMemcpyAsync(cnt.data(), c->g.dump_count, 4 * T, hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipStreamSynchronize(s));
+        int64_t at = 0, coff = 0;
+        for (int t = 0; t < T; ++t) {
+            if (resident_counts) resident_counts[t] = cnt[t];
+            if (resident_dump && cnt[t])
+                HIP_TRY(hipMemcpy(resident_dump + at, c->g.dump + coff, 4 * (size_t)cnt[t], hipMemcpyDeviceToHost));
+            at += cnt[t];
+            coff += c->geo[t].cap;
+        }
+    }
+    g_last_error.clear();
+    return RECMG_OK;
+}
+
+int32_t recmg_stage_times(recmg_cache_t *c, double *ms, int64_t *calls, int32_t reset) {
+    int32_t rc = check_handle(c);
+    if (rc) return rc;
+    if (!ms) return fail(RECMG_E_INVALID, "ms is NULL");
+    if ((rc = set_device(c))) return rc;
+    for (auto &m : c->marks) {
+        HIP_TRY(hipEventSynchronize(m.b));
+        float t = 0.f;
+        HIP_TRY(hipEventElapsedTime(&t, m.a, m.b));
+        c->stage_ms[m.stage] += t;
+        c->stage_calls[m.stage] += 1;
+        c->ev_free.push_back(m.a);
+        c->ev_free.push_back(m.b);
+    }
+    c->marks.clear();
+    for (int k = 0; k < RECMG_NUM_STAGES; ++k) {
+        ms[k] = c->stage_ms[k];
+        if (calls) calls[k] = c->stage_calls[k];
+        if (reset) {
+            c->stage_ms[k] = 0;
+            c->stage_calls[k] = 0;
+        }
+    }
+    return RECMG_OK;
+}
+
+int32_t recmg_cache_destroy(recmg_cache_t *c) {
+    if (!c) return RECMG_OK;
+    if (c->magic != kMagic) return fail(RECMG_E_STATE, "handle is not live");
+    (void)set_device(c);
+    int32_t rc = RECMG_OK;
+    if (hipStreamSynchronize(c->last_stream) != hipSuccess) rc = fail(RECMG_E_HIP, "synchronize failed at destroy");
+    for (auto &m : c->marks) {
+        c->ev_free.push_back(m.a);
+        c->ev_free.push_back(m.b);
+    }
+    for (hipEvent_t e : c->ev_free) (void)hipEventDestroy(e);
+    if (c->ev_ready) (void)hipEventDestroy(c->ev_ready);
+    if (c->ev_copied) (void)hipEventDestroy(c->ev_copied);
+    c->magic = 0;
+    delete c;
+    return rc;
+}
+
+}  // extern "C"

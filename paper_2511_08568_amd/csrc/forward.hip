@@ -1,0 +1,306 @@
+// Forward of one batch: pooled embedding-bag lookup over the two-tier store.
+//
+// Order of work on the stream (dedup and probe live in dedup.hip):
+//   k_fwd_prep   validate bag offsets, record each table's index range
+//   k_mark / count / scan / emit(FORWARD)   distinct rows, sorted; map probe
+//   k_fwd_src    per index: rank of its row among the distinct rows (the
+//                inverse map) and where its data lives (slot or staging row)
+//   k_fetch      ZERO_COPY: copy each distinct missing row once from pinned
+//                host memory to HBM staging (GPU reads over the host link)
+//   k_pool       per bag, sum of its rows in fp32 (Sec. II, pooling by sum)
+//   k_fwd_finalize  publish the counters
+#include <type_traits>
+
+#include "launch.h"
+
+namespace recmg {
+
+__global__ void __launch_bounds__(kBlock) k_fwd_prep(DGlobal g, const int64_t *__restrict__ offsets, int32_t B,
+                                                     int64_t n) {
+    const int64_t nb = (int64_t)g.T * B;
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < nb && offsets[i] > offsets[i + 1]) atomicOr(g.err, ERR_OFFSETS);
+    if (i == 0 && (offsets[0] != 0 || offsets[nb] != n)) atomicOr(g.err, ERR_OFFSETS);
+    if (i <= g.T) g.tstart[i] = offsets[i * (int64_t)B];
+    if (i < g.T) {
+        TState &st = g.st[i];
+        st.ucount = 0;
+        st.mcount = 0;
+        st.hits = 0;
+        st.hits_pf = 0;
+    }
+}
+
+// inverse map and data location of every index
+__global__ void __launch_bounds__(kBlock) k_fwd_src(DGlobal g, const int32_t *__restrict__ indices, int64_t n) {
+    if (*g.err) return;
+    __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
+    __shared__ const uint2 *s_rank[RECMG_MAX_TABLES];
+    for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
+        s_start[t] = g.tstart[t];
+        if (t < g.T) s_rank[t] = g.tabs[t].rank;
+    }
+    __syncthreads();
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const int t = find_seg(s_start, g.T, i);
+        const int32_t r = indices[i];
+        const uint2 rk = s_rank[t][r >> 5];
+        const int32_t u = (int32_t)rk.x + __popc(rk.y & ((1u << (r & 31)) - 1u));
+        g.inv[i] = u;
+        g.src[i] = g.slotU[s_start[t] + u];
+    }
+}
+
+// ----------------------------------------------------------------- miss fetch
+
+template <typename V>
+__device__ __forceinline__ void copy_rows(int64_t items, int nunit, const DTable &tb,
+                                          const DGlobal &g, int64_t ts) {
+    const int64_t S = (int64_t)gridDim.x * blockDim.x;
+    const int rb = tb.row_bytes;
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; base < items; base += 4 * S) {
+        V v[4];
+        int64_t dst[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t it = base + q * S;
+            if (it < items) {
+                const int64_t m = it / nunit;
+                const int vv = (int)(it - m * nunit);
+                const int32_t row = g.M[ts + m];
+                v[q] = *reinterpret_cast<const V *>(tb.host + (int64_t)row * rb + (int64_t)vv * sizeof(V));
+                dst[q] = (ts + m) * g.stage_stride + (int64_t)vv * sizeof(V);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int64_t it = base + q * S;
+            if (it < items) *reinterpret_cast<V *>(g.staging + dst[q]) = v[q];
+        }
+    }
+}
+
+// ZERO_COPY miss fetch: each distinct miss is read once from pinned host
+// memory (device-visible mapping) and written to its staging row.
+__global__ void __launch_bounds__(kBlock) k_fetch(DGlobal g) {
+    if (*g.err) return;
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    const int32_t nm = g.st[t].mcount;
+    if (nm == 0) return;
+    const int unit = tb.copy_unit;
+    const int nunit = tb.row_bytes / unit;
+    const int64_t items = (int64_t)nm * nunit;
+    const int64_t ts = g.tstart[t];
+    if (unit == 16) copy_rows<uint4>(items, nunit, tb, g, ts);
+    else if (unit == 4) copy_rows<uint32_t>(items, nunit, tb, g, ts);
+    else copy_rows<uint16_t>(items, nunit, tb, g, ts);
+}
+
+// ----------------------------------------------------------------- pooling
+
+template <int DT>
+struct Elem;
+template <>
+struct Elem<RECMG_F32> {
+    static constexpr int bytes = 4;
+    __device__ static float widen(uint32_t x) { return __builtin_bit_cast(float, x); }
+};
+template <>
+struct Elem<RECMG_F16> {
+    static constexpr int bytes = 2;
+    __device__ static float widen(uint32_t x) { return f16_to_f32(x & 0xffffu); }
+};
+template <>
+struct Elem<RECMG_BF16> {
+    static constexpr int bytes = 2;
+    __device__ static float widen(uint32_t x) { return bf16_to_f32(x & 0xffffu); }
+};
+
+// 16-byte vector of elements -> VE floats added into acc
+template <int DT>
+__device__ __forceinline__ void accum_vec(float *acc, const uint4 v) {
+    if constexpr (DT == RECMG_F32) {
+        acc[0] += __builtin_bit_cast(float, v.x);
+        acc[1] += __builtin_bit_cast(float, v.y);
+        acc[2] += __builtin_bit_cast(float, v.z);
+        acc[3] += __builtin_bit_cast(float, v.w);
+    } else {
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if constexpr (DT == RECMG_BF16) {
+                acc[2 * k] += __builtin_bit_cast(float, w[k] << 16);
+                acc[2 * k + 1] += __builtin_bit_cast(float, w[k] & 0xffff0000u);
+            } else {
+                acc[2 * k] += f16_to_f32(w[k] & 0xffffu);
+                acc[2 * k + 1] += f16_to_f32(w[k] >> 16);
+            }
+        }
+    }
+}
+
+template <int DT, bool VEC>
+struct Lane {
+    static constexpr int VE = VEC ? 16 / Elem<DT>::bytes : 1;
+    using V = typename std::conditional<VEC, uint4, typename std::conditional<Elem<DT>::bytes == 4, uint32_t,
+                                                                               uint16_t>::type>::type;
+    __device__ static void add(float *acc, const V v) {
+        if constexpr (VEC) accum_vec<DT>(acc, v);
+        else acc[0] += Elem<DT>::widen((uint32_t)v);
+    }
+};
+
+// One group of G lanes sums one bag.  Lookup p of the bag goes to
+// accumulator p mod 4; the four partial sums are combined pairwise at the end.
+// The order is fixed per bag, so the result does not depend on which tier
+// served each row.
+template <int DT, bool VEC>
+__device__ __forceinline__ void pool_table(const DGlobal &g, const DTable &tb, int t, int32_t B,
+                                           const int64_t *__restrict__ offsets, float *__restrict__ out,
+                                           int blk_in_table) {
+    using L = Lane<DT, VEC>;
+    using V = typename L::V;
+    constexpr int VE = L::VE;
+    constexpr int EB = Elem<DT>::bytes;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int G = tb.gsz;
+    const int gl = lane & (G - 1);
+    const int gi = lane / G;
+    const int bpw = 64 / G;
+    const int j = (blk_in_table * (kBlock / 64) + wave) * bpw + gi;
+    if (j >= B) return;
+    const int64_t a = offsets[(int64_t)t * B + j], e = offsets[(int64_t)t * B + j + 1];
+    const int D = tb.dim;
+    const int64_t rb = tb.row_bytes;
+    const char *__restrict__ pool = tb.pool;
+    const int64_t sstride = g.stage_stride;
+    const char *__restrict__ stg = g.staging + g.tstart[t] * sstride;
+    const int32_t *__restrict__ src = g.src;
+    float *orow = out + (int64_t)B * tb.out_elem_off + (int64_t)j * D;
+
+    for (int ch = 0; ch < tb.nchunk; ++ch) {
+        const int e0 = (ch * G + gl) * VE;
+        const bool lane_ok = e0 < D;
+        const int64_t eoff = lane_ok ? (int64_t)e0 * EB : 0;
+        float acc[4][VE];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int x = 0; x < VE; ++x) acc[k][x] = 0.f;
+
+        for (int64_t c = a; c < e; c += G) {
+            const int n = (int)((e - c) < G ? (e - c) : G);
+            const int my = gl < n ? src[c + gl] : 0;
+            int q = 0;
+            for (; q + 8 <= n; q += 8) {
+                V v[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const int s = __shfl(my, q + u, G);
+                    const char *p = s >= 0 ? pool + (int64_t)s * rb : stg + (int64_t)(-s - 1) * sstride;
+                    v[u] = *reinterpret_cast<const V *>(p + eoff);
+                }
+#pragma unroll
+                for (int u = 0; u < 8; ++u) L::add(acc[u & 3], v[u]);
+            }
+            for (; q < n; q += 4) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (q + u < n) {
+                        const int s = __shfl(my, q + u, G);
+                        const char *p = s >= 0 ? pool + (int64_t)s * rb : stg + (int64_t)(-s - 1) * sstride;
+                        L::add(acc[u], *reinterpret_cast<const V *>(p + eoff));
+                    }
+                }
+            }
+        }
+        if (lane_ok) {
+            float r[VE];
+#pragma unroll
+            for (int x = 0; x < VE; ++x) r[x] = (acc[0][x] + acc[1][x]) + (acc[2][x] + acc[3][x]);
+            float *o = orow + e0;
+            if (VE % 4 == 0 && (((uintptr_t)o) & 15) == 0) {
+#pragma unroll
+                for (int x = 0; x < VE; x += 4)
+                    *reinterpret_cast<float4 *>(o + x) = make_float4(r[x], r[x + 1], r[x + 2], r[x + 3]);
+            } else {
+#pragma unroll
+                for (int x = 0; x < VE; ++x) o[x] = r[x];
+            }
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) k_pool(DGlobal g, const int64_t *__restrict__ offsets, int32_t B,
+                                                 float *__restrict__ out, const int32_t *__restrict__ bstart) {
+    if (*g.err) return;
+    __shared__ int s_t;
+    if (threadIdx.x == 0) s_t = find_seg32(bstart, g.T, (int32_t)blockIdx.x);
+    __syncthreads();
+    const int t = s_t;
+    const DTable &tb = g.tabs[t];
+    const int bi = (int)blockIdx.x - bstart[t];
+    switch (tb.dtype * 2 + tb.vec) {
+    case RECMG_F32 * 2 + 1: pool_table<RECMG_F32, true>(g, tb, t, B, offsets, out, bi); break;
+    case RECMG_F32 * 2 + 0: pool_table<RECMG_F32, false>(g, tb, t, B, offsets, out, bi); break;
+    case RECMG_F16 * 2 + 1: pool_table<RECMG_F16, true>(g, tb, t, B, offsets, out, bi); break;
+    case RECMG_F16 * 2 + 0: pool_table<RECMG_F16, false>(g, tb, t, B, offsets, out, bi); break;
+    case RECMG_BF16 * 2 + 1: pool_table<RECMG_BF16, true>(g, tb, t, B, offsets, out, bi); break;
+    default: pool_table<RECMG_BF16, false>(g, tb, t, B, offsets, out, bi); break;
+    }
+}
+
+__global__ void k_fwd_finalize(DGlobal g) {
+    if (*g.err) return;
+    for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
+        TState &st = g.st[t];
+        const DTable &tb = g.tabs[t];
+        int64_t v[6];
+        v[0] = g.tstart[t + 1] - g.tstart[t];
+        v[1] = st.ucount;
+        v[2] = st.hits;
+        v[3] = st.hits_pf;
+        v[4] = st.mcount;
+        v[5] = (int64_t)st.mcount * tb.row_bytes;
+        for (int k = 0; k < 6; ++k) {
+            st.last[k] = v[k];
+            st.total[k] += v[k];
+        }
+    }
+}
+
+// ----------------------------------------------------------------- launchers
+
+static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
+    int64_t b = (n + per_block - 1) / per_block;
+    if (b < 1) b = 1;
+    if (b > (int64_t)cap) b = cap;
+    return (unsigned)b;
+}
+
+void launch_fwd_prep(const DGlobal &g, const int64_t *offsets, int32_t B, int64_t n, hipStream_t s) {
+    const int64_t items = ((int64_t)g.T * B + 1) > (g.T + 1) ? ((int64_t)g.T * B + 1) : (g.T + 1);
+    k_fwd_prep<<<(unsigned)((items + kBlock - 1) / kBlock), kBlock, 0, s>>>(g, offsets, B, n);
+}
+
+void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStream_t s) {
+    if (n <= 0) return;
+    k_fwd_src<<<grid_for(n, kBlock * 4, 16384), kBlock, 0, s>>>(g, indices, n);
+}
+
+void launch_fetch(const DGlobal &g, hipStream_t s) {
+    const unsigned gx = (unsigned)(4096 / g.T > 0 ? 4096 / g.T : 1);
+    k_fetch<<<dim3(gx > 512 ? 512 : gx, g.T), kBlock, 0, s>>>(g);
+}
+
+void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, int64_t nblocks,
+                 const int32_t *bstart, hipStream_t s) {
+    if (nblocks <= 0) return;
+    k_pool<<<(unsigned)nblocks, kBlock, 0, s>>>(g, offsets, B, out, bstart);
+}
+
+void launch_fwd_finalize(const DGlobal &g, hipStream_t s) { k_fwd_finalize<<<1, kBlock, 0, s>>>(g); }
+
+}  // namespace recmg

@@ -1,0 +1,516 @@
+// Placement between batches: the batched form of Alg. 1 (load_embeddings)
+// and Alg. 2 (gpu_buffer_populate), Sec. VI-B.
+//
+// Per table t the candidate set is K = R ∪ M ∪ set(P): resident slots, the
+// last batch's misses (already in HBM staging) and the prefetch list.  Every
+// member gets a score (aging, touch, prefetch, below), and the cache keeps the
+// min(Cap, |K|) largest keys (score, row).  Instead of one victim scan per
+// insertion, one radix select per placement finds the threshold key: 11-bit
+// digits from the top, each pass one kernel whose last block picks the digit
+// holding the Cap-th largest key.  Keys are distinct (rows are distinct), so
+// exactly min(Cap, |K|) keys are >= the threshold.
+//
+// Scores:  LRU_BATCH  touched by the last batch: lru_touch; prefetched:
+//                     max(score, pscore) with pscore = lru_touch + 1
+//          PRIORITY   residents first age by one, saturating at 0 (Alg. 2);
+//                     touched: caching bit + ES (Alg. 1); prefetched:
+//                     max(score, ES); a touched resident loses its prefetch flag.
+//
+// Kernels on the stream: k_plc_prep, [k_plc_bits], dedup of P with the
+// EMIT_PREFETCH visitor (dedup.hip), k_plc_update (scores + select pass 0),
+// k_plc_select (passes 1..), k_plc_evict, k_map_clear / k_map_refill (rebuild
+// when deleted entries pile up), k_plc_admit, k_plc_fill, k_plc_finalize.
+#include "launch.h"
+
+namespace recmg {
+
+__global__ void k_plc_prep(DGlobal g, const int64_t *__restrict__ poff, int64_t np) {
+    for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
+        const int64_t v = poff[t];
+        g.pstart[t] = v;
+        if (t < g.T && v > poff[t + 1]) atomicOr(g.err, ERR_OFFSETS);
+        if ((t == 0 && v != 0) || (t == g.T && v != np)) atomicOr(g.err, ERR_OFFSETS);
+        if (t < g.T) {
+            TState &st = g.st[t];
+            st.pcount = 0;
+            st.npcount = 0;
+            st.popped = 0;
+            st.done = 0;
+            st.p_res = 0;
+            st.evicted = 0;
+            st.adm_miss = 0;
+            st.p_fill = 0;
+            st.p_drop = 0;
+            st.m_drop = 0;
+            st.digest_acc = 0ull;
+        }
+    }
+}
+
+// caching bits of the last batch: OR into the slot (hit) or the miss entry
+__global__ void __launch_bounds__(kBlock) k_plc_bits(DGlobal g, const uint8_t *__restrict__ bits, int64_t n) {
+    if (*g.err) return;
+    __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
+    for (int t = threadIdx.x; t <= g.T; t += blockDim.x) s_start[t] = g.tstart[t];
+    __syncthreads();
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        if (!bits[i]) continue;
+        const int t = find_seg(s_start, g.T, i);
+        const int32_t s = g.src[i];
+        if (s >= 0) atomicOr(&g.tabs[t].slot_flags[s], F_CBIT);
+        else atomicOr(&g.mflags[s_start[t] + (-(int64_t)s - 1)], F_CBIT);
+    }
+}
+
+// ----------------------------------------------------------------- ranking
+
+struct Counts {
+    int32_t cap, nm, nnp, mode, keep;
+};
+
+__device__ __forceinline__ Counts table_counts(const DTable &tb, const TState &st, const PlcParams &p) {
+    Counts c;
+    c.cap = tb.cap;
+    c.nm = p.have_fwd ? st.mcount : 0;
+    c.nnp = st.npcount;
+    const int64_t nk = (int64_t)st.n_res + c.nm + c.nnp;
+    c.keep = (int32_t)(nk < c.cap ? nk : c.cap);
+    c.mode = nk <= c.cap ? SEL_ALL : (c.keep == 0 ? SEL_NONE : SEL_SELECT);
+    return c;
+}
+
+__device__ __forceinline__ int pass_shift(const PlcParams &p, int pass) { return kRadixBits * (p.passes - 1 - pass); }
+__device__ __forceinline__ int pass_width(const PlcParams &p, int pass) {
+    return pass == 0 ? p.total_bits - kRadixBits * (p.passes - 1) : kRadixBits;
+}
+
+// Merge the block's histogram; the last block of the table picks the digit.
+__device__ void select_finish(const DGlobal &g, int t, int pass, const PlcParams &p, int need0, int *s_hist,
+                              int *tmp) {
+    TState &st = g.st[t];
+    int *gh = g.hist + (int64_t)t * kRadix;
+    for (int b = threadIdx.x; b < kRadix; b += blockDim.x)
+        if (s_hist[b]) atomicAdd(&gh[b], s_hist[b]);
+    __threadfence();
+    __syncthreads();
+    __shared__ int s_last;
+    if (threadIdx.x == 0) s_last = atomicAdd(&st.done, 1u) == gridDim.x - 1;
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    for (int b = threadIdx.x; b < kRadix; b += blockDim.x) {
+        s_hist[b] = __hip_atomic_load(&gh[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        gh[b] = 0;
+    }
+    __syncthreads();
+    const int need = pass == 0 ? need0 : st.need;
+    // thread k owns bin group 255-k, so an inclusive scan gives suffix sums
+    constexpr int per = kRadix / kBlock;
+    const int grp = kBlock - 1 - (int)threadIdx.x;
+    int cs = 0;
+#pragma unroll
+    for (int b = 0; b < per; ++b) cs += s_hist[grp * per + b];
+    int tot;
+    const int above = block_excl_scan(cs, tmp, &tot);  // keys in groups above grp
+    if (above < need && above + cs >= need) {
+        int cum = above;
+        for (int b = grp * per + per - 1; b >= grp * per; --b) {
+            if (cum + s_hist[b] >= need) {
+                st.prefix = pass == 0 ? (uint64_t)b : ((st.prefix << kRadixBits) | (uint64_t)b);
+                st.need = need - cum;
+                break;
+            }
+            cum += s_hist[b];
+        }
+    }
+    if (threadIdx.x == 0) st.done = 0;
+}
+
+// Scores of every candidate (written back) and the first select pass.
+__global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
+    if (*g.err) return;
+    __shared__ int s_hist[kRadix];
+    __shared__ int tmp[16];
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    const Counts c = table_counts(tb, st, p);
+    if (blockIdx.x == 0 && threadIdx.x == 0) st.sel_mode = c.mode;
+    const bool sel = c.mode == SEL_SELECT;
+    if (sel)
+        for (int b = threadIdx.x; b < kRadix; b += blockDim.x) s_hist[b] = 0;
+    __syncthreads();
+    const int64_t ts = g.tstart[t], ps = g.pstart[t];
+    const int shift = pass_shift(p, 0);
+    const uint32_t dmask = (1u << pass_width(p, 0)) - 1u;
+    const int64_t items = (int64_t)c.cap + c.nm + c.nnp;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < items; k += stride) {
+        int32_t row, s;
+        if (k < c.cap) {
+            row = tb.slot_row[k];
+            if (row < 0) continue;
+            s = tb.slot_score[k];
+            uint32_t f = tb.slot_flags[k];
+            if (p.prio) s = s > 0 ? s - 1 : 0;
+            if (tb.slot_touch[k] == p.last_stamp) {
+                f &= ~F_PF;
+                s = p.prio ? (int32_t)((f & F_CBIT) ? 1 : 0) + p.es : p.lru_touch;
+            }
+            if ((f & F_INP) && s < p.pscore) s = p.pscore;
+            tb.slot_score[k] = s;
+            tb.slot_flags[k] = f & ~(F_CBIT | F_INP);
+        } else if (k < (int64_t)c.cap + c.nm) {
+            const int64_t m = ts + (k - c.cap);
+            row = g.M[m];
+            const uint32_t f = g.mflags[m];
+            s = p.prio ? (int32_t)((f & F_CBIT) ? 1 : 0) + p.es : p.lru_touch;
+            if ((f & F_INP) && s < p.pscore) s = p.pscore;
+            g.mscore[m] = s;
+        } else {
+            row = g.NP[ps + (k - c.cap - c.nm)];
+            s = p.pscore;
+        }
+        if (sel) atomicAdd(&s_hist[(uint32_t)(make_key(s, row, p.rowbits) >> shift) & dmask], 1);
+    }
+    __syncthreads();
+    if (sel) select_finish(g, t, 0, p, c.keep, s_hist, tmp);
+}
+
+__device__ __forceinline__ bool item_key(const DGlobal &g, const DTable &tb, const Counts &c, const PlcParams &p,
+                                         int64_t ts, int64_t ps, int64_t k, uint64_t *key) {
+    int32_t row, s;
+    if (k < c.cap) {
+        row = tb.slot_row[k];
+        if (row < 0) return false;
+        s = tb.slot_score[k];
+    } else if (k < (int64_t)c.cap + c.nm) {
+        const int64_t m = ts + (k - c.cap);
+        row = g.M[m];
+        s = g.mscore[m];
+    } else {
+        row = g.NP[ps + (k - c.cap - c.nm)];
+        s = p.pscore;
+    }
+    *key = make_key(s, row, p.rowbits);
+    return true;
+}
+
+__global__ void __launch_bounds__(kBlock) k_plc_select(DGlobal g, PlcParams p, int pass) {
+    if (*g.err) return;
+    __shared__ int s_hist[kRadix];
+    __shared__ int tmp[16];
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    if (st.sel_mode != SEL_SELECT) return;  // uniform over the table's blocks
+    const Counts c = table_counts(tb, st, p);
+    for (int b = threadIdx.x; b < kRadix; b += blockDim.x) s_hist[b] = 0;
+    __syncthreads();
+    const int64_t ts = g.tstart[t], ps = g.pstart[t];
+    const int shift = pass_shift(p, pass);
+    const uint64_t prefix = st.prefix;
+    const int64_t items = (int64_t)c.cap + c.nm + c.nnp;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < items; k += stride) {
+        uint64_t key;
+        if (!item_key(g, tb, c, p, ts, ps, k, &key)) continue;
+        if ((key >> (shift + kRadixBits)) != prefix) continue;
+        atomicAdd(&s_hist[(uint32_t)(key >> shift) & (kRadix - 1)], 1);
+    }
+    __syncthreads();
+    select_finish(g, t, pass, p, 0, s_hist, tmp);
+}
+
+__device__ __forceinline__ bool kept(int mode, uint64_t key, uint64_t thr) {
+    return mode == SEL_ALL || (mode == SEL_SELECT && key >= thr);
+}
+
+// ----------------------------------------------------------------- evict / admit
+
+__global__ void __launch_bounds__(kBlock) k_plc_evict(DGlobal g, PlcParams p) {
+    if (*g.err) return;
+    __shared__ int tmp[16];
+    __shared__ int s_base;
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    const int mode = st.sel_mode;
+    const uint64_t thr = st.prefix;
+    int nev = 0;
+    unsigned long long dig = 0;
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < tb.cap; base += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t k = base + threadIdx.x;
+        int ev = 0;
+        if (k < tb.cap) {
+            const int32_t row = tb.slot_row[k];
+            if (row >= 0) {
+                if (kept(mode, make_key(tb.slot_score[k], row, p.rowbits), thr)) {
+                    dig += mix64(((unsigned long long)t << 40) | (unsigned long long)row);
+                } else {
+                    ev = 1;
+                    map_delete(tb, row);
+                    tb.slot_row[k] = -1;
+                    tb.slot_flags[k] = 0;
+                }
+            }
+        }
+        int tot;
+        const int ex = block_excl_scan(ev, tmp, &tot);
+        if (threadIdx.x == 0 && tot) s_base = atomicAdd(&st.free_top, tot);
+        __syncthreads();
+        if (ev) {
+            const int64_t at = (int64_t)s_base + ex;
+            if (at < tb.cap) tb.free_stack[at] = (int32_t)k;
+            else atomicOr(g.err, ERR_INTERNAL);
+        }
+        nev += ev;
+        __syncthreads();
+    }
+    const int e = block_sum(nev, tmp);
+    const unsigned long long d = wave_sum64(dig);
+    if ((threadIdx.x & 63) == 0 && d) atomicAdd(&st.digest_acc, d);
+    if (threadIdx.x == 0 && e) {
+        atomicAdd(&st.evicted, e);
+        atomicAdd(&st.tomb, e);
+    }
+}
+
+// Rebuild the map when deleted entries exceed 1/8 of it: clear it here and
+// re-insert the surviving residents in k_map_refill.
+__global__ void __launch_bounds__(kBlock) k_map_clear(DGlobal g) {
+    if (*g.err) return;
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    const int64_t mcap = (int64_t)tb.map_mask + 1;
+    if ((int64_t)st.tomb * 8 <= mcap) return;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < mcap; i += (int64_t)gridDim.x * blockDim.x)
+        tb.map[i] = make_int2(kEmpty, -1);
+    if (blockIdx.x == 0 && threadIdx.x == 0) st.rebuild = 1;
+}
+
+__global__ void __launch_bounds__(kBlock) k_map_refill(DGlobal g) {
+    if (*g.err) return;
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    if (!st.rebuild) return;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < tb.cap; k += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t row = tb.slot_row[k];
+        if (row >= 0) map_insert(tb, row, (int32_t)k);
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) st.tomb = 0;
+}
+
+__global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
+    if (*g.err) return;
+    __shared__ int tmp[16];
+    __shared__ int s_base;
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    const Counts c = table_counts(tb, st, p);
+    const int mode = st.sel_mode;
+    const uint64_t thr = st.prefix;
+    const int32_t top = st.free_top;
+    const int64_t ts = g.tstart[t], ps = g.pstart[t];
+    const int64_t items = (int64_t)c.nm + c.nnp;
+    int n_adm_miss = 0, n_fill = 0, n_pdrop = 0, n_mdrop = 0, n_reuse = 0;
+    unsigned long long dig = 0;
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < items; base += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t k = base + threadIdx.x;
+        int adm = 0;
+        int32_t row = 0, s = 0;
+        bool is_miss = false, inp = false;
+        if (k < items) {
+            is_miss = k < c.nm;
+            if (is_miss) {
+                row = g.M[ts + k];
+                s = g.mscore[ts + k];
+                inp = (g.mflags[ts + k] & F_INP) != 0;
+            } else {
+                row = g.NP[ps + (k - c.nm)];
+                s = p.pscore;
+                inp = true;
+            }
+            adm = kept(mode, make_key(s, row, p.rowbits), thr) ? 1 : 0;
+        }
+        int tot;
+        const int ex = block_excl_scan(adm, tmp, &tot);
+        if (threadIdx.x == 0 && tot) s_base = atomicAdd(&st.popped, tot);
+        __syncthreads();
+        if (k < items) {
+            int32_t slot = -1;
+            const int64_t fi = (int64_t)top - 1 - (s_base + ex);
+            if (adm && (fi < 0 || fi >= tb.cap || (uint32_t)tb.free_stack[fi] >= (uint32_t)tb.cap)) {
+                atomicOr(g.err, ERR_INTERNAL);
+                adm = 0;
+            }
+            if (adm) {
+                slot = tb.free_stack[fi];
+                tb.slot_row[slot] = row;
+                tb.slot_score[slot] = s;
+                tb.slot_flags[slot] = inp ? F_PF : 0u;
+                tb.slot_touch[slot] = -1;
+                n_reuse += map_insert(tb, row, slot);
+                dig += mix64(((unsigned long long)t << 40) | (unsigned long long)row);
+                if (is_miss) ++n_adm_miss;
+                else ++n_fill;
+            } else {
+                if (is_miss) ++n_mdrop;
+                if (inp) ++n_pdrop;
+            }
+            if (is_miss) g.mslot[ts + k] = slot;
+            else g.npslot[ps + (k - c.nm)] = slot;
+        }
+        __syncthreads();
+    }
+    const int a = block_sum(n_adm_miss, tmp), f = block_sum(n_fill, tmp);
+    const int pd = block_sum(n_pdrop, tmp), md = block_sum(n_mdrop, tmp), ru = block_sum(n_reuse, tmp);
+    const unsigned long long d = wave_sum64(dig);
+    if ((threadIdx.x & 63) == 0 && d) atomicAdd(&st.digest_acc, d);
+    if (threadIdx.x == 0) {
+        if (a) atomicAdd(&st.adm_miss, a);
+        if (f) atomicAdd(&st.p_fill, f);
+        if (pd) atomicAdd(&st.p_drop, pd);
+        if (md) atomicAdd(&st.m_drop, md);
+        if (ru) atomicSub(&st.tomb, ru);
+    }
+}
+
+// Copy admitted rows into their slots: misses from HBM staging, prefetch
+// fills from pinned host memory over the host link.
+template <typename V>
+__device__ __forceinline__ void fill_rows(const DGlobal &g, const DTable &tb, const Counts &c, int64_t ts, int64_t ps,
+                                          int nunit) {
+    const int64_t items = ((int64_t)c.nm + c.nnp) * nunit;
+    const int64_t S = (int64_t)gridDim.x * blockDim.x;
+    const int64_t rb = tb.row_bytes;
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; base < items; base += 4 * S) {
+        V v[4];
+        int64_t dst[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            dst[q] = -1;
+            const int64_t it = base + q * S;
+            if (it < items) {
+                const int64_t cand = it / nunit;
+                const int64_t vo = (it - cand * nunit) * (int64_t)sizeof(V);
+                int32_t slot;
+                const char *src;
+                if (cand < c.nm) {
+                    slot = g.mslot[ts + cand];
+                    src = g.staging + (ts + cand) * g.stage_stride;
+                } else {
+                    const int64_t j = ps + (cand - c.nm);
+                    slot = g.npslot[j];
+                    src = tb.host + (int64_t)g.NP[j] * rb;
+                }
+                if (slot >= 0) {
+                    v[q] = *reinterpret_cast<const V *>(src + vo);
+                    dst[q] = (int64_t)slot * rb + vo;
+                }
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            if (dst[q] >= 0) *reinterpret_cast<V *>(tb.pool + dst[q]) = v[q];
+    }
+}
+
+__global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, PlcParams p) {
+    if (*g.err) return;
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    const TState &st = g.st[t];
+    const Counts c = table_counts(tb, st, p);
+    if (c.nm + c.nnp == 0 || st.sel_mode == SEL_NONE) return;
+    const int64_t ts = g.tstart[t], ps = g.pstart[t];
+    const int unit = tb.copy_unit;
+    const int nunit = tb.row_bytes / unit;
+    if (unit == 16) fill_rows<uint4>(g, tb, c, ts, ps, nunit);
+    else if (unit == 4) fill_rows<uint32_t>(g, tb, c, ts, ps, nunit);
+    else fill_rows<uint16_t>(g, tb, c, ts, ps, nunit);
+}
+
+__global__ void k_plc_finalize(DGlobal g) {
+    if (*g.err) return;
+    for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
+        TState &st = g.st[t];
+        const DTable &tb = g.tabs[t];
+        st.free_top -= st.popped;
+        st.popped = 0;
+        st.n_res = tb.cap - st.free_top;
+        st.rebuild = 0;
+        int64_t v[8];
+        v[0] = st.evicted;
+        v[1] = st.adm_miss;
+        v[2] = st.p_fill;
+        v[3] = st.p_res;
+        v[4] = st.p_drop;
+        v[5] = st.m_drop;
+        v[6] = st.n_res;
+        v[7] = (int64_t)st.p_fill * tb.row_bytes;
+        for (int k = 0; k < 8; ++k) {
+            st.last[6 + k] = v[k];
+            st.total[6 + k] += v[k];
+        }
+        st.digest = st.digest_acc;
+    }
+}
+
+// Initial state: every slot free, the free stack handing out slot 0 first.
+__global__ void __launch_bounds__(kBlock) k_init_state(DGlobal g) {
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < tb.cap; k += (int64_t)gridDim.x * blockDim.x)
+        tb.free_stack[k] = tb.cap - 1 - (int32_t)k;
+    if (blockIdx.x == 0 && threadIdx.x == 0) g.st[t].free_top = tb.cap;
+}
+
+// ----------------------------------------------------------------- launchers
+
+static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
+    int64_t b = (n + per_block - 1) / per_block;
+    if (b < 1) b = 1;
+    if (b > (int64_t)cap) b = cap;
+    return (unsigned)b;
+}
+
+void launch_plc_prep(const DGlobal &g, const int64_t *poff, int64_t np, hipStream_t s) {
+    k_plc_prep<<<1, kBlock, 0, s>>>(g, poff, np);
+}
+
+void launch_plc_bits(const DGlobal &g, const uint8_t *bits, int64_t n_last, hipStream_t s) {
+    if (n_last <= 0) return;
+    k_plc_bits<<<grid_for(n_last, kBlock * 4, 16384), kBlock, 0, s>>>(g, bits, n_last);
+}
+
+void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s) {
+    const dim3 grid(grid_for(item_bound, kBlock * 4, 2048), g.T);
+    k_plc_update<<<grid, kBlock, 0, s>>>(g, p);
+    for (int pass = 1; pass < p.passes; ++pass) k_plc_select<<<grid, kBlock, 0, s>>>(g, p, pass);
+}
+
+void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,
+                      hipStream_t s) {
+    const dim3 gcap(grid_for(max_cap, kBlock * 4, 2048), g.T);
+    k_plc_evict<<<gcap, kBlock, 0, s>>>(g, p);
+    k_map_clear<<<dim3(grid_for(max_map, kBlock * 8, 2048), g.T), kBlock, 0, s>>>(g);
+    k_map_refill<<<gcap, kBlock, 0, s>>>(g);
+    k_plc_admit<<<dim3(grid_for(cand_bound, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
+}
+
+void launch_plc_fill(const DGlobal &g, const PlcParams &p, int64_t cand_bound, int32_t max_units, hipStream_t s) {
+    k_plc_fill<<<dim3(grid_for(cand_bound * max_units, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
+}
+
+void launch_plc_finalize(const DGlobal &g, hipStream_t s) { k_plc_finalize<<<1, kBlock, 0, s>>>(g); }
+
+void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s) {
+    k_init_state<<<dim3(grid_for(max_cap, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g);
+}
+
+}  // namespace recmg

@@ -1,0 +1,277 @@
+// Device-side data layout and helpers of the tiered pooled-embedding lookup.
+// Internal to the HIP sources of this package; the public boundary is
+// include/recmg.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/recmg.h"
+
+namespace recmg {
+
+constexpr int kBlock = 256;                         // threads per block (4 waves)
+constexpr int kWordsPerThread = 4;                  // presence-bitmap words per thread
+constexpr int kWordsPerBlock = kBlock * kWordsPerThread;  // 1024 words = 32768 rows
+constexpr int kRadixBits = 11;                      // radix-select digit
+constexpr int kRadix = 1 << kRadixBits;
+constexpr int32_t kEmpty = -1;                      // map key of a never-used entry
+constexpr int32_t kTomb = -2;                       // map key of a deleted entry
+constexpr int32_t kPending = INT32_MIN;             // probe result before miss numbering
+
+// per-slot flag bits
+constexpr uint32_t F_PF = 1u;    // admitted by a prefetch and not accessed since
+constexpr uint32_t F_CBIT = 2u;  // OR of the caching bits of the last batch
+constexpr uint32_t F_INP = 4u;   // named by the current placement's prefetch list
+
+// device error flag bits
+constexpr int32_t ERR_RANGE = 1;
+constexpr int32_t ERR_OFFSETS = 2;
+constexpr int32_t ERR_INTERNAL = 4;  // a slot-accounting invariant failed (never expected)
+
+// outcome of the top-Cap ranking of one table
+constexpr int32_t SEL_SELECT = 0;  // keep keys >= threshold
+constexpr int32_t SEL_ALL = 1;     // |K| <= Cap: keep everything
+constexpr int32_t SEL_NONE = 2;    // Cap == 0 or K empty: keep nothing
+
+// Static description of one table, resident in the workspace.
+struct DTable {
+    const char *host;      // device-visible pointer to the pinned host table
+    char *pool;            // HBM slot pool [cap][row_bytes]
+    int32_t *slot_row;     // [cap] row held by the slot, -1 if free
+    int32_t *slot_score;   // [cap] ranking score
+    uint32_t *slot_flags;  // [cap] F_* bits
+    int32_t *slot_touch;   // [cap] stamp of the last forward that hit the slot
+    int32_t *free_stack;   // [cap] free slot ids, top at free_top
+    int2 *map;             // [map_mask + 1] open-addressed row -> slot map (key, slot)
+    uint32_t *bitmap;      // [bm_words] presence bitmap, zero between uses
+    uint2 *rank;           // [bm_words] (rank of the word's first set bit, word) after an emit
+    int64_t rows;
+    int64_t out_elem_off;  // sum of dims of the earlier tables
+    int64_t cap_off;       // sum of caps of the earlier tables
+    int32_t dim, dtype, row_bytes, cap;
+    int32_t map_mask, bm_words, bm_block0, bm_nblk;
+    int32_t gsz;           // lanes per bag in the pooled kernel (power of two, 4..64)
+    int32_t nchunk;        // element chunks per row in the pooled kernel
+    int32_t vec;           // 1: 16-byte vector path, 0: scalar path
+    int32_t bags_per_block;
+    int32_t copy_unit;     // 16, 4 or 2 bytes
+    int32_t pad[3];
+};
+
+// Mutable per-table state and counters, resident in the workspace.
+struct TState {
+    int32_t ucount;   // distinct rows of the last forward (sorted in U)
+    int32_t mcount;   // misses of the last forward (in M, staged at the same index)
+    int32_t pcount;   // distinct prefetch rows of the current placement
+    int32_t npcount;  // prefetch rows neither resident nor missed (in NP)
+    int32_t n_res, free_top, popped, tomb;
+    int32_t rebuild, sel_mode, need, pad0;
+    uint64_t prefix;  // radix-select prefix; the threshold key after the last pass
+    uint32_t done;    // blocks finished in the current select pass
+    int32_t pad1;
+    // accumulators of the call in flight
+    int32_t hits, hits_pf, p_res, evicted, adm_miss, p_fill, p_drop, m_drop;
+    unsigned long long digest_acc;
+    // published counters, in recmg_table_stats_t order
+    int64_t last[14];
+    unsigned long long digest;
+    int64_t total[14];
+};
+
+// Device pointers into the workspace, passed by value to every kernel.
+struct DGlobal {
+    DTable *tabs;
+    TState *st;
+    int32_t *err;
+    int32_t *bm_block_start;  // [T+1] first bitmap block of each table
+    int32_t *blocksum;        // [total bitmap blocks]
+    int32_t *blockoff;        // [total bitmap blocks]
+    int64_t *tstart;          // [T+1] first index of each table in the last forward
+    int64_t *pstart;          // [T+1] first prefetch id of each table in this placement
+    int32_t *src;             // [max_indices] per access: slot (>= 0) or -(miss + 1)
+    int32_t *inv;             // [max_indices] per access: rank of its row in U
+    int32_t *U;               // [max_indices] sorted distinct rows, table t at tstart[t]
+    int32_t *slotU;           // [max_indices] per distinct row: slot or -(miss + 1)
+    int32_t *M;               // [max_indices] missed rows, table t at tstart[t]
+    uint32_t *mflags;         // [max_indices] F_CBIT / F_INP of each miss
+    int32_t *mscore;          // [max_indices] ranking score of each miss
+    int32_t *mslot;           // [max_indices] slot given to an admitted miss, else -1
+    int32_t *NP;              // [max_prefetch] new prefetch candidates, table t at pstart[t]
+    int32_t *ptag;            // [max_prefetch] classification scratch
+    int32_t *npslot;          // [max_prefetch] slot given to an admitted candidate, else -1
+    int32_t *hist;            // [T][kRadix]
+    int32_t *dump;            // [sum cap] sorted resident rows
+    int32_t *dump_count;      // [T]
+    char *staging;            // [max_indices][stage_stride] miss rows in HBM
+    int64_t stage_stride;
+    int32_t T;
+    int32_t total_bm_blocks;
+};
+
+// Parameters of one placement.
+struct PlcParams {
+    int32_t prio;        // 1: PRIORITY, 0: LRU_BATCH
+    int32_t es;          // eviction_speed
+    int32_t lru_touch;   // LRU score of a row touched by the last batch
+    int32_t pscore;      // score of a prefetched row
+    int32_t last_stamp;  // stamp of the last forward, -2 if none since the last placement
+    int32_t have_fwd;
+    int32_t rowbits, total_bits, passes;
+    int32_t pad;
+};
+
+// -------------------------------------------------------------------- helpers
+
+__device__ __forceinline__ uint32_t hash_row(int32_t r) {
+    // murmur3 32-bit finaliser
+    uint32_t h = (uint32_t)r;
+    h ^= h >> 16;
+    h *= 0x85ebca6bu;
+    h ^= h >> 13;
+    h *= 0xc2b2ae35u;
+    h ^= h >> 16;
+    return h;
+}
+
+// Slot of `row` or -1.  Linear probing; deleted entries are skipped.
+__device__ __forceinline__ int32_t map_find(const DTable &tb, int32_t row) {
+    const int32_t mask = tb.map_mask;
+    uint32_t i = hash_row(row) & (uint32_t)mask;
+    for (int32_t n = 0; n <= mask; ++n) {
+        int2 e = tb.map[i];
+        if (e.x == row) return e.y;
+        if (e.x == kEmpty) return -1;
+        i = (i + 1) & (uint32_t)mask;
+    }
+    return -1;
+}
+
+// Insert a row known to be absent.  Concurrent inserts of distinct rows are
+// safe; no lookup may run concurrently.  Returns 1 if a deleted entry was reused.
+__device__ __forceinline__ int map_insert(const DTable &tb, int32_t row, int32_t slot) {
+    const int32_t mask = tb.map_mask;
+    uint32_t i = hash_row(row) & (uint32_t)mask;
+    for (int32_t n = 0; n <= mask; ++n) {
+        int32_t k = tb.map[i].x;  // may be stale (L1); the CAS result is not
+        while (k == kEmpty || k == kTomb) {
+            const int32_t prev = atomicCAS(&tb.map[i].x, k, row);
+            if (prev == k) {
+                tb.map[i].y = slot;
+                return k == kTomb;
+            }
+            k = prev;  // lost the entry to another insert
+        }
+        i = (i + 1) & (uint32_t)mask;
+    }
+    return 0;
+}
+
+// Delete a present row (distinct rows may be deleted concurrently).
+__device__ __forceinline__ void map_delete(const DTable &tb, int32_t row) {
+    const int32_t mask = tb.map_mask;
+    uint32_t i = hash_row(row) & (uint32_t)mask;
+    for (int32_t n = 0; n <= mask; ++n) {
+        int32_t k = tb.map[i].x;
+        if (k == row) {
+            tb.map[i].x = kTomb;
+            return;
+        }
+        if (k == kEmpty) return;
+        i = (i + 1) & (uint32_t)mask;
+    }
+}
+
+// SplitMix64 output mix (Steele, Lea & Flood, OOPSLA 2014).
+__device__ __forceinline__ unsigned long long mix64(unsigned long long z) {
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebULL;
+    return z ^ (z >> 31);
+}
+
+// Largest t in [0, T) with starts[t] <= i (starts non-decreasing).
+__device__ __forceinline__ int find_seg(const int64_t *starts, int T, int64_t i) {
+    int lo = 0, hi = T - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (starts[mid] <= i) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int find_seg32(const int32_t *starts, int T, int32_t i) {
+    int lo = 0, hi = T - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (starts[mid] <= i) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int wave_incl_scan(int x) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        int y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
+    }
+    return x;
+}
+
+// Exclusive scan over the block (blockDim.x a multiple of 64, <= 1024).
+// `tmp` is __shared__ int[16]; every thread must call.
+__device__ __forceinline__ int block_excl_scan(int v, int *tmp, int *total) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    int x = wave_incl_scan(v);
+    if (lane == 63) tmp[wid] = x;
+    __syncthreads();
+    int pre = 0, tot = 0;
+    for (int k = 0; k < nw; ++k) {
+        int s = tmp[k];
+        pre += (k < wid) ? s : 0;
+        tot += s;
+    }
+    __syncthreads();
+    *total = tot;
+    return pre + x - v;
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+    return v;
+}
+
+__device__ __forceinline__ unsigned long long wave_sum64(unsigned long long v) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+        unsigned lo = __shfl_xor((unsigned)v, d, 64);
+        unsigned hi = __shfl_xor((unsigned)(v >> 32), d, 64);
+        v += ((unsigned long long)hi << 32) | lo;
+    }
+    return v;
+}
+
+// Sum over the block; result valid in every thread.  `tmp` is __shared__ int[16].
+__device__ __forceinline__ int block_sum(int v, int *tmp) {
+    int dummy;
+    int excl = block_excl_scan(v, tmp, &dummy);
+    (void)excl;
+    return dummy;
+}
+
+__device__ __forceinline__ uint64_t make_key(int32_t score, int32_t row, int rowbits) {
+    return ((uint64_t)(uint32_t)score << rowbits) | (uint64_t)(uint32_t)row;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+    return __builtin_bit_cast(float, bits16 << 16);
+}
+
+__device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+}
+
+}  // namespace recmg

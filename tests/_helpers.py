@@ -38,3 +38,116 @@ def l1_mass(tables_f64, dims, indices, offsets, bags):
             a, e = offsets[t * bags + j], offsets[t * bags + j + 1]
             out.append(tab[indices[a:e]].sum(axis=0) if e > a else np.zeros(dims[t]))
     return np.concatenate(out) if out else np.zeros(0)
+
+
+RTOL = {"f32": 1e-5, "f16": 2e-2, "bf16": 2e-2}
+
+
+def accumulation_bound(n):
+    """fp32 error bound of the kernel's summation order relative to the L1 mass:
+    four interleaved running sums (ceil(n/4) - 1 additions each) combined
+    pairwise (2 more), unit roundoff 2^-24; one more rounding for the fp32
+    result of the reference."""
+    return ((np.ceil(np.asarray(n) / 4.0) - 1).clip(min=0) + 3) * 2.0 ** -24
+
+
+def bag_lengths(w, offsets):
+    """Length of the bag behind every output element (table-major)."""
+    out = []
+    for t, tb in enumerate(w.tables):
+        ln = np.diff(offsets[t * w.bags:(t + 1) * w.bags + 1])
+        out.append(np.repeat(ln, tb.dim))
+    return np.concatenate(out) if out else np.zeros(0, np.int64)
+
+
+def check_pooled(w, tabs_f64, idx, off, got, ref64, label=""):
+    """Element passes iff |got - ref| <= rtol * (sum of |x_i| over its bag)."""
+    dims = [tb.dim for tb in w.tables]
+    mass = l1_mass(tabs_f64, dims, idx, off, w.bags)
+    err = np.abs(got.astype(np.float64) - ref64)
+    lens = bag_lengths(w, off)
+    at = 0
+    for t, tb in enumerate(w.tables):
+        n = w.bags * tb.dim
+        e, m, ln = err[at:at + n], mass[at:at + n], lens[at:at + n]
+        assert np.all(e <= RTOL[tb.dtype] * m), f"{label} table {t}: error above rtol * L1 mass"
+        # the kernel sums in fp32 whatever the storage type: the derived bound holds too
+        assert np.all(e <= accumulation_bound(ln) * m + 0.0), f"{label} table {t}: error above the fp32 bound"
+        at += n
+    return float((err / np.maximum(mass, 1e-300)).max()) if err.size else 0.0
+
+
+class GpuRunner:
+    """Drives the HIP path through a workload (test helper; marshalling only)."""
+
+    def __init__(self, w, tabs, miss_mode="zero_copy", validate=False, max_indices=None, max_prefetch=None,
+                 nbatches=None):
+        import torch
+        from paper_2511_08568_amd import TieredEmbeddingCache
+        self.torch = torch
+        self.w = w
+        self.dev = torch.device("cuda", 0)
+        nb = nbatches or w.batches
+        if max_indices is None:
+            max_indices = max(max(w.batch(b)[0].size for b in range(nb)), 1)
+        if max_prefetch is None:
+            max_prefetch = max(max(w.prefetch_list(b)[0].size for b in range(nb)), 1)
+        self.host = [torch.from_numpy(np.ascontiguousarray(a)).pin_memory() for a in tabs]
+        self.cache = TieredEmbeddingCache(self.host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables],
+                                          policy=w.policy, eviction_speed=w.eviction_speed, miss_mode=miss_mode,
+                                          max_bags_per_table=w.bags, max_indices=max_indices,
+                                          max_prefetch=max_prefetch, validate=validate)
+
+    def to_dev(self, a):
+        return self.torch.from_numpy(np.ascontiguousarray(a)).to(self.dev)
+
+    def placement(self, P, poff, bits=None):
+        self.cache.placement(self.to_dev(P) if P.size else None, self.to_dev(poff),
+                             None if bits is None else self.to_dev(bits))
+
+    def forward(self, idx, off):
+        return self.cache.forward(self.to_dev(idx), self.to_dev(off), self.w.bags).cpu().numpy()
+
+    def run(self, nbatches=None, dump=True):
+        recs = []
+        w = self.w
+        for b in range(nbatches or w.batches):
+            P, poff = w.prefetch_list(b)
+            bits = w.cache_bits(b - 1) if b > 0 else None
+            self.placement(P, poff, bits)
+            if dump:
+                place, _, res = self.cache.stats(dump=True)
+            else:
+                (place, _), res = self.cache.stats(), None
+            idx, off = w.batch(b)
+            out = self.forward(idx, off)
+            fwd, _ = self.cache.stats()
+            recs.append(dict(place=place, resident=res, fwd=fwd, out=out, idx=idx, off=off))
+        return recs
+
+    def close(self):
+        self.cache.close()
+
+
+PLACE_KEYS = ("evicted", "admitted_miss", "prefetch_fill", "prefetch_resident", "prefetch_dropped",
+              "miss_dropped", "resident", "prefetch_bytes", "digest")
+FWD_KEYS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand_bytes")
+
+
+def compare_runs(w, tabs, ora, gpu, label=""):
+    """Bit-exact counters and resident sets, pooled outputs within tolerance."""
+    import tracegen as tg
+    f64 = [tg.storage_to_f64(a, tb.dtype) for a, tb in zip(tabs, w.tables)]
+    worst = 0.0
+    for b, (o, g) in enumerate(zip(ora, gpu)):
+        for t in range(w.num_tables):
+            for k in PLACE_KEYS:
+                assert g["place"][t][k] == o["place"][t][k], f"{label} batch {b} table {t} placement {k}: gpu {g['place'][t][k]} oracle {o['place'][t][k]}"
+            if g["resident"] is not None:
+                assert np.array_equal(g["resident"][t], o["resident"][t]), f"{label} batch {b} table {t}: resident set"
+            for k in FWD_KEYS:
+                assert g["fwd"][t][k] == o["fwd"][t][k], f"{label} batch {b} table {t} forward {k}: gpu {g['fwd'][t][k]} oracle {o['fwd'][t][k]}"
+        if w.integer_values:
+            assert np.array_equal(g["out"], o["out32"]), f"{label} batch {b}: integer-valued sums must be exact"
+        worst = max(worst, check_pooled(w, f64, o["idx"], o["off"], g["out"], o["out64"], f"{label} batch {b}"))
+    return worst

@@ -1,0 +1,84 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/recmg.h declares, and recmg_query_workspace validates
+configurations."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2511_08568_amd as pk
+from paper_2511_08568_amd import binding as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "recmg.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:int32_t|const char \*)\s*(recmg_\w+)\s*\(", src, re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    assert names == sorted(bd.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = pk.load_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert isinstance(pk.recmg_last_error(), str)
+
+
+def _cfg(rows=(1000,), dims=(64,), dtypes=(0,), caps=(100,), policy=0, miss=0, max_idx=5000, max_pf=5000,
+         bags=256, es=4):
+    T = len(rows)
+    keep = []
+    cfg = bd.recmg_config_t()
+    cfg.num_tables = T
+    for name, ctype, vals in (("rows", ctypes.c_int64, rows), ("dims", ctypes.c_int32, dims),
+                              ("dtypes", ctypes.c_int32, dtypes), ("cache_rows", ctypes.c_int64, caps)):
+        arr = (ctype * T)(*vals)
+        keep.append(arr)
+        setattr(cfg, name, arr)
+    bufs = [np.zeros(16 * r * d + 64, np.uint8) for r, d in zip(rows, dims)]
+    ptrs = (ctypes.c_void_p * T)(*[(b.ctypes.data + 15) // 16 * 16 for b in bufs])
+    keep += [bufs, ptrs]
+    cfg.host_tables = ptrs
+    cfg.policy, cfg.miss_mode, cfg.eviction_speed = policy, miss, es
+    cfg.max_indices, cfg.max_prefetch, cfg.max_bags_per_table = max_idx, max_pf, bags
+    cfg._keep = keep
+    return cfg
+
+
+def test_query_workspace_sizes():
+    dev, host = bd.recmg_query_workspace(_cfg())
+    # at least the slot pool, its map and the staging rows
+    assert dev >= 100 * 256 + 256 * 8 + 5000 * 256
+    assert host == 0
+    dev2, host2 = bd.recmg_query_workspace(_cfg(miss=1))
+    assert dev2 == dev and host2 >= 5000 * 256
+
+
+def test_query_scales_with_capacity():
+    a, _ = bd.recmg_query_workspace(_cfg(caps=(100,)))
+    b, _ = bd.recmg_query_workspace(_cfg(caps=(1000,)))
+    assert b - a >= 900 * 256
+
+
+@pytest.mark.parametrize("kw", [dict(rows=(0,)), dict(dims=(0,)), dict(dtypes=(7,)), dict(caps=(-1,)),
+                                dict(policy=5), dict(miss=9), dict(max_idx=-1), dict(es=-1),
+                                dict(max_idx=1 << 31)])
+def test_query_rejects_bad_configs(kw):
+    with pytest.raises(bd.RecmgError) as e:
+        bd.recmg_query_workspace(_cfg(**kw))
+    assert e.value.code == bd.RECMG_E_INVALID
+    assert pk.recmg_last_error()
+
+
+def test_null_handle_is_rejected():
+    lib = pk.load_library()
+    assert lib.recmg_embbag_forward(None, None, None, 0, 0, None, None) == bd.RECMG_E_INVALID
+    assert lib.recmg_apply_placement(None, None, None, 0, None, None) == bd.RECMG_E_INVALID
+    assert lib.recmg_cache_destroy(None) == bd.RECMG_OK

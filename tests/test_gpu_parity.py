@@ -1,0 +1,136 @@
+"""HIP path vs the CPU oracle, through the C ABI: counters and resident sets
+bit-exact, pooled outputs within rtol * L1 mass (1e-5 fp32, 2e-2 fp16/bf16)."""
+import numpy as np
+import pytest
+
+import tracegen as tg
+from _helpers import GpuRunner, compare_runs, golden_table, load_golden
+from oracle_pins import GOLDEN_FILES, run_oracle
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+def _parity(w, nbatches=None, miss_mode="zero_copy", label=""):
+    nb = nbatches or w.batches
+    tabs, ora = run_oracle(w, nbatches=nb)
+    g = GpuRunner(w, tabs, miss_mode=miss_mode, nbatches=nb)
+    try:
+        gpu = g.run(nb)
+    finally:
+        g.close()
+    return compare_runs(w, tabs, ora, gpu, label=label or w.name)
+
+
+@pytest.mark.parametrize("name", GOLDEN_FILES)
+def test_hand_examples(name):
+    gd = load_golden(name)
+    tab = golden_table(gd)
+    w = tg.Workload(0, name, [tg.Table(gd["rows"], gd["dim"], "f32", gd["cap"], 1.0, ("fixed", 1))],
+                    batches=len(gd["steps"]), bags=1, policy=gd["policy"], eviction_speed=gd["eviction_speed"])
+    import torch as th
+    from paper_2511_08568_amd import TieredEmbeddingCache
+    dev = th.device("cuda", 0)
+    cache = TieredEmbeddingCache([th.from_numpy(tab).pin_memory()], ["f32"], [gd["cap"]], policy=gd["policy"],
+                                 eviction_speed=gd["eviction_speed"], max_bags_per_table=4, max_indices=16,
+                                 max_prefetch=16)
+    for b, step in enumerate(gd["steps"]):
+        P = np.array(step["prefetch"], np.int32)
+        bits = None if step["bits"] is None else th.tensor(step["bits"], dtype=th.uint8, device=dev)
+        cache.placement(th.from_numpy(P).to(dev) if P.size else None, th.tensor([0, P.size], device=dev), bits)
+        last, _, res = cache.stats(dump=True)
+        for k, v in step["expect_placement"].items():
+            assert last[0][k] == v, (name, b, k)
+        assert res[0].tolist() == step["resident"], (name, b)
+        off = np.array(step["offsets"], np.int64)
+        out = cache.forward(th.tensor(step["indices"], dtype=th.int32, device=dev), th.from_numpy(off).to(dev),
+                            off.size - 1)
+        last, _ = cache.stats()
+        for k, v in step["expect_forward"].items():
+            assert last[0][k] == v, (name, b, k)
+        assert out.cpu().numpy().tolist() == np.array(step["out"], np.float32).reshape(-1).tolist()
+    cache.close()
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_tiny_random(seed):
+    w = tg.random_tiny(seed, max_rows=40, max_cap=12, max_dim=9, batches=6, bags=5)
+    _parity(w, label=f"tiny{seed}")
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_small_random_real_values(seed):
+    w = tg.random_tiny(100 + seed, max_rows=3000, max_cap=600, max_dim=70, batches=5, bags=40,
+                       integer_values=False)
+    _parity(w, label=f"small{seed}")
+
+
+def test_config1_full():
+    """Config 1 at full size (1 x 100,000 x 64 fp32, cache 10,000), first 40 batches."""
+    _parity(tg.make_config(1), nbatches=40)
+
+
+@pytest.mark.parametrize("cid,scale,bags,tables", [(2, 0.02, 256, 3), (3, 0.01, 256, 6), (4, 0.0005, 512, 2),
+                                                   (5, 0.01, 256, 8)])
+def test_configs_scaled(cid, scale, bags, tables):
+    """Configs 2-5 with rows and caches scaled down (same dims, dtypes, policies,
+    pooling laws, Zipf exponents and prefetch recipes), several tiles of rows
+    per table and ragged bags."""
+    w = tg.scaled_config(cid, row_scale=scale, batches=6, bags=bags, max_tables=tables)
+    _parity(w, label=f"c{cid}-scaled")
+
+
+def test_config4_no_prefetch_scaled():
+    w = tg.scaled_config(4, row_scale=0.0005, batches=6, bags=512, max_tables=2, prefetch=("none",))
+    _parity(w, label="c4-noprefetch")
+
+
+def test_staged_matches_oracle():
+    w = tg.scaled_config(3, row_scale=0.01, batches=5, bags=256, max_tables=5)
+    _parity(w, miss_mode="staged", label="c3-staged")
+
+
+def test_cap_zero_and_full_give_identical_outputs():
+    """Metamorphic: the tier that serves a row must not change the pooled sum."""
+    base = tg.scaled_config(2, row_scale=0.005, batches=3, bags=128, max_tables=2)
+    outs = []
+    for cap in ("zero", "full"):
+        w = tg.scaled_config(2, row_scale=0.005, batches=3, bags=128, max_tables=2)
+        for tb in w.tables:
+            tb.cap = 0 if cap == "zero" else tb.rows
+        tabs = [w.table_values(t) for t in range(w.num_tables)]
+        g = GpuRunner(w, tabs)
+        recs = g.run(dump=False)
+        g.close()
+        outs.append([r["out"] for r in recs])
+        if cap == "zero":
+            assert all(r["fwd"][t]["hits"] == 0 for r in recs for t in range(w.num_tables))
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
+    del base
+
+
+def test_zero_copy_and_staged_bitwise_equal():
+    outs = []
+    for mode in ("zero_copy", "staged"):
+        w = tg.scaled_config(5, row_scale=0.005, batches=4, bags=128, max_tables=4)
+        tabs = [w.table_values(t) for t in range(w.num_tables)]
+        g = GpuRunner(w, tabs, miss_mode=mode)
+        outs.append(g.run())
+        g.close()
+    for a, b in zip(*outs):
+        assert np.array_equal(a["out"], b["out"])
+        assert a["fwd"] == b["fwd"] and a["place"] == b["place"]
+
+
+def test_run_twice_is_deterministic():
+    res = []
+    for _ in range(2):
+        w = tg.scaled_config(3, row_scale=0.005, batches=4, bags=256, max_tables=4)
+        tabs = [w.table_values(t) for t in range(w.num_tables)]
+        g = GpuRunner(w, tabs)
+        res.append(g.run())
+        g.close()
+    for a, b in zip(*res):
+        assert np.array_equal(a["out"], b["out"]) and a["fwd"] == b["fwd"] and a["place"] == b["place"]
