@@ -44,6 +44,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-link-peak", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run 3 device-to-device copies of MIB MiB (scale for HBM byte counters) and exit")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -59,6 +61,15 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda", 0)
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        a = torch.ones(n, dtype=torch.uint8, device=dev)
+        z = torch.empty_like(a)
+        for _ in range(3):
+            z.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "copies": 3}), flush=True)
+        return
     if args.row_scale < 1.0:
         w = tg.scaled_config(args.config, row_scale=args.row_scale)
     else:
@@ -130,13 +141,20 @@ def main():
     lookups = sum(int(batches[b][0].size) for b in range(W, nb))
     delta = {k: sum(tot1[t][k] - tot0[t][k] for t in range(T)) for k in tot1[0] if k != "digest"}
     pool_ms, pool_calls = stages["fwd_pool"]
-    # algorithmic bytes of one pooled launch: per lookup row + 4-byte index, per bag 8-byte offset + fp32 output
-    alg_bytes = 0
+    # Bytes of one pooled launch.  Algorithmic minimum: every distinct row of the
+    # batch read once (repeats need not come from HBM again), a 4-byte location
+    # per index, an 8-byte offset and the fp32 output per bag.  Logical: a full
+    # row per index.
+    alg_bytes, logical_bytes = 0, 0
+    for t, tb in enumerate(w.tables):
+        alg_bytes += (tot1[t]["unique"] - tot0[t]["unique"]) * tb.row_bytes
     for b in range(W, nb):
         idx, off = batches[b]
         for t, tb in enumerate(w.tables):
             s, e = w.table_segment(off, t)
-            alg_bytes += (e - s) * (tb.row_bytes + 4) + w.bags * (8 + 4 * tb.dim)
+            per_bag = w.bags * (8 + 4 * tb.dim)
+            alg_bytes += (e - s) * 4 + per_bag
+            logical_bytes += (e - s) * (tb.row_bytes + 4) + per_bag
     bytes_per_launch = alg_bytes / K
     pool_s = pool_ms / max(pool_calls, 1) / 1e3
     achieved = bytes_per_launch / pool_s / 1e9 if pool_s > 0 else 0.0
@@ -191,6 +209,8 @@ def main():
             "traffic": None,
             "alg_bytes_per_launch": bytes_per_launch,
             "avg_launch_us": pool_s * 1e6,
+            "logical_bytes_per_launch": logical_bytes / K,
+            "logical_GBs": logical_bytes / K / pool_s / 1e9 if pool_s > 0 else 0.0,
         },
         "ondemand_fetches_per_batch": delta["misses"] / K,
         "prefetch_fills_per_batch": delta["prefetch_fill"] / K,
