@@ -12,7 +12,8 @@ import os
 from typing import Optional, Sequence
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "librecmg.so")
+# RECMG_LIBRARY points the binding at another build of the same library
+LIB_PATH = os.environ.get("RECMG_LIBRARY") or os.path.join(HERE, "librecmg.so")
 
 RECMG_OK, RECMG_E_INVALID, RECMG_E_RANGE, RECMG_E_STATE, RECMG_E_HIP, RECMG_E_NOMEM = range(6)
 RECMG_F32, RECMG_F16, RECMG_BF16 = range(3)
@@ -161,7 +162,7 @@ class TieredEmbeddingCache:
     def __init__(self, host_tables: Sequence, dtypes: Sequence[str], cache_rows: Sequence[int], *,
                  policy: str = "lru", eviction_speed: int = 4, miss_mode: str = "zero_copy",
                  max_bags_per_table: int, max_indices: int, max_prefetch: int, validate: bool = False,
-                 timing: bool = False, device: int = 0):
+                 timing: bool = False, overlap: bool = True, device: int = 0):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", device)
@@ -194,7 +195,8 @@ class TieredEmbeddingCache:
         dev_bytes, host_bytes = recmg_query_workspace(cfg)
         with torch.cuda.device(self.device):
             self.workspace = torch.empty(dev_bytes, dtype=torch.uint8, device=self.device)
-            self.copy_stream = torch.cuda.Stream(device=self.device) if miss_mode == "staged" else None
+            # side stream: staged miss copies and prefetch fills (which then overlap the next forward's dedup)
+            self.copy_stream = torch.cuda.Stream(device=self.device) if (overlap or miss_mode == "staged") else None
         self.staging = torch.empty(host_bytes, dtype=torch.uint8, pin_memory=True) if host_bytes else None
         cfg.device_workspace = self.workspace.data_ptr()
         cfg.device_workspace_bytes = dev_bytes

@@ -59,7 +59,8 @@ struct Layout {
     std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, free_stack, map, bitmap, rank;
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, inv = 0, U = 0, slotU = 0, M = 0, mflags = 0, mscore = 0, mslot = 0;
-    size_t NP = 0, ptag = 0, npslot = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, staging = 0;
+    size_t NP = 0, PU = 0, npslot = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, ftstart = 0;
+    size_t staging[2] = {0, 0};
     int64_t stage_stride = 0, sum_cap = 0;
     int32_t total_bm_blocks = 0;
 };
@@ -92,7 +93,7 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
         g.esz = g.dtype == RECMG_F32 ? 4 : 2;
         g.row_bytes = g.dim * g.esz;
         g.cap = (int32_t)std::min<int64_t>(cfg->cache_rows[t], g.rows);
-        g.map_cap = pow2ceil(std::max<int64_t>(64, 2 * (int64_t)g.cap));
+        g.map_cap = pow2ceil(std::max<int64_t>(64, 4 * (int64_t)g.cap));  // load <= 1/4
         const int64_t words = (g.rows + 31) / 32;
         g.bm_nblk = (int32_t)((words + kWordsPerBlock - 1) / kWordsPerBlock);
         g.bm_words = (int64_t)g.bm_nblk * kWordsPerBlock;
@@ -130,7 +131,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
         L->free_stack.push_back(take((size_t)g.cap * 4));
         L->map.push_back(take((size_t)g.map_cap * 8));
         L->bitmap.push_back(take((size_t)g.bm_words * 4));
-        L->rank.push_back(take((size_t)g.bm_words * 8));
+        L->rank.push_back(take((size_t)g.bm_words * 16));
         L->total_bm_blocks += g.bm_nblk;
         L->sum_cap += g.cap;
     }
@@ -152,13 +153,15 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->mscore = take(4 * mi);
     L->mslot = take(4 * mi);
     L->NP = take(4 * mp);
-    L->ptag = take(4 * mp);
+    L->PU = take(4 * mp);
     L->npslot = take(4 * mp);
     L->hist = take(4 * (size_t)kRadix * T);
     L->dump = take(4 * (size_t)L->sum_cap);
     L->dump_count = take(4 * T);
     L->pool_bstart = take(4 * (T + 1));
-    L->staging = take(mi * (size_t)L->stage_stride);
+    L->ftstart = take(8 * (T + 1));
+    L->staging[0] = take(mi * (size_t)L->stage_stride);
+    L->staging[1] = take(mi * (size_t)L->stage_stride);
     L->total = off;
     L->host_total = cfg->miss_mode == RECMG_STAGED ? align256(4 * std::max<size_t>(mi, 1)) + mi * (size_t)L->stage_stride : 0;
 }
@@ -175,11 +178,16 @@ struct recmg_cache {
     DGlobal g{};
     std::vector<const char *> host;  // host tables (host pointers)
     int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1;
+    uint32_t pool_classes = 0;  // bit (dtype * 2 + vec) per class of table present
     int64_t max_rows = 0;
     int64_t placements = 0, forwards = 0, last_n = 0;
     bool have_fwd = false;
     hipStream_t last_stream = nullptr;
     int32_t pool_B = -1;
+    char *stage[2] = {nullptr, nullptr};  // staging buffers, alternating between forwards
+    int cur = 0;                          // buffer of the latest forward
+    bool fill_pending = false;            // a prefetch fill runs on the side stream
+    hipEvent_t ev_admit = nullptr, ev_fill = nullptr;
     int64_t pool_blocks = 0;
     std::vector<int32_t> pool_bstart;
     // STAGED
@@ -393,12 +401,15 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.mscore = reinterpret_cast<int32_t *>(ws + L.mscore);
     g.mslot = reinterpret_cast<int32_t *>(ws + L.mslot);
     g.NP = reinterpret_cast<int32_t *>(ws + L.NP);
-    g.ptag = reinterpret_cast<int32_t *>(ws + L.ptag);
+    g.PU = reinterpret_cast<int32_t *>(ws + L.PU);
+    g.ftstart = reinterpret_cast<int64_t *>(ws + L.ftstart);
     g.npslot = reinterpret_cast<int32_t *>(ws + L.npslot);
     g.hist = reinterpret_cast<int32_t *>(ws + L.hist);
     g.dump = reinterpret_cast<int32_t *>(ws + L.dump);
     g.dump_count = reinterpret_cast<int32_t *>(ws + L.dump_count);
-    g.staging = ws + L.staging;
+    c->stage[0] = ws + L.staging[0];
+    c->stage[1] = ws + L.staging[1];
+    g.staging = c->stage[0];
     g.stage_stride = L.stage_stride;
     g.T = T;
     g.total_bm_blocks = L.total_bm_blocks;
@@ -419,7 +430,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         d.free_stack = reinterpret_cast<int32_t *>(ws + L.free_stack[t]);
         d.map = reinterpret_cast<int2 *>(ws + L.map[t]);
         d.bitmap = reinterpret_cast<uint32_t *>(ws + L.bitmap[t]);
-        d.rank = reinterpret_cast<uint2 *>(ws + L.rank[t]);
+        d.rank = reinterpret_cast<uint4 *>(ws + L.rank[t]);
         d.rows = ge.rows;
         d.out_elem_off = out_off;
         d.cap_off = cap_off;
@@ -443,6 +454,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         c->max_map = (int32_t)std::max<int64_t>(c->max_map, ge.map_cap);
         c->max_units = std::max(c->max_units, ge.row_bytes / ge.copy_unit);
         c->max_rows = std::max(c->max_rows, ge.rows);
+        c->pool_classes |= 1u << (ge.dtype * 2 + ge.vec);
     }
     c->rowbits = std::max(1, bitlen((uint64_t)(c->max_rows - 1)));
 
@@ -456,6 +468,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         HIP_TRY(hipMemsetAsync(ws + L.slot_touch[t], 0xff, (size_t)ge.cap * 4, s0));
         HIP_TRY(hipMemsetAsync(ws + L.map[t], 0xff, (size_t)ge.map_cap * 8, s0));
         HIP_TRY(hipMemsetAsync(ws + L.bitmap[t], 0, (size_t)ge.bm_words * 4, s0));
+        HIP_TRY(hipMemsetAsync(ws + L.rank[t], 0xff, (size_t)ge.bm_words * 16, s0));  // stamp -1
     }
     HIP_TRY(hipMemsetAsync(ws + L.st, 0, sizeof(TState) * T, s0));
     HIP_TRY(hipMemsetAsync(ws + L.err, 0, 4, s0));
@@ -466,10 +479,14 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipDeviceSynchronize());
 
+    c->copy_stream = static_cast<hipStream_t>(cfg->copy_stream);
+    if (c->copy_stream) {
+        HIP_TRY(hipEventCreateWithFlags(&c->ev_admit, hipEventDisableTiming));
+        HIP_TRY(hipEventCreateWithFlags(&c->ev_fill, hipEventDisableTiming));
+    }
     if (cfg->miss_mode == RECMG_STAGED) {
         c->h_mrows = static_cast<int32_t *>(cfg->host_staging);
         c->h_rows = static_cast<char *>(cfg->host_staging) + align256(4 * std::max<size_t>((size_t)cfg->max_indices, 1));
-        c->copy_stream = static_cast<hipStream_t>(cfg->copy_stream);
         HIP_TRY(hipEventCreateWithFlags(&c->ev_ready, hipEventDisableTiming));
         HIP_TRY(hipEventCreateWithFlags(&c->ev_copied, hipEventDisableTiming));
     }
@@ -492,6 +509,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (c->cfg.validate && (rc = host_check_ids(prefetch_rows, prefetch_offsets, c->T + 1, 1, num_prefetch, c->geo, s)))
         return rc;
+    c->g.staging = c->stage[c->cur];  // misses of the latest forward
     const DGlobal &g = c->g;
     const int64_t b = c->placements;
     if (b + 2 >= (int64_t(1) << 31)) return fail(RECMG_E_STATE, "placement count exhausted");
@@ -514,8 +532,10 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         if (p.prio && cache_bits && c->have_fwd) launch_plc_bits(g, cache_bits, c->last_n, s);
         if (num_prefetch > 0) {
             launch_mark(g, prefetch_rows, g.pstart, num_prefetch, s);
-            launch_dedup(g, 1, reinterpret_cast<int32_t *>(reinterpret_cast<char *>(g.st) + offsetof(TState, pcount)),
-                         (int)(sizeof(TState) / 4), 0, p.have_fwd, s);
+            launch_dedup(g, EMIT_PREFETCH,
+                         reinterpret_cast<int32_t *>(reinterpret_cast<char *>(g.st) + offsetof(TState, pcount)),
+                         (int)(sizeof(TState) / 4), 0, s);
+            launch_plc_classify(g, p.last_stamp, num_prefetch, s);
         }
     }
     const int64_t cand = (c->have_fwd ? c->last_n : 0) + num_prefetch;
@@ -529,7 +549,17 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         StageTimer tm(c, RECMG_STAGE_PLC_APPLY, s);
         launch_plc_apply(g, p, c->max_cap, c->max_map, cand_grid, s);
     }
-    {
+    if (c->copy_stream) {
+        // the fill overlaps the next forward's dedup; that forward's pooling waits for it
+        HIP_TRY(hipEventRecord(c->ev_admit, s));
+        HIP_TRY(hipStreamWaitEvent(c->copy_stream, c->ev_admit, 0));
+        {
+            StageTimer tm(c, RECMG_STAGE_PLC_FILL, c->copy_stream);
+            launch_plc_fill(g, p, cand_grid, c->max_units, c->copy_stream);
+        }
+        HIP_TRY(hipEventRecord(c->ev_fill, c->copy_stream));
+        c->fill_pending = true;
+    } else {
         StageTimer tm(c, RECMG_STAGE_PLC_FILL, s);
         launch_plc_fill(g, p, cand_grid, c->max_units, s);
     }
@@ -567,13 +597,17 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
     }
     if (c->forwards + 1 >= (int64_t(1) << 31)) return fail(RECMG_E_STATE, "forward count exhausted");
     const int32_t stamp = (int32_t)c->forwards;
+    c->cur ^= 1;  // the other staging buffer: a pending fill may still read this one
+    c->g.staging = c->stage[c->cur];
     {
         StageTimer tm(c, RECMG_STAGE_FWD_DEDUP, s);
         launch_fwd_prep(g, offsets, (int32_t)B, n, s);
         if (n > 0) {
             launch_mark(g, indices, g.tstart, n, s);
-            launch_dedup(g, 0, reinterpret_cast<int32_t *>(reinterpret_cast<char *>(g.st) + offsetof(TState, ucount)),
-                         (int)(sizeof(TState) / 4), stamp, 0, s);
+            launch_dedup(g, EMIT_FORWARD,
+                         reinterpret_cast<int32_t *>(reinterpret_cast<char *>(g.st) + offsetof(TState, ucount)),
+                         (int)(sizeof(TState) / 4), stamp, s);
+            launch_fwd_probe(g, stamp, n, s);
             launch_fwd_src(g, indices, n, s);
         }
     }
@@ -585,11 +619,15 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
             return rc;
         }
     }
+    if (c->fill_pending) {
+        HIP_TRY(hipStreamWaitEvent(s, c->ev_fill, 0));
+        c->fill_pending = false;
+    }
     {
         StageTimer tm(c, RECMG_STAGE_FWD_POOL, s);
         launch_pool(g, offsets, (int32_t)B, out, c->pool_blocks,
                     reinterpret_cast<const int32_t *>(static_cast<char *>(c->cfg.device_workspace) + c->L.pool_bstart),
-                    s);
+                    c->pool_classes, s);
     }
     launch_fwd_finalize(g, s);
     HIP_TRY(hipGetLastError());
@@ -606,6 +644,10 @@ int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_sta
     if (rc) return rc;
     if ((rc = set_device(c))) return rc;
     hipStream_t s = c->last_stream;
+    if (c->fill_pending) {
+        HIP_TRY(hipStreamWaitEvent(s, c->ev_fill, 0));
+        c->fill_pending = false;
+    }
     HIP_TRY(hipStreamSynchronize(s));
     const int T = c->T;
     std::vector<TState> st(T);
@@ -629,7 +671,7 @@ int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_sta
         for (int t = 0; t < T; ++t) need += st[t].n_res;
         if (resident_dump && dump_capacity < need) return fail(RECMG_E_INVALID, "dump_capacity too small");
         launch_mark_resident(c->g, c->max_cap, s);
-        launch_dedup(c->g, 2, c->g.dump_count, 1, 0, 0, s);
+        launch_dedup(c->g, EMIT_DUMP, c->g.dump_count, 1, 0, s);
         HIP_TRY(hipGetLastError());
         std::vector<int32_t> cnt(T);
         HIP_TRY(hipMemcpyAsync(cnt.data(), c->g.dump_count, 4 * T, hipMemcpyDeviceToHost, s));
@@ -679,6 +721,10 @@ int32_t recmg_cache_destroy(recmg_cache_t *c) {
     (void)set_device(c);
     int32_t rc = RECMG_OK;
     if (hipStreamSynchronize(c->last_stream) != hipSuccess) rc = fail(RECMG_E_HIP, "synchronize failed at destroy");
+    if (c->copy_stream && hipStreamSynchronize(c->copy_stream) != hipSuccess)
+        rc = fail(RECMG_E_HIP, "synchronize failed at destroy");
+    if (c->ev_admit) (void)hipEventDestroy(c->ev_admit);
+    if (c->ev_fill) (void)hipEventDestroy(c->ev_fill);
     for (auto &m : c->marks) {
         c->ev_free.push_back(m.a);
         c->ev_free.push_back(m.b);

@@ -4,23 +4,22 @@
 // of ids is deduplicated by setting one bit per id; the distinct ids then come
 // out in ascending order by scanning the bitmap: a block-wide popcount gives
 // each 1024-word block its count, a per-table scan turns counts into offsets,
-// and the emit pass writes every set bit's row at its rank.  For every
-// non-zero word the emit also stores (rank of its first bit, the word), so the
-// rank of any id in the distinct list is one load plus a popcount.  Cost is
+// and the emit pass writes every set bit's row at its rank.  For a forward the
+// emit also stores, per non-zero word, (rank of its first set bit, the word,
+// the forward's stamp), so the rank of any id of the batch is one load plus a
+// popcount, and "was row r in the last batch" is one load.  Cost is
 // O(ids + N_t / 32) with no comparison passes, which suits ids drawn from a
 // bounded domain; the emit clears the bitmap behind it.
 //
-// The emit runs one of three visitors on every distinct id:
-//   EMIT_FORWARD  probe the row -> slot map (the lookup's cache probe), count
-//                 hits, stamp hit slots, number the misses;
-//   EMIT_PREFETCH classify a prefetch id as resident / missed by the last
-//                 batch / new candidate (Alg. 1's prefetch loop, as a set);
-//   EMIT_DUMP     write the sorted resident rows for recmg_stats.
+// Marking: Zipf-popular rows make many threads set the same bit.  Each block
+// first deduplicates its ids in a small LDS hash set, so a popular row costs
+// one global atomic per block instead of one per occurrence.
 #include "launch.h"
 
 namespace recmg {
 
-// ------------------------------------------------------------------- mark
+constexpr int kLdsSet = 2048;  // entries of the per-block LDS set (power of two)
+constexpr int kLdsProbes = 8;
 
 __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__restrict__ keys,
                                                  const int64_t *__restrict__ starts, int64_t n) {
@@ -28,6 +27,7 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
     __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
     __shared__ int64_t s_rows[RECMG_MAX_TABLES];
     __shared__ uint32_t *s_bm[RECMG_MAX_TABLES];
+    __shared__ unsigned long long s_set[kLdsSet];
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         s_start[t] = starts[t];
         if (t < g.T) {
@@ -35,18 +35,37 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
             s_bm[t] = g.tabs[t].bitmap;
         }
     }
+    for (int k = threadIdx.x; k < kLdsSet; k += blockDim.x) s_set[k] = ~0ull;
     __syncthreads();
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    // each block takes a contiguous chunk, so repeats within the chunk meet in LDS
+    const int64_t chunk = (n + gridDim.x - 1) / gridDim.x;
+    const int64_t lo = (int64_t)blockIdx.x * chunk;
+    const int64_t hi = lo + chunk < n ? lo + chunk : n;
+    for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
         const int t = find_seg(s_start, g.T, i);
         const int32_t r = keys[i];
         if (r < 0 || (int64_t)r >= s_rows[t]) {
             atomicOr(g.err, ERR_RANGE);
             continue;
         }
-        uint32_t *w = s_bm[t] + (r >> 5);
-        const uint32_t bit = 1u << (r & 31);
-        if (!(__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit)) atomicOr(w, bit);
+        const unsigned long long key = ((unsigned long long)t << 32) | (uint32_t)r;
+        bool mine = true;  // this thread must set the global bit
+        uint32_t h = hash_row(r ^ (t * 0x9e3779b9)) & (kLdsSet - 1);
+        for (int p = 0; p < kLdsProbes; ++p) {
+            unsigned long long cur = s_set[h];
+            if (cur == ~0ull) cur = atomicCAS(&s_set[h], ~0ull, key);
+            if (cur == ~0ull) break;           // inserted here: mark globally
+            if (cur == key) {                  // another thread of the block marks it
+                mine = false;
+                break;
+            }
+            h = (h + 1) & (kLdsSet - 1);
+        }
+        if (mine) {
+            uint32_t *w = s_bm[t] + (r >> 5);
+            const uint32_t bit = 1u << (r & 31);
+            if (!(__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit)) atomicOr(w, bit);
+        }
     }
 }
 
@@ -60,8 +79,6 @@ __global__ void __launch_bounds__(kBlock) k_mark_resident(DGlobal g) {
         if (r >= 0) atomicOr(tb.bitmap + (r >> 5), 1u << (r & 31));
     }
 }
-
-// ------------------------------------------------------------------- count
 
 __device__ __forceinline__ int block_table(const DGlobal &g, int blk) {
     __shared__ int s_t;
@@ -102,128 +119,38 @@ __global__ void __launch_bounds__(1024) k_bm_scan(DGlobal g, int32_t *counts, in
     if (threadIdx.x == 0) counts[(int64_t)t * count_stride] = carry;
 }
 
-// ------------------------------------------------------------------- emit
-
-enum { EMIT_FORWARD = 0, EMIT_PREFETCH = 1, EMIT_DUMP = 2 };
-
-struct EmitCtx {
-    int32_t stamp;     // EMIT_FORWARD: stamp of this forward
-    int32_t have_fwd;  // EMIT_PREFETCH: a forward ran since the last placement
-};
-
+// Write the distinct ids in ascending order (U, PU or the resident dump).
 template <int MODE>
-__global__ void __launch_bounds__(kBlock) k_bm_emit(DGlobal g, EmitCtx ctx) {
+__global__ void __launch_bounds__(kBlock) k_bm_emit(DGlobal g, int32_t stamp) {
     if (*g.err) return;
     __shared__ int tmp[16];
-    __shared__ int s_base;
     const int blk = blockIdx.x;
     const int t = block_table(g, blk);
     const DTable &tb = g.tabs[t];
-    TState &st = g.st[t];
     const int64_t wbase = (int64_t)(blk - tb.bm_block0) * kWordsPerBlock + threadIdx.x * kWordsPerThread;
-    uint4 w4 = *reinterpret_cast<const uint4 *>(tb.bitmap + wbase);
-    uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
+    const uint4 w4 = *reinterpret_cast<const uint4 *>(tb.bitmap + wbase);
+    const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
     const int cnt = __popc(w[0]) + __popc(w[1]) + __popc(w[2]) + __popc(w[3]);
     int tot;
     const int first = g.blockoff[blk] + block_excl_scan(cnt, tmp, &tot);
     if (tot == 0) return;  // block-uniform
-
-    int64_t seg;  // where table t's distinct ids start in the output arrays
-    if (MODE == EMIT_FORWARD) seg = g.tstart[t];
-    else if (MODE == EMIT_PREFETCH) seg = g.pstart[t];
-    else seg = tb.cap_off;
-
-    int hits = 0, hits_pf = 0, pres = 0, nappend = 0;
-    // pass 1: rank words, emit rows, run the visitor
+    int32_t *out;
+    if (MODE == EMIT_FORWARD) out = g.U + g.tstart[t];
+    else if (MODE == EMIT_PREFETCH) out = g.PU + g.pstart[t];
+    else out = g.dump + tb.cap_off;
     int u = first;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
         uint32_t bits = w[q];
         if (!bits) continue;
         const int64_t word = wbase + q;
-        if (MODE == EMIT_FORWARD) tb.rank[word] = make_uint2((uint32_t)u, bits);
+        if (MODE == EMIT_FORWARD) tb.rank[word] = make_uint4((uint32_t)u, bits, (uint32_t)stamp, 0u);
         tb.bitmap[word] = 0;
         while (bits) {
             const int b = __ffs(bits) - 1;
             bits &= bits - 1;
-            const int32_t row = (int32_t)(word * 32 + b);
-            if (MODE == EMIT_FORWARD) {
-                g.U[seg + u] = row;
-                const int32_t slot = map_find(tb, row);
-                if (slot >= 0) {
-                    g.slotU[seg + u] = slot;
-                    tb.slot_touch[slot] = ctx.stamp;
-                    ++hits;
-                    hits_pf += (tb.slot_flags[slot] & F_PF) ? 1 : 0;
-                } else {
-                    g.slotU[seg + u] = kPending;
-                    ++nappend;
-                }
-            } else if (MODE == EMIT_PREFETCH) {
-                int32_t tag = -1;  // the row itself if it becomes a new candidate
-                const int32_t slot = map_find(tb, row);
-                if (slot >= 0) {
-                    atomicOr(&tb.slot_flags[slot], F_INP);
-                    ++pres;
-                } else {
-                    int64_t m = -1;
-                    if (ctx.have_fwd) {
-                        // was it missed by the last batch?  U of that batch is sorted.
-                        const int64_t ts = g.tstart[t];
-                        int lo = 0, hi = st.ucount;
-                        while (lo < hi) {
-                            const int mid = (lo + hi) >> 1;
-                            if (g.U[ts + mid] < row) lo = mid + 1;
-                            else hi = mid;
-                        }
-                        if (lo < st.ucount && g.U[ts + lo] == row) m = -(int64_t)g.slotU[ts + lo] - 1;
-                        if (m >= 0) atomicOr(&g.mflags[ts + m], F_INP);
-                    }
-                    if (m < 0) {
-                        tag = row;
-                        ++nappend;
-                    }
-                }
-                g.ptag[seg + u] = tag;
-            } else {
-                g.dump[seg + u] = row;
-            }
-            ++u;
+            out[u++] = (int32_t)(word * 32 + b);
         }
-    }
-    if (MODE == EMIT_DUMP) return;
-
-    // pass 2: number the appended ids (misses / new candidates) block-wide
-    const int app_ex = block_excl_scan(nappend, tmp, &tot);
-    if (threadIdx.x == 0 && tot > 0)
-        s_base = atomicAdd(MODE == EMIT_FORWARD ? &st.mcount : &st.npcount, tot);
-    __syncthreads();
-    if (nappend) {
-        int a = s_base + app_ex;
-        for (int k = first; k < first + cnt; ++k) {
-            if (MODE == EMIT_FORWARD) {
-                if (g.slotU[seg + k] == kPending) {
-                    g.slotU[seg + k] = -(a + 1);
-                    g.M[seg + a] = g.U[seg + k];
-                    g.mflags[seg + a] = 0;
-                    ++a;
-                }
-            } else {
-                const int32_t row = g.ptag[seg + k];
-                if (row >= 0) g.NP[seg + a++] = row;
-            }
-        }
-    }
-    if (MODE == EMIT_FORWARD) {
-        const int h = block_sum(hits, tmp);
-        const int hp = block_sum(hits_pf, tmp);
-        if (threadIdx.x == 0) {
-            if (h) atomicAdd(&st.hits, h);
-            if (hp) atomicAdd(&st.hits_pf, hp);
-        }
-    } else {
-        const int p = block_sum(pres, tmp);
-        if (threadIdx.x == 0 && p) atomicAdd(&st.p_res, p);
     }
 }
 
@@ -238,7 +165,7 @@ static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
 
 void launch_mark(const DGlobal &g, const int32_t *keys, const int64_t *starts, int64_t n, hipStream_t s) {
     if (n <= 0) return;
-    k_mark<<<grid_for(n, kBlock * 4, 16384), kBlock, 0, s>>>(g, keys, starts, n);
+    k_mark<<<grid_for(n, kBlock * 8, 4096), kBlock, 0, s>>>(g, keys, starts, n);
 }
 
 void launch_mark_resident(const DGlobal &g, int32_t max_cap, hipStream_t s) {
@@ -247,14 +174,12 @@ void launch_mark_resident(const DGlobal &g, int32_t max_cap, hipStream_t s) {
     k_mark_resident<<<grid, kBlock, 0, s>>>(g);
 }
 
-void launch_dedup(const DGlobal &g, int mode, int32_t *counts, int count_stride, int32_t stamp, int32_t have_fwd,
-                  hipStream_t s) {
+void launch_dedup(const DGlobal &g, int mode, int32_t *counts, int count_stride, int32_t stamp, hipStream_t s) {
     k_bm_count<<<g.total_bm_blocks, kBlock, 0, s>>>(g);
     k_bm_scan<<<g.T, 1024, 0, s>>>(g, counts, count_stride);
-    EmitCtx ctx{stamp, have_fwd};
-    if (mode == EMIT_FORWARD) k_bm_emit<EMIT_FORWARD><<<g.total_bm_blocks, kBlock, 0, s>>>(g, ctx);
-    else if (mode == EMIT_PREFETCH) k_bm_emit<EMIT_PREFETCH><<<g.total_bm_blocks, kBlock, 0, s>>>(g, ctx);
-    else k_bm_emit<EMIT_DUMP><<<g.total_bm_blocks, kBlock, 0, s>>>(g, ctx);
+    if (mode == EMIT_FORWARD) k_bm_emit<EMIT_FORWARD><<<g.total_bm_blocks, kBlock, 0, s>>>(g, stamp);
+    else if (mode == EMIT_PREFETCH) k_bm_emit<EMIT_PREFETCH><<<g.total_bm_blocks, kBlock, 0, s>>>(g, stamp);
+    else k_bm_emit<EMIT_DUMP><<<g.total_bm_blocks, kBlock, 0, s>>>(g, stamp);
 }
 
 }  // namespace recmg

@@ -31,11 +31,58 @@ __global__ void __launch_bounds__(kBlock) k_fwd_prep(DGlobal g, const int64_t *_
     }
 }
 
+// Cache probe of every distinct row (row -> slot map): hits are stamped and
+// counted, misses are numbered (their staging row) block by block.
+__global__ void __launch_bounds__(kBlock) k_fwd_probe(DGlobal g, int32_t stamp) {
+    if (*g.err) return;
+    __shared__ int tmp[16];
+    __shared__ int s_base;
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    const int32_t nu = st.ucount;
+    const int64_t ts = g.tstart[t];
+    int hits = 0, hits_pf = 0;
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < nu; base += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t k = base + threadIdx.x;
+        int miss = 0;
+        int32_t row = 0;
+        if (k < nu) {
+            row = g.U[ts + k];
+            const int32_t slot = map_find(tb, row);
+            if (slot >= 0) {
+                g.slotU[ts + k] = slot;
+                tb.slot_touch[slot] = stamp;
+                ++hits;
+                hits_pf += (tb.slot_flags[slot] & F_PF) ? 1 : 0;
+            } else {
+                miss = 1;
+            }
+        }
+        int tot;
+        const int ex = block_excl_scan(miss, tmp, &tot);
+        if (threadIdx.x == 0 && tot) s_base = atomicAdd(&st.mcount, tot);
+        __syncthreads();
+        if (miss) {
+            const int64_t m = s_base + ex;
+            g.slotU[ts + k] = -(int32_t)(m + 1);
+            g.M[ts + m] = row;
+            g.mflags[ts + m] = 0;
+        }
+        __syncthreads();
+    }
+    const int h = block_sum(hits, tmp), hp = block_sum(hits_pf, tmp);
+    if (threadIdx.x == 0) {
+        if (h) atomicAdd(&st.hits, h);
+        if (hp) atomicAdd(&st.hits_pf, hp);
+    }
+}
+
 // inverse map and data location of every index
 __global__ void __launch_bounds__(kBlock) k_fwd_src(DGlobal g, const int32_t *__restrict__ indices, int64_t n) {
     if (*g.err) return;
     __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
-    __shared__ const uint2 *s_rank[RECMG_MAX_TABLES];
+    __shared__ const uint4 *s_rank[RECMG_MAX_TABLES];
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         s_start[t] = g.tstart[t];
         if (t < g.T) s_rank[t] = g.tabs[t].rank;
@@ -45,7 +92,7 @@ __global__ void __launch_bounds__(kBlock) k_fwd_src(DGlobal g, const int32_t *__
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
         const int t = find_seg(s_start, g.T, i);
         const int32_t r = indices[i];
-        const uint2 rk = s_rank[t][r >> 5];
+        const uint4 rk = s_rank[t][r >> 5];
         const int32_t u = (int32_t)rk.x + __popc(rk.y & ((1u << (r & 31)) - 1u));
         g.inv[i] = u;
         g.src[i] = g.slotU[s_start[t] + u];
@@ -155,7 +202,8 @@ struct Lane {
 // One group of G lanes sums one bag.  Lookup p of the bag goes to
 // accumulator p mod 4; the four partial sums are combined pairwise at the end.
 // The order is fixed per bag, so the result does not depend on which tier
-// served each row.
+// served each row.  The group keeps up to 16 row loads in flight and loads the
+// next chunk of locations while the current chunk's rows are in flight.
 template <int DT, bool VEC>
 __device__ __forceinline__ void pool_table(const DGlobal &g, const DTable &tb, int t, int32_t B,
                                            const int64_t *__restrict__ offsets, float *__restrict__ out,
@@ -164,6 +212,11 @@ __device__ __forceinline__ void pool_table(const DGlobal &g, const DTable &tb, i
     using V = typename L::V;
     constexpr int VE = L::VE;
     constexpr int EB = Elem<DT>::bytes;
+#ifndef RECMG_POOL_UNROLL
+#define RECMG_POOL_UNROLL 16
+#endif
+    // loads in flight per group, within the register budget
+    constexpr int UNROLL = EB == 4 ? RECMG_POOL_UNROLL : (RECMG_POOL_UNROLL > 8 ? 8 : RECMG_POOL_UNROLL);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int G = tb.gsz;
     const int gl = lane & (G - 1);
@@ -190,31 +243,37 @@ __device__ __forceinline__ void pool_table(const DGlobal &g, const DTable &tb, i
 #pragma unroll
             for (int x = 0; x < VE; ++x) acc[k][x] = 0.f;
 
+        int my = (a + gl < e) ? src[a + gl] : 0;
         for (int64_t c = a; c < e; c += G) {
             const int n = (int)((e - c) < G ? (e - c) : G);
-            const int my = gl < n ? src[c + gl] : 0;
+            const int nxt = (c + G + gl < e) ? src[c + G + gl] : 0;  // next chunk, in flight meanwhile
             int q = 0;
-            for (; q + 8 <= n; q += 8) {
-                V v[8];
+            for (; q + UNROLL <= n; q += UNROLL) {
+                V v[UNROLL];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
+                for (int u = 0; u < UNROLL; ++u) {
                     const int s = __shfl(my, q + u, G);
                     const char *p = s >= 0 ? pool + (int64_t)s * rb : stg + (int64_t)(-s - 1) * sstride;
                     v[u] = *reinterpret_cast<const V *>(p + eoff);
                 }
 #pragma unroll
-                for (int u = 0; u < 8; ++u) L::add(acc[u & 3], v[u]);
+                for (int u = 0; u < UNROLL; ++u) L::add(acc[u & 3], v[u]);
             }
             for (; q < n; q += 4) {
+                V v[4];
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
                     if (q + u < n) {
                         const int s = __shfl(my, q + u, G);
                         const char *p = s >= 0 ? pool + (int64_t)s * rb : stg + (int64_t)(-s - 1) * sstride;
-                        L::add(acc[u], *reinterpret_cast<const V *>(p + eoff));
+                        v[u] = *reinterpret_cast<const V *>(p + eoff);
                     }
                 }
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (q + u < n) L::add(acc[u], v[u]);
             }
+            my = nxt;
         }
         if (lane_ok) {
             float r[VE];
@@ -233,23 +292,27 @@ __device__ __forceinline__ void pool_table(const DGlobal &g, const DTable &tb, i
     }
 }
 
+// One launch per (storage type, vector path) class present; a block whose
+// table belongs to another class returns at once.
+template <int DT, bool VEC>
 __global__ void __launch_bounds__(kBlock) k_pool(DGlobal g, const int64_t *__restrict__ offsets, int32_t B,
                                                  float *__restrict__ out, const int32_t *__restrict__ bstart) {
     if (*g.err) return;
+    // Workgroups are dealt round-robin to the 8 XCDs; give each XCD one
+    // contiguous range of bags so a table's hot rows stay in one L2.
+#ifndef RECMG_POOL_NO_XCD_MAP
+    const int nb = (int)gridDim.x, x = (int)blockIdx.x & 7, q = nb >> 3, r = nb & 7;
+    const int lb = x * q + (x < r ? x : r) + ((int)blockIdx.x >> 3);
+#else
+    const int lb = (int)blockIdx.x;
+#endif
     __shared__ int s_t;
-    if (threadIdx.x == 0) s_t = find_seg32(bstart, g.T, (int32_t)blockIdx.x);
+    if (threadIdx.x == 0) s_t = find_seg32(bstart, g.T, lb);
     __syncthreads();
     const int t = s_t;
     const DTable &tb = g.tabs[t];
-    const int bi = (int)blockIdx.x - bstart[t];
-    switch (tb.dtype * 2 + tb.vec) {
-    case RECMG_F32 * 2 + 1: pool_table<RECMG_F32, true>(g, tb, t, B, offsets, out, bi); break;
-    case RECMG_F32 * 2 + 0: pool_table<RECMG_F32, false>(g, tb, t, B, offsets, out, bi); break;
-    case RECMG_F16 * 2 + 1: pool_table<RECMG_F16, true>(g, tb, t, B, offsets, out, bi); break;
-    case RECMG_F16 * 2 + 0: pool_table<RECMG_F16, false>(g, tb, t, B, offsets, out, bi); break;
-    case RECMG_BF16 * 2 + 1: pool_table<RECMG_BF16, true>(g, tb, t, B, offsets, out, bi); break;
-    default: pool_table<RECMG_BF16, false>(g, tb, t, B, offsets, out, bi); break;
-    }
+    if (tb.dtype != DT || tb.vec != (VEC ? 1 : 0)) return;
+    pool_table<DT, VEC>(g, tb, t, B, offsets, out, lb - bstart[t]);
 }
 
 __global__ void k_fwd_finalize(DGlobal g) {
@@ -285,6 +348,11 @@ void launch_fwd_prep(const DGlobal &g, const int64_t *offsets, int32_t B, int64_
     k_fwd_prep<<<(unsigned)((items + kBlock - 1) / kBlock), kBlock, 0, s>>>(g, offsets, B, n);
 }
 
+void launch_fwd_probe(const DGlobal &g, int32_t stamp, int64_t n, hipStream_t s) {
+    if (n <= 0) return;
+    k_fwd_probe<<<dim3(grid_for(n / g.T + 1, kBlock, 1024), g.T), kBlock, 0, s>>>(g, stamp);
+}
+
 void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStream_t s) {
     if (n <= 0) return;
     k_fwd_src<<<grid_for(n, kBlock * 4, 16384), kBlock, 0, s>>>(g, indices, n);
@@ -296,9 +364,15 @@ void launch_fetch(const DGlobal &g, hipStream_t s) {
 }
 
 void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, int64_t nblocks,
-                 const int32_t *bstart, hipStream_t s) {
+                 const int32_t *bstart, uint32_t classes, hipStream_t s) {
     if (nblocks <= 0) return;
-    k_pool<<<(unsigned)nblocks, kBlock, 0, s>>>(g, offsets, B, out, bstart);
+    const unsigned nbk = (unsigned)nblocks;
+    if (classes & (1u << (RECMG_F32 * 2 + 1))) k_pool<RECMG_F32, true><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
+    if (classes & (1u << (RECMG_F32 * 2))) k_pool<RECMG_F32, false><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
+    if (classes & (1u << (RECMG_F16 * 2 + 1))) k_pool<RECMG_F16, true><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
+    if (classes & (1u << (RECMG_F16 * 2))) k_pool<RECMG_F16, false><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
+    if (classes & (1u << (RECMG_BF16 * 2 + 1))) k_pool<RECMG_BF16, true><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
+    if (classes & (1u << (RECMG_BF16 * 2))) k_pool<RECMG_BF16, false><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
 }
 
 void launch_fwd_finalize(const DGlobal &g, hipStream_t s) { k_fwd_finalize<<<1, kBlock, 0, s>>>(g); }

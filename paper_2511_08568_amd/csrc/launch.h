@@ -8,21 +8,24 @@ namespace recmg {
 // dedup.hip
 void launch_mark(const DGlobal &g, const int32_t *keys, const int64_t *starts, int64_t n, hipStream_t s);
 void launch_mark_resident(const DGlobal &g, int32_t max_cap, hipStream_t s);
-// mode: 0 forward probe, 1 prefetch classification, 2 resident dump
-void launch_dedup(const DGlobal &g, int mode, int32_t *counts, int count_stride, int32_t stamp, int32_t have_fwd,
-                  hipStream_t s);
+enum { EMIT_FORWARD = 0, EMIT_PREFETCH = 1, EMIT_DUMP = 2 };
+// mode: where the sorted distinct ids go (U of a forward, PU of a placement, the resident dump)
+void launch_dedup(const DGlobal &g, int mode, int32_t *counts, int count_stride, int32_t stamp, hipStream_t s);
 
 // forward.hip
 void launch_fwd_prep(const DGlobal &g, const int64_t *offsets, int32_t B, int64_t n, hipStream_t s);
+void launch_fwd_probe(const DGlobal &g, int32_t stamp, int64_t n, hipStream_t s);
 void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStream_t s);
 void launch_fetch(const DGlobal &g, hipStream_t s);
+// classes: bit (dtype * 2 + vec) set for every (storage type, vector path) class of a table
 void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, int64_t nblocks,
-                 const int32_t *bstart, hipStream_t s);
+                 const int32_t *bstart, uint32_t classes, hipStream_t s);
 void launch_fwd_finalize(const DGlobal &g, hipStream_t s);
 
 // placement.hip
 void launch_plc_prep(const DGlobal &g, const int64_t *poff, int64_t np, hipStream_t s);
 void launch_plc_bits(const DGlobal &g, const uint8_t *bits, int64_t n_last, hipStream_t s);
+void launch_plc_classify(const DGlobal &g, int32_t last_stamp, int64_t np, hipStream_t s);
 void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s);
 void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,
                       hipStream_t s);

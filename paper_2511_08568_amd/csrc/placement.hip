@@ -28,6 +28,7 @@ __global__ void k_plc_prep(DGlobal g, const int64_t *__restrict__ poff, int64_t 
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         const int64_t v = poff[t];
         g.pstart[t] = v;
+        g.ftstart[t] = g.tstart[t];
         if (t < g.T && v > poff[t + 1]) atomicOr(g.err, ERR_OFFSETS);
         if ((t == 0 && v != 0) || (t == g.T && v != np)) atomicOr(g.err, ERR_OFFSETS);
         if (t < g.T) {
@@ -61,6 +62,53 @@ __global__ void __launch_bounds__(kBlock) k_plc_bits(DGlobal g, const uint8_t *_
         if (s >= 0) atomicOr(&g.tabs[t].slot_flags[s], F_CBIT);
         else atomicOr(&g.mflags[s_start[t] + (-(int64_t)s - 1)], F_CBIT);
     }
+}
+
+// Classify every distinct prefetch row (Alg. 1's prefetch loop taken as a
+// set): resident -> flag the slot; missed by the last batch -> flag the miss;
+// otherwise a new candidate, numbered block by block into NP.
+__global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last_stamp) {
+    if (*g.err) return;
+    __shared__ int tmp[16];
+    __shared__ int s_base;
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    const int32_t np = st.pcount;
+    const int64_t ps = g.pstart[t], ts = g.tstart[t];
+    int pres = 0;
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < np; base += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t k = base + threadIdx.x;
+        int isnew = 0;
+        int32_t row = 0;
+        if (k < np) {
+            row = g.PU[ps + k];
+            const int32_t slot = map_find(tb, row);
+            if (slot >= 0) {
+                atomicOr(&tb.slot_flags[slot], F_INP);
+                ++pres;
+            } else {
+                // distinct rows of the last batch carry its stamp in the rank word
+                const uint4 rk = tb.rank[row >> 5];
+                const uint32_t bit = 1u << (row & 31);
+                if ((int32_t)rk.z == last_stamp && (rk.y & bit)) {
+                    const int32_t u = (int32_t)rk.x + __popc(rk.y & (bit - 1u));
+                    const int64_t m = -(int64_t)g.slotU[ts + u] - 1;
+                    atomicOr(&g.mflags[ts + m], F_INP);
+                } else {
+                    isnew = 1;
+                }
+            }
+        }
+        int tot;
+        const int ex = block_excl_scan(isnew, tmp, &tot);
+        if (threadIdx.x == 0 && tot) s_base = atomicAdd(&st.npcount, tot);
+        __syncthreads();
+        if (isnew) g.NP[ps + s_base + ex] = row;
+        __syncthreads();
+    }
+    const int p = block_sum(pres, tmp);
+    if (threadIdx.x == 0 && p) atomicAdd(&st.p_res, p);
 }
 
 // ----------------------------------------------------------------- ranking
@@ -136,7 +184,10 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
     const DTable &tb = g.tabs[t];
     TState &st = g.st[t];
     const Counts c = table_counts(tb, st, p);
-    if (blockIdx.x == 0 && threadIdx.x == 0) st.sel_mode = c.mode;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        st.sel_mode = c.mode;
+        st.plc_nm = c.nm;
+    }
     const bool sel = c.mode == SEL_SELECT;
     if (sel)
         for (int b = threadIdx.x; b < kRadix; b += blockDim.x) s_hist[b] = 0;
@@ -277,7 +328,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_evict(DGlobal g, PlcParams p) {
     }
 }
 
-// Rebuild the map when deleted entries exceed 1/8 of it: clear it here and
+// Rebuild the map when deleted entries exceed 1/4 of it: clear it here and
 // re-insert the surviving residents in k_map_refill.
 __global__ void __launch_bounds__(kBlock) k_map_clear(DGlobal g) {
     if (*g.err) return;
@@ -285,7 +336,7 @@ __global__ void __launch_bounds__(kBlock) k_map_clear(DGlobal g) {
     const DTable &tb = g.tabs[t];
     TState &st = g.st[t];
     const int64_t mcap = (int64_t)tb.map_mask + 1;
-    if ((int64_t)st.tomb * 8 <= mcap) return;
+    if ((int64_t)st.tomb * 4 <= mcap) return;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < mcap; i += (int64_t)gridDim.x * blockDim.x)
         tb.map[i] = make_int2(kEmpty, -1);
     if (blockIdx.x == 0 && threadIdx.x == 0) st.rebuild = 1;
@@ -420,14 +471,19 @@ __device__ __forceinline__ void fill_rows(const DGlobal &g, const DTable &tb, co
     }
 }
 
+// May run on a side stream, concurrently with the next forward's dedup: it
+// reads only placement-owned state (plc_nm, ftstart, mslot, NP, npslot) and the
+// staging buffer of the previous forward, which the next forward does not use.
 __global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, PlcParams p) {
     if (*g.err) return;
     const int t = blockIdx.y;
     const DTable &tb = g.tabs[t];
     const TState &st = g.st[t];
-    const Counts c = table_counts(tb, st, p);
+    Counts c;
+    c.nm = st.plc_nm;
+    c.nnp = st.npcount;
     if (c.nm + c.nnp == 0 || st.sel_mode == SEL_NONE) return;
-    const int64_t ts = g.tstart[t], ps = g.pstart[t];
+    const int64_t ts = g.ftstart[t], ps = g.pstart[t];
     const int unit = tb.copy_unit;
     const int nunit = tb.row_bytes / unit;
     if (unit == 16) fill_rows<uint4>(g, tb, c, ts, ps, nunit);
@@ -488,8 +544,14 @@ void launch_plc_bits(const DGlobal &g, const uint8_t *bits, int64_t n_last, hipS
     k_plc_bits<<<grid_for(n_last, kBlock * 4, 16384), kBlock, 0, s>>>(g, bits, n_last);
 }
 
+void launch_plc_classify(const DGlobal &g, int32_t last_stamp, int64_t np, hipStream_t s) {
+    if (np <= 0) return;
+    k_plc_classify<<<dim3(grid_for(np / g.T + 1, kBlock, 1024), g.T), kBlock, 0, s>>>(g, last_stamp);
+}
+
 void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s) {
-    const dim3 grid(grid_for(item_bound, kBlock * 4, 2048), g.T);
+    // few blocks per table: each block merges a 2048-bin histogram into global memory
+    const dim3 grid(grid_for(item_bound, kBlock * 32, 512), g.T);
     k_plc_update<<<grid, kBlock, 0, s>>>(g, p);
     for (int pass = 1; pass < p.passes; ++pass) k_plc_select<<<grid, kBlock, 0, s>>>(g, p, pass);
 }
@@ -504,7 +566,10 @@ void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int
 }
 
 void launch_plc_fill(const DGlobal &g, const PlcParams &p, int64_t cand_bound, int32_t max_units, hipStream_t s) {
-    k_plc_fill<<<dim3(grid_for(cand_bound * max_units, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
+    // The host link saturates with a few hundred waves of 4-deep 16-byte loads;
+    // a small grid leaves the other CUs to the forward that runs alongside.
+    const unsigned per_table = (unsigned)(256 / g.T > 0 ? 256 / g.T : 1);
+    k_plc_fill<<<dim3(grid_for(cand_bound * max_units, kBlock * 4, per_table), g.T), kBlock, 0, s>>>(g, p);
 }
 
 void launch_plc_finalize(const DGlobal &g, hipStream_t s) { k_plc_finalize<<<1, kBlock, 0, s>>>(g); }

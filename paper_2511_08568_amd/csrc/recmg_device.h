@@ -45,7 +45,8 @@ struct DTable {
     int32_t *free_stack;   // [cap] free slot ids, top at free_top
     int2 *map;             // [map_mask + 1] open-addressed row -> slot map (key, slot)
     uint32_t *bitmap;      // [bm_words] presence bitmap, zero between uses
-    uint2 *rank;           // [bm_words] (rank of the word's first set bit, word) after an emit
+    uint4 *rank;           // [bm_words] (rank of the word's first set bit, word, forward stamp, 0)
+                           // written for the non-zero words of a forward's dedup
     int64_t rows;
     int64_t out_elem_off;  // sum of dims of the earlier tables
     int64_t cap_off;       // sum of caps of the earlier tables
@@ -66,7 +67,7 @@ struct TState {
     int32_t pcount;   // distinct prefetch rows of the current placement
     int32_t npcount;  // prefetch rows neither resident nor missed (in NP)
     int32_t n_res, free_top, popped, tomb;
-    int32_t rebuild, sel_mode, need, pad0;
+    int32_t rebuild, sel_mode, need, plc_nm;  // plc_nm: misses the current placement ranks
     uint64_t prefix;  // radix-select prefix; the threshold key after the last pass
     uint32_t done;    // blocks finished in the current select pass
     int32_t pad1;
@@ -98,12 +99,14 @@ struct DGlobal {
     int32_t *mscore;          // [max_indices] ranking score of each miss
     int32_t *mslot;           // [max_indices] slot given to an admitted miss, else -1
     int32_t *NP;              // [max_prefetch] new prefetch candidates, table t at pstart[t]
-    int32_t *ptag;            // [max_prefetch] classification scratch
+    int32_t *PU;              // [max_prefetch] sorted distinct prefetch rows, table t at pstart[t]
     int32_t *npslot;          // [max_prefetch] slot given to an admitted candidate, else -1
     int32_t *hist;            // [T][kRadix]
     int32_t *dump;            // [sum cap] sorted resident rows
     int32_t *dump_count;      // [T]
-    char *staging;            // [max_indices][stage_stride] miss rows in HBM
+    char *staging;            // [max_indices][stage_stride] miss rows of the latest forward
+                              // (two buffers alternate between forwards; the host picks one)
+    int64_t *ftstart;         // [T+1] tstart as seen by the current placement (read by the fill)
     int64_t stage_stride;
     int32_t T;
     int32_t total_bm_blocks;
@@ -146,6 +149,9 @@ __device__ __forceinline__ int32_t map_find(const DTable &tb, int32_t row) {
     }
     return -1;
 }
+
+// The map holds at most Cap live rows in >= 4 Cap entries, and is rebuilt when
+// deleted entries pass a quarter of it, so at least half of it stays empty.
 
 // Insert a row known to be absent.  Concurrent inserts of distinct rows are
 // safe; no lookup may run concurrently.  Returns 1 if a deleted entry was reused.
