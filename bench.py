@@ -221,21 +221,37 @@ def main():
         "stage_ms_per_step": {k: v[0] / K for k, v in stages.items()},
     }
 
+    last_out = outs[(nb - 1) & 1].cpu().numpy()
+    last_digest = [tot1[t]["digest"] for t in range(T)]
     cache.close()
 
     if not args.no_cpu_baseline:
+        # The oracle replays the same batches on the host: timed as the CPU
+        # baseline, and compared with the GPU run (all counters summed over
+        # every batch, the final resident digests, the last batch's sums).
         import oracle
         cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
         nth = max(1, min(cores, T))
         tabs_np = [h.numpy() for h in host]
         o = oracle.for_workload(w, tabs_np, nthreads=nth)
-        done, n_lookups, t_start = 0, 0, time.time()
+        sums = [dict.fromkeys(tot1[0], 0) for _ in range(T)]
+        done, n_lookups, t_start, ref64 = 0, 0, time.time(), None
         for b in range(nb):
             P, poff = prefetch[b]
             assert o.placement(P, poff, bits[b]) == 0
+            plc = [o.stats(t) for t in range(T)]
             idx, off = batches[b]
-            st, _, _ = o.forward(idx, off, w.bags)
+            st, _, ref64 = o.forward(idx, off, w.bags, want64=(b == nb - 1))
             assert st == 0
+            for t in range(T):
+                fw = o.stats(t)
+                for k in sums[t]:
+                    if k == "digest":
+                        sums[t][k] = plc[t][k]
+                    elif k in oracle.FWD_FIELDS:
+                        sums[t][k] += fw[k]
+                    else:
+                        sums[t][k] += plc[t][k]
             n_lookups += idx.size
             done += 1
             if time.time() - t_start > args.cpu_seconds:
@@ -250,6 +266,27 @@ def main():
             "sample": f"batches 0..{done - 1} of the same workload (placement + forward each), {secs:.1f}s, "
                       f"{nth} threads (one per table)",
         }
+        if done == nb:
+            counters_equal = all(sums[t][k] == tot1[t][k] for t in range(T) for k in sums[t] if k != "digest")
+            digest_equal = all(sums[t]["digest"] == last_digest[t] for t in range(T))
+            idx, off = batches[nb - 1]
+            rtol = {"f32": 1e-5, "f16": 2e-2, "bf16": 2e-2}
+            worst, ok, at = 0.0, True, 0
+            for t, tb in enumerate(w.tables):
+                s, e = w.table_segment(off, t)
+                tab = np.abs(tg.storage_to_f64(host[t].numpy(), tb.dtype)) if tb.dtype != "f32" else \
+                    np.abs(host[t].numpy().astype(np.float64))
+                lens = np.diff(off[t * w.bags:(t + 1) * w.bags + 1])
+                seg = np.repeat(np.arange(w.bags), lens)
+                mass = np.zeros((w.bags, tb.dim))
+                np.add.at(mass, seg, tab[idx[s:e]])
+                n = w.bags * tb.dim
+                err = np.abs(last_out[at:at + n].astype(np.float64) - ref64[at:at + n]).reshape(w.bags, tb.dim)
+                ok &= bool(np.all(err <= rtol[tb.dtype] * mass))
+                worst = max(worst, float((err / np.maximum(mass, 1e-300)).max()))
+                at += n
+            result["parity"] = {"batches": nb, "counters_equal": counters_equal, "digest_equal": digest_equal,
+                                "last_batch_pooled_within_tol": ok, "last_batch_max_err_over_l1": worst}
     print(json.dumps(result), flush=True)
 
 

@@ -213,7 +213,7 @@ __device__ __forceinline__ void pool_table(const DGlobal &g, const DTable &tb, i
     constexpr int VE = L::VE;
     constexpr int EB = Elem<DT>::bytes;
 #ifndef RECMG_POOL_UNROLL
-#define RECMG_POOL_UNROLL 16
+#define RECMG_POOL_UNROLL 8
 #endif
     // loads in flight per group, within the register budget
     constexpr int UNROLL = EB == 4 ? RECMG_POOL_UNROLL : (RECMG_POOL_UNROLL > 8 ? 8 : RECMG_POOL_UNROLL);
