@@ -162,7 +162,7 @@ class TieredEmbeddingCache:
     def __init__(self, host_tables: Sequence, dtypes: Sequence[str], cache_rows: Sequence[int], *,
                  policy: str = "lru", eviction_speed: int = 4, miss_mode: str = "zero_copy",
                  max_bags_per_table: int, max_indices: int, max_prefetch: int, validate: bool = False,
-                 timing: bool = False, overlap: bool = True, device: int = 0):
+                 timing: bool = False, overlap: bool = True, workspace=None, device: int = 0):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", device)
@@ -194,7 +194,12 @@ class TieredEmbeddingCache:
         cfg.max_prefetch = int(max_prefetch)
         dev_bytes, host_bytes = recmg_query_workspace(cfg)
         with torch.cuda.device(self.device):
-            self.workspace = torch.empty(dev_bytes, dtype=torch.uint8, device=self.device)
+            if workspace is not None:  # caller-provided device memory (any contents)
+                if workspace.numel() * workspace.element_size() < dev_bytes or not workspace.is_cuda:
+                    raise ValueError(f"workspace must be a device tensor of >= {dev_bytes} bytes")
+                self.workspace = workspace
+            else:
+                self.workspace = torch.empty(dev_bytes, dtype=torch.uint8, device=self.device)
             # side stream: staged miss copies and prefetch fills (which then overlap the next forward's dedup)
             self.copy_stream = torch.cuda.Stream(device=self.device) if (overlap or miss_mode == "staged") else None
         self.staging = torch.empty(host_bytes, dtype=torch.uint8, pin_memory=True) if host_bytes else None

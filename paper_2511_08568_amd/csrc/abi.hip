@@ -58,8 +58,8 @@ struct Layout {
     size_t total = 0, host_total = 0;
     std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, free_stack, map, bitmap, rank;
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
-    size_t src = 0, inv = 0, U = 0, slotU = 0, M = 0, mflags = 0, mscore = 0, mslot = 0;
-    size_t NP = 0, PU = 0, npslot = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, ftstart = 0;
+    size_t src = 0, inv = 0, U = 0, slotU = 0, M = 0, mflags = 0, mscore = 0, fill_src = 0, fill_slot = 0;
+    size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, ftstart = 0;
     size_t staging[2] = {0, 0};
     int64_t stage_stride = 0, sum_cap = 0;
     int32_t total_bm_blocks = 0;
@@ -107,6 +107,7 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
         g.bpb = (kBlock / 64) * (64 / g.gsz);
         g.copy_unit = g.row_bytes % 16 == 0 ? 16 : (g.row_bytes % 4 == 0 ? 4 : 2);
     }
+
     return RECMG_OK;
 }
 
@@ -151,10 +152,10 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->M = take(4 * mi);
     L->mflags = take(4 * mi);
     L->mscore = take(4 * mi);
-    L->mslot = take(4 * mi);
     L->NP = take(4 * mp);
     L->PU = take(4 * mp);
-    L->npslot = take(4 * mp);
+    L->fill_src = take(4 * (mi + mp));
+    L->fill_slot = take(4 * (mi + mp));
     L->hist = take(4 * (size_t)kRadix * T);
     L->dump = take(4 * (size_t)L->sum_cap);
     L->dump_count = take(4 * T);
@@ -399,11 +400,12 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.M = reinterpret_cast<int32_t *>(ws + L.M);
     g.mflags = reinterpret_cast<uint32_t *>(ws + L.mflags);
     g.mscore = reinterpret_cast<int32_t *>(ws + L.mscore);
-    g.mslot = reinterpret_cast<int32_t *>(ws + L.mslot);
     g.NP = reinterpret_cast<int32_t *>(ws + L.NP);
     g.PU = reinterpret_cast<int32_t *>(ws + L.PU);
     g.ftstart = reinterpret_cast<int64_t *>(ws + L.ftstart);
-    g.npslot = reinterpret_cast<int32_t *>(ws + L.npslot);
+    g.fill_src = reinterpret_cast<int32_t *>(ws + L.fill_src);
+    g.fill_slot = reinterpret_cast<int32_t *>(ws + L.fill_slot);
+    g.fill_cap = cfg->max_indices + cfg->max_prefetch;
     g.hist = reinterpret_cast<int32_t *>(ws + L.hist);
     g.dump = reinterpret_cast<int32_t *>(ws + L.dump);
     g.dump_count = reinterpret_cast<int32_t *>(ws + L.dump_count);
@@ -471,6 +473,9 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         HIP_TRY(hipMemsetAsync(ws + L.rank[t], 0xff, (size_t)ge.bm_words * 16, s0));  // stamp -1
     }
     HIP_TRY(hipMemsetAsync(ws + L.st, 0, sizeof(TState) * T, s0));
+    HIP_TRY(hipMemsetAsync(ws + L.tstart, 0, 8 * (T + 1), s0));
+    HIP_TRY(hipMemsetAsync(ws + L.pstart, 0, 8 * (T + 1), s0));
+    HIP_TRY(hipMemsetAsync(ws + L.ftstart, 0, 8 * (T + 1), s0));
     HIP_TRY(hipMemsetAsync(ws + L.err, 0, 4, s0));
     HIP_TRY(hipMemsetAsync(ws + L.hist, 0, 4 * (size_t)kRadix * T, s0));
     HIP_TRY(hipMemcpy(ws + L.tabs, tabs.data(), sizeof(DTable) * T, hipMemcpyHostToDevice));
@@ -528,7 +533,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
 
     {
         StageTimer tm(c, RECMG_STAGE_PLC_CLASSIFY, s);
-        launch_plc_prep(g, prefetch_offsets, num_prefetch, s);
+        launch_plc_prep(g, prefetch_offsets, num_prefetch, p.have_fwd, s);
         if (p.prio && cache_bits && c->have_fwd) launch_plc_bits(g, cache_bits, c->last_n, s);
         if (num_prefetch > 0) {
             launch_mark(g, prefetch_rows, g.pstart, num_prefetch, s);
@@ -555,13 +560,13 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         HIP_TRY(hipStreamWaitEvent(c->copy_stream, c->ev_admit, 0));
         {
             StageTimer tm(c, RECMG_STAGE_PLC_FILL, c->copy_stream);
-            launch_plc_fill(g, p, cand_grid, c->max_units, c->copy_stream);
+            launch_plc_fill(g, c->copy_stream);
         }
         HIP_TRY(hipEventRecord(c->ev_fill, c->copy_stream));
         c->fill_pending = true;
     } else {
         StageTimer tm(c, RECMG_STAGE_PLC_FILL, s);
-        launch_plc_fill(g, p, cand_grid, c->max_units, s);
+        launch_plc_fill(g, s);
     }
     launch_plc_finalize(g, s);
     HIP_TRY(hipGetLastError());

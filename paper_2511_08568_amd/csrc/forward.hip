@@ -32,49 +32,50 @@ __global__ void __launch_bounds__(kBlock) k_fwd_prep(DGlobal g, const int64_t *_
 }
 
 // Cache probe of every distinct row (row -> slot map): hits are stamped and
-// counted, misses are numbered (their staging row) block by block.
-__global__ void __launch_bounds__(kBlock) k_fwd_probe(DGlobal g, int32_t stamp) {
+// counted, misses are numbered (their staging row).  One thread per slot of
+// the index space; table t's distinct rows occupy [tstart[t], + ucount).
+__global__ void __launch_bounds__(kBlock) k_fwd_probe(DGlobal g, int32_t stamp, int64_t n) {
     if (*g.err) return;
-    __shared__ int tmp[16];
-    __shared__ int s_base;
-    const int t = blockIdx.y;
-    const DTable &tb = g.tabs[t];
-    TState &st = g.st[t];
-    const int32_t nu = st.ucount;
-    const int64_t ts = g.tstart[t];
-    int hits = 0, hits_pf = 0;
-    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < nu; base += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t k = base + threadIdx.x;
-        int miss = 0;
+    __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
+    __shared__ int32_t s_uc[RECMG_MAX_TABLES];
+    for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
+        s_start[t] = g.tstart[t];
+        if (t < g.T) s_uc[t] = g.st[t].ucount;
+    }
+    __syncthreads();
+    int32_t *mcount0 = &g.st[0].mcount;
+    const int stride_st = (int)(sizeof(TState) / 4);
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < n; base += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = base + threadIdx.x;
+        int t = 0;
+        bool miss = false, valid = false, hit = false, hit_pf = false;
         int32_t row = 0;
-        if (k < nu) {
-            row = g.U[ts + k];
+        if (i < n) {
+            t = find_seg(s_start, g.T, i);
+            valid = i - s_start[t] < s_uc[t];
+        }
+        if (valid) {
+            const DTable &tb = g.tabs[t];
+            row = g.U[i];
             const int32_t slot = map_find(tb, row);
             if (slot >= 0) {
-                g.slotU[ts + k] = slot;
+                g.slotU[i] = slot;
                 tb.slot_touch[slot] = stamp;
-                ++hits;
-                hits_pf += (tb.slot_flags[slot] & F_PF) ? 1 : 0;
+                hit = true;
+                hit_pf = (tb.slot_flags[slot] & F_PF) != 0;
             } else {
-                miss = 1;
+                miss = true;
             }
         }
-        int tot;
-        const int ex = block_excl_scan(miss, tmp, &tot);
-        if (threadIdx.x == 0 && tot) s_base = atomicAdd(&st.mcount, tot);
-        __syncthreads();
+        (void)wave_append(hit, t, &g.st[0].hits, stride_st);  // counts only
+        (void)wave_append(hit_pf, t, &g.st[0].hits_pf, stride_st);
+        const int32_t m = wave_append(miss, t, mcount0, stride_st);
         if (miss) {
-            const int64_t m = s_base + ex;
-            g.slotU[ts + k] = -(int32_t)(m + 1);
-            g.M[ts + m] = row;
-            g.mflags[ts + m] = 0;
+            const int64_t at = s_start[t] + m;
+            g.slotU[i] = -(m + 1);
+            g.M[at] = row;
+            g.mflags[at] = 0;
         }
-        __syncthreads();
-    }
-    const int h = block_sum(hits, tmp), hp = block_sum(hits_pf, tmp);
-    if (threadIdx.x == 0) {
-        if (h) atomicAdd(&st.hits, h);
-        if (hp) atomicAdd(&st.hits_pf, hp);
     }
 }
 
@@ -101,48 +102,19 @@ __global__ void __launch_bounds__(kBlock) k_fwd_src(DGlobal g, const int32_t *__
 
 // ----------------------------------------------------------------- miss fetch
 
-template <typename V>
-__device__ __forceinline__ void copy_rows(int64_t items, int nunit, const DTable &tb,
-                                          const DGlobal &g, int64_t ts) {
-    const int64_t S = (int64_t)gridDim.x * blockDim.x;
-    const int rb = tb.row_bytes;
-    for (int64_t base = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; base < items; base += 4 * S) {
-        V v[4];
-        int64_t dst[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int64_t it = base + q * S;
-            if (it < items) {
-                const int64_t m = it / nunit;
-                const int vv = (int)(it - m * nunit);
-                const int32_t row = g.M[ts + m];
-                v[q] = *reinterpret_cast<const V *>(tb.host + (int64_t)row * rb + (int64_t)vv * sizeof(V));
-                dst[q] = (ts + m) * g.stage_stride + (int64_t)vv * sizeof(V);
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int64_t it = base + q * S;
-            if (it < items) *reinterpret_cast<V *>(g.staging + dst[q]) = v[q];
-        }
-    }
-}
-
 // ZERO_COPY miss fetch: each distinct miss is read once from pinned host
 // memory (device-visible mapping) and written to its staging row.
 __global__ void __launch_bounds__(kBlock) k_fetch(DGlobal g) {
     if (*g.err) return;
-    const int t = blockIdx.y;
-    const DTable &tb = g.tabs[t];
-    const int32_t nm = g.st[t].mcount;
-    if (nm == 0) return;
-    const int unit = tb.copy_unit;
-    const int nunit = tb.row_bytes / unit;
-    const int64_t items = (int64_t)nm * nunit;
-    const int64_t ts = g.tstart[t];
-    if (unit == 16) copy_rows<uint4>(items, nunit, tb, g, ts);
-    else if (unit == 4) copy_rows<uint32_t>(items, nunit, tb, g, ts);
-    else copy_rows<uint16_t>(items, nunit, tb, g, ts);
+    __shared__ int32_t s_cnt[RECMG_MAX_TABLES];
+    for (int t = threadIdx.x; t < g.T; t += blockDim.x) s_cnt[t] = g.st[t].mcount;
+    __syncthreads();
+    copy_flat(
+        g, s_cnt,
+        [&](int t, const DTable &tb, int64_t j) {
+            return tb.host + (int64_t)g.M[g.tstart[t] + j] * tb.row_bytes;
+        },
+        [&](int t, const DTable &tb, int64_t j) { return g.staging + (g.tstart[t] + j) * g.stage_stride; });
 }
 
 // ----------------------------------------------------------------- pooling
@@ -350,7 +322,7 @@ void launch_fwd_prep(const DGlobal &g, const int64_t *offsets, int32_t B, int64_
 
 void launch_fwd_probe(const DGlobal &g, int32_t stamp, int64_t n, hipStream_t s) {
     if (n <= 0) return;
-    k_fwd_probe<<<dim3(grid_for(n / g.T + 1, kBlock, 1024), g.T), kBlock, 0, s>>>(g, stamp);
+    k_fwd_probe<<<grid_for(n, kBlock, 8192), kBlock, 0, s>>>(g, stamp, n);
 }
 
 void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStream_t s) {
@@ -358,10 +330,7 @@ void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStre
     k_fwd_src<<<grid_for(n, kBlock * 4, 16384), kBlock, 0, s>>>(g, indices, n);
 }
 
-void launch_fetch(const DGlobal &g, hipStream_t s) {
-    const unsigned gx = (unsigned)(4096 / g.T > 0 ? 4096 / g.T : 1);
-    k_fetch<<<dim3(gx > 512 ? 512 : gx, g.T), kBlock, 0, s>>>(g);
-}
+void launch_fetch(const DGlobal &g, hipStream_t s) { k_fetch<<<1024, kBlock, 0, s>>>(g); }
 
 void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, int64_t nblocks,
                  const int32_t *bstart, uint32_t classes, hipStream_t s) {

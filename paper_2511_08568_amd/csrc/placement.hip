@@ -24,11 +24,13 @@
 
 namespace recmg {
 
-__global__ void k_plc_prep(DGlobal g, const int64_t *__restrict__ poff, int64_t np) {
+__global__ void k_plc_prep(DGlobal g, const int64_t *__restrict__ poff, int64_t np, int32_t have_fwd) {
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         const int64_t v = poff[t];
         g.pstart[t] = v;
-        g.ftstart[t] = g.tstart[t];
+        // table t's fill list lives at ftstart[t] + pstart[t] and holds at most
+        // (its last-batch indices) + (its prefetch ids) entries
+        g.ftstart[t] = have_fwd ? g.tstart[t] : 0;
         if (t < g.T && v > poff[t + 1]) atomicOr(g.err, ERR_OFFSETS);
         if ((t == 0 && v != 0) || (t == g.T && v != np)) atomicOr(g.err, ERR_OFFSETS);
         if (t < g.T) {
@@ -66,49 +68,52 @@ __global__ void __launch_bounds__(kBlock) k_plc_bits(DGlobal g, const uint8_t *_
 
 // Classify every distinct prefetch row (Alg. 1's prefetch loop taken as a
 // set): resident -> flag the slot; missed by the last batch -> flag the miss;
-// otherwise a new candidate, numbered block by block into NP.
-__global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last_stamp) {
+// otherwise a new candidate, appended to NP.  One thread per slot of the
+// prefetch index space; table t's distinct rows occupy [pstart[t], + pcount).
+__global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last_stamp, int64_t np) {
     if (*g.err) return;
-    __shared__ int tmp[16];
-    __shared__ int s_base;
-    const int t = blockIdx.y;
-    const DTable &tb = g.tabs[t];
-    TState &st = g.st[t];
-    const int32_t np = st.pcount;
-    const int64_t ps = g.pstart[t], ts = g.tstart[t];
-    int pres = 0;
+    __shared__ int64_t s_pstart[RECMG_MAX_TABLES + 1];
+    __shared__ int32_t s_pc[RECMG_MAX_TABLES];
+    for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
+        s_pstart[t] = g.pstart[t];
+        if (t < g.T) s_pc[t] = g.st[t].pcount;
+    }
+    __syncthreads();
+    const int stride_st = (int)(sizeof(TState) / 4);
     for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < np; base += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t k = base + threadIdx.x;
-        int isnew = 0;
+        const int64_t i = base + threadIdx.x;
+        int t = 0;
+        bool valid = false, isnew = false, resident = false;
         int32_t row = 0;
-        if (k < np) {
-            row = g.PU[ps + k];
+        if (i < np) {
+            t = find_seg(s_pstart, g.T, i);
+            valid = i - s_pstart[t] < s_pc[t];
+        }
+        if (valid) {
+            const DTable &tb = g.tabs[t];
+            row = g.PU[i];
             const int32_t slot = map_find(tb, row);
             if (slot >= 0) {
                 atomicOr(&tb.slot_flags[slot], F_INP);
-                ++pres;
+                resident = true;
             } else {
                 // distinct rows of the last batch carry its stamp in the rank word
                 const uint4 rk = tb.rank[row >> 5];
                 const uint32_t bit = 1u << (row & 31);
                 if ((int32_t)rk.z == last_stamp && (rk.y & bit)) {
+                    const int64_t ts = g.tstart[t];
                     const int32_t u = (int32_t)rk.x + __popc(rk.y & (bit - 1u));
                     const int64_t m = -(int64_t)g.slotU[ts + u] - 1;
                     atomicOr(&g.mflags[ts + m], F_INP);
                 } else {
-                    isnew = 1;
+                    isnew = true;
                 }
             }
         }
-        int tot;
-        const int ex = block_excl_scan(isnew, tmp, &tot);
-        if (threadIdx.x == 0 && tot) s_base = atomicAdd(&st.npcount, tot);
-        __syncthreads();
-        if (isnew) g.NP[ps + s_base + ex] = row;
-        __syncthreads();
+        (void)wave_append(resident, t, &g.st[0].p_res, stride_st);  // counts only
+        const int32_t k = wave_append(isnew, t, &g.st[0].npcount, stride_st);
+        if (isnew) g.NP[s_pstart[t] + k] = row;
     }
-    const int p = block_sum(pres, tmp);
-    if (threadIdx.x == 0 && p) atomicAdd(&st.p_res, p);
 }
 
 // ----------------------------------------------------------------- ranking
@@ -366,7 +371,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
     const int mode = st.sel_mode;
     const uint64_t thr = st.prefix;
     const int32_t top = st.free_top;
-    const int64_t ts = g.tstart[t], ps = g.pstart[t];
+    const int64_t ts = g.ftstart[t], ps = g.pstart[t];
     const int64_t items = (int64_t)c.nm + c.nnp;
     int n_adm_miss = 0, n_fill = 0, n_pdrop = 0, n_mdrop = 0, n_reuse = 0;
     unsigned long long dig = 0;
@@ -395,7 +400,9 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
         if (k < items) {
             int32_t slot = -1;
             const int64_t fi = (int64_t)top - 1 - (s_base + ex);
-            if (adm && (fi < 0 || fi >= tb.cap || (uint32_t)tb.free_stack[fi] >= (uint32_t)tb.cap)) {
+            const int64_t fj = ts + ps + (s_base + ex);  // this row's entry in the fill list
+            if (adm && (fi < 0 || fi >= tb.cap || (uint32_t)tb.free_stack[fi] >= (uint32_t)tb.cap || fj < 0 ||
+                        fj >= g.fill_cap)) {
                 atomicOr(g.err, ERR_INTERNAL);
                 adm = 0;
             }
@@ -406,6 +413,9 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
                 tb.slot_flags[slot] = inp ? F_PF : 0u;
                 tb.slot_touch[slot] = -1;
                 n_reuse += map_insert(tb, row, slot);
+                // the fill list: admitted row j of this table, its source and slot
+                g.fill_src[fj] = is_miss ? (int32_t)k : -(row + 1);
+                g.fill_slot[fj] = slot;
                 dig += mix64(((unsigned long long)t << 40) | (unsigned long long)row);
                 if (is_miss) ++n_adm_miss;
                 else ++n_fill;
@@ -413,8 +423,6 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
                 if (is_miss) ++n_mdrop;
                 if (inp) ++n_pdrop;
             }
-            if (is_miss) g.mslot[ts + k] = slot;
-            else g.npslot[ps + (k - c.nm)] = slot;
         }
         __syncthreads();
     }
@@ -432,63 +440,30 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
 }
 
 // Copy admitted rows into their slots: misses from HBM staging, prefetch
-// fills from pinned host memory over the host link.
-template <typename V>
-__device__ __forceinline__ void fill_rows(const DGlobal &g, const DTable &tb, const Counts &c, int64_t ts, int64_t ps,
-                                          int nunit) {
-    const int64_t items = ((int64_t)c.nm + c.nnp) * nunit;
-    const int64_t S = (int64_t)gridDim.x * blockDim.x;
-    const int64_t rb = tb.row_bytes;
-    for (int64_t base = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; base < items; base += 4 * S) {
-        V v[4];
-        int64_t dst[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            dst[q] = -1;
-            const int64_t it = base + q * S;
-            if (it < items) {
-                const int64_t cand = it / nunit;
-                const int64_t vo = (it - cand * nunit) * (int64_t)sizeof(V);
-                int32_t slot;
-                const char *src;
-                if (cand < c.nm) {
-                    slot = g.mslot[ts + cand];
-                    src = g.staging + (ts + cand) * g.stage_stride;
-                } else {
-                    const int64_t j = ps + (cand - c.nm);
-                    slot = g.npslot[j];
-                    src = tb.host + (int64_t)g.NP[j] * rb;
-                }
-                if (slot >= 0) {
-                    v[q] = *reinterpret_cast<const V *>(src + vo);
-                    dst[q] = (int64_t)slot * rb + vo;
-                }
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-            if (dst[q] >= 0) *reinterpret_cast<V *>(tb.pool + dst[q]) = v[q];
-    }
-}
-
-// May run on a side stream, concurrently with the next forward's dedup: it
-// reads only placement-owned state (plc_nm, ftstart, mslot, NP, npslot) and the
+// fills from pinned host memory over the host link.  May run on a side
+// stream, concurrently with the next forward's dedup: it reads only
+// placement-owned state (popped, ftstart, pstart, the fill list) and the
 // staging buffer of the previous forward, which the next forward does not use.
-__global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, PlcParams p) {
+__global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g) {
     if (*g.err) return;
-    const int t = blockIdx.y;
-    const DTable &tb = g.tabs[t];
-    const TState &st = g.st[t];
-    Counts c;
-    c.nm = st.plc_nm;
-    c.nnp = st.npcount;
-    if (c.nm + c.nnp == 0 || st.sel_mode == SEL_NONE) return;
-    const int64_t ts = g.ftstart[t], ps = g.pstart[t];
-    const int unit = tb.copy_unit;
-    const int nunit = tb.row_bytes / unit;
-    if (unit == 16) fill_rows<uint4>(g, tb, c, ts, ps, nunit);
-    else if (unit == 4) fill_rows<uint32_t>(g, tb, c, ts, ps, nunit);
-    else fill_rows<uint16_t>(g, tb, c, ts, ps, nunit);
+    __shared__ int32_t s_cnt[RECMG_MAX_TABLES];
+    for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
+        const int64_t base = g.ftstart[t] + g.pstart[t];
+        const int32_t n = g.st[t].popped;
+        // admit wrote entries [base, base + n) and checked them against fill_cap
+        s_cnt[t] = (base >= 0 && n >= 0 && base + n <= g.fill_cap) ? n : 0;
+    }
+    __syncthreads();
+    copy_flat(
+        g, s_cnt,
+        [&](int t, const DTable &tb, int64_t j) -> const char * {
+            const int64_t fts = g.ftstart[t];
+            const int32_t src = g.fill_src[fts + g.pstart[t] + j];
+            return src >= 0 ? g.staging + (fts + src) * g.stage_stride : tb.host + (int64_t)(-src - 1) * tb.row_bytes;
+        },
+        [&](int t, const DTable &tb, int64_t j) {
+            return tb.pool + (int64_t)g.fill_slot[g.ftstart[t] + g.pstart[t] + j] * tb.row_bytes;
+        });
 }
 
 __global__ void k_plc_finalize(DGlobal g) {
@@ -496,8 +471,7 @@ __global__ void k_plc_finalize(DGlobal g) {
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         TState &st = g.st[t];
         const DTable &tb = g.tabs[t];
-        st.free_top -= st.popped;
-        st.popped = 0;
+        st.free_top -= st.popped;  // popped stays: the fill may still read it
         st.n_res = tb.cap - st.free_top;
         st.rebuild = 0;
         int64_t v[8];
@@ -535,8 +509,8 @@ static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
     return (unsigned)b;
 }
 
-void launch_plc_prep(const DGlobal &g, const int64_t *poff, int64_t np, hipStream_t s) {
-    k_plc_prep<<<1, kBlock, 0, s>>>(g, poff, np);
+void launch_plc_prep(const DGlobal &g, const int64_t *poff, int64_t np, int32_t have_fwd, hipStream_t s) {
+    k_plc_prep<<<1, kBlock, 0, s>>>(g, poff, np, have_fwd);
 }
 
 void launch_plc_bits(const DGlobal &g, const uint8_t *bits, int64_t n_last, hipStream_t s) {
@@ -546,7 +520,7 @@ void launch_plc_bits(const DGlobal &g, const uint8_t *bits, int64_t n_last, hipS
 
 void launch_plc_classify(const DGlobal &g, int32_t last_stamp, int64_t np, hipStream_t s) {
     if (np <= 0) return;
-    k_plc_classify<<<dim3(grid_for(np / g.T + 1, kBlock, 1024), g.T), kBlock, 0, s>>>(g, last_stamp);
+    k_plc_classify<<<grid_for(np, kBlock, 8192), kBlock, 0, s>>>(g, last_stamp, np);
 }
 
 void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s) {
@@ -565,11 +539,10 @@ void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int
     k_plc_admit<<<dim3(grid_for(cand_bound, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
 }
 
-void launch_plc_fill(const DGlobal &g, const PlcParams &p, int64_t cand_bound, int32_t max_units, hipStream_t s) {
+void launch_plc_fill(const DGlobal &g, hipStream_t s) {
     // The host link saturates with a few hundred waves of 4-deep 16-byte loads;
-    // a small grid leaves the other CUs to the forward that runs alongside.
-    const unsigned per_table = (unsigned)(256 / g.T > 0 ? 256 / g.T : 1);
-    k_plc_fill<<<dim3(grid_for(cand_bound * max_units, kBlock * 4, per_table), g.T), kBlock, 0, s>>>(g, p);
+    // a modest grid leaves the other CUs to the forward that runs alongside.
+    k_plc_fill<<<512, kBlock, 0, s>>>(g);
 }
 
 void launch_plc_finalize(const DGlobal &g, hipStream_t s) { k_plc_finalize<<<1, kBlock, 0, s>>>(g); }

@@ -97,16 +97,19 @@ struct DGlobal {
     int32_t *M;               // [max_indices] missed rows, table t at tstart[t]
     uint32_t *mflags;         // [max_indices] F_CBIT / F_INP of each miss
     int32_t *mscore;          // [max_indices] ranking score of each miss
-    int32_t *mslot;           // [max_indices] slot given to an admitted miss, else -1
     int32_t *NP;              // [max_prefetch] new prefetch candidates, table t at pstart[t]
     int32_t *PU;              // [max_prefetch] sorted distinct prefetch rows, table t at pstart[t]
-    int32_t *npslot;          // [max_prefetch] slot given to an admitted candidate, else -1
+    int32_t *fill_src;        // [max_indices + max_prefetch] admitted row's source: staging row (>= 0)
+                              // or -(host row + 1); table t at ftstart[t] + pstart[t]
+    int32_t *fill_slot;       // [max_indices + max_prefetch] its slot
     int32_t *hist;            // [T][kRadix]
     int32_t *dump;            // [sum cap] sorted resident rows
     int32_t *dump_count;      // [T]
     char *staging;            // [max_indices][stage_stride] miss rows of the latest forward
                               // (two buffers alternate between forwards; the host picks one)
-    int64_t *ftstart;         // [T+1] tstart as seen by the current placement (read by the fill)
+    int64_t *ftstart;         // [T+1] base of each table's fill list and admitted misses in the
+                              // current placement: tstart of the last forward, or 0 if none ran
+    int64_t fill_cap;         // entries of fill_src / fill_slot (max_indices + max_prefetch)
     int64_t stage_stride;
     int32_t T;
     int32_t total_bm_blocks;
@@ -244,6 +247,28 @@ __device__ __forceinline__ int block_excl_scan(int v, int *tmp, int *total) {
     return pre + x - v;
 }
 
+// 64-bit exclusive scan over the block; `tmp` is __shared__ long long[16].
+__device__ __forceinline__ long long block_excl_scan64(long long v, long long *tmp, long long *total) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    long long x = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const long long y = __shfl_up(x, d, 64);
+        if (lane >= d) x += y;
+    }
+    if (lane == 63) tmp[wid] = x;
+    __syncthreads();
+    long long pre = 0, tot = 0;
+    for (int k = 0; k < nw; ++k) {
+        const long long s = tmp[k];
+        pre += (k < wid) ? s : 0;
+        tot += s;
+    }
+    __syncthreads();
+    *total = tot;
+    return pre + x - v;
+}
+
 __device__ __forceinline__ int wave_sum(int v) {
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
@@ -268,6 +293,27 @@ __device__ __forceinline__ int block_sum(int v, int *tmp) {
     return dummy;
 }
 
+// Append for the lanes with `want`, to the counter of their own table:
+// returns each such lane's index (one atomic per table present in the wave).
+// Every lane of the wave must call.
+__device__ __forceinline__ int32_t wave_append(bool want, int t, int32_t *counter0, int counter_stride) {
+    const int lane = threadIdx.x & 63;
+    const unsigned long long below = (1ull << lane) - 1ull;
+    unsigned long long pending = __ballot(want);
+    int32_t mine = -1;
+    while (pending) {
+        const int leader = __ffsll((long long)pending) - 1;
+        const int lt = __shfl(t, leader, 64);
+        const unsigned long long grp = __ballot(want && t == lt);
+        int32_t base = 0;
+        if (lane == leader) base = atomicAdd(counter0 + (int64_t)lt * counter_stride, (int32_t)__popcll(grp));
+        base = __shfl(base, leader, 64);
+        if (want && t == lt) mine = base + (int32_t)__popcll(grp & below);
+        pending &= ~grp;
+    }
+    return mine;
+}
+
 __device__ __forceinline__ uint64_t make_key(int32_t score, int32_t row, int rowbits) {
     return ((uint64_t)(uint32_t)score << rowbits) | (uint64_t)(uint32_t)row;
 }
@@ -278,6 +324,59 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
 
 __device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+}
+
+// Copy `count[t]` rows of every table in 16/4/2-byte units, the tables' work
+// laid end to end so every table gets its share of the grid.  src_of / dst_of
+// give the byte addresses of unit v of item j of table t.
+template <class Src, class Dst>
+__device__ __forceinline__ void copy_flat(const DGlobal &g, const int32_t *count, Src src_of, Dst dst_of) {
+    __shared__ int64_t s_pre[RECMG_MAX_TABLES + 1];
+    __shared__ long long tmp[16];
+    // per-table unit counts, scanned (T <= 256 = blockDim)
+    long long mine = 0;
+    const int t0 = threadIdx.x;
+    if (t0 < g.T) mine = (long long)count[t0] * (g.tabs[t0].row_bytes / g.tabs[t0].copy_unit);
+    long long tot;
+    const long long ex = block_excl_scan64(mine, tmp, &tot);
+    if (t0 < g.T) s_pre[t0] = ex;
+    if (t0 == 0) s_pre[g.T] = tot;
+    __syncthreads();
+    const int64_t items = s_pre[g.T];
+    const int64_t S = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; base < items; base += 4 * S) {
+        uint4 v16[4];
+        uint32_t v4[4];
+        uint16_t v2[4];
+        char *dst[4];
+        int unit[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            dst[q] = nullptr;
+            unit[q] = 0;
+            const int64_t it = base + q * S;
+            if (it < items) {
+                const int t = find_seg(s_pre, g.T, it);
+                const DTable &tb = g.tabs[t];
+                const int u = tb.copy_unit, nunit = tb.row_bytes / u;
+                const int64_t loc = it - s_pre[t];
+                const int64_t j = loc / nunit;
+                const int64_t vo = (loc - j * nunit) * u;
+                const char *sp = src_of(t, tb, j) + vo;
+                dst[q] = dst_of(t, tb, j) + vo;
+                unit[q] = u;
+                if (u == 16) v16[q] = *reinterpret_cast<const uint4 *>(sp);
+                else if (u == 4) v4[q] = *reinterpret_cast<const uint32_t *>(sp);
+                else v2[q] = *reinterpret_cast<const uint16_t *>(sp);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (unit[q] == 16) *reinterpret_cast<uint4 *>(dst[q]) = v16[q];
+            else if (unit[q] == 4) *reinterpret_cast<uint32_t *>(dst[q]) = v4[q];
+            else if (unit[q] == 2) *reinterpret_cast<uint16_t *>(dst[q]) = v2[q];
+        }
+    }
 }
 
 }  // namespace recmg

@@ -134,3 +134,32 @@ def test_run_twice_is_deterministic():
         g.close()
     for a, b in zip(*res):
         assert np.array_equal(a["out"], b["out"]) and a["fwd"] == b["fwd"] and a["place"] == b["place"]
+
+
+@pytest.mark.parametrize("fill", [0xFF, 0x5A])
+def test_workspace_contents_do_not_matter(fill):
+    """Regression: init must clear every workspace field a first placement
+    reads (a placement before any forward once indexed its fill list from an
+    uninitialised field)."""
+    import torch as th
+    from paper_2511_08568_amd import TieredEmbeddingCache
+    w = tg.random_tiny(17, max_rows=40, max_cap=12, max_dim=9, batches=6, bags=5)
+    tabs, ora = run_oracle(w)
+    probe = GpuRunner(w, tabs)
+    nbytes = probe.cache.workspace_bytes
+    probe.close()
+    ws = th.full((nbytes,), fill, dtype=th.uint8, device="cuda")
+    g = GpuRunner.__new__(GpuRunner)
+    g.torch, g.w, g.dev = th, w, th.device("cuda", 0)
+    g.host = [th.from_numpy(np.ascontiguousarray(a)).pin_memory() for a in tabs]
+    g.cache = TieredEmbeddingCache(g.host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables],
+                                   policy=w.policy, eviction_speed=w.eviction_speed,
+                                   max_bags_per_table=w.bags,
+                                   max_indices=max(w.batch(b)[0].size for b in range(w.batches)),
+                                   max_prefetch=max(max(w.prefetch_list(b)[0].size for b in range(w.batches)), 1),
+                                   workspace=ws)
+    try:
+        gpu = g.run()
+    finally:
+        g.close()
+    compare_runs(w, tabs, ora, gpu, label=f"garbage-workspace-{fill:#x}")

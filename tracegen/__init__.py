@@ -20,6 +20,9 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
+import threading
+from concurrent.futures import ThreadPoolExecutor
 from typing import List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -34,6 +37,22 @@ POLICY_CODES = {"lru": 0, "priority": 1}
 
 _U64 = np.uint64
 _MASK64 = (1 << 64) - 1
+
+
+_POOL: Optional[ThreadPoolExecutor] = None
+
+
+def _pmap(fn, items):
+    """Map over tables on a thread pool (numpy releases the GIL); results in order.
+    Every table draws from streams of its own, so the result does not depend on
+    the thread count."""
+    global _POOL
+    items = list(items)
+    if len(items) <= 1:
+        return [fn(x) for x in items]
+    if _POOL is None:
+        _POOL = ThreadPoolExecutor(max_workers=max(1, min(16, os.cpu_count() or 1)))
+    return list(_POOL.map(fn, items))
 
 
 def rng(config: int, table: int, purpose: int, batch: int) -> np.random.Generator:
@@ -133,18 +152,21 @@ def make_perm(config: int, table: int, n: int, variant: int = 0) -> FeistelPerm:
 # ----------------------------------------------------------------------------
 
 _CDF_CACHE: dict = {}
+_CDF_LOCK = threading.Lock()
+_CDF_CACHE_BYTES = 4 << 30
 
 
 def zipf_cdf(n: int, alpha: float) -> np.ndarray:
     """Cumulative (unnormalised) mass of p_k ∝ k^-alpha for k = 1..n, fp64."""
     key = (int(n), float(alpha))
-    c = _CDF_CACHE.get(key)
-    if c is None:
-        k = np.arange(1, n + 1, dtype=np.float64)
-        c = np.cumsum(k ** (-float(alpha)))
-        if len(_CDF_CACHE) > 8:
-            _CDF_CACHE.clear()
-        _CDF_CACHE[key] = c
+    with _CDF_LOCK:
+        c = _CDF_CACHE.get(key)
+        if c is None:
+            k = np.arange(1, n + 1, dtype=np.float64)
+            c = np.cumsum(k ** (-float(alpha)))
+            if sum(v.nbytes for v in _CDF_CACHE.values()) + c.nbytes > _CDF_CACHE_BYTES:
+                _CDF_CACHE.clear()
+            _CDF_CACHE[key] = c
     return c
 
 
@@ -268,12 +290,14 @@ class Workload:
         hit = self._cache.get(key)
         if hit is not None:
             return hit
-        idx_parts, lens = [], []
-        for t in range(self.num_tables):
+        def one(t):
             pf = self.pooling_factors(t, b)
-            lens.append(pf)
-            idx_parts.append(self.table_indices(t, b, int(pf.sum())))
-        lens = np.concatenate(lens)
+            return pf, self.table_indices(t, b, int(pf.sum()))
+        for t in range(self.num_tables):  # permutations are built once, outside the pool
+            self._perm(t)
+        parts = _pmap(one, range(self.num_tables))
+        lens = np.concatenate([p[0] for p in parts])
+        idx_parts = [p[1] for p in parts]
         offsets = np.zeros(lens.size + 1, dtype=np.int64)
         np.cumsum(lens, out=offsets[1:])
         indices = np.concatenate(idx_parts).astype(np.int32) if idx_parts else np.zeros(0, np.int32)
@@ -292,11 +316,16 @@ class Workload:
         Used only to draw lookahead prefetch lists and caching bits."""
         if b < 0 or b >= self.batches:
             return [np.zeros(0, np.int32) for _ in self.tables]
+        key = ("uniq", b)
+        hit = self._cache.get(key)
+        if hit is not None:
+            return hit
         idx, off = self.batch(b)
-        out = []
-        for t in range(self.num_tables):
-            s, e = self.table_segment(off, t)
-            out.append(np.unique(idx[s:e]))
+        out = _pmap(lambda t: np.unique(idx[slice(*self.table_segment(off, t))]), range(self.num_tables))
+        uk = [k for k in self._cache if k[0] == "uniq"]
+        if len(uk) > 6:
+            del self._cache[min(uk, key=lambda k: k[1])]
+        self._cache[key] = out
         return out
 
     # -- prefetch lists ------------------------------------------------------------
@@ -311,7 +340,8 @@ class Workload:
         else:
             ub = self.uniques(b)
             ubm1 = self.uniques(b - 1) if kind == "headroom" else None
-            for t in range(T):
+
+            def one(t):
                 u = ub[t].astype(np.int64)
                 n = self.tables[t].rows
                 g = rng(self.config, t, P_PREFETCH, b)
@@ -338,7 +368,8 @@ class Workload:
                     p = np.concatenate([u[keep], g.integers(0, n, size=length - k)])
                 else:
                     raise ValueError(kind)
-                parts.append(p.astype(np.int32))
+                return p.astype(np.int32)
+            parts = _pmap(one, range(T))
         offs = np.zeros(T + 1, dtype=np.int64)
         offs[1:] = np.cumsum([p.size for p in parts])
         rows = np.concatenate(parts).astype(np.int32) if parts else np.zeros(0, np.int32)
@@ -354,14 +385,14 @@ class Workload:
         idx, off = self.batch(b)
         fut1, fut2 = self.uniques(b + 1), self.uniques(b + 2)
         out = np.zeros(idx.size, dtype=np.uint8)
-        for t in range(self.num_tables):
+
+        def one(t):
             s, e = self.table_segment(off, t)
-            seg = idx[s:e]
-            u, inv = np.unique(seg, return_inverse=True)
+            u, inv = np.unique(idx[s:e], return_inverse=True)
             reuse = np.isin(u, fut1[t]) | np.isin(u, fut2[t])
             flip = rng(self.config, t, P_BITS, b).random(u.size) < self.bit_flip
-            c = (reuse ^ flip).astype(np.uint8)
-            out[s:e] = c[inv]
+            out[s:e] = (reuse ^ flip).astype(np.uint8)[inv]
+        _pmap(one, range(self.num_tables))
         return out
 
 
