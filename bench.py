@@ -159,7 +159,7 @@ def main():
     pool_s = pool_ms / max(pool_calls, 1) / 1e3
     achieved = bytes_per_launch / pool_s / 1e9 if pool_s > 0 else 0.0
     link_bytes = delta["ondemand_bytes"] + delta["prefetch_bytes"]
-    link_ms = stages["fwd_fetch"][0] + stages["plc_fill"][0]
+    link_ms = stages["host_link"][0]  # union of miss-fetch and fill intervals (they overlap on two streams)
     link_gbs = link_bytes / (link_ms / 1e3) / 1e9 if link_ms > 0 else 0.0
 
     link_peak = None

@@ -110,7 +110,9 @@ typedef enum {
     RECMG_STAGE_PLC_RANK = 4,   /* scoring + radix select of the kept keys */
     RECMG_STAGE_PLC_APPLY = 5,  /* evict, map maintenance, admit, counters */
     RECMG_STAGE_PLC_FILL = 6,   /* copy of admitted rows into slots (host link for prefetch) */
-    RECMG_NUM_STAGES = 7
+    RECMG_STAGE_HOST_LINK = 7,  /* union of the FWD_FETCH and PLC_FILL intervals: the time the host
+                                   link was in use (the two can overlap on different streams) */
+    RECMG_NUM_STAGES = 8
 } recmg_stage_t;
 
 /* Counters of one table.  The first group describes a forward, the second a

@@ -31,7 +31,7 @@ STAT_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand
 
 EXPORTED = ("recmg_query_workspace", "recmg_cache_init", "recmg_apply_placement", "recmg_embbag_forward",
             "recmg_stats", "recmg_stage_times", "recmg_cache_destroy", "recmg_last_error")
-STAGES = ("fwd_dedup", "fwd_fetch", "fwd_pool", "plc_classify", "plc_rank", "plc_apply", "plc_fill")
+STAGES = ("fwd_dedup", "fwd_fetch", "fwd_pool", "plc_classify", "plc_rank", "plc_apply", "plc_fill", "host_link")
 
 
 class recmg_config_t(ctypes.Structure):

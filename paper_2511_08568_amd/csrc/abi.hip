@@ -56,9 +56,9 @@ struct Geom {
 
 struct Layout {
     size_t total = 0, host_total = 0;
-    std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, free_stack, map, bitmap, rank;
+    std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, slot_cbit, free_stack, map, bitmap, rank;
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
-    size_t src = 0, inv = 0, U = 0, slotU = 0, M = 0, mflags = 0, mscore = 0, fill_src = 0, fill_slot = 0;
+    size_t src = 0, inv = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
     size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, ftstart = 0;
     size_t staging[2] = {0, 0};
     int64_t stage_stride = 0, sum_cap = 0;
@@ -129,6 +129,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
         L->slot_score.push_back(take((size_t)g.cap * 4));
         L->slot_flags.push_back(take((size_t)g.cap * 4));
         L->slot_touch.push_back(take((size_t)g.cap * 4));
+        L->slot_cbit.push_back(take((size_t)g.cap));
         L->free_stack.push_back(take((size_t)g.cap * 4));
         L->map.push_back(take((size_t)g.map_cap * 8));
         L->bitmap.push_back(take((size_t)g.bm_words * 4));
@@ -151,6 +152,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->slotU = take(4 * mi);
     L->M = take(4 * mi);
     L->mflags = take(4 * mi);
+    L->mcbit = take(mi);
     L->mscore = take(4 * mi);
     L->NP = take(4 * mp);
     L->PU = take(4 * mp);
@@ -211,6 +213,17 @@ struct recmg_cache {
 
 namespace {
 
+hipEvent_t take_event(recmg_cache_t *c) {
+    if (c->ev_free.empty()) {
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+    hipEvent_t e = c->ev_free.back();
+    c->ev_free.pop_back();
+    return e;
+}
+
 // Stage timing: an event pair per stage per call, resolved in recmg_stage_times.
 struct StageTimer {
     recmg_cache_t *c;
@@ -222,16 +235,7 @@ struct StageTimer {
         a = take();
         if (a) (void)hipEventRecord(a, s);
     }
-    hipEvent_t take() {
-        if (c->ev_free.empty()) {
-            hipEvent_t e = nullptr;
-            if (hipEventCreate(&e) != hipSuccess) return nullptr;
-            return e;
-        }
-        hipEvent_t e = c->ev_free.back();
-        c->ev_free.pop_back();
-        return e;
-    }
+    hipEvent_t take() { return take_event(c); }
     ~StageTimer() {
         if (!a) return;
         hipEvent_t b = take();
@@ -399,6 +403,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.slotU = reinterpret_cast<int32_t *>(ws + L.slotU);
     g.M = reinterpret_cast<int32_t *>(ws + L.M);
     g.mflags = reinterpret_cast<uint32_t *>(ws + L.mflags);
+    g.mcbit = reinterpret_cast<uint8_t *>(ws + L.mcbit);
     g.mscore = reinterpret_cast<int32_t *>(ws + L.mscore);
     g.NP = reinterpret_cast<int32_t *>(ws + L.NP);
     g.PU = reinterpret_cast<int32_t *>(ws + L.PU);
@@ -429,6 +434,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         d.slot_score = reinterpret_cast<int32_t *>(ws + L.slot_score[t]);
         d.slot_flags = reinterpret_cast<uint32_t *>(ws + L.slot_flags[t]);
         d.slot_touch = reinterpret_cast<int32_t *>(ws + L.slot_touch[t]);
+        d.slot_cbit = reinterpret_cast<uint8_t *>(ws + L.slot_cbit[t]);
         d.free_stack = reinterpret_cast<int32_t *>(ws + L.free_stack[t]);
         d.map = reinterpret_cast<int2 *>(ws + L.map[t]);
         d.bitmap = reinterpret_cast<uint32_t *>(ws + L.bitmap[t]);
@@ -468,6 +474,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         HIP_TRY(hipMemsetAsync(ws + L.slot_score[t], 0, (size_t)ge.cap * 4, s0));
         HIP_TRY(hipMemsetAsync(ws + L.slot_flags[t], 0, (size_t)ge.cap * 4, s0));
         HIP_TRY(hipMemsetAsync(ws + L.slot_touch[t], 0xff, (size_t)ge.cap * 4, s0));
+        HIP_TRY(hipMemsetAsync(ws + L.slot_cbit[t], 0, (size_t)ge.cap, s0));
         HIP_TRY(hipMemsetAsync(ws + L.map[t], 0xff, (size_t)ge.map_cap * 8, s0));
         HIP_TRY(hipMemsetAsync(ws + L.bitmap[t], 0, (size_t)ge.bm_words * 4, s0));
         HIP_TRY(hipMemsetAsync(ws + L.rank[t], 0xff, (size_t)ge.bm_words * 16, s0));  // stamp -1
@@ -629,10 +636,20 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
         c->fill_pending = false;
     }
     {
-        StageTimer tm(c, RECMG_STAGE_FWD_POOL, s);
+        // the pooled kernel is timed by events its own dispatch records
+        hipEvent_t a = nullptr, b = nullptr;
+        if (c->cfg.timing && c->pool_blocks > 0) {
+            a = take_event(c);
+            b = a ? take_event(c) : nullptr;
+            if (!b && a) {
+                c->ev_free.push_back(a);
+                a = nullptr;
+            }
+        }
         launch_pool(g, offsets, (int32_t)B, out, c->pool_blocks,
                     reinterpret_cast<const int32_t *>(static_cast<char *>(c->cfg.device_workspace) + c->L.pool_bstart),
-                    c->pool_classes, s);
+                    c->pool_classes, a, b, s);
+        if (a) c->marks.push_back({RECMG_STAGE_FWD_POOL, a, b});
     }
     launch_fwd_finalize(g, s);
     HIP_TRY(hipGetLastError());
@@ -699,12 +716,35 @@ int32_t recmg_stage_times(recmg_cache_t *c, double *ms, int64_t *calls, int32_t 
     if (rc) return rc;
     if (!ms) return fail(RECMG_E_INVALID, "ms is NULL");
     if ((rc = set_device(c))) return rc;
+    // every interval on one time line (offsets from the first mark's start)
+    std::vector<std::pair<double, double>> link;
     for (auto &m : c->marks) {
         HIP_TRY(hipEventSynchronize(m.b));
-        float t = 0.f;
+        float t = 0.f, t0 = 0.f, t1 = 0.f;
         HIP_TRY(hipEventElapsedTime(&t, m.a, m.b));
         c->stage_ms[m.stage] += t;
         c->stage_calls[m.stage] += 1;
+        if (m.stage == RECMG_STAGE_FWD_FETCH || m.stage == RECMG_STAGE_PLC_FILL) {
+            HIP_TRY(hipEventElapsedTime(&t0, c->marks[0].a, m.a));
+            HIP_TRY(hipEventElapsedTime(&t1, c->marks[0].a, m.b));
+            link.emplace_back(t0, t1);
+        }
+    }
+    std::sort(link.begin(), link.end());
+    double busy = 0, cur_a = 0, cur_b = -1;
+    for (auto &iv : link) {
+        if (iv.first > cur_b) {
+            if (cur_b > cur_a) busy += cur_b - cur_a;
+            cur_a = iv.first;
+            cur_b = iv.second;
+        } else if (iv.second > cur_b) {
+            cur_b = iv.second;
+        }
+    }
+    if (cur_b > cur_a) busy += cur_b - cur_a;
+    c->stage_ms[RECMG_STAGE_HOST_LINK] += busy;
+    c->stage_calls[RECMG_STAGE_HOST_LINK] += (int64_t)link.size();
+    for (auto &m : c->marks) {
         c->ev_free.push_back(m.a);
         c->ev_free.push_back(m.b);
     }

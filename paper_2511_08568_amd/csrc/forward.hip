@@ -11,6 +11,8 @@
 //   k_fwd_finalize  publish the counters
 #include <type_traits>
 
+#include <hip/hip_ext.h>
+
 #include "launch.h"
 
 namespace recmg {
@@ -75,6 +77,7 @@ __global__ void __launch_bounds__(kBlock) k_fwd_probe(DGlobal g, int32_t stamp, 
             g.slotU[i] = -(m + 1);
             g.M[at] = row;
             g.mflags[at] = 0;
+            g.mcbit[at] = 0;
         }
     }
 }
@@ -165,6 +168,11 @@ struct Lane {
     static constexpr int VE = VEC ? 16 / Elem<DT>::bytes : 1;
     using V = typename std::conditional<VEC, uint4, typename std::conditional<Elem<DT>::bytes == 4, uint32_t,
                                                                                uint16_t>::type>::type;
+    __device__ static V load(const char *p) {
+        if constexpr (VEC) return gload16(p);
+        else if constexpr (Elem<DT>::bytes == 4) return gload4(p);
+        else return gload2(p);
+    }
     __device__ static void add(float *acc, const V v) {
         if constexpr (VEC) accum_vec<DT>(acc, v);
         else acc[0] += Elem<DT>::widen((uint32_t)v);
@@ -187,8 +195,12 @@ __device__ __forceinline__ void pool_table(const DGlobal &g, const DTable &tb, i
 #ifndef RECMG_POOL_UNROLL
 #define RECMG_POOL_UNROLL 8
 #endif
-    // loads in flight per group, within the register budget
-    constexpr int UNROLL = EB == 4 ? RECMG_POOL_UNROLL : (RECMG_POOL_UNROLL > 8 ? 8 : RECMG_POOL_UNROLL);
+#ifndef RECMG_POOL_UNROLL_HALF
+#define RECMG_POOL_UNROLL_HALF 8
+#endif
+    // row loads in flight per group (fp32 / 2-byte storage): measured best on
+    // gfx950, where more depth costs more in occupancy than it gains
+    constexpr int UNROLL = EB == 4 ? RECMG_POOL_UNROLL : RECMG_POOL_UNROLL_HALF;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int G = tb.gsz;
     const int gl = lane & (G - 1);
@@ -209,38 +221,42 @@ __device__ __forceinline__ void pool_table(const DGlobal &g, const DTable &tb, i
         const int e0 = (ch * G + gl) * VE;
         const bool lane_ok = e0 < D;
         const int64_t eoff = lane_ok ? (int64_t)e0 * EB : 0;
+        // slot s >= 0: the HBM pool; s < 0: staging row -(s + 1); no branch
+        auto row_ptr = [&](int s) -> const char * {
+            const bool hit = s >= 0;
+            const char *base = hit ? pool : stg;
+            const int64_t idx = hit ? s : -(int64_t)s - 1;
+            return base + idx * (hit ? rb : sstride) + eoff;
+        };
         float acc[4][VE];
 #pragma unroll
         for (int k = 0; k < 4; ++k)
 #pragma unroll
             for (int x = 0; x < VE; ++x) acc[k][x] = 0.f;
 
-        int my = (a + gl < e) ? src[a + gl] : 0;
+        int my = (a + gl < e) ? (int)gload4(src + a + gl) : 0;
         for (int64_t c = a; c < e; c += G) {
             const int n = (int)((e - c) < G ? (e - c) : G);
-            const int nxt = (c + G + gl < e) ? src[c + G + gl] : 0;  // next chunk, in flight meanwhile
+            const int nxt = (c + G + gl < e) ? (int)gload4(src + c + G + gl) : 0;  // next chunk, in flight meanwhile
             int q = 0;
             for (; q + UNROLL <= n; q += UNROLL) {
+                int sv[UNROLL];
+#pragma unroll
+                for (int u = 0; u < UNROLL; ++u) sv[u] = __shfl(my, q + u, G);
                 V v[UNROLL];
 #pragma unroll
-                for (int u = 0; u < UNROLL; ++u) {
-                    const int s = __shfl(my, q + u, G);
-                    const char *p = s >= 0 ? pool + (int64_t)s * rb : stg + (int64_t)(-s - 1) * sstride;
-                    v[u] = *reinterpret_cast<const V *>(p + eoff);
-                }
+                for (int u = 0; u < UNROLL; ++u) v[u] = L::load(row_ptr(sv[u]));
 #pragma unroll
                 for (int u = 0; u < UNROLL; ++u) L::add(acc[u & 3], v[u]);
             }
             for (; q < n; q += 4) {
+                int sv[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) sv[u] = __shfl(my, q + u < n ? q + u : q, G);
                 V v[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    if (q + u < n) {
-                        const int s = __shfl(my, q + u, G);
-                        const char *p = s >= 0 ? pool + (int64_t)s * rb : stg + (int64_t)(-s - 1) * sstride;
-                        v[u] = *reinterpret_cast<const V *>(p + eoff);
-                    }
-                }
+                for (int u = 0; u < 4; ++u)
+                    if (q + u < n) v[u] = L::load(row_ptr(sv[u]));
 #pragma unroll
                 for (int u = 0; u < 4; ++u)
                     if (q + u < n) L::add(acc[u], v[u]);
@@ -332,16 +348,27 @@ void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStre
 
 void launch_fetch(const DGlobal &g, hipStream_t s) { k_fetch<<<1024, kBlock, 0, s>>>(g); }
 
+// ev0 / ev1 (may be null): recorded by the first / last dispatch itself, so
+// they bracket the kernels' execution without the dispatch gap.
 void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, int64_t nblocks,
-                 const int32_t *bstart, uint32_t classes, hipStream_t s) {
+                 const int32_t *bstart, uint32_t classes, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
     if (nblocks <= 0) return;
     const unsigned nbk = (unsigned)nblocks;
-    if (classes & (1u << (RECMG_F32 * 2 + 1))) k_pool<RECMG_F32, true><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
-    if (classes & (1u << (RECMG_F32 * 2))) k_pool<RECMG_F32, false><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
-    if (classes & (1u << (RECMG_F16 * 2 + 1))) k_pool<RECMG_F16, true><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
-    if (classes & (1u << (RECMG_F16 * 2))) k_pool<RECMG_F16, false><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
-    if (classes & (1u << (RECMG_BF16 * 2 + 1))) k_pool<RECMG_BF16, true><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
-    if (classes & (1u << (RECMG_BF16 * 2))) k_pool<RECMG_BF16, false><<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
+    using K = void (*)(DGlobal, const int64_t *, int32_t, float *, const int32_t *);
+    const K ks[6] = {k_pool<RECMG_F32, false>, k_pool<RECMG_F32, true>, k_pool<RECMG_F16, false>,
+                     k_pool<RECMG_F16, true>, k_pool<RECMG_BF16, false>, k_pool<RECMG_BF16, true>};
+    int first = -1, last = -1;
+    for (int c = 0; c < 6; ++c)
+        if (classes & (1u << c)) {
+            if (first < 0) first = c;
+            last = c;
+        }
+    for (int c = 0; c < 6; ++c) {
+        if (!(classes & (1u << c))) continue;
+        hipEvent_t a = c == first ? ev0 : nullptr, b = c == last ? ev1 : nullptr;
+        if (a || b) hipExtLaunchKernelGGL(ks[c], dim3(nbk), dim3(kBlock), 0, s, a, b, 0, g, offsets, B, out, bstart);
+        else ks[c]<<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
+    }
 }
 
 void launch_fwd_finalize(const DGlobal &g, hipStream_t s) { k_fwd_finalize<<<1, kBlock, 0, s>>>(g); }

@@ -19,7 +19,7 @@ void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStre
 void launch_fetch(const DGlobal &g, hipStream_t s);
 // classes: bit (dtype * 2 + vec) set for every (storage type, vector path) class of a table
 void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, int64_t nblocks,
-                 const int32_t *bstart, uint32_t classes, hipStream_t s);
+                 const int32_t *bstart, uint32_t classes, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
 void launch_fwd_finalize(const DGlobal &g, hipStream_t s);
 
 // placement.hip

@@ -50,7 +50,9 @@ __global__ void k_plc_prep(DGlobal g, const int64_t *__restrict__ poff, int64_t 
     }
 }
 
-// caching bits of the last batch: OR into the slot (hit) or the miss entry
+// Caching bits of the last batch, OR-ed per row into a byte of the slot (hit)
+// or of the miss entry.  Every writer stores the same value 1, so plain byte
+// stores suffice (no read-modify-write atomics on popular rows).
 __global__ void __launch_bounds__(kBlock) k_plc_bits(DGlobal g, const uint8_t *__restrict__ bits, int64_t n) {
     if (*g.err) return;
     __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
@@ -61,8 +63,8 @@ __global__ void __launch_bounds__(kBlock) k_plc_bits(DGlobal g, const uint8_t *_
         if (!bits[i]) continue;
         const int t = find_seg(s_start, g.T, i);
         const int32_t s = g.src[i];
-        if (s >= 0) atomicOr(&g.tabs[t].slot_flags[s], F_CBIT);
-        else atomicOr(&g.mflags[s_start[t] + (-(int64_t)s - 1)], F_CBIT);
+        uint8_t *f = s >= 0 ? &g.tabs[t].slot_cbit[s] : &g.mcbit[s_start[t] + (-(int64_t)s - 1)];
+        if (!*f) *f = 1;
     }
 }
 
@@ -209,19 +211,21 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
             if (row < 0) continue;
             s = tb.slot_score[k];
             uint32_t f = tb.slot_flags[k];
+            const int cb = tb.slot_cbit[k];
+            if (cb) tb.slot_cbit[k] = 0;
             if (p.prio) s = s > 0 ? s - 1 : 0;
             if (tb.slot_touch[k] == p.last_stamp) {
                 f &= ~F_PF;
-                s = p.prio ? (int32_t)((f & F_CBIT) ? 1 : 0) + p.es : p.lru_touch;
+                s = p.prio ? cb + p.es : p.lru_touch;
             }
             if ((f & F_INP) && s < p.pscore) s = p.pscore;
             tb.slot_score[k] = s;
-            tb.slot_flags[k] = f & ~(F_CBIT | F_INP);
+            tb.slot_flags[k] = f & ~F_INP;
         } else if (k < (int64_t)c.cap + c.nm) {
             const int64_t m = ts + (k - c.cap);
             row = g.M[m];
             const uint32_t f = g.mflags[m];
-            s = p.prio ? (int32_t)((f & F_CBIT) ? 1 : 0) + p.es : p.lru_touch;
+            s = p.prio ? (int32_t)g.mcbit[m] + p.es : p.lru_touch;
             if ((f & F_INP) && s < p.pscore) s = p.pscore;
             g.mscore[m] = s;
         } else {

@@ -21,7 +21,6 @@ constexpr int32_t kPending = INT32_MIN;             // probe result before miss 
 
 // per-slot flag bits
 constexpr uint32_t F_PF = 1u;    // admitted by a prefetch and not accessed since
-constexpr uint32_t F_CBIT = 2u;  // OR of the caching bits of the last batch
 constexpr uint32_t F_INP = 4u;   // named by the current placement's prefetch list
 
 // device error flag bits
@@ -42,6 +41,7 @@ struct DTable {
     int32_t *slot_score;   // [cap] ranking score
     uint32_t *slot_flags;  // [cap] F_* bits
     int32_t *slot_touch;   // [cap] stamp of the last forward that hit the slot
+    uint8_t *slot_cbit;    // [cap] OR of the caching bits of the last batch (zero between placements)
     int32_t *free_stack;   // [cap] free slot ids, top at free_top
     int2 *map;             // [map_mask + 1] open-addressed row -> slot map (key, slot)
     uint32_t *bitmap;      // [bm_words] presence bitmap, zero between uses
@@ -95,7 +95,8 @@ struct DGlobal {
     int32_t *U;               // [max_indices] sorted distinct rows, table t at tstart[t]
     int32_t *slotU;           // [max_indices] per distinct row: slot or -(miss + 1)
     int32_t *M;               // [max_indices] missed rows, table t at tstart[t]
-    uint32_t *mflags;         // [max_indices] F_CBIT / F_INP of each miss
+    uint32_t *mflags;         // [max_indices] F_INP of each miss
+    uint8_t *mcbit;           // [max_indices] OR of each miss's caching bits
     int32_t *mscore;          // [max_indices] ranking score of each miss
     int32_t *NP;              // [max_prefetch] new prefetch candidates, table t at pstart[t]
     int32_t *PU;              // [max_prefetch] sorted distinct prefetch rows, table t at pstart[t]
@@ -129,6 +130,24 @@ struct PlcParams {
 
 // -------------------------------------------------------------------- helpers
 
+// Loads through the global address space.  Pointers read from the workspace
+// are generic, and generic (flat) loads also count against the LDS counter, so
+// a wave that shuffles between loads would wait for every load in flight.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef int i32x2_t __attribute__((ext_vector_type(2)));
+#define RECMG_GLOBAL(T, p) (*(const __attribute__((address_space(1))) T *)(p))
+
+__device__ __forceinline__ uint4 gload16(const void *p) {
+    const u32x4_t v = RECMG_GLOBAL(u32x4_t, p);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ uint32_t gload4(const void *p) { return RECMG_GLOBAL(uint32_t, p); }
+__device__ __forceinline__ uint16_t gload2(const void *p) { return RECMG_GLOBAL(uint16_t, p); }
+__device__ __forceinline__ int2 gload_int2(const void *p) {
+    const i32x2_t v = RECMG_GLOBAL(i32x2_t, p);
+    return make_int2(v[0], v[1]);
+}
+
 __device__ __forceinline__ uint32_t hash_row(int32_t r) {
     // murmur3 32-bit finaliser
     uint32_t h = (uint32_t)r;
@@ -145,7 +164,7 @@ __device__ __forceinline__ int32_t map_find(const DTable &tb, int32_t row) {
     const int32_t mask = tb.map_mask;
     uint32_t i = hash_row(row) & (uint32_t)mask;
     for (int32_t n = 0; n <= mask; ++n) {
-        int2 e = tb.map[i];
+        const int2 e = gload_int2(tb.map + i);
         if (e.x == row) return e.y;
         if (e.x == kEmpty) return -1;
         i = (i + 1) & (uint32_t)mask;
@@ -365,9 +384,9 @@ __device__ __forceinline__ void copy_flat(const DGlobal &g, const int32_t *count
                 const char *sp = src_of(t, tb, j) + vo;
                 dst[q] = dst_of(t, tb, j) + vo;
                 unit[q] = u;
-                if (u == 16) v16[q] = *reinterpret_cast<const uint4 *>(sp);
-                else if (u == 4) v4[q] = *reinterpret_cast<const uint32_t *>(sp);
-                else v2[q] = *reinterpret_cast<const uint16_t *>(sp);
+                if (u == 16) v16[q] = gload16(sp);
+                else if (u == 4) v4[q] = gload4(sp);
+                else v2[q] = gload2(sp);
             }
         }
 #pragma unroll
