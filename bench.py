@@ -19,7 +19,6 @@ import json
 import os
 import sys
 import time
-from concurrent.futures import ThreadPoolExecutor
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
@@ -41,6 +40,8 @@ def main():
     ap.add_argument("--config", type=int, default=2, help="configuration id (1..5)")
     ap.add_argument("--row-scale", type=float, default=1.0, help="<1 shrinks rows and caches (debug only)")
     ap.add_argument("--miss-mode", default="zero_copy", choices=["zero_copy", "staged"])
+    ap.add_argument("--prefetch", default=None, choices=["none", "exact"],
+                    help="override the configuration's prefetch recipe (configuration 4 is run both ways)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-link-peak", action="store_true")
@@ -74,6 +75,8 @@ def main():
         w = tg.scaled_config(args.config, row_scale=args.row_scale)
     else:
         w = tg.make_config(args.config)
+    if args.prefetch is not None:
+        w.prefetch = (args.prefetch,)
     W, K = args.warmup, args.steps
     nb = W + K
     T = w.num_tables
@@ -82,8 +85,8 @@ def main():
     t0 = time.time()
     tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.uint16}
     host = [torch.empty((tb.rows, tb.dim), dtype=tdt[tb.dtype], pin_memory=True) for tb in w.tables]
-    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
-        list(ex.map(lambda t: w.table_values(t, out=host[t].numpy()), range(T)))
+    for t in range(T):  # each table's rows are drawn in parallel chunks
+        w.table_values(t, out=host[t].numpy())
     log(f"tables ready ({sum(h.numel() * h.element_size() for h in host) / 1e9:.2f} GB pinned) "
         f"in {time.time() - t0:.1f}s")
 

@@ -235,7 +235,8 @@ class Workload:
         if out is None:
             out = np.empty((tb.rows, tb.dim), dtype=NP_STORAGE[tb.dtype])
         assert out.shape == (tb.rows, tb.dim) and out.dtype == NP_STORAGE[tb.dtype]
-        for c0 in range(0, tb.rows, chunk_rows):
+
+        def chunk(c0):  # every chunk of rows has a stream of its own
             c1 = min(tb.rows, c0 + chunk_rows)
             g = rng(self.config, t, P_VALUES, c0 // chunk_rows)
             n = (c1 - c0) * tb.dim
@@ -244,6 +245,7 @@ class Workload:
             else:
                 x = g.random(n) * 2.0 - 1.0
             out[c0:c1] = to_storage(x, tb.dtype).reshape(c1 - c0, tb.dim)
+        _pmap(chunk, range(0, tb.rows, chunk_rows))
         return out
 
     # -- per-batch trace ---------------------------------------------------------
