@@ -84,10 +84,11 @@ def main():
     # -- tables in pinned host memory -------------------------------------------------------------
     t0 = time.time()
     tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.uint16}
-    host = [torch.empty((tb.rows, tb.dim), dtype=tdt[tb.dtype], pin_memory=True) for tb in w.tables]
+    pin = args.miss_mode == "zero_copy"  # staged mode reads the tables on the host only
+    host = [torch.empty((tb.rows, tb.dim), dtype=tdt[tb.dtype], pin_memory=pin) for tb in w.tables]
     for t in range(T):  # each table's rows are drawn in parallel chunks
         w.table_values(t, out=host[t].numpy())
-    log(f"tables ready ({sum(h.numel() * h.element_size() for h in host) / 1e9:.2f} GB pinned) "
+    log(f"tables ready ({sum(h.numel() * h.element_size() for h in host) / 1e9:.2f} GB, pinned={pin}) "
         f"in {time.time() - t0:.1f}s")
 
     # -- traces, staged into HBM before timing ----------------------------------------------------

@@ -65,8 +65,9 @@ typedef enum { RECMG_F32 = 0, RECMG_F16 = 1, RECMG_BF16 = 2 } recmg_dtype_t;
 typedef enum { RECMG_LRU_BATCH = 0, RECMG_PRIORITY = 1 } recmg_policy_t;
 typedef enum {
     RECMG_ZERO_COPY = 0, /* misses are read from host memory by a GPU kernel over the host link */
-    RECMG_STAGED = 1     /* miss ids go to the host, a host gather packs rows into pinned
-                            staging, and one copy per table moves them on the copy stream */
+    RECMG_STAGED = 1     /* miss ids (and the placement's prefetch fills) go to the host, a
+                            host gather packs rows into pinned staging, and one copy per table
+                            moves them on the copy stream; the GPU never reads host tables */
 } recmg_miss_mode_t;
 
 typedef struct recmg_cache recmg_cache_t; /* opaque handle */
@@ -78,10 +79,11 @@ typedef struct {
     const int64_t *rows;                /* N_t, 1 .. 2^31-1 */
     const int32_t *dims;                /* D_t >= 1 (elements per row) */
     const int32_t *dtypes;              /* recmg_dtype_t per table */
-    const void *const *host_tables;     /* pinned host memory (hipHostMalloc / torch
-                                           pin_memory), row-major [N_t][D_t]; caller-owned,
-                                           read-only while the handle lives; 16-byte aligned
-                                           when D_t*elem is a multiple of 16 */
+    const void *const *host_tables;     /* row-major [N_t][D_t], caller-owned, read-only while
+                                           the handle lives.  ZERO_COPY: pinned host memory
+                                           (hipHostMalloc / torch pin_memory), 16-byte aligned
+                                           when D_t*elem is a multiple of 16; the GPU reads it.
+                                           STAGED: any host memory; only the host reads it */
     const int64_t *cache_rows;          /* Cap_t >= 0 HBM slots (clamped to N_t) */
     int32_t policy;                     /* recmg_policy_t */
     int32_t eviction_speed;             /* PRIORITY only; 0 .. 1<<20 (the paper uses 4) */

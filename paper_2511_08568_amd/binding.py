@@ -156,8 +156,9 @@ def _stream_ptr(stream) -> int:
 class TieredEmbeddingCache:
     """One handle over a set of pinned host tables.
 
-    host_tables: CPU tensors in pinned memory, [rows, dim], float32 / float16 /
-    bfloat16 (or uint16 holding bfloat16 bits).  They must outlive the cache."""
+    host_tables: CPU tensors [rows, dim], float32 / float16 / bfloat16 (or
+    uint16 holding bfloat16 bits), pinned for miss_mode="zero_copy".  They must
+    outlive the cache."""
 
     def __init__(self, host_tables: Sequence, dtypes: Sequence[str], cache_rows: Sequence[int], *,
                  policy: str = "lru", eviction_speed: int = 4, miss_mode: str = "zero_copy",
@@ -168,8 +169,8 @@ class TieredEmbeddingCache:
         self.device = torch.device("cuda", device)
         self.T = len(host_tables)
         for t in host_tables:
-            if not t.is_pinned():
-                raise ValueError("host tables must be pinned (pin_memory=True)")
+            if miss_mode == "zero_copy" and not t.is_pinned():
+                raise ValueError("zero_copy needs pinned host tables (pin_memory=True); staged takes any")
         self._host = list(host_tables)
         self.dims = [int(t.shape[1]) for t in host_tables]
         self._rows = (ctypes.c_int64 * self.T)(*[int(t.shape[0]) for t in host_tables])

@@ -59,7 +59,9 @@ struct Layout {
     std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, slot_cbit, free_stack, map, bitmap, rank;
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, inv = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
-    size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, ftstart = 0;
+    size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, ftstart = 0, fstage = 0;
+    // pinned host staging (STAGED): miss ids, miss rows, fill sources, prefetch rows
+    size_t h_mrows = 0, h_rows = 0, h_fsrc = 0, h_frows = 0;
     size_t staging[2] = {0, 0};
     int64_t stage_stride = 0, sum_cap = 0;
     int32_t total_bm_blocks = 0;
@@ -165,8 +167,22 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->ftstart = take(8 * (T + 1));
     L->staging[0] = take(mi * (size_t)L->stage_stride);
     L->staging[1] = take(mi * (size_t)L->stage_stride);
+    const bool staged = cfg->miss_mode == RECMG_STAGED;
+    L->fstage = take(staged ? mp * (size_t)L->stage_stride : 0);
     L->total = off;
-    L->host_total = cfg->miss_mode == RECMG_STAGED ? align256(4 * std::max<size_t>(mi, 1)) + mi * (size_t)L->stage_stride : 0;
+    if (staged) {
+        size_t h = 0;
+        auto htake = [&](size_t bytes) {
+            const size_t at = h;
+            h = align256(h + std::max<size_t>(bytes, 1));
+            return at;
+        };
+        L->h_mrows = htake(4 * mi);
+        L->h_rows = htake(mi * (size_t)L->stage_stride);
+        L->h_fsrc = htake(4 * (mi + mp));
+        L->h_frows = htake(mp * (size_t)L->stage_stride);
+        L->host_total = h;
+    }
 }
 
 }  // namespace
@@ -198,6 +214,9 @@ struct recmg_cache {
     hipEvent_t ev_ready = nullptr, ev_copied = nullptr;
     int32_t *h_mrows = nullptr;
     char *h_rows = nullptr;
+    int32_t *h_fsrc = nullptr;  // fill sources of a placement, rewritten to staged rows
+    char *h_frows = nullptr;    // prefetch rows gathered on the host
+    std::vector<int64_t> h_pstart, h_ftstart;
     std::vector<TState> h_st;
     std::vector<int64_t> h_tstart;
     // stage timing
@@ -258,6 +277,71 @@ int32_t set_device(recmg_cache_t *c) {
     int cur = -1;
     HIP_TRY(hipGetDevice(&cur));
     if (cur != c->device) HIP_TRY(hipSetDevice(c->device));
+    return RECMG_OK;
+}
+
+// STAGED prefetch fill: the fill list comes back to the host, the host
+// gathers the prefetch rows from its tables into pinned staging and rewrites
+// their sources to staged rows, one copy per table moves both to the device,
+// and the fill kernel copies rows into their slots, all on stream cs.
+int32_t staged_fill(recmg_cache_t *c, hipStream_t s, hipStream_t cs) {
+    const int T = c->T;
+    HIP_TRY(hipMemcpyAsync(c->h_st.data(), c->g.st, sizeof(TState) * T, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(c->h_pstart.data(), c->g.pstart, 8 * (T + 1), hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipMemcpyAsync(c->h_ftstart.data(), c->g.ftstart, 8 * (T + 1), hipMemcpyDeviceToHost, s));
+    int32_t err = 0;
+    HIP_TRY(hipMemcpyAsync(&err, c->g.err, 4, hipMemcpyDeviceToHost, s));
+    HIP_TRY(hipStreamSynchronize(s));
+    if (err) return RECMG_OK;
+    std::vector<int64_t> base(T), nfill(T, 0), nhost(T, 0);
+    int64_t total = 0;
+    for (int t = 0; t < T; ++t) {
+        base[t] = c->h_ftstart[t] + c->h_pstart[t];
+        nfill[t] = c->h_st[t].popped;
+        if (base[t] < 0 || nfill[t] < 0 || base[t] + nfill[t] > c->g.fill_cap)
+            return fail(RECMG_E_STATE, "fill list outside its buffer");
+        if (nfill[t])
+            HIP_TRY(hipMemcpyAsync(c->h_fsrc + base[t], c->g.fill_src + base[t], 4 * (size_t)nfill[t],
+                                   hipMemcpyDeviceToHost, s));
+        total += nfill[t];
+    }
+    if (total == 0) return RECMG_OK;
+    HIP_TRY(hipStreamSynchronize(s));
+    const int64_t stride = c->L.stage_stride;
+    auto gather = [&](int t) {
+        const int64_t rb = c->geo[t].row_bytes, p0 = c->h_pstart[t];
+        int64_t k = 0;
+        for (int64_t j = 0; j < nfill[t]; ++j) {
+            int32_t &src = c->h_fsrc[base[t] + j];
+            if (src >= 0) continue;  // an admitted miss: already in HBM staging
+            const int64_t row = -(int64_t)src - 1;
+            std::memcpy(c->h_frows + (p0 + k) * stride, c->host[t] + row * rb, (size_t)rb);
+            src = -(int32_t)(p0 + k) - 1;  // now: staged prefetch row p0 + k
+            ++k;
+        }
+        nhost[t] = k;
+    };
+    const unsigned hw = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+    if (T == 1 || hw == 1) {
+        for (int t = 0; t < T; ++t) gather(t);
+    } else {
+        std::vector<std::thread> th;
+        const int nth = (int)std::min<unsigned>(hw, (unsigned)T);
+        for (int k = 0; k < nth; ++k)
+            th.emplace_back([&, k] {
+                for (int t = k; t < T; t += nth) gather(t);
+            });
+        for (auto &x : th) x.join();
+    }
+    for (int t = 0; t < T; ++t) {
+        if (nhost[t] > c->h_pstart[t + 1] - c->h_pstart[t]) return fail(RECMG_E_STATE, "staged fills exceed the list");
+        if (!nfill[t]) continue;
+        HIP_TRY(hipMemcpyAsync(c->g.fill_src + base[t], c->h_fsrc + base[t], 4 * (size_t)nfill[t],
+                               hipMemcpyHostToDevice, cs));
+        if (nhost[t])
+            HIP_TRY(hipMemcpyAsync(c->g.fstage + c->h_pstart[t] * stride, c->h_frows + c->h_pstart[t] * stride,
+                                   (size_t)(nhost[t] * stride), hipMemcpyHostToDevice, cs));
+    }
     return RECMG_OK;
 }
 
@@ -379,13 +463,17 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     // host tables: must be pinned memory visible to the device
     std::vector<const char *> dev_host(T);
     for (int t = 0; t < T; ++t) {
+        c->host.push_back(static_cast<const char *>(cfg->host_tables[t]));
+        if (cfg->miss_mode == RECMG_STAGED) {
+            dev_host[t] = nullptr;  // only the host reads the tables: any host memory will do
+            continue;
+        }
         void *dp = nullptr;
         if (hipHostGetDevicePointer(&dp, const_cast<void *>(cfg->host_tables[t]), 0) != hipSuccess || !dp) {
             (void)hipGetLastError();
             return fail(RECMG_E_INVALID, "host table " + std::to_string(t) + " is not pinned host memory");
         }
         dev_host[t] = static_cast<const char *>(dp);
-        c->host.push_back(static_cast<const char *>(cfg->host_tables[t]));
     }
     char *ws = static_cast<char *>(cfg->device_workspace);
     DGlobal &g = c->g;
@@ -411,6 +499,8 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.fill_src = reinterpret_cast<int32_t *>(ws + L.fill_src);
     g.fill_slot = reinterpret_cast<int32_t *>(ws + L.fill_slot);
     g.fill_cap = cfg->max_indices + cfg->max_prefetch;
+    g.fstage = ws + L.fstage;
+    g.staged_fill = cfg->miss_mode == RECMG_STAGED ? 1 : 0;
     g.hist = reinterpret_cast<int32_t *>(ws + L.hist);
     g.dump = reinterpret_cast<int32_t *>(ws + L.dump);
     g.dump_count = reinterpret_cast<int32_t *>(ws + L.dump_count);
@@ -497,8 +587,13 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         HIP_TRY(hipEventCreateWithFlags(&c->ev_fill, hipEventDisableTiming));
     }
     if (cfg->miss_mode == RECMG_STAGED) {
-        c->h_mrows = static_cast<int32_t *>(cfg->host_staging);
-        c->h_rows = static_cast<char *>(cfg->host_staging) + align256(4 * std::max<size_t>((size_t)cfg->max_indices, 1));
+        char *hs = static_cast<char *>(cfg->host_staging);
+        c->h_mrows = reinterpret_cast<int32_t *>(hs + L.h_mrows);
+        c->h_rows = hs + L.h_rows;
+        c->h_fsrc = reinterpret_cast<int32_t *>(hs + L.h_fsrc);
+        c->h_frows = hs + L.h_frows;
+        c->h_pstart.resize(T + 1);
+        c->h_ftstart.resize(T + 1);
         HIP_TRY(hipEventCreateWithFlags(&c->ev_ready, hipEventDisableTiming));
         HIP_TRY(hipEventCreateWithFlags(&c->ev_copied, hipEventDisableTiming));
     }
@@ -521,6 +616,10 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (c->cfg.validate && (rc = host_check_ids(prefetch_rows, prefetch_offsets, c->T + 1, 1, num_prefetch, c->geo, s)))
         return rc;
+    if (c->fill_pending) {  // two placements in a row: the earlier fill must finish first
+        HIP_TRY(hipStreamWaitEvent(s, c->ev_fill, 0));
+        c->fill_pending = false;
+    }
     c->g.staging = c->stage[c->cur];  // misses of the latest forward
     const DGlobal &g = c->g;
     const int64_t b = c->placements;
@@ -561,7 +660,21 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         StageTimer tm(c, RECMG_STAGE_PLC_APPLY, s);
         launch_plc_apply(g, p, c->max_cap, c->max_map, cand_grid, s);
     }
-    if (c->copy_stream) {
+    if (c->cfg.miss_mode == RECMG_STAGED) {
+        // host-staged prefetch rows; the fill overlaps the next forward when a copy stream is given
+        hipStream_t cs = c->copy_stream ? c->copy_stream : s;
+        if (cs != s) {
+            HIP_TRY(hipEventRecord(c->ev_admit, s));
+            HIP_TRY(hipStreamWaitEvent(cs, c->ev_admit, 0));
+        }
+        StageTimer tm(c, RECMG_STAGE_PLC_FILL, cs);
+        if ((rc = staged_fill(c, s, cs))) return rc;
+        launch_plc_fill(g, cs);
+        if (cs != s) {
+            HIP_TRY(hipEventRecord(c->ev_fill, cs));
+            c->fill_pending = true;
+        }
+    } else if (c->copy_stream) {
         // the fill overlaps the next forward's dedup; that forward's pooling waits for it
         HIP_TRY(hipEventRecord(c->ev_admit, s));
         HIP_TRY(hipStreamWaitEvent(c->copy_stream, c->ev_admit, 0));

@@ -444,7 +444,8 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
 }
 
 // Copy admitted rows into their slots: misses from HBM staging, prefetch
-// fills from pinned host memory over the host link.  May run on a side
+// fills from pinned host memory over the host link (ZERO_COPY) or from rows the
+// host staged and copied in (STAGED).  May run on a side
 // stream, concurrently with the next forward's dedup: it reads only
 // placement-owned state (popped, ftstart, pstart, the fill list) and the
 // staging buffer of the previous forward, which the next forward does not use.
@@ -463,7 +464,9 @@ __global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g) {
         [&](int t, const DTable &tb, int64_t j) -> const char * {
             const int64_t fts = g.ftstart[t];
             const int32_t src = g.fill_src[fts + g.pstart[t] + j];
-            return src >= 0 ? g.staging + (fts + src) * g.stage_stride : tb.host + (int64_t)(-src - 1) * tb.row_bytes;
+            if (src >= 0) return g.staging + (fts + src) * g.stage_stride;  // admitted miss
+            return g.staged_fill ? g.fstage + (int64_t)(-src - 1) * g.stage_stride  // prefetch row, host-staged
+                                 : tb.host + (int64_t)(-src - 1) * tb.row_bytes;    // prefetch row, zero-copy
         },
         [&](int t, const DTable &tb, int64_t j) {
             return tb.pool + (int64_t)g.fill_slot[g.ftstart[t] + g.pstart[t] + j] * tb.row_bytes;

@@ -111,6 +111,8 @@ struct DGlobal {
     int64_t *ftstart;         // [T+1] base of each table's fill list and admitted misses in the
                               // current placement: tstart of the last forward, or 0 if none ran
     int64_t fill_cap;         // entries of fill_src / fill_slot (max_indices + max_prefetch)
+    char *fstage;             // [max_prefetch][stage_stride] prefetch rows staged by the host (STAGED)
+    int32_t staged_fill;      // 1: a fill source -(k + 1) is fstage row k, not host row k
     int64_t stage_stride;
     int32_t T;
     int32_t total_bm_blocks;

@@ -81,7 +81,7 @@ class GpuRunner:
     """Drives the HIP path through a workload (test helper; marshalling only)."""
 
     def __init__(self, w, tabs, miss_mode="zero_copy", validate=False, max_indices=None, max_prefetch=None,
-                 nbatches=None):
+                 nbatches=None, pin=True):
         import torch
         from paper_2511_08568_amd import TieredEmbeddingCache
         self.torch = torch
@@ -92,7 +92,9 @@ class GpuRunner:
             max_indices = max(max(w.batch(b)[0].size for b in range(nb)), 1)
         if max_prefetch is None:
             max_prefetch = max(max(w.prefetch_list(b)[0].size for b in range(nb)), 1)
-        self.host = [torch.from_numpy(np.ascontiguousarray(a)).pin_memory() for a in tabs]
+        self.host = [torch.from_numpy(np.ascontiguousarray(a)) for a in tabs]
+        if pin:
+            self.host = [h.pin_memory() for h in self.host]
         self.cache = TieredEmbeddingCache(self.host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables],
                                           policy=w.policy, eviction_speed=w.eviction_speed, miss_mode=miss_mode,
                                           max_bags_per_table=w.bags, max_indices=max_indices,

@@ -12,10 +12,10 @@ pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
 
 
-def _parity(w, nbatches=None, miss_mode="zero_copy", label=""):
+def _parity(w, nbatches=None, miss_mode="zero_copy", label="", pin=True):
     nb = nbatches or w.batches
     tabs, ora = run_oracle(w, nbatches=nb)
-    g = GpuRunner(w, tabs, miss_mode=miss_mode, nbatches=nb)
+    g = GpuRunner(w, tabs, miss_mode=miss_mode, nbatches=nb, pin=pin)
     try:
         gpu = g.run(nb)
     finally:
@@ -89,6 +89,41 @@ def test_config4_no_prefetch_scaled():
 def test_staged_matches_oracle():
     w = tg.scaled_config(3, row_scale=0.01, batches=5, bags=256, max_tables=5)
     _parity(w, miss_mode="staged", label="c3-staged")
+
+
+@pytest.mark.parametrize("cid,scale,tables", [(3, 0.01, 5), (4, 0.0005, 2), (5, 0.005, 6)])
+def test_staged_with_unpinned_tables(cid, scale, tables):
+    """STAGED mode never reads host tables from the GPU (misses and prefetch
+    fills are gathered on the host), so the tables may be ordinary memory."""
+    w = tg.scaled_config(cid, row_scale=scale, batches=5, bags=256, max_tables=tables)
+    _parity(w, miss_mode="staged", label=f"c{cid}-staged-unpinned", pin=False)
+
+
+def test_two_placements_in_a_row():
+    """A placement right after another (no forward between) waits for the
+    earlier one's fill; both must match the oracle."""
+    w = tg.scaled_config(2, row_scale=0.01, batches=4, bags=128, max_tables=2)
+    tabs = [w.table_values(t) for t in range(w.num_tables)]
+    import oracle
+    o = oracle.for_workload(w, tabs)
+    g = GpuRunner(w, tabs)
+    try:
+        for b in range(w.batches):
+            for rep in range(2):
+                P, poff = w.prefetch_list(b + rep)
+                g.placement(P, poff)
+                assert o.placement(P, poff) == 0
+                last, _, res = g.cache.stats(dump=True)
+                for t in range(w.num_tables):
+                    assert res[t].tolist() == o.resident(t).tolist()
+                    assert last[t]["digest"] == o.stats(t)["digest"]
+            idx, off = w.batch(b)
+            out = g.forward(idx, off)
+            st, ref32, _ = o.forward(idx, off, w.bags)
+            assert np.allclose(out, ref32, rtol=1e-5, atol=1e-5)
+    finally:
+        g.close()
+        o.close()
 
 
 def test_cap_zero_and_full_give_identical_outputs():
