@@ -2,6 +2,7 @@
 // order, the STAGED miss path and counter readback.  All arithmetic of the
 // lookup runs in the kernels of dedup.hip, forward.hip and placement.hip.
 #include <algorithm>
+#include <atomic>
 #include <cstddef>
 #include <cstring>
 #include <memory>
@@ -280,10 +281,70 @@ int32_t set_device(recmg_cache_t *c) {
     return RECMG_OK;
 }
 
+// Host gather for the STAGED paths.  Each table's list of n[t] rows is cut
+// into chunks of kChunk rows, and consecutive chunks into copy groups of
+// kGroup rows.  Worker threads gather chunks in order; the calling thread
+// issues a group's copies to the device as soon as all its chunks are done,
+// so the gather and the host-to-device copies overlap.
+constexpr int64_t kChunk = 2048, kGroup = 16384;
+// Rows are scattered over the tables, so each is a cache and TLB miss; the
+// gather loops touch the row kAhead entries ahead to keep several in flight.
+constexpr int64_t kAhead = 12;
+
+inline void prefetch_row(const char *p, int64_t bytes) {
+    for (int64_t o = 0; o < bytes; o += 64) __builtin_prefetch(p + o, 0, 0);
+}
+
+template <class Work, class Copy>
+int32_t gather_and_copy(const std::vector<int64_t> &n, Work work, Copy copy) {
+    struct Chunk {
+        int t;
+        int64_t lo, hi;
+        int group;
+    };
+    struct Group {
+        int t;
+        int64_t lo, hi;
+        int nchunks;
+    };
+    std::vector<Chunk> chunks;
+    std::vector<Group> groups;
+    for (int t = 0; t < (int)n.size(); ++t)
+        for (int64_t g0 = 0; g0 < n[t]; g0 += kGroup) {
+            const int64_t g1 = std::min(n[t], g0 + kGroup);
+            groups.push_back({t, g0, g1, 0});
+            for (int64_t c0 = g0; c0 < g1; c0 += kChunk) {
+                chunks.push_back({t, c0, std::min(g1, c0 + kChunk), (int)groups.size() - 1});
+                groups.back().nchunks++;
+            }
+        }
+    if (chunks.empty()) return RECMG_OK;
+    std::unique_ptr<std::atomic<int>[]> done(new std::atomic<int>[groups.size()]);
+    for (size_t k = 0; k < groups.size(); ++k) done[k].store(0);
+    std::atomic<size_t> next(0);
+    const unsigned hw = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+    const unsigned nth = (unsigned)std::min<size_t>(hw, chunks.size());
+    std::vector<std::thread> th;
+    for (unsigned k = 0; k < nth; ++k)
+        th.emplace_back([&] {
+            for (size_t i; (i = next.fetch_add(1)) < chunks.size();) {
+                work(chunks[i].t, chunks[i].lo, chunks[i].hi);
+                done[chunks[i].group].fetch_add(1, std::memory_order_release);
+            }
+        });
+    int32_t rc = RECMG_OK;
+    for (size_t k = 0; k < groups.size(); ++k) {
+        while (done[k].load(std::memory_order_acquire) < groups[k].nchunks) std::this_thread::yield();
+        if (rc == RECMG_OK) rc = copy(groups[k].t, groups[k].lo, groups[k].hi);
+    }
+    for (auto &x : th) x.join();
+    return rc;
+}
+
 // STAGED prefetch fill: the fill list comes back to the host, the host
 // gathers the prefetch rows from its tables into pinned staging and rewrites
-// their sources to staged rows, one copy per table moves both to the device,
-// and the fill kernel copies rows into their slots, all on stream cs.
+// their sources to staged rows, copies move both to the device on stream cs,
+// and the fill kernel (launched by the caller on cs) copies rows into slots.
 int32_t staged_fill(recmg_cache_t *c, hipStream_t s, hipStream_t cs) {
     const int T = c->T;
     HIP_TRY(hipMemcpyAsync(c->h_st.data(), c->g.st, sizeof(TState) * T, hipMemcpyDeviceToHost, s));
@@ -293,7 +354,7 @@ int32_t staged_fill(recmg_cache_t *c, hipStream_t s, hipStream_t cs) {
     HIP_TRY(hipMemcpyAsync(&err, c->g.err, 4, hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     if (err) return RECMG_OK;
-    std::vector<int64_t> base(T), nfill(T, 0), nhost(T, 0);
+    std::vector<int64_t> base(T), nfill(T, 0);
     int64_t total = 0;
     for (int t = 0; t < T; ++t) {
         base[t] = c->h_ftstart[t] + c->h_pstart[t];
@@ -308,10 +369,26 @@ int32_t staged_fill(recmg_cache_t *c, hipStream_t s, hipStream_t cs) {
     if (total == 0) return RECMG_OK;
     HIP_TRY(hipStreamSynchronize(s));
     const int64_t stride = c->L.stage_stride;
-    auto gather = [&](int t) {
+    // host-sourced entries are packed in list order: chunk k of table t starts
+    // at kbase[t][k] among them
+    std::vector<std::vector<int64_t>> kbase(T);
+    for (int t = 0; t < T; ++t) {
+        const int64_t nck = (nfill[t] + kChunk - 1) / kChunk;
+        kbase[t].assign(nck + 1, 0);
+        for (int64_t k = 0; k < nck; ++k) {
+            int64_t cnt = 0;
+            for (int64_t j = k * kChunk; j < std::min(nfill[t], (k + 1) * kChunk); ++j) cnt += c->h_fsrc[base[t] + j] < 0;
+            kbase[t][k + 1] = kbase[t][k] + cnt;
+        }
+        if (kbase[t][nck] > c->h_pstart[t + 1] - c->h_pstart[t])
+            return fail(RECMG_E_STATE, "staged fills exceed the list");
+    }
+    auto work = [&](int t, int64_t lo, int64_t hi) {
         const int64_t rb = c->geo[t].row_bytes, p0 = c->h_pstart[t];
-        int64_t k = 0;
-        for (int64_t j = 0; j < nfill[t]; ++j) {
+        int64_t k = kbase[t][lo / kChunk];
+        for (int64_t j = lo; j < hi; ++j) {
+            if (j + kAhead < hi && c->h_fsrc[base[t] + j + kAhead] < 0)
+                prefetch_row(c->host[t] + (-(int64_t)c->h_fsrc[base[t] + j + kAhead] - 1) * rb, rb);
             int32_t &src = c->h_fsrc[base[t] + j];
             if (src >= 0) continue;  // an admitted miss: already in HBM staging
             const int64_t row = -(int64_t)src - 1;
@@ -319,34 +396,23 @@ int32_t staged_fill(recmg_cache_t *c, hipStream_t s, hipStream_t cs) {
             src = -(int32_t)(p0 + k) - 1;  // now: staged prefetch row p0 + k
             ++k;
         }
-        nhost[t] = k;
     };
-    const unsigned hw = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
-    if (T == 1 || hw == 1) {
-        for (int t = 0; t < T; ++t) gather(t);
-    } else {
-        std::vector<std::thread> th;
-        const int nth = (int)std::min<unsigned>(hw, (unsigned)T);
-        for (int k = 0; k < nth; ++k)
-            th.emplace_back([&, k] {
-                for (int t = k; t < T; t += nth) gather(t);
-            });
-        for (auto &x : th) x.join();
-    }
-    for (int t = 0; t < T; ++t) {
-        if (nhost[t] > c->h_pstart[t + 1] - c->h_pstart[t]) return fail(RECMG_E_STATE, "staged fills exceed the list");
-        if (!nfill[t]) continue;
-        HIP_TRY(hipMemcpyAsync(c->g.fill_src + base[t], c->h_fsrc + base[t], 4 * (size_t)nfill[t],
+    auto copy = [&](int t, int64_t lo, int64_t hi) -> int32_t {
+        HIP_TRY(hipMemcpyAsync(c->g.fill_src + base[t] + lo, c->h_fsrc + base[t] + lo, 4 * (size_t)(hi - lo),
                                hipMemcpyHostToDevice, cs));
-        if (nhost[t])
-            HIP_TRY(hipMemcpyAsync(c->g.fstage + c->h_pstart[t] * stride, c->h_frows + c->h_pstart[t] * stride,
-                                   (size_t)(nhost[t] * stride), hipMemcpyHostToDevice, cs));
-    }
-    return RECMG_OK;
+        const int64_t k0 = kbase[t][lo / kChunk], k1 = kbase[t][(hi + kChunk - 1) / kChunk];
+        const int64_t r0 = c->h_pstart[t] + k0;
+        if (k1 > k0)
+            HIP_TRY(hipMemcpyAsync(c->g.fstage + r0 * stride, c->h_frows + r0 * stride, (size_t)((k1 - k0) * stride),
+                                   hipMemcpyHostToDevice, cs));
+        return RECMG_OK;
+    };
+    return gather_and_copy(nfill, work, copy);
 }
 
-// STAGED miss path: miss ids to the host, host gather into pinned staging,
-// one copy per table on the copy stream, compute stream waits for it.
+// STAGED miss path: miss ids to the host, a parallel host gather into pinned
+// staging overlapped with the copies on the copy stream; the compute stream
+// waits for the copies.
 int32_t staged_fetch(recmg_cache_t *c, hipStream_t s) {
     const int T = c->T;
     HIP_TRY(hipMemcpyAsync(c->h_st.data(), c->g.st, sizeof(TState) * T, hipMemcpyDeviceToHost, s));
@@ -355,50 +421,38 @@ int32_t staged_fetch(recmg_cache_t *c, hipStream_t s) {
     HIP_TRY(hipMemcpyAsync(&err, c->g.err, 4, hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
     if (err) return RECMG_OK;  // the device flag already disables the rest
+    std::vector<int64_t> nm(T);
     int64_t total = 0;
     for (int t = 0; t < T; ++t) {
-        const int32_t nm = c->h_st[t].mcount;
-        if (nm)
-            HIP_TRY(hipMemcpyAsync(c->h_mrows + c->h_tstart[t], c->g.M + c->h_tstart[t], 4 * (size_t)nm,
+        nm[t] = c->h_st[t].mcount;
+        if (nm[t])
+            HIP_TRY(hipMemcpyAsync(c->h_mrows + c->h_tstart[t], c->g.M + c->h_tstart[t], 4 * (size_t)nm[t],
                                    hipMemcpyDeviceToHost, s));
-        total += nm;
+        total += nm[t];
     }
     if (total == 0) return RECMG_OK;
     HIP_TRY(hipStreamSynchronize(s));
     const int64_t stride = c->L.stage_stride;
-    auto gather = [&](int64_t lo, int64_t hi) {
-        int64_t k = 0;
-        for (int t = 0; t < T && k < hi; ++t) {
-            const int64_t nm = c->h_st[t].mcount, ts = c->h_tstart[t];
-            const int64_t rb = c->geo[t].row_bytes;
-            for (int64_t m = std::max<int64_t>(0, lo - k); m < nm && k + m < hi; ++m) {
-                const int64_t row = c->h_mrows[ts + m];
-                std::memcpy(c->h_rows + (ts + m) * stride, c->host[t] + row * rb, (size_t)rb);
-            }
-            k += nm;
-        }
-    };
-    const unsigned hw = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
-    const unsigned nth = (unsigned)std::min<int64_t>(hw, std::max<int64_t>(1, total / 2048));
-    if (nth <= 1) {
-        gather(0, total);
-    } else {
-        std::vector<std::thread> th;
-        for (unsigned k = 0; k < nth; ++k)
-            th.emplace_back(gather, total * k / nth, total * (k + 1) / nth);
-        for (auto &x : th) x.join();
-    }
     hipStream_t cs = c->copy_stream ? c->copy_stream : s;
     if (cs != s) {
         HIP_TRY(hipEventRecord(c->ev_ready, s));
         HIP_TRY(hipStreamWaitEvent(cs, c->ev_ready, 0));
     }
-    for (int t = 0; t < T; ++t) {
-        const int64_t nm = c->h_st[t].mcount, ts = c->h_tstart[t];
-        if (nm)
-            HIP_TRY(hipMemcpyAsync(c->g.staging + ts * stride, c->h_rows + ts * stride, (size_t)(nm * stride),
-                                   hipMemcpyHostToDevice, cs));
-    }
+    auto work = [&](int t, int64_t lo, int64_t hi) {
+        const int64_t ts = c->h_tstart[t], rb = c->geo[t].row_bytes;
+        for (int64_t m = lo; m < hi; ++m) {
+            if (m + kAhead < hi) prefetch_row(c->host[t] + (int64_t)c->h_mrows[ts + m + kAhead] * rb, rb);
+            std::memcpy(c->h_rows + (ts + m) * stride, c->host[t] + (int64_t)c->h_mrows[ts + m] * rb, (size_t)rb);
+        }
+    };
+    auto copy = [&](int t, int64_t lo, int64_t hi) -> int32_t {
+        const int64_t r0 = c->h_tstart[t] + lo;
+        HIP_TRY(hipMemcpyAsync(c->g.staging + r0 * stride, c->h_rows + r0 * stride, (size_t)((hi - lo) * stride),
+                               hipMemcpyHostToDevice, cs));
+        return RECMG_OK;
+    };
+    int32_t rc = gather_and_copy(nm, work, copy);
+    if (rc) return rc;
     if (cs != s) {
         HIP_TRY(hipEventRecord(c->ev_copied, cs));
         HIP_TRY(hipStreamWaitEvent(s, c->ev_copied, 0));
