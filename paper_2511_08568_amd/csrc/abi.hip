@@ -53,14 +53,16 @@ struct Geom {
     int32_t dim = 0, dtype = 0, esz = 0, row_bytes = 0, cap = 0;
     int64_t map_cap = 0, bm_words = 0;
     int32_t bm_nblk = 0, gsz = 0, nchunk = 0, vec = 0, bpb = 0, copy_unit = 0;
+    int32_t wlw = 0, wr = 0, wnch = 0, kind = 0;
 };
 
 struct Layout {
     size_t total = 0, host_total = 0;
     std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, slot_cbit, free_stack, map, bitmap, rank;
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
-    size_t src = 0, inv = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
-    size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, ftstart = 0, fstage = 0;
+    size_t src = 0, raddr = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
+    size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, pool_btab = 0, ftstart = 0;
+    size_t fstage = 0;
     // pinned host staging (STAGED): miss ids, miss rows, fill sources, prefetch rows
     size_t h_mrows = 0, h_rows = 0, h_fsrc = 0, h_frows = 0;
     size_t staging[2] = {0, 0};
@@ -108,6 +110,19 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
         g.gsz = (int32_t)std::min<int64_t>(64, std::max<int64_t>(4, pow2ceil(lanes)));
         g.nchunk = (lanes + g.gsz - 1) / g.gsz;
         g.bpb = (kBlock / 64) * (64 / g.gsz);
+        // wave-per-bag pooling: rows of 1024 bytes (or whole multiples) are
+        // read 64 lanes x 16 bytes per load instruction; 512- and 256-byte
+        // rows 2 or 4 to an instruction (16 bytes per lane), 128- and 64-byte
+        // rows 4 to an instruction (8 or 4 bytes per lane)
+        const int32_t rb = g.row_bytes;
+        g.wlw = 0;
+        if (rb % 1024 == 0) g.wlw = 16, g.wr = 1, g.wnch = rb / 1024;
+        else if (rb == 512) g.wlw = 16, g.wr = 2, g.wnch = 1;
+        else if (rb == 256) g.wlw = 16, g.wr = 4, g.wnch = 1;
+        else if (rb == 128) g.wlw = 8, g.wr = 4, g.wnch = 1;
+        else if (rb == 64) g.wlw = 4, g.wr = 4, g.wnch = 1;
+        if (g.wlw) g.bpb = (kBlock / 64) * kWaveBags;
+        g.kind = pool_kind(g.dtype, g.vec, g.wlw, g.wr);
         g.copy_unit = g.row_bytes % 16 == 0 ? 16 : (g.row_bytes % 4 == 0 ? 4 : 2);
     }
 
@@ -150,7 +165,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->tstart = take(8 * (T + 1));
     L->pstart = take(8 * (T + 1));
     L->src = take(4 * mi);
-    L->inv = take(4 * mi);
+    L->raddr = take(8 * (mi + kWaveRows));  // a block of row addresses may be read past the end
     L->U = take(4 * mi);
     L->slotU = take(4 * mi);
     L->M = take(4 * mi);
@@ -165,6 +180,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->dump = take(4 * (size_t)L->sum_cap);
     L->dump_count = take(4 * T);
     L->pool_bstart = take(4 * (T + 1));
+    L->pool_btab = take(4 * T);
     L->ftstart = take(8 * (T + 1));
     L->staging[0] = take(mi * (size_t)L->stage_stride);
     L->staging[1] = take(mi * (size_t)L->stage_stride);
@@ -198,7 +214,8 @@ struct recmg_cache {
     DGlobal g{};
     std::vector<const char *> host;  // host tables (host pointers)
     int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1;
-    uint32_t pool_classes = 0;  // bit (dtype * 2 + vec) per class of table present
+    std::vector<int32_t> pool_order;  // table ids ordered by pooled-kernel kind
+    std::vector<PoolLaunch> pool_launches;
     int64_t max_rows = 0;
     int64_t placements = 0, forwards = 0, last_n = 0;
     bool have_fwd = false;
@@ -540,7 +557,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.tstart = reinterpret_cast<int64_t *>(ws + L.tstart);
     g.pstart = reinterpret_cast<int64_t *>(ws + L.pstart);
     g.src = reinterpret_cast<int32_t *>(ws + L.src);
-    g.inv = reinterpret_cast<int32_t *>(ws + L.inv);
+    g.raddr = reinterpret_cast<uint64_t *>(ws + L.raddr);
     g.U = reinterpret_cast<int32_t *>(ws + L.U);
     g.slotU = reinterpret_cast<int32_t *>(ws + L.slotU);
     g.M = reinterpret_cast<int32_t *>(ws + L.M);
@@ -599,6 +616,9 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         d.vec = ge.vec;
         d.bags_per_block = ge.bpb;
         d.copy_unit = ge.copy_unit;
+        d.wlw = ge.wlw;
+        d.wr = ge.wr;
+        d.wnch = ge.wnch;
         bstart[t + 1] = bstart[t] + ge.bm_nblk;
         out_off += ge.dim;
         cap_off += ge.cap;
@@ -606,9 +626,12 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         c->max_map = (int32_t)std::max<int64_t>(c->max_map, ge.map_cap);
         c->max_units = std::max(c->max_units, ge.row_bytes / ge.copy_unit);
         c->max_rows = std::max(c->max_rows, ge.rows);
-        c->pool_classes |= 1u << (ge.dtype * 2 + ge.vec);
     }
     c->rowbits = std::max(1, bitlen((uint64_t)(c->max_rows - 1)));
+    c->pool_order.resize(T);
+    for (int t = 0; t < T; ++t) c->pool_order[t] = t;
+    std::stable_sort(c->pool_order.begin(), c->pool_order.end(),
+                     [&](int x, int y) { return geo[x].kind < geo[y].kind; });
 
     // clear the metadata (not the slot pool or staging), set "free" markers
     hipStream_t s0 = nullptr;
@@ -631,6 +654,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     HIP_TRY(hipMemsetAsync(ws + L.hist, 0, 4 * (size_t)kRadix * T, s0));
     HIP_TRY(hipMemcpy(ws + L.tabs, tabs.data(), sizeof(DTable) * T, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(ws + L.bm_block_start, bstart.data(), 4 * (T + 1), hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(ws + L.pool_btab, c->pool_order.data(), 4 * T, hipMemcpyHostToDevice));
     launch_init_state(g, c->max_cap, s0);
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipDeviceSynchronize());
@@ -765,9 +789,18 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
     if (c->cfg.validate && (rc = host_check_ids(indices, offsets, (int64_t)c->T * B + 1, B, n, c->geo, s))) return rc;
     const DGlobal &g = c->g;
     if (c->pool_B != (int32_t)B) {
+        // blocks of the pooled kernels: tables grouped by kernel kind, one
+        // launch per kind over its contiguous range of blocks
         c->pool_bstart.assign(c->T + 1, 0);
-        for (int t = 0; t < c->T; ++t)
-            c->pool_bstart[t + 1] = c->pool_bstart[t] + (int32_t)((B + c->geo[t].bpb - 1) / c->geo[t].bpb);
+        c->pool_launches.clear();
+        for (int k = 0; k < c->T; ++k) {
+            const Geom &ge = c->geo[c->pool_order[k]];
+            const int32_t nb = (int32_t)((B + ge.bpb - 1) / ge.bpb);
+            c->pool_bstart[k + 1] = c->pool_bstart[k] + nb;
+            if (c->pool_launches.empty() || c->pool_launches.back().kind != ge.kind)
+                c->pool_launches.push_back({ge.kind, c->pool_bstart[k], 0});
+            c->pool_launches.back().nblk += nb;
+        }
         HIP_TRY(hipMemcpyAsync(static_cast<char *>(c->cfg.device_workspace) + c->L.pool_bstart, c->pool_bstart.data(),
                                4 * (c->T + 1), hipMemcpyHostToDevice, s));
         HIP_TRY(hipStreamSynchronize(s));
@@ -813,9 +846,10 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
                 a = nullptr;
             }
         }
-        launch_pool(g, offsets, (int32_t)B, out, c->pool_blocks,
-                    reinterpret_cast<const int32_t *>(static_cast<char *>(c->cfg.device_workspace) + c->L.pool_bstart),
-                    c->pool_classes, a, b, s);
+        char *ws = static_cast<char *>(c->cfg.device_workspace);
+        launch_pool(g, offsets, (int32_t)B, out, reinterpret_cast<const int32_t *>(ws + c->L.pool_bstart),
+                    reinterpret_cast<const int32_t *>(ws + c->L.pool_btab), c->T, c->pool_launches.data(),
+                    (int)c->pool_launches.size(), a, b, s);
         if (a) c->marks.push_back({RECMG_STAGE_FWD_POOL, a, b});
     }
     launch_fwd_finalize(g, s);

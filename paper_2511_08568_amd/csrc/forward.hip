@@ -3,8 +3,9 @@
 // Order of work on the stream (dedup and probe live in dedup.hip):
 //   k_fwd_prep   validate bag offsets, record each table's index range
 //   k_mark / count / scan / emit(FORWARD)   distinct rows, sorted; map probe
-//   k_fwd_src    per index: rank of its row among the distinct rows (the
-//                inverse map) and where its data lives (slot or staging row)
+//   k_fwd_src    per index: where its row lives (slot or staging row, and
+//                that row's device address), through the rank of the row
+//                among the distinct rows
 //   k_fetch      ZERO_COPY: copy each distinct missing row once from pinned
 //                host memory to HBM staging (GPU reads over the host link)
 //   k_pool       per bag, sum of its rows in fp32 (Sec. II, pooling by sum)
@@ -87,9 +88,15 @@ __global__ void __launch_bounds__(kBlock) k_fwd_src(DGlobal g, const int32_t *__
     if (*g.err) return;
     __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
     __shared__ const uint4 *s_rank[RECMG_MAX_TABLES];
+    __shared__ const char *s_pool[RECMG_MAX_TABLES];
+    __shared__ int32_t s_rb[RECMG_MAX_TABLES];
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         s_start[t] = g.tstart[t];
-        if (t < g.T) s_rank[t] = g.tabs[t].rank;
+        if (t < g.T) {
+            s_rank[t] = g.tabs[t].rank;
+            s_pool[t] = g.tabs[t].pool;
+            s_rb[t] = g.tabs[t].row_bytes;
+        }
     }
     __syncthreads();
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -98,8 +105,10 @@ __global__ void __launch_bounds__(kBlock) k_fwd_src(DGlobal g, const int32_t *__
         const int32_t r = indices[i];
         const uint4 rk = s_rank[t][r >> 5];
         const int32_t u = (int32_t)rk.x + __popc(rk.y & ((1u << (r & 31)) - 1u));
-        g.inv[i] = u;
-        g.src[i] = g.slotU[s_start[t] + u];
+        const int32_t sl = g.slotU[s_start[t] + u];
+        g.src[i] = sl;
+        g.raddr[i] = sl >= 0 ? (uint64_t)(s_pool[t] + (int64_t)sl * s_rb[t])
+                             : (uint64_t)(g.staging + (s_start[t] - (int64_t)sl - 1) * g.stage_stride);
     }
 }
 
@@ -280,27 +289,269 @@ __device__ __forceinline__ void pool_table(const DGlobal &g, const DTable &tb, i
     }
 }
 
-// One launch per (storage type, vector path) class present; a block whose
-// table belongs to another class returns at once.
+// Workgroups are dealt round-robin to the 8 XCDs; give each XCD one
+// contiguous range of a launch's blocks so a table's hot rows stay in one L2.
+__device__ __forceinline__ int xcd_block(int nb) {
+#ifndef RECMG_POOL_NO_XCD_MAP
+    const int x = (int)blockIdx.x & 7, q = nb >> 3, r = nb & 7;
+    return x * q + (x < r ? x : r) + ((int)blockIdx.x >> 3);
+#else
+    return (int)blockIdx.x;
+#endif
+}
+
+// Group-per-bag kernel for the tables the wave-per-bag kernel does not take.
+// Each launch covers the blocks [boff, boff + nblk) of one class; block lb
+// belongs to table btab[k] for the k with bstart[k] <= lb < bstart[k + 1].
 template <int DT, bool VEC>
 __global__ void __launch_bounds__(kBlock) k_pool(DGlobal g, const int64_t *__restrict__ offsets, int32_t B,
-                                                 float *__restrict__ out, const int32_t *__restrict__ bstart) {
+                                                 float *__restrict__ out, const int32_t *__restrict__ bstart,
+                                                 const int32_t *__restrict__ btab, int32_t nt, int32_t boff,
+                                                 int32_t nblk) {
     if (*g.err) return;
-    // Workgroups are dealt round-robin to the 8 XCDs; give each XCD one
-    // contiguous range of bags so a table's hot rows stay in one L2.
-#ifndef RECMG_POOL_NO_XCD_MAP
-    const int nb = (int)gridDim.x, x = (int)blockIdx.x & 7, q = nb >> 3, r = nb & 7;
-    const int lb = x * q + (x < r ? x : r) + ((int)blockIdx.x >> 3);
-#else
-    const int lb = (int)blockIdx.x;
-#endif
-    __shared__ int s_t;
-    if (threadIdx.x == 0) s_t = find_seg32(bstart, g.T, lb);
+    const int lb = boff + xcd_block(nblk);
+    __shared__ int s_k;
+    if (threadIdx.x == 0) s_k = find_seg32(bstart, nt, lb);
     __syncthreads();
-    const int t = s_t;
+    const int k = s_k, t = btab[k];
+    pool_table<DT, VEC>(g, g.tabs[t], t, B, offsets, out, lb - bstart[k]);
+}
+
+// ------------------------------------------------- wave-per-bag pooled sum
+//
+// One wave sums one bag.  Every lookup of the bag reads the same row in all
+// lanes, so the row addresses (written per index by k_fwd_src) are
+// wave-uniform: they arrive through scalar loads, and each lane only adds its
+// LW-byte slice -- no per-lookup address arithmetic in vector registers.  For
+// short rows (R > 1) the wave splits into R groups of 64 / R lanes and group
+// h takes the lookups p with p mod R = h.  Lookup p still goes to partial sum
+// p mod 4 and the four are combined as (S0 + S1) + (S2 + S3), the same fixed
+// order as the group-per-bag kernel.
+
+template <int LW>
+struct WVec;
+template <>
+struct WVec<4> {
+    using V = uint32_t;
+    __device__ static void words(const V v, uint32_t *w) { w[0] = v; }
+};
+template <>
+struct WVec<8> {
+    using V = u32x2_t;
+    __device__ static void words(const V v, uint32_t *w) {
+        w[0] = v.x;
+        w[1] = v.y;
+    }
+};
+template <>
+struct WVec<16> {
+    using V = u32x4_t;
+    __device__ static void words(const V v, uint32_t *w) {
+        w[0] = v.x;
+        w[1] = v.y;
+        w[2] = v.z;
+        w[3] = v.w;
+    }
+};
+
+template <int DT, int LW>
+__device__ __forceinline__ void wadd(float *acc, const typename WVec<LW>::V v) {
+    uint32_t w[LW / 4];
+    WVec<LW>::words(v, w);
+#pragma unroll
+    for (int k = 0; k < LW / 4; ++k) {
+        if constexpr (DT == RECMG_F32) {
+            acc[k] += __builtin_bit_cast(float, w[k]);
+        } else if constexpr (DT == RECMG_BF16) {
+            acc[2 * k] += __builtin_bit_cast(float, w[k] << 16);
+            acc[2 * k + 1] += __builtin_bit_cast(float, w[k] & 0xffff0000u);
+        } else {
+            acc[2 * k] += f16_to_f32(w[k] & 0xffffu);
+            acc[2 * k + 1] += f16_to_f32(w[k] >> 16);
+        }
+    }
+}
+
+// LW-byte load at global address base + off
+template <class V>
+__device__ __forceinline__ V wload(uint64_t base, uint32_t off) {
+    typedef const __attribute__((address_space(1))) char gchar;
+    return *(const __attribute__((address_space(1))) V *)((gchar *)base + off);
+}
+
+// Address for group h among the R uniform addresses q[0 .. R), of which the
+// first m are lookups of the bag (m >= 1); a group past the bag's end takes
+// q[0] (loaded, never added).
+template <int R>
+__device__ __forceinline__ uint64_t wpick(const uint64_t *q, int h, int m) {
+    uint64_t x = q[0];
+#pragma unroll
+    for (int k = 1; k < R; ++k) {
+        // the empty asm pins q[k] as a scalar value, so the per-lane select
+        // is not turned into a load through a selected pointer (which would
+        // move the address block out of registers)
+        uint64_t y = q[k];
+        asm("" : "+s"(y));
+        x = (h == k && k < m) ? y : x;
+    }
+    return x;
+}
+
+// The lane offset is passed through an empty asm in every block of loads so
+// that its zero extension is visible where the loads are selected: a uniform
+// 64-bit base plus a 32-bit lane offset then becomes the scalar-base form of
+// global_load, with no vector address arithmetic at all.
+__device__ __forceinline__ uint32_t opaque(uint32_t x) {
+    asm volatile("" : "+v"(x));
+    return x;
+}
+
+
+// Wave-uniform row addresses of one block of UR lookups starting at index i.
+// A block may run past the bag (and past the batch: the address array has
+// kWaveRows entries of padding); such entries are never dereferenced.
+template <int UR>
+__device__ __forceinline__ void wblock_addrs(uint64_t *nx, const uint64_t *__restrict__ raddr, int64_t i) {
+#pragma unroll
+    for (int k = 0; k < UR; ++k) nx[k] = raddr[i + k];
+}
+
+// One wave sums BPW consecutive bags.  Software pipeline: the scalar loads of
+// the next block's row addresses (in this bag or the next) are in flight while
+// the current block's row loads are; UR = U * R lookups per block.
+template <int DT, int LW, int R>
+__device__ __forceinline__ void pool_wave(const uint64_t *__restrict__ raddr, const int64_t *__restrict__ ob, int j0,
+                                          int nbags, int wnch, int D, float *__restrict__ obase) {
+    using V = typename WVec<LW>::V;
+    constexpr int EB = Elem<DT>::bytes, NE = LW / EB, GL = 64 / R, NA = 4 / R;
+    constexpr int UR = kWaveRows;                  // lookups per block (row addresses held in SGPRs)
+    constexpr int U0 = UR / R;                        // load instructions per block
+    constexpr int U = U0 * LW > 128 ? 128 / LW : U0;  // at most 8 KB of rows in flight per wave
+    static_assert(U % NA == 0, "partial-sum slot must not depend on the block start");
+    constexpr int BPW = kWaveBags;
+    const int lane = threadIdx.x & 63, h = lane / GL, gl = lane % GL;
+    int64_t offs[BPW + 1];
+#pragma unroll
+    for (int b = 0; b <= BPW; ++b) offs[b] = ob[j0 + (b < nbags ? b : nbags)];
+    for (int ch = 0; ch < wnch; ++ch) {
+        const uint32_t eoff = (uint32_t)((ch * GL + gl) * LW);
+        uint64_t nx[U * R];
+        // first block of the first non-empty bag after bag b (all indices
+        // static, so offs and nx stay in scalar registers)
+        auto next_bag_addrs = [&](uint64_t *dst, int b) {
+            bool found = false;
+#pragma unroll
+            for (int b2 = 0; b2 < BPW; ++b2)
+                if (b2 > b && !found && b2 < nbags && offs[b2 + 1] > offs[b2]) {
+                    wblock_addrs<U * R>(dst, raddr, offs[b2]);
+                    found = true;
+                }
+        };
+        next_bag_addrs(nx, -1);
+#pragma unroll
+        for (int b = 0; b < BPW; ++b) {
+            if (b >= nbags) continue;
+            const int64_t a = offs[b];
+            const int n = (int)(offs[b + 1] - a);
+            float acc[NA][NE];
+#pragma unroll
+            for (int k = 0; k < NA; ++k)
+#pragma unroll
+                for (int x = 0; x < NE; ++x) acc[k][x] = 0.f;
+            int p = 0;
+            // full blocks: straight-line loads from the scalar-base form
+            for (; p + U * R <= n; p += U * R) {
+                V v[U];
+                const uint32_t eo = opaque(eoff);
+#pragma unroll
+                for (int u = 0; u < U; ++u) v[u] = wload<V>(wpick<R>(nx + u * R, h, R), eo);
+                // next block: this bag's, else the next non-empty bag's first.
+                // The barrier keeps these scalar loads after the row loads
+                // above, so one block of addresses is live at a time.
+                asm volatile("" ::: "memory");
+                if (p + U * R < n) wblock_addrs<U * R>(nx, raddr, a + p + U * R);
+                else next_bag_addrs(nx, b);
+#pragma unroll
+                for (int u = 0; u < U; ++u) wadd<DT, LW>(acc[u % NA], v[u]);
+            }
+            if (p < n) {
+                // partial block, in quads of load instructions; with one row
+                // per instruction a lookup past the bag's end re-reads the
+                // quad's first row and is not added
+                V v[U];
+#pragma unroll
+                for (int q = 0; q < U; q += 4)
+                    if (p + q * R < n) {
+                        const uint32_t eo = opaque(eoff);
+#pragma unroll
+                        for (int u = q; u < q + 4; ++u) {
+                            if constexpr (R == 1) {
+                                v[u] = wload<V>(p + u < n ? nx[u] : nx[q], eo);
+                            } else if (p + u * R + h < n) {
+                                // lanes of a group past the bag's end load nothing
+                                v[u] = wload<V>(wpick<R>(nx + u * R, h, R), eo);
+                            }
+                        }
+                    }
+                asm volatile("" ::: "memory");
+                next_bag_addrs(nx, b);
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (p + u * R + h < n) wadd<DT, LW>(acc[u % NA], v[u]);
+            }
+            float r[NE];
+#pragma unroll
+            for (int x = 0; x < NE; ++x) {
+                if constexpr (R == 1) {
+                    r[x] = (acc[0][x] + acc[1][x]) + (acc[2][x] + acc[3][x]);
+                } else if constexpr (R == 2) {
+                    // group 0 holds S0, S2 and group 1 holds S1, S3
+                    const float o0 = __shfl_xor(acc[0][x], 32), o1 = __shfl_xor(acc[1][x], 32);
+                    r[x] = (acc[0][x] + o0) + (acc[1][x] + o1);
+                } else {
+                    // group h holds S_h
+                    const float s01 = acc[0][x] + __shfl_xor(acc[0][x], 16);
+                    r[x] = s01 + __shfl_xor(s01, 32);
+                }
+            }
+            if (h == 0) {
+                // the output block of a table starts at B * (sum of the earlier
+                // dims) floats, so vector stores need a run-time alignment check
+                float *o = obase + (int64_t)(j0 + b) * D + (ch * GL + gl) * NE;
+                const uintptr_t oa = reinterpret_cast<uintptr_t>(o);
+                if (NE % 4 == 0 && (oa & 15) == 0) {
+#pragma unroll
+                    for (int x = 0; x + 3 < NE; x += 4)
+                        *reinterpret_cast<float4 *>(o + x) = make_float4(r[x], r[x + 1], r[x + 2], r[x + 3]);
+                } else if (NE == 2 && (oa & 7) == 0) {
+                    *reinterpret_cast<float2 *>(o) = make_float2(r[0], r[NE - 1]);
+                } else {
+#pragma unroll
+                    for (int x = 0; x < NE; ++x) o[x] = r[x];
+                }
+            }
+        }
+    }
+}
+
+template <int DT, int LW, int R>
+__global__ void __launch_bounds__(kBlock) k_pool_w(DGlobal g, const int64_t *__restrict__ offsets,
+                                                   const uint64_t *__restrict__ raddr, int32_t B,
+                                                   float *__restrict__ out, const int32_t *__restrict__ bstart,
+                                                   const int32_t *__restrict__ btab, int32_t nt, int32_t boff,
+                                                   int32_t nblk) {
+    if (*g.err) return;
+    const int lb = boff + xcd_block(nblk);
+    const int k = find_seg32(bstart, nt, lb);
+    const int t = btab[k];
     const DTable &tb = g.tabs[t];
-    if (tb.dtype != DT || tb.vec != (VEC ? 1 : 0)) return;
-    pool_table<DT, VEC>(g, tb, t, B, offsets, out, lb - bstart[t]);
+    const int D = tb.dim, wnch = tb.wnch;
+    const int64_t ooff = (int64_t)B * tb.out_elem_off;
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    const int j0 = ((lb - bstart[k]) * (kBlock / 64) + wave) * kWaveBags;
+    if (j0 >= B) return;
+    const int nbags = B - j0 < kWaveBags ? B - j0 : kWaveBags;
+    pool_wave<DT, LW, R>(raddr, offsets + (int64_t)t * B, j0, nbags, wnch, D, out + ooff);
 }
 
 __global__ void k_fwd_finalize(DGlobal g) {
@@ -348,26 +599,51 @@ void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStre
 
 void launch_fetch(const DGlobal &g, hipStream_t s) { k_fetch<<<1024, kBlock, 0, s>>>(g); }
 
+int pool_kind(int dtype, int vec, int wlw, int wr) {
+    if (wlw == 0) return dtype * 2 + vec;
+    const int v = wlw == 16 ? (wr == 1 ? 0 : wr == 2 ? 1 : 2) : wlw == 8 ? 3 : 4;
+    return kPoolKindsGroup + dtype * 5 + v;
+}
+
 // ev0 / ev1 (may be null): recorded by the first / last dispatch itself, so
 // they bracket the kernels' execution without the dispatch gap.
-void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, int64_t nblocks,
-                 const int32_t *bstart, uint32_t classes, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s) {
-    if (nblocks <= 0) return;
-    const unsigned nbk = (unsigned)nblocks;
-    using K = void (*)(DGlobal, const int64_t *, int32_t, float *, const int32_t *);
-    const K ks[6] = {k_pool<RECMG_F32, false>, k_pool<RECMG_F32, true>, k_pool<RECMG_F16, false>,
-                     k_pool<RECMG_F16, true>, k_pool<RECMG_BF16, false>, k_pool<RECMG_BF16, true>};
+void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, const int32_t *bstart,
+                 const int32_t *btab, int32_t nt, const PoolLaunch *ls, int nl, hipEvent_t ev0, hipEvent_t ev1,
+                 hipStream_t s) {
+    using KG = void (*)(DGlobal, const int64_t *, int32_t, float *, const int32_t *, const int32_t *, int32_t,
+                        int32_t, int32_t);
+    using KW = void (*)(DGlobal, const int64_t *, const uint64_t *, int32_t, float *, const int32_t *,
+                        const int32_t *, int32_t, int32_t, int32_t);
+    static const KG kg[kPoolKindsGroup] = {k_pool<RECMG_F32, false>,  k_pool<RECMG_F32, true>,
+                                           k_pool<RECMG_F16, false>,  k_pool<RECMG_F16, true>,
+                                           k_pool<RECMG_BF16, false>, k_pool<RECMG_BF16, true>};
+#define RECMG_WK(DT) k_pool_w<DT, 16, 1>, k_pool_w<DT, 16, 2>, k_pool_w<DT, 16, 4>, k_pool_w<DT, 8, 4>, k_pool_w<DT, 4, 4>
+    static const KW kw[kPoolKinds - kPoolKindsGroup] = {RECMG_WK(RECMG_F32), RECMG_WK(RECMG_F16),
+                                                        RECMG_WK(RECMG_BF16)};
+#undef RECMG_WK
     int first = -1, last = -1;
-    for (int c = 0; c < 6; ++c)
-        if (classes & (1u << c)) {
-            if (first < 0) first = c;
-            last = c;
+    for (int i = 0; i < nl; ++i)
+        if (ls[i].nblk > 0) {
+            if (first < 0) first = i;
+            last = i;
         }
-    for (int c = 0; c < 6; ++c) {
-        if (!(classes & (1u << c))) continue;
-        hipEvent_t a = c == first ? ev0 : nullptr, b = c == last ? ev1 : nullptr;
-        if (a || b) hipExtLaunchKernelGGL(ks[c], dim3(nbk), dim3(kBlock), 0, s, a, b, 0, g, offsets, B, out, bstart);
-        else ks[c]<<<nbk, kBlock, 0, s>>>(g, offsets, B, out, bstart);
+    for (int i = 0; i < nl; ++i) {
+        const PoolLaunch &L = ls[i];
+        if (L.nblk <= 0) continue;
+        hipEvent_t a = i == first ? ev0 : nullptr, b = i == last ? ev1 : nullptr;
+        const dim3 grid((unsigned)L.nblk), blk(kBlock);
+        if (L.kind < kPoolKindsGroup) {
+            const KG k = kg[L.kind];
+            if (a || b) hipExtLaunchKernelGGL(k, grid, blk, 0, s, a, b, 0, g, offsets, B, out, bstart, btab, nt,
+                                              L.boff, L.nblk);
+            else k<<<grid, blk, 0, s>>>(g, offsets, B, out, bstart, btab, nt, L.boff, L.nblk);
+        } else {
+            const KW k = kw[L.kind - kPoolKindsGroup];
+            const uint64_t *ra = g.raddr;
+            if (a || b) hipExtLaunchKernelGGL(k, grid, blk, 0, s, a, b, 0, g, offsets, ra, B, out, bstart, btab, nt,
+                                              L.boff, L.nblk);
+            else k<<<grid, blk, 0, s>>>(g, offsets, ra, B, out, bstart, btab, nt, L.boff, L.nblk);
+        }
     }
 }
 

@@ -17,9 +17,18 @@ void launch_fwd_prep(const DGlobal &g, const int64_t *offsets, int32_t B, int64_
 void launch_fwd_probe(const DGlobal &g, int32_t stamp, int64_t n, hipStream_t s);
 void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStream_t s);
 void launch_fetch(const DGlobal &g, hipStream_t s);
-// classes: bit (dtype * 2 + vec) set for every (storage type, vector path) class of a table
-void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, int64_t nblocks,
-                 const int32_t *bstart, uint32_t classes, hipEvent_t ev0, hipEvent_t ev1, hipStream_t s);
+// Pooled-sum kernels: kinds [0, kPoolKindsGroup) are the group-per-bag kernel
+// (dtype * 2 + vec), the rest the wave-per-bag kernel per (dtype, wlw, wr).
+constexpr int kPoolKindsGroup = 6, kPoolKinds = kPoolKindsGroup + 15;
+int pool_kind(int dtype, int vec, int wlw, int wr);
+// one launch per kind present, over the blocks [boff, boff + nblk) of the
+// tables btab[k] ordered by kind; bstart[k] = first block of btab[k]
+struct PoolLaunch {
+    int32_t kind, boff, nblk;
+};
+void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, const int32_t *bstart,
+                 const int32_t *btab, int32_t nt, const PoolLaunch *ls, int nl, hipEvent_t ev0, hipEvent_t ev1,
+                 hipStream_t s);
 void launch_fwd_finalize(const DGlobal &g, hipStream_t s);
 
 // placement.hip

@@ -26,6 +26,14 @@ constexpr uint32_t F_INP = 4u;   // named by the current placement's prefetch li
 // device error flag bits
 constexpr int32_t ERR_RANGE = 1;
 constexpr int32_t ERR_OFFSETS = 2;
+#ifndef RECMG_WPOOL_BAGS
+#define RECMG_WPOOL_BAGS 2
+#endif
+constexpr int kWaveBags = RECMG_WPOOL_BAGS;  // consecutive bags per wave in the wave-per-bag pooled kernel
+#ifndef RECMG_WPOOL_ROWS
+#define RECMG_WPOOL_ROWS 8
+#endif
+constexpr int kWaveRows = RECMG_WPOOL_ROWS;  // lookups per block of loads in that kernel (power of two <= 16)
 constexpr int32_t ERR_INTERNAL = 4;  // a slot-accounting invariant failed (never expected)
 
 // outcome of the top-Cap ranking of one table
@@ -57,7 +65,10 @@ struct DTable {
     int32_t vec;           // 1: 16-byte vector path, 0: scalar path
     int32_t bags_per_block;
     int32_t copy_unit;     // 16, 4 or 2 bytes
-    int32_t pad[3];
+    // wave-per-bag pooled kernel (0 in wlw: not used for this table): each
+    // load instruction reads wr rows of 64 / wr lanes x wlw bytes; a row is
+    // wnch such chunks
+    int32_t wlw, wr, wnch;
 };
 
 // Mutable per-table state and counters, resident in the workspace.
@@ -91,7 +102,7 @@ struct DGlobal {
     int64_t *tstart;          // [T+1] first index of each table in the last forward
     int64_t *pstart;          // [T+1] first prefetch id of each table in this placement
     int32_t *src;             // [max_indices] per access: slot (>= 0) or -(miss + 1)
-    int32_t *inv;             // [max_indices] per access: rank of its row in U
+    uint64_t *raddr;          // [max_indices] per access: device address of its row (slot or staging)
     int32_t *U;               // [max_indices] sorted distinct rows, table t at tstart[t]
     int32_t *slotU;           // [max_indices] per distinct row: slot or -(miss + 1)
     int32_t *M;               // [max_indices] missed rows, table t at tstart[t]
@@ -137,6 +148,7 @@ struct PlcParams {
 // a wave that shuffles between loads would wait for every load in flight.
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef int i32x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 #define RECMG_GLOBAL(T, p) (*(const __attribute__((address_space(1))) T *)(p))
 
 __device__ __forceinline__ uint4 gload16(const void *p) {

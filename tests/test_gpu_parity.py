@@ -81,6 +81,40 @@ def test_configs_scaled(cid, scale, bags, tables):
     _parity(w, label=f"c{cid}-scaled")
 
 
+# Row sizes that pick each pooled-kernel shape: 64 and 128 bytes (4 or 2 rows
+# per load instruction), 256 / 512 / 1024 bytes (one row per instruction, 4, 8
+# or 16 bytes per lane), 2048 bytes (two chunks per row), and sizes the
+# wave-per-bag kernel does not take (the group-per-bag kernel, vector and
+# scalar forms).
+POOL_DIMS = {"f32": [16, 32, 64, 128, 256, 512, 24, 7],
+             "f16": [32, 64, 128, 256, 512, 1024, 40, 5],
+             "bf16": [32, 64, 128, 256, 512, 1024, 40, 5]}
+
+
+def _kinds_workload(dtypes, seed, policy):
+    """Tables of every pooled-kernel shape (interleaved dtypes when several),
+    ragged bags: empty, single-row, shorter and longer than one block of
+    loads, and long geometric tails."""
+    g = np.random.default_rng(seed)
+    tabs = []
+    pools = [("poisson", 6.0, 0, 200), ("geometric", 45.0), ("poisson", 70.0, 1, 200), ("onehot",)]
+    for k in range(max(len(POOL_DIMS[d]) for d in dtypes)):
+        for d in dtypes:
+            dims = POOL_DIMS[d]
+            if k < len(dims):
+                rows = int(g.integers(500, 4000))
+                tabs.append(tg.Table(rows, dims[k], d, int(rows * g.uniform(0.02, 0.3)),
+                                     float(g.uniform(0.8, 1.3)), pools[(k + len(tabs)) % len(pools)]))
+    return tg.Workload(900 + seed, f"kinds{seed}", tabs, batches=4, bags=37, policy=policy,
+                       prefetch=("mix", 0.7))
+
+
+@pytest.mark.parametrize("dtypes,seed,policy", [(("f32",), 1, "lru"), (("f16",), 2, "priority"),
+                                                (("bf16",), 3, "lru"), (("bf16", "f32", "f16"), 4, "priority")])
+def test_pool_kernel_shapes(dtypes, seed, policy):
+    _parity(_kinds_workload(dtypes, seed, policy), label=f"kinds-{'-'.join(dtypes)}")
+
+
 def test_config4_no_prefetch_scaled():
     w = tg.scaled_config(4, row_scale=0.0005, batches=6, bags=512, max_tables=2, prefetch=("none",))
     _parity(w, label="c4-noprefetch")
