@@ -165,7 +165,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->tstart = take(8 * (T + 1));
     L->pstart = take(8 * (T + 1));
     L->src = take(4 * mi);
-    L->raddr = take(8 * (mi + kWaveRows));  // a block of row addresses may be read past the end
+    L->raddr = take(8 * (mi + kRaddrPad));  // blocks of row addresses are read past the end
     L->U = take(4 * mi);
     L->slotU = take(4 * mi);
     L->M = take(4 * mi);

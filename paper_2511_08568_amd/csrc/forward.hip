@@ -319,14 +319,17 @@ __global__ void __launch_bounds__(kBlock) k_pool(DGlobal g, const int64_t *__res
 
 // ------------------------------------------------- wave-per-bag pooled sum
 //
-// One wave sums one bag.  Every lookup of the bag reads the same row in all
-// lanes, so the row addresses (written per index by k_fwd_src) are
-// wave-uniform: they arrive through scalar loads, and each lane only adds its
-// LW-byte slice -- no per-lookup address arithmetic in vector registers.  For
-// short rows (R > 1) the wave splits into R groups of 64 / R lanes and group
-// h takes the lookups p with p mod R = h.  Lookup p still goes to partial sum
-// p mod 4 and the four are combined as (S0 + S1) + (S2 + S3), the same fixed
-// order as the group-per-bag kernel.
+// One wave sums kWaveBags consecutive bags, one bag at a time.  Each lane
+// adds its LW-byte slice of every row; row addresses come from the per-index
+// array written by k_fwd_src, so the kernel does no slot or staging lookups.
+//   R == 1 (rows of 1024 bytes or whole multiples): all lanes read the same
+//     row, so its address is wave-uniform and comes in through scalar loads.
+//   R > 1 (shorter rows): the wave splits into R groups of 64 / R lanes that
+//     read R different rows per load instruction, group h taking the lookups
+//     p with p mod R = h.  Each lane holds one address of a window of 64
+//     lookups; a ds_bpermute hands every group its row's address.
+// Either way lookup p goes to partial sum p mod 4 and the four are combined
+// as (S0 + S1) + (S2 + S3): a fixed order per bag, whichever tier served a row.
 
 template <int LW>
 struct WVec;
@@ -354,6 +357,19 @@ struct WVec<16> {
     }
 };
 
+// acc + the fp16 value in the low / high half of w: one mixed-precision FMA
+// (x * 1 + acc) converts exactly and rounds once, like convert-then-add
+__device__ __forceinline__ float add_f16_lo(float acc, uint32_t w) {
+    float r;
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel_hi:[1,0,0]" : "=v"(r) : "v"(w), "v"(acc));
+    return r;
+}
+__device__ __forceinline__ float add_f16_hi(float acc, uint32_t w) {
+    float r;
+    asm("v_fma_mix_f32 %0, %1, 1.0, %2 op_sel:[1,0,0] op_sel_hi:[1,0,0]" : "=v"(r) : "v"(w), "v"(acc));
+    return r;
+}
+
 template <int DT, int LW>
 __device__ __forceinline__ void wadd(float *acc, const typename WVec<LW>::V v) {
     uint32_t w[LW / 4];
@@ -366,8 +382,8 @@ __device__ __forceinline__ void wadd(float *acc, const typename WVec<LW>::V v) {
             acc[2 * k] += __builtin_bit_cast(float, w[k] << 16);
             acc[2 * k + 1] += __builtin_bit_cast(float, w[k] & 0xffff0000u);
         } else {
-            acc[2 * k] += f16_to_f32(w[k] & 0xffffu);
-            acc[2 * k + 1] += f16_to_f32(w[k] >> 16);
+            acc[2 * k] = add_f16_lo(acc[2 * k], w[k]);
+            acc[2 * k + 1] = add_f16_hi(acc[2 * k + 1], w[k]);
         }
     }
 }
@@ -379,24 +395,6 @@ __device__ __forceinline__ V wload(uint64_t base, uint32_t off) {
     return *(const __attribute__((address_space(1))) V *)((gchar *)base + off);
 }
 
-// Address for group h among the R uniform addresses q[0 .. R), of which the
-// first m are lookups of the bag (m >= 1); a group past the bag's end takes
-// q[0] (loaded, never added).
-template <int R>
-__device__ __forceinline__ uint64_t wpick(const uint64_t *q, int h, int m) {
-    uint64_t x = q[0];
-#pragma unroll
-    for (int k = 1; k < R; ++k) {
-        // the empty asm pins q[k] as a scalar value, so the per-lane select
-        // is not turned into a load through a selected pointer (which would
-        // move the address block out of registers)
-        uint64_t y = q[k];
-        asm("" : "+s"(y));
-        x = (h == k && k < m) ? y : x;
-    }
-    return x;
-}
-
 // The lane offset is passed through an empty asm in every block of loads so
 // that its zero extension is visible where the loads are selected: a uniform
 // 64-bit base plus a 32-bit lane offset then becomes the scalar-base form of
@@ -406,131 +404,213 @@ __device__ __forceinline__ uint32_t opaque(uint32_t x) {
     return x;
 }
 
-
-// Wave-uniform row addresses of one block of UR lookups starting at index i.
-// A block may run past the bag (and past the batch: the address array has
-// kWaveRows entries of padding); such entries are never dereferenced.
-template <int UR>
-__device__ __forceinline__ void wblock_addrs(uint64_t *nx, const uint64_t *__restrict__ raddr, int64_t i) {
+// Combine the NA partial sums of each of the R groups in the order
+// (S0 + S1) + (S2 + S3) and store the bag's NE floats of this lane (group 0).
+template <int NE, int R, int NA>
+__device__ __forceinline__ void wstore(float (&acc)[NA][NE], int h, float *o) {
+    float r[NE];
 #pragma unroll
-    for (int k = 0; k < UR; ++k) nx[k] = raddr[i + k];
+    for (int x = 0; x < NE; ++x) {
+        if constexpr (R == 1) {
+            r[x] = (acc[0][x] + acc[1][x]) + (acc[2][x] + acc[3][x]);
+        } else if constexpr (R == 2) {
+            // group 0 holds S0, S2 and group 1 holds S1, S3
+            const float o0 = __shfl_xor(acc[0][x], 32), o1 = __shfl_xor(acc[1][x], 32);
+            r[x] = (acc[0][x] + o0) + (acc[1][x] + o1);
+        } else {
+            // group h holds S_h
+            const float s01 = acc[0][x] + __shfl_xor(acc[0][x], 16);
+            r[x] = s01 + __shfl_xor(s01, 32);
+        }
+    }
+    if (h != 0) return;
+    // a table's output block starts at B * (sum of the earlier dims) floats,
+    // so vector stores need a run-time alignment check
+    const uintptr_t oa = reinterpret_cast<uintptr_t>(o);
+    if (NE % 4 == 0 && (oa & 15) == 0) {
+#pragma unroll
+        for (int x = 0; x + 3 < NE; x += 4)
+            *reinterpret_cast<float4 *>(o + x) = make_float4(r[x], r[x + 1], r[x + 2], r[x + 3]);
+    } else if (NE == 2 && (oa & 7) == 0) {
+        *reinterpret_cast<float2 *>(o) = make_float2(r[0], r[NE - 1]);
+    } else {
+#pragma unroll
+        for (int x = 0; x < NE; ++x) o[x] = r[x];
+    }
 }
 
-// One wave sums BPW consecutive bags.  Software pipeline: the scalar loads of
-// the next block's row addresses (in this bag or the next) are in flight while
-// the current block's row loads are; UR = U * R lookups per block.
-template <int DT, int LW, int R>
-__device__ __forceinline__ void pool_wave(const uint64_t *__restrict__ raddr, const int64_t *__restrict__ ob, int j0,
-                                          int nbags, int wnch, int D, float *__restrict__ obase) {
-    using V = typename WVec<LW>::V;
-    constexpr int EB = Elem<DT>::bytes, NE = LW / EB, GL = 64 / R, NA = 4 / R;
-    constexpr int UR = kWaveRows;                  // lookups per block (row addresses held in SGPRs)
-    constexpr int U0 = UR / R;                        // load instructions per block
-    constexpr int U = U0 * LW > 128 ? 128 / LW : U0;  // at most 8 KB of rows in flight per wave
-    static_assert(U % NA == 0, "partial-sum slot must not depend on the block start");
-    constexpr int BPW = kWaveBags;
-    const int lane = threadIdx.x & 63, h = lane / GL, gl = lane % GL;
-    int64_t offs[BPW + 1];
+// the bag offsets of the wave's bags, clamped to the last one present
+template <int BPW>
+__device__ __forceinline__ void wave_offsets(int64_t (&offs)[BPW + 1], const int64_t *__restrict__ ob, int nbags) {
 #pragma unroll
-    for (int b = 0; b <= BPW; ++b) offs[b] = ob[j0 + (b < nbags ? b : nbags)];
+    for (int b = 0; b <= BPW; ++b) offs[b] = ob[b < nbags ? b : nbags];
+}
+
+// R == 1.  Software pipeline: the scalar loads of the next block's U row
+// addresses (this bag's, else the next non-empty bag's first) are in flight
+// while the current block's row loads are.  A block may run past the bag and
+// past the batch (the address array has kRaddrPad entries of padding); such
+// addresses are never dereferenced.
+template <int DT, int LW>
+__device__ __forceinline__ void pool_wave_s(const uint64_t *__restrict__ raddr, const int64_t *__restrict__ ob,
+                                            int nbags, int wnch, int D, float *__restrict__ obase) {
+    using V = typename WVec<LW>::V;
+    constexpr int EB = Elem<DT>::bytes, NE = LW / EB;
+    constexpr int U = 8;  // rows in flight per wave (8 KB)
+    constexpr int BPW = kWaveBags;
+    const int lane = threadIdx.x & 63;
+    int64_t offs[BPW + 1];
+    wave_offsets<BPW>(offs, ob, nbags);
     for (int ch = 0; ch < wnch; ++ch) {
-        const uint32_t eoff = (uint32_t)((ch * GL + gl) * LW);
-        uint64_t nx[U * R];
+        const uint32_t eoff = (uint32_t)((ch * 64 + lane) * LW);
+        uint64_t nx[U];
         // first block of the first non-empty bag after bag b (all indices
         // static, so offs and nx stay in scalar registers)
-        auto next_bag_addrs = [&](uint64_t *dst, int b) {
+        auto next_bag_addrs = [&](int b) {
             bool found = false;
 #pragma unroll
             for (int b2 = 0; b2 < BPW; ++b2)
                 if (b2 > b && !found && b2 < nbags && offs[b2 + 1] > offs[b2]) {
-                    wblock_addrs<U * R>(dst, raddr, offs[b2]);
+#pragma unroll
+                    for (int k = 0; k < U; ++k) nx[k] = raddr[offs[b2] + k];
                     found = true;
                 }
         };
-        next_bag_addrs(nx, -1);
+        next_bag_addrs(-1);
 #pragma unroll
         for (int b = 0; b < BPW; ++b) {
             if (b >= nbags) continue;
             const int64_t a = offs[b];
             const int n = (int)(offs[b + 1] - a);
-            float acc[NA][NE];
+            float acc[4][NE];
 #pragma unroll
-            for (int k = 0; k < NA; ++k)
+            for (int k = 0; k < 4; ++k)
 #pragma unroll
                 for (int x = 0; x < NE; ++x) acc[k][x] = 0.f;
             int p = 0;
-            // full blocks: straight-line loads from the scalar-base form
-            for (; p + U * R <= n; p += U * R) {
+            for (; p + U <= n; p += U) {
                 V v[U];
                 const uint32_t eo = opaque(eoff);
 #pragma unroll
-                for (int u = 0; u < U; ++u) v[u] = wload<V>(wpick<R>(nx + u * R, h, R), eo);
-                // next block: this bag's, else the next non-empty bag's first.
-                // The barrier keeps these scalar loads after the row loads
-                // above, so one block of addresses is live at a time.
+                for (int u = 0; u < U; ++u) v[u] = wload<V>(nx[u], eo);
+                // the barrier keeps the next block's scalar loads after the
+                // row loads above, so one block of addresses is live at a time
                 asm volatile("" ::: "memory");
-                if (p + U * R < n) wblock_addrs<U * R>(nx, raddr, a + p + U * R);
-                else next_bag_addrs(nx, b);
+                if (p + U < n) {
 #pragma unroll
-                for (int u = 0; u < U; ++u) wadd<DT, LW>(acc[u % NA], v[u]);
+                    for (int k = 0; k < U; ++k) nx[k] = raddr[a + p + U + k];
+                } else {
+                    next_bag_addrs(b);
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u) wadd<DT, LW>(acc[u & 3], v[u]);
             }
             if (p < n) {
-                // partial block, in quads of load instructions; with one row
-                // per instruction a lookup past the bag's end re-reads the
-                // quad's first row and is not added
+                // partial block, in quads of loads; a lookup past the bag's end
+                // re-reads the quad's first row and is not added
                 V v[U];
 #pragma unroll
                 for (int q = 0; q < U; q += 4)
-                    if (p + q * R < n) {
+                    if (p + q < n) {
                         const uint32_t eo = opaque(eoff);
 #pragma unroll
-                        for (int u = q; u < q + 4; ++u) {
-                            if constexpr (R == 1) {
-                                v[u] = wload<V>(p + u < n ? nx[u] : nx[q], eo);
-                            } else if (p + u * R + h < n) {
-                                // lanes of a group past the bag's end load nothing
-                                v[u] = wload<V>(wpick<R>(nx + u * R, h, R), eo);
-                            }
-                        }
+                        for (int u = q; u < q + 4; ++u) v[u] = wload<V>(p + u < n ? nx[u] : nx[q], eo);
                     }
                 asm volatile("" ::: "memory");
-                next_bag_addrs(nx, b);
+                next_bag_addrs(b);
 #pragma unroll
                 for (int u = 0; u < U; ++u)
-                    if (p + u * R + h < n) wadd<DT, LW>(acc[u % NA], v[u]);
+                    if (p + u < n) wadd<DT, LW>(acc[u & 3], v[u]);
             }
-            float r[NE];
-#pragma unroll
-            for (int x = 0; x < NE; ++x) {
-                if constexpr (R == 1) {
-                    r[x] = (acc[0][x] + acc[1][x]) + (acc[2][x] + acc[3][x]);
-                } else if constexpr (R == 2) {
-                    // group 0 holds S0, S2 and group 1 holds S1, S3
-                    const float o0 = __shfl_xor(acc[0][x], 32), o1 = __shfl_xor(acc[1][x], 32);
-                    r[x] = (acc[0][x] + o0) + (acc[1][x] + o1);
-                } else {
-                    // group h holds S_h
-                    const float s01 = acc[0][x] + __shfl_xor(acc[0][x], 16);
-                    r[x] = s01 + __shfl_xor(s01, 32);
-                }
-            }
-            if (h == 0) {
-                // the output block of a table starts at B * (sum of the earlier
-                // dims) floats, so vector stores need a run-time alignment check
-                float *o = obase + (int64_t)(j0 + b) * D + (ch * GL + gl) * NE;
-                const uintptr_t oa = reinterpret_cast<uintptr_t>(o);
-                if (NE % 4 == 0 && (oa & 15) == 0) {
-#pragma unroll
-                    for (int x = 0; x + 3 < NE; x += 4)
-                        *reinterpret_cast<float4 *>(o + x) = make_float4(r[x], r[x + 1], r[x + 2], r[x + 3]);
-                } else if (NE == 2 && (oa & 7) == 0) {
-                    *reinterpret_cast<float2 *>(o) = make_float2(r[0], r[NE - 1]);
-                } else {
-#pragma unroll
-                    for (int x = 0; x < NE; ++x) o[x] = r[x];
-                }
-            }
+            wstore<NE, 1, 4>(acc, 0, obase + (int64_t)b * D + ch * 64 * NE + lane * NE);
         }
+    }
+}
+
+// R > 1.  Lane i holds the address of lookup w + i of a window of 64 lookups
+// of the bag starting at w (a whole bag when it has at most 64); the next
+// window (this bag's, else the next non-empty bag's first) is loaded while
+// the current one's rows are read.  Window entries past the bag, and past the
+// batch (kRaddrPad entries of padding), are never dereferenced.
+template <int DT, int LW, int R>
+__device__ __forceinline__ void pool_wave_v(const uint64_t *__restrict__ raddr, const int64_t *__restrict__ ob,
+                                            int nbags, int D, float *__restrict__ obase) {
+    using V = typename WVec<LW>::V;
+    constexpr int EB = Elem<DT>::bytes, NE = LW / EB, GL = 64 / R, NA = 4 / R;
+    constexpr int U0 = 128 / LW;                 // load instructions per sub-block (8 KB in flight)
+    constexpr int U = U0 * R > 64 ? 64 / R : U0;  // a sub-block stays inside its window
+    constexpr int UR = U * R;                    // lookups per sub-block, divides 64
+    static_assert(64 % UR == 0 && U % NA == 0, "sub-blocks tile a window; slot = u mod NA");
+    constexpr int BPW = kWaveBags;
+    const int lane = threadIdx.x & 63, h = lane / GL, gl = lane % GL;
+    const uint32_t eoff = (uint32_t)(gl * LW);
+    int64_t offs[BPW + 1];
+    wave_offsets<BPW>(offs, ob, nbags);
+    uint64_t wnext = 0;
+    auto next_bag_window = [&](int b) {
+        bool found = false;
+#pragma unroll
+        for (int b2 = 0; b2 < BPW; ++b2)
+            if (b2 > b && !found && b2 < nbags && offs[b2 + 1] > offs[b2]) {
+                wnext = RECMG_GLOBAL(uint64_t, raddr + offs[b2] + lane);
+                found = true;
+            }
+    };
+    next_bag_window(-1);
+#pragma unroll
+    for (int b = 0; b < BPW; ++b) {
+        if (b >= nbags) continue;
+        const int64_t a = offs[b];
+        const int n = (int)(offs[b + 1] - a);
+        float acc[NA][NE];
+#pragma unroll
+        for (int k = 0; k < NA; ++k)
+#pragma unroll
+            for (int x = 0; x < NE; ++x) acc[k][x] = 0.f;
+        for (int p = 0; p < n; p += 64) {
+            const uint64_t wcur = wnext;
+            const int m = n - p < 64 ? n - p : 64;  // lookups in this window
+            const int wlo = (int)(uint32_t)wcur, whi = (int)(uint32_t)(wcur >> 32);
+            // one sub-block of U load instructions; FULL: all UR lookups are
+            // in the bag (no masking).  The two forms are separate code paths
+            // so that no loaded value has to be merged (and waited for) early.
+            auto sub_block = [&](int s, auto full_tag) {
+                constexpr bool FULL = decltype(full_tag)::value;
+                V v[U];
+                const int bidx = (s + h) * 4;  // bpermute byte index of lookup s + h
+                if constexpr (FULL) {
+                    uint32_t lo[U], hi[U];
+#pragma unroll
+                    for (int u = 0; u < U; ++u) {
+                        lo[u] = (uint32_t)__builtin_amdgcn_ds_bpermute(bidx + u * R * 4, wlo);
+                        hi[u] = (uint32_t)__builtin_amdgcn_ds_bpermute(bidx + u * R * 4, whi);
+                    }
+#pragma unroll
+                    for (int u = 0; u < U; ++u) v[u] = wload<V>(((uint64_t)hi[u] << 32) | lo[u], eoff);
+                } else {
+#pragma unroll
+                    for (int u = 0; u < U; ++u)
+                        if (s + u * R < m) {
+                            const uint32_t lo = (uint32_t)__builtin_amdgcn_ds_bpermute(bidx + u * R * 4, wlo);
+                            const uint32_t hi = (uint32_t)__builtin_amdgcn_ds_bpermute(bidx + u * R * 4, whi);
+                            if (s + u * R + h < m) v[u] = wload<V>(((uint64_t)hi << 32) | lo, eoff);
+                        }
+                }
+                if (s == 0) {
+                    // the next window, issued after this sub-block's row loads
+                    asm volatile("" ::: "memory");
+                    if (p + 64 < n) wnext = RECMG_GLOBAL(uint64_t, raddr + a + p + 64 + lane);
+                    else next_bag_window(b);
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (FULL || s + u * R + h < m) wadd<DT, LW>(acc[u % NA], v[u]);
+            };
+            int s = 0;
+            for (; s + UR <= m; s += UR) sub_block(s, std::true_type{});
+            if (s < m) sub_block(s, std::false_type{});
+        }
+        wstore<NE, R, NA>(acc, h, obase + (int64_t)b * D + gl * NE);
     }
 }
 
@@ -545,13 +625,16 @@ __global__ void __launch_bounds__(kBlock) k_pool_w(DGlobal g, const int64_t *__r
     const int k = find_seg32(bstart, nt, lb);
     const int t = btab[k];
     const DTable &tb = g.tabs[t];
-    const int D = tb.dim, wnch = tb.wnch;
+    const int D = tb.dim;
     const int64_t ooff = (int64_t)B * tb.out_elem_off;
     const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int j0 = ((lb - bstart[k]) * (kBlock / 64) + wave) * kWaveBags;
     if (j0 >= B) return;
     const int nbags = B - j0 < kWaveBags ? B - j0 : kWaveBags;
-    pool_wave<DT, LW, R>(raddr, offsets + (int64_t)t * B, j0, nbags, wnch, D, out + ooff);
+    const int64_t *ob = offsets + (int64_t)t * B + j0;
+    float *ob_out = out + ooff + (int64_t)j0 * D;
+    if constexpr (R == 1) pool_wave_s<DT, LW>(raddr, ob, nbags, tb.wnch, D, ob_out);
+    else pool_wave_v<DT, LW, R>(raddr, ob, nbags, D, ob_out);
 }
 
 __global__ void k_fwd_finalize(DGlobal g) {

@@ -30,10 +30,7 @@ constexpr int32_t ERR_OFFSETS = 2;
 #define RECMG_WPOOL_BAGS 2
 #endif
 constexpr int kWaveBags = RECMG_WPOOL_BAGS;  // consecutive bags per wave in the wave-per-bag pooled kernel
-#ifndef RECMG_WPOOL_ROWS
-#define RECMG_WPOOL_ROWS 8
-#endif
-constexpr int kWaveRows = RECMG_WPOOL_ROWS;  // lookups per block of loads in that kernel (power of two <= 16)
+constexpr int kRaddrPad = 64;  // entries past the batch in the per-index row-address array (read, never used)
 constexpr int32_t ERR_INTERNAL = 4;  // a slot-accounting invariant failed (never expected)
 
 // outcome of the top-Cap ranking of one table
