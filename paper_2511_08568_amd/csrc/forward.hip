@@ -527,6 +527,10 @@ __device__ __forceinline__ void pool_wave_s(const uint64_t *__restrict__ raddr, 
     }
 }
 
+#ifndef RECMG_WPOOL_KB
+#define RECMG_WPOOL_KB 8
+#endif
+
 // R > 1.  Lane i holds the address of lookup w + i of a window of 64 lookups
 // of the bag starting at w (a whole bag when it has at most 64); the next
 // window (this bag's, else the next non-empty bag's first) is loaded while
@@ -537,7 +541,7 @@ __device__ __forceinline__ void pool_wave_v(const uint64_t *__restrict__ raddr, 
                                             int nbags, int D, float *__restrict__ obase) {
     using V = typename WVec<LW>::V;
     constexpr int EB = Elem<DT>::bytes, NE = LW / EB, GL = 64 / R, NA = 4 / R;
-    constexpr int U0 = 128 / LW;                 // load instructions per sub-block (8 KB in flight)
+    constexpr int U0 = RECMG_WPOOL_KB * 16 / LW;  // load instructions per sub-block (KB of rows in flight)
     constexpr int U = U0 * R > 64 ? 64 / R : U0;  // a sub-block stays inside its window
     constexpr int UR = U * R;                    // lookups per sub-block, divides 64
     static_assert(64 % UR == 0 && U % NA == 0, "sub-blocks tile a window; slot = u mod NA");
@@ -614,8 +618,13 @@ __device__ __forceinline__ void pool_wave_v(const uint64_t *__restrict__ raddr, 
     }
 }
 
+#ifndef RECMG_WPOOL_OCC
+#define RECMG_WPOOL_OCC 1
+#endif
+
+// RECMG_WPOOL_OCC: waves per SIMD the register allocation must allow
 template <int DT, int LW, int R>
-__global__ void __launch_bounds__(kBlock) k_pool_w(DGlobal g, const int64_t *__restrict__ offsets,
+__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RECMG_WPOOL_OCC))) k_pool_w(DGlobal g, const int64_t *__restrict__ offsets,
                                                    const uint64_t *__restrict__ raddr, int32_t B,
                                                    float *__restrict__ out, const int32_t *__restrict__ bstart,
                                                    const int32_t *__restrict__ btab, int32_t nt, int32_t boff,

@@ -6,9 +6,10 @@
 // member gets a score (aging, touch, prefetch, below), and the cache keeps the
 // min(Cap, |K|) largest keys (score, row).  Instead of one victim scan per
 // insertion, one radix select per placement finds the threshold key: 11-bit
-// digits from the top, each pass one kernel whose last block picks the digit
-// holding the Cap-th largest key.  Keys are distinct (rows are distinct), so
-// exactly min(Cap, |K|) keys are >= the threshold.
+// digits from the top, each pass a histogram kernel and a one-block-per-table
+// kernel that picks the digit holding the Cap-th largest key.  Keys are
+// distinct (rows are distinct), so exactly min(Cap, |K|) keys are >= the
+// threshold.
 //
 // Scores:  LRU_BATCH  touched by the last batch: lru_touch; prefetched:
 //                     max(score, pscore) with pscore = lru_touch + 1
@@ -17,8 +18,9 @@
 //                     max(score, ES); a touched resident loses its prefetch flag.
 //
 // Kernels on the stream: k_plc_prep, [k_plc_bits], dedup of P with the
-// EMIT_PREFETCH visitor (dedup.hip), k_plc_update (scores + select pass 0),
-// k_plc_select (passes 1..), k_plc_evict, k_map_clear / k_map_refill (rebuild
+// EMIT_PREFETCH visitor (dedup.hip), k_plc_update (scores + histogram of
+// pass 0), k_plc_pick, { k_plc_select (histogram of pass 1..), k_plc_pick }*,
+// k_plc_evict, k_map_clear / k_map_refill (rebuild
 // when deleted entries pile up), k_plc_admit, k_plc_fill, k_plc_finalize.
 #include "launch.h"
 
@@ -38,7 +40,6 @@ __global__ void k_plc_prep(DGlobal g, const int64_t *__restrict__ poff, int64_t 
             st.pcount = 0;
             st.npcount = 0;
             st.popped = 0;
-            st.done = 0;
             st.p_res = 0;
             st.evicted = 0;
             st.adm_miss = 0;
@@ -140,26 +141,47 @@ __device__ __forceinline__ int pass_width(const PlcParams &p, int pass) {
     return pass == 0 ? p.total_bits - kRadixBits * (p.passes - 1) : kRadixBits;
 }
 
-// Merge the block's histogram; the last block of the table picks the digit.
-__device__ void select_finish(const DGlobal &g, int t, int pass, const PlcParams &p, int need0, int *s_hist,
-                              int *tmp) {
-    TState &st = g.st[t];
+// Histogram increment, aggregated over the wave for the first active lane's
+// bin: the keys of one table bunch up in few digits (LRU scores are batch
+// numbers), and 64 lanes adding 1 to one LDS word would serialise.
+__device__ __forceinline__ void hist_add(int *h, bool active, uint32_t bin) {
+    const uint64_t act = __ballot(active);
+    if (act == 0) return;
+    const int lead = __ffsll((unsigned long long)act) - 1;
+    const uint32_t b0 = (uint32_t)__shfl((int)bin, lead);
+    const uint64_t same = __ballot(active && bin == b0);
+    if ((int)(threadIdx.x & 63) == lead) atomicAdd(&h[b0], __popcll(same));
+    if (active && bin != b0) atomicAdd(&h[bin], 1);
+}
+
+// Merge the block's histogram into the table's global one (non-zero bins).
+// No fence and no "last block" here: on this GPU an agent-scope fence writes
+// back the XCD's whole L2, and a histogram kernel has many blocks; the digit
+// is picked by k_plc_pick after the kernel boundary instead.
+__device__ __forceinline__ void hist_merge(const DGlobal &g, int t, const int *s_hist) {
     int *gh = g.hist + (int64_t)t * kRadix;
     for (int b = threadIdx.x; b < kRadix; b += blockDim.x)
         if (s_hist[b]) atomicAdd(&gh[b], s_hist[b]);
-    __threadfence();
-    __syncthreads();
-    __shared__ int s_last;
-    if (threadIdx.x == 0) s_last = atomicAdd(&st.done, 1u) == gridDim.x - 1;
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
+}
+
+// One block per table: the digit of this pass.  Bins are taken from the top
+// until `need` keys are covered; the bin reached extends the threshold prefix
+// and the keys still needed inside it carry over to the next pass.  Clears the
+// histogram for the next pass.
+__global__ void __launch_bounds__(kBlock) k_plc_pick(DGlobal g, PlcParams p, int pass) {
+    if (*g.err) return;
+    __shared__ int s_hist[kRadix];
+    __shared__ int tmp[16];
+    const int t = blockIdx.x;
+    TState &st = g.st[t];
+    if (st.sel_mode != SEL_SELECT) return;  // uniform over the block
+    int *gh = g.hist + (int64_t)t * kRadix;
     for (int b = threadIdx.x; b < kRadix; b += blockDim.x) {
-        s_hist[b] = __hip_atomic_load(&gh[b], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_hist[b] = gh[b];
         gh[b] = 0;
     }
     __syncthreads();
-    const int need = pass == 0 ? need0 : st.need;
+    const int need = pass == 0 ? table_counts(g.tabs[t], st, p).keep : st.need;
     // thread k owns bin group 255-k, so an inclusive scan gives suffix sums
     constexpr int per = kRadix / kBlock;
     const int grp = kBlock - 1 - (int)threadIdx.x;
@@ -179,14 +201,12 @@ __device__ void select_finish(const DGlobal &g, int t, int pass, const PlcParams
             cum += s_hist[b];
         }
     }
-    if (threadIdx.x == 0) st.done = 0;
 }
 
 // Scores of every candidate (written back) and the first select pass.
 __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
     if (*g.err) return;
     __shared__ int s_hist[kRadix];
-    __shared__ int tmp[16];
     const int t = blockIdx.y;
     const DTable &tb = g.tabs[t];
     TState &st = g.st[t];
@@ -204,11 +224,13 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
     const uint32_t dmask = (1u << pass_width(p, 0)) - 1u;
     const int64_t items = (int64_t)c.cap + c.nm + c.nnp;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < items; k += stride) {
-        int32_t row, s;
-        if (k < c.cap) {
+    // every lane runs the same number of iterations (hist_add is wave-wide)
+    const int64_t items_r = (items + 63) & ~(int64_t)63;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < items_r; k += stride) {
+        int32_t row = -1, s = 0;
+        if (k >= items) {
+        } else if (k < c.cap) {
             row = tb.slot_row[k];
-            if (row < 0) continue;
             s = tb.slot_score[k];
             uint32_t f = tb.slot_flags[k];
             const int cb = tb.slot_cbit[k];
@@ -219,8 +241,10 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
                 s = p.prio ? cb + p.es : p.lru_touch;
             }
             if ((f & F_INP) && s < p.pscore) s = p.pscore;
-            tb.slot_score[k] = s;
-            tb.slot_flags[k] = f & ~F_INP;
+            if (row >= 0) {
+                tb.slot_score[k] = s;
+                tb.slot_flags[k] = f & ~F_INP;
+            }
         } else if (k < (int64_t)c.cap + c.nm) {
             const int64_t m = ts + (k - c.cap);
             row = g.M[m];
@@ -232,10 +256,10 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
             row = g.NP[ps + (k - c.cap - c.nm)];
             s = p.pscore;
         }
-        if (sel) atomicAdd(&s_hist[(uint32_t)(make_key(s, row, p.rowbits) >> shift) & dmask], 1);
+        if (sel) hist_add(s_hist, row >= 0, (uint32_t)(make_key(s, row < 0 ? 0 : row, p.rowbits) >> shift) & dmask);
     }
     __syncthreads();
-    if (sel) select_finish(g, t, 0, p, c.keep, s_hist, tmp);
+    if (sel) hist_merge(g, t, s_hist);
 }
 
 __device__ __forceinline__ bool item_key(const DGlobal &g, const DTable &tb, const Counts &c, const PlcParams &p,
@@ -260,7 +284,6 @@ __device__ __forceinline__ bool item_key(const DGlobal &g, const DTable &tb, con
 __global__ void __launch_bounds__(kBlock) k_plc_select(DGlobal g, PlcParams p, int pass) {
     if (*g.err) return;
     __shared__ int s_hist[kRadix];
-    __shared__ int tmp[16];
     const int t = blockIdx.y;
     const DTable &tb = g.tabs[t];
     TState &st = g.st[t];
@@ -273,14 +296,14 @@ __global__ void __launch_bounds__(kBlock) k_plc_select(DGlobal g, PlcParams p, i
     const uint64_t prefix = st.prefix;
     const int64_t items = (int64_t)c.cap + c.nm + c.nnp;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < items; k += stride) {
-        uint64_t key;
-        if (!item_key(g, tb, c, p, ts, ps, k, &key)) continue;
-        if ((key >> (shift + kRadixBits)) != prefix) continue;
-        atomicAdd(&s_hist[(uint32_t)(key >> shift) & (kRadix - 1)], 1);
+    const int64_t items_r = (items + 63) & ~(int64_t)63;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < items_r; k += stride) {
+        uint64_t key = 0;
+        const bool in = k < items && item_key(g, tb, c, p, ts, ps, k, &key) && (key >> (shift + kRadixBits)) == prefix;
+        hist_add(s_hist, in, (uint32_t)(key >> shift) & (kRadix - 1));
     }
     __syncthreads();
-    select_finish(g, t, pass, p, 0, s_hist, tmp);
+    hist_merge(g, t, s_hist);
 }
 
 __device__ __forceinline__ bool kept(int mode, uint64_t key, uint64_t thr) {
@@ -531,10 +554,18 @@ void launch_plc_classify(const DGlobal &g, int32_t last_stamp, int64_t np, hipSt
 }
 
 void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s) {
-    // few blocks per table: each block merges a 2048-bin histogram into global memory
-    const dim3 grid(grid_for(item_bound, kBlock * 32, 512), g.T);
+    // few blocks per table: each block merges its non-zero histogram bins
+    // into global memory
+#ifndef RECMG_RANK_IPT
+#define RECMG_RANK_IPT 32
+#endif
+    const dim3 grid(grid_for(item_bound, kBlock * RECMG_RANK_IPT, 512), g.T);
     k_plc_update<<<grid, kBlock, 0, s>>>(g, p);
-    for (int pass = 1; pass < p.passes; ++pass) k_plc_select<<<grid, kBlock, 0, s>>>(g, p, pass);
+    k_plc_pick<<<g.T, kBlock, 0, s>>>(g, p, 0);
+    for (int pass = 1; pass < p.passes; ++pass) {
+        k_plc_select<<<grid, kBlock, 0, s>>>(g, p, pass);
+        k_plc_pick<<<g.T, kBlock, 0, s>>>(g, p, pass);
+    }
 }
 
 void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,

@@ -27,7 +27,7 @@ constexpr uint32_t F_INP = 4u;   // named by the current placement's prefetch li
 constexpr int32_t ERR_RANGE = 1;
 constexpr int32_t ERR_OFFSETS = 2;
 #ifndef RECMG_WPOOL_BAGS
-#define RECMG_WPOOL_BAGS 2
+#define RECMG_WPOOL_BAGS 1
 #endif
 constexpr int kWaveBags = RECMG_WPOOL_BAGS;  // consecutive bags per wave in the wave-per-bag pooled kernel
 constexpr int kRaddrPad = 64;  // entries past the batch in the per-index row-address array (read, never used)
@@ -77,7 +77,7 @@ struct TState {
     int32_t n_res, free_top, popped, tomb;
     int32_t rebuild, sel_mode, need, plc_nm;  // plc_nm: misses the current placement ranks
     uint64_t prefix;  // radix-select prefix; the threshold key after the last pass
-    uint32_t done;    // blocks finished in the current select pass
+    uint32_t pad0;
     int32_t pad1;
     // accumulators of the call in flight
     int32_t hits, hits_pf, p_res, evicted, adm_miss, p_fill, p_drop, m_drop;
