@@ -164,9 +164,11 @@ def main():
                                  max_bags_per_table=w.bags, max_indices=max_idx, max_prefetch=max_pf, timing=True)
     log(f"cache ready: workspace {cache.workspace_bytes / 1e9:.2f} GB")
 
-    def step(b):
+    def step(b, marks=None):
         P, po = d_prefetch[b]
         cache.placement(P, po, d_bits[b])
+        if marks is not None:
+            marks[b].record(torch.cuda.current_stream())
         i, o = d_batches[b]
         cache.forward(i, o, w.bags, out=outs[b & 1])
 
@@ -179,12 +181,19 @@ def main():
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    # events before each placement and between it and its forward split the
+    # step into placement time and forward time (the forward's share includes
+    # waiting for the placement's prefetch fill on the side stream)
+    marks = {b: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for b in range(W, nb)}
     ev0.record(stream)
     for b in range(W, nb):
-        step(b)
+        marks[b][0].record(stream)
+        step(b, {b: marks[b][1]})
     ev1.record(stream)
     torch.cuda.synchronize()
     elapsed_ms = ev0.elapsed_time(ev1)
+    plc_ms = sum(marks[b][0].elapsed_time(marks[b][1]) for b in range(W, nb))
+    fwd_ms = sum(marks[b][1].elapsed_time(marks[b + 1][0] if b + 1 < nb else ev1) for b in range(W, nb))
     stages = cache.stage_times(reset=True)
     _, tot1 = cache.stats()
     log(f"timed {K} steps: {elapsed_ms:.3f} ms; stages {json.dumps({k: round(v[0], 3) for k, v in stages.items()})}")
@@ -221,7 +230,7 @@ def main():
         buf = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
         dbuf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         best = 0.0
-        for _ in range(5):
+        for _ in range(10):
             a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
             dbuf.copy_(buf, non_blocking=True)
@@ -267,6 +276,8 @@ def main():
             "logical_bytes_per_launch": logical_bytes / K,
             "logical_GBs": logical_bytes / K / pool_s / 1e9 if pool_s > 0 else 0.0,
         },
+        "split": {"placement_ms_per_step": plc_ms / K, "forward_ms_per_step": fwd_ms / K,
+                  "forward_only_lookups_per_s": lookups / (fwd_ms / 1e3) if fwd_ms > 0 else None},
         "ondemand_fetches_per_batch": delta["misses"] / K,
         "prefetch_fills_per_batch": delta["prefetch_fill"] / K,
         "host_link": {"bytes_per_batch": link_bytes / K, "achieved_GBs": link_gbs,
