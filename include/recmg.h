@@ -99,11 +99,11 @@ typedef struct {
     size_t host_staging_bytes;
     void *copy_stream;                  /* hipStream_t for STAGED copies; NULL = the
                                            compute stream */
-    int32_t timing;                     /* 1: record HIP events around every stage (see
-                                           recmg_stage_times); 0: none */
+    int32_t timing;                     /* initial timing level (see recmg_set_timing): 0 none,
+                                           1 the pooled kernel only, 2 every stage */
 } recmg_config_t;
 
-/* Stages timed when recmg_config_t.timing = 1. */
+/* Stages timed at timing level 2 (RECMG_STAGE_FWD_POOL from level 1 on). */
 typedef enum {
     RECMG_STAGE_FWD_DEDUP = 0,  /* offsets check, dedup + sort, map probe, inverse map */
     RECMG_STAGE_FWD_FETCH = 1,  /* on-demand miss fetch (zero-copy kernel or staged copy) */
@@ -189,8 +189,20 @@ int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_sta
 /* Device time per stage, summed over the calls since the last reset, in
  * milliseconds (ms[RECMG_NUM_STAGES]), and how many times each stage ran
  * (calls[RECMG_NUM_STAGES], may be NULL).  Synchronises.  reset != 0 clears
- * the sums afterwards.  All zero unless the handle was created with timing = 1. */
+ * the sums afterwards.  Only stages timed at the level in force when a call
+ * ran are counted (see recmg_set_timing). */
 int32_t recmg_stage_times(recmg_cache_t *c, double *ms, int64_t *calls, int32_t reset);
+
+/* Timing level for later calls:
+ *   0  none;
+ *   1  the pooled kernels only, by events their own dispatches record (no
+ *      command is added to the stream; the first pooled dispatch of a call
+ *      starts a little later, by a few microseconds);
+ *   2  every stage: an event pair per stage per call around the stage's
+ *      commands (two extra stream commands per stage, a few microseconds each).
+ * Returns RECMG_E_INVALID for another level.  Not thread-safe with calls in
+ * flight on another host thread (the handle is single-threaded anyway). */
+int32_t recmg_set_timing(recmg_cache_t *c, int32_t level);
 
 /* Waits for outstanding work and releases the handle (not the caller's
  * buffers).  NULL is accepted. */

@@ -18,6 +18,7 @@ from .binding import (  # noqa: F401
     recmg_embbag_forward,
     recmg_last_error,
     recmg_query_workspace,
+    recmg_set_timing,
     recmg_stage_times,
     recmg_stats,
     recmg_table_stats_t,

@@ -30,7 +30,7 @@ STAT_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand
                "resident", "prefetch_bytes")
 
 EXPORTED = ("recmg_query_workspace", "recmg_cache_init", "recmg_apply_placement", "recmg_embbag_forward",
-            "recmg_stats", "recmg_stage_times", "recmg_cache_destroy", "recmg_last_error")
+            "recmg_stats", "recmg_stage_times", "recmg_set_timing", "recmg_cache_destroy", "recmg_last_error")
 STAGES = ("fwd_dedup", "fwd_fetch", "fwd_pool", "plc_classify", "plc_rank", "plc_apply", "plc_fill", "host_link")
 
 
@@ -89,6 +89,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.recmg_stats.argtypes = [P, ctypes.POINTER(recmg_table_stats_t), ctypes.POINTER(recmg_table_stats_t), P,
                                 ctypes.c_int64, P]
     lib.recmg_stage_times.argtypes = [P, P, P, ctypes.c_int32]
+    lib.recmg_set_timing.argtypes = [P, ctypes.c_int32]
     lib.recmg_cache_destroy.argtypes = [P]
     for name in EXPORTED[:-1]:
         getattr(lib, name).restype = ctypes.c_int32
@@ -141,6 +142,10 @@ def recmg_stage_times(handle: int, ms: int, calls: int, reset: int) -> int:
     return int(load_library().recmg_stage_times(handle, ms or None, calls or None, int(reset)))
 
 
+def recmg_set_timing(handle: int, level: int) -> int:
+    return int(load_library().recmg_set_timing(handle, int(level)))
+
+
 def recmg_cache_destroy(handle: int) -> int:
     return int(load_library().recmg_cache_destroy(handle or None))
 
@@ -163,7 +168,7 @@ class TieredEmbeddingCache:
     def __init__(self, host_tables: Sequence, dtypes: Sequence[str], cache_rows: Sequence[int], *,
                  policy: str = "lru", eviction_speed: int = 4, miss_mode: str = "zero_copy",
                  max_bags_per_table: int, max_indices: int, max_prefetch: int, validate: bool = False,
-                 timing: bool = False, overlap: bool = True, workspace=None, device: int = 0):
+                 timing: int = 0, overlap: bool = True, workspace=None, device: int = 0):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", device)
@@ -189,7 +194,7 @@ class TieredEmbeddingCache:
         cfg.eviction_speed = int(eviction_speed)
         cfg.miss_mode = MISS_CODES[miss_mode]
         cfg.validate = int(bool(validate))
-        cfg.timing = int(bool(timing))
+        cfg.timing = 2 if timing is True else int(timing)  # 0 off, 1 pooled kernel, 2 every stage
         cfg.max_bags_per_table = int(max_bags_per_table)
         cfg.max_indices = int(max_indices)
         cfg.max_prefetch = int(max_prefetch)
@@ -260,8 +265,12 @@ class TieredEmbeddingCache:
             at += int(counts[t])
         return (L, Tt, res, code) if not strict else (L, Tt, res)
 
+    def set_timing(self, level: int):
+        """0 off, 1 the pooled kernel only (no stream commands added), 2 every stage."""
+        _check(recmg_set_timing(self.handle, int(level)), "recmg_set_timing")
+
     def stage_times(self, reset: bool = True):
-        """{stage: (milliseconds, launches)} summed since the last reset (timing=True only)."""
+        """{stage: (milliseconds, launches)} summed since the last reset (stages timed at the level in force)."""
         import numpy as np
         ms = np.zeros(len(STAGES), np.float64)
         calls = np.zeros(len(STAGES), np.int64)

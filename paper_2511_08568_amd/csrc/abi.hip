@@ -80,6 +80,7 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
     if (cfg->eviction_speed < 0 || cfg->eviction_speed > (1 << 20))
         return fail(RECMG_E_INVALID, "eviction_speed out of [0, 2^20]");
     if (cfg->miss_mode != RECMG_ZERO_COPY && cfg->miss_mode != RECMG_STAGED) return fail(RECMG_E_INVALID, "bad miss_mode");
+    if (cfg->timing < 0 || cfg->timing > 2) return fail(RECMG_E_INVALID, "timing must be 0, 1 or 2");
     if (cfg->max_bags_per_table < 0 || cfg->max_indices < 0 || cfg->max_indices >= (int64_t(1) << 31) ||
         cfg->max_prefetch < 0 || cfg->max_prefetch >= (int64_t(1) << 31))
         return fail(RECMG_E_INVALID, "max_* sizes out of range");
@@ -237,7 +238,8 @@ struct recmg_cache {
     std::vector<int64_t> h_pstart, h_ftstart;
     std::vector<TState> h_st;
     std::vector<int64_t> h_tstart;
-    // stage timing
+    // stage timing: 0 off, 1 the pooled kernel only, 2 every stage
+    int32_t timing = 0;
     struct Mark {
         int stage;
         hipEvent_t a, b;
@@ -261,14 +263,15 @@ hipEvent_t take_event(recmg_cache_t *c) {
     return e;
 }
 
-// Stage timing: an event pair per stage per call, resolved in recmg_stage_times.
+// Stage timing (level 2): an event pair per stage per call, resolved in
+// recmg_stage_times.  Each pair adds two commands to the stream (a few us).
 struct StageTimer {
     recmg_cache_t *c;
     int stage;
     hipStream_t s;
     hipEvent_t a = nullptr;
     StageTimer(recmg_cache_t *c_, int stage_, hipStream_t s_) : c(c_), stage(stage_), s(s_) {
-        if (!c->cfg.timing) return;
+        if (c->timing < 2) return;
         a = take();
         if (a) (void)hipEventRecord(a, s);
     }
@@ -529,6 +532,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     HIP_TRY(hipGetDevice(&c->device));
     c->T = T;
     c->cfg = *cfg;
+    c->timing = cfg->timing;
     c->geo = geo;
     c->L = L;
     // host tables: must be pinned memory visible to the device
@@ -838,7 +842,7 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
     {
         // the pooled kernel is timed by events its own dispatch records
         hipEvent_t a = nullptr, b = nullptr;
-        if (c->cfg.timing && c->pool_blocks > 0) {
+        if (c->timing >= 1 && c->pool_blocks > 0) {
             a = take_event(c);
             b = a ? take_event(c) : nullptr;
             if (!b && a) {
@@ -909,6 +913,14 @@ int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_sta
         }
     }
     g_last_error.clear();
+    return RECMG_OK;
+}
+
+int32_t recmg_set_timing(recmg_cache_t *c, int32_t level) {
+    int32_t rc = check_handle(c);
+    if (rc) return rc;
+    if (level < 0 || level > 2) return fail(RECMG_E_INVALID, "timing level must be 0, 1 or 2");
+    c->timing = level;
     return RECMG_OK;
 }
 
