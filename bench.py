@@ -59,6 +59,25 @@ def measured_traffic(args):
     return rec["read_bytes_per_launch"] + rec["write_bytes_per_launch"], rec
 
 
+def huge_page_tensor(shape, dtype):
+    """Pageable host tensor on transparent 2 MB pages where the kernel offers
+    them (madvise mode): the STAGED host gather reads rows at random, and small
+    pages would cost a TLB miss per row."""
+    import mmap
+
+    import numpy as np
+    import torch
+    nbytes = int(np.prod(shape)) * torch.empty((), dtype=dtype).element_size()
+    buf = mmap.mmap(-1, max(nbytes, 1), flags=mmap.MAP_PRIVATE | mmap.MAP_ANONYMOUS)
+    if hasattr(mmap, "MADV_HUGEPAGE"):
+        try:
+            buf.madvise(mmap.MADV_HUGEPAGE)
+        except OSError:
+            pass
+    arr = np.frombuffer(buf, dtype=np.uint8, count=nbytes)
+    return torch.from_numpy(arr).view(dtype).view(shape)
+
+
 def describe_workload(cid, w):
     """One line naming the configuration by its shapes."""
     tabs = w.tables
@@ -139,7 +158,10 @@ def main():
     t0 = time.time()
     tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.uint16}
     pin = args.miss_mode == "zero_copy"  # staged mode reads the tables on the host only
-    host = [torch.empty((tb.rows, tb.dim), dtype=tdt[tb.dtype], pin_memory=pin) for tb in w.tables]
+    if pin:
+        host = [torch.empty((tb.rows, tb.dim), dtype=tdt[tb.dtype], pin_memory=True) for tb in w.tables]
+    else:
+        host = [huge_page_tensor((tb.rows, tb.dim), tdt[tb.dtype]) for tb in w.tables]
     for t in range(T):  # each table's rows are drawn in parallel chunks
         w.table_values(t, out=host[t].numpy())
     log(f"tables ready ({sum(h.numel() * h.element_size() for h in host) / 1e9:.2f} GB, pinned={pin}) "
