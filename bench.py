@@ -325,6 +325,12 @@ def main():
                                                  if fwd_ms > 0 else None),
                   "measured_over": f"{KB} breakdown steps (every stage timed)"},
         "ondemand_fetches_per_batch": delta["misses"] / K,
+        # Sec. IV Eq. coverage (unique vectors) and Sec. VII-E prefetch accuracy
+        # (useful prefetches over prefetches issued), over the timed steps
+        "prefetch_quality": {"coverage": delta["prefetch_covered"] / max(delta["unique"], 1),
+                             "accuracy": (delta["hits_prefetch"] / delta["prefetch_fill"]
+                                          if delta["prefetch_fill"] else None),
+                             "prefetch_distinct_per_batch": delta["prefetch_distinct"] / K},
         "prefetch_fills_per_batch": delta["prefetch_fill"] / K,
         "host_link": {"bytes_per_batch": link_bytes / max(KB, 1), "achieved_GBs": link_gbs,
                       "measured_over": f"{KB} breakdown steps after the timed ones",

@@ -119,7 +119,11 @@ typedef enum {
 
 /* Counters of one table.  The first group describes a forward, the second a
  * placement (Sec. VII-E splits accesses into hits from caching, hits from
- * prefetching and on-demand fetches). */
+ * prefetching and on-demand fetches).  Prefetch quality (Sec. IV, Eq. coverage;
+ * Sec. VII-E): coverage = prefetch_covered / unique of a forward, with P the
+ * prefetch list of the placement just before it; prefetch accuracy (useful
+ * prefetches over prefetches issued) = hits_prefetch / prefetch_fill summed
+ * over calls. */
 typedef struct {
     int64_t lookups;           /* indices of this table in the batch */
     int64_t unique;            /* distinct rows U */
@@ -127,6 +131,8 @@ typedef struct {
     int64_t hits_prefetch;     /* hits on rows still flagged as prefetched */
     int64_t misses;            /* |U \ R| = on-demand fetches, each row fetched once */
     int64_t ondemand_bytes;    /* misses * row bytes */
+    int64_t prefetch_covered;  /* |set(P) ∩ U|, P of the placement just before this forward
+                                  (0 if another forward came between) */
     int64_t evicted;           /* |R \ R'| */
     int64_t admitted_miss;     /* |(R' \ R) ∩ M| */
     int64_t prefetch_fill;     /* |(R' \ R) \ M|: rows fetched from host for prefetch */
@@ -135,6 +141,7 @@ typedef struct {
     int64_t miss_dropped;      /* |M \ R'| */
     int64_t resident;          /* |R'| */
     int64_t prefetch_bytes;    /* prefetch_fill * row bytes */
+    int64_t prefetch_distinct; /* |set(P)| */
     uint64_t digest;           /* sum over R' of SplitMix64-mix((t << 40) | row) mod 2^64 */
 } recmg_table_stats_t;
 

@@ -17,9 +17,9 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "recmg_oracle.c")
 
-FWD_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand_bytes")
+FWD_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand_bytes", "prefetch_covered")
 PLC_FIELDS = ("evicted", "admitted_miss", "prefetch_fill", "prefetch_resident",
-              "prefetch_dropped", "miss_dropped", "resident", "prefetch_bytes")
+              "prefetch_dropped", "miss_dropped", "resident", "prefetch_bytes", "prefetch_distinct")
 DTYPES = {"f32": 0, "f16": 1, "bf16": 2}
 POLICIES = {"lru": 0, "priority": 1}
 
@@ -131,8 +131,8 @@ class Oracle:
         return st, out32[:n], (out64[:n] if want64 else None)
 
     def stats(self, t: int) -> dict:
-        fwd = np.zeros(6, np.int64)
-        plc = np.zeros(8, np.int64)
+        fwd = np.zeros(len(FWD_FIELDS), np.int64)
+        plc = np.zeros(len(PLC_FIELDS), np.int64)
         dig = np.zeros(1, np.uint64)
         self.lib.oracle_table_stats(self.h, int(t), _ptr(fwd), _ptr(plc), _ptr(dig))
         d = {k: int(v) for k, v in zip(FWD_FIELDS, fwd)}

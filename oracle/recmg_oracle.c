@@ -20,6 +20,9 @@
  *   U = distinct rows of the batch, H = U ∩ R, M = U \ R.
  *   lookups, unique = |U|, hits = |H|, hits_prefetch = |{r in H : pf(r)}|,
  *   misses = |M| (on-demand fetches), ondemand_bytes = |M| * row_bytes.
+ *   prefetch_covered = |set(P) ∩ U| with P the prefetch list of the placement
+ *   just before this forward (0 if another forward came between): the
+ *   numerator of Sec. IV's coverage (Eq. coverage), whose denominator is |U|.
  *   out[bag] = sum of the bag's rows, repeats counted, empty bag = 0.
  *   The forward reads residency and never changes it.
  *
@@ -40,7 +43,8 @@
  *      scores the lower row id goes first (Alg. 2's minimum-priority victim).
  *   6. newly admitted rows get pf(r) = [r in P].
  *   Counters: evicted, admitted_miss, prefetch_fill, prefetch_resident,
- *   prefetch_dropped, miss_dropped, resident, prefetch_bytes, and the digest
+ *   prefetch_dropped, miss_dropped, resident, prefetch_bytes,
+ *   prefetch_distinct = |set(P)|, and the digest
  *   sum over R' of SplitMix64's output mix of ((t << 40) | r), mod 2^64.
  *
  * Compile-time ORACLE_MUTANT = k (k > 0) plants one known mistake; the test
@@ -77,9 +81,14 @@ typedef struct {
     int64_t nU, nM;
     /* scratch marks, indexed by row; all zero between calls */
     uint8_t *in_u, *in_m, *in_p, *c;
+    /* the distinct prefetch rows of the latest placement, for the next
+     * forward's coverage (Sec. IV, Eq. coverage); have_plc: no forward since */
+    int32_t *lastP;
+    int64_t nlastP;
+    int have_plc;
     /* counters */
-    int64_t fwd[6];
-    int64_t plc[8];
+    int64_t fwd[7];
+    int64_t plc[9];
     uint64_t digest;
 } otab;
 
@@ -131,6 +140,7 @@ void oracle_destroy(void *h) {
         free(tb->in_r); free(tb->pf); free(tb->s); free(tb->res);
         free(tb->last_idx); free(tb->U); free(tb->M);
         free(tb->in_u); free(tb->in_m); free(tb->in_p); free(tb->c);
+        free(tb->lastP);
     }
     free(o->t);
     free(o);
@@ -222,10 +232,14 @@ static void place_table(oracle_t *o, int32_t t, const int32_t *P, int64_t nP, co
 #endif
     int64_t np_new = 0, p_res = 0;
     int32_t *pnew = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nP + 1));
+    free(tb->lastP);
+    tb->lastP = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nP + 1));
+    tb->nlastP = 0;
     for (int64_t k = 0; k < nP; ++k) {
         int32_t r = P[k];
         if (tb->in_p[r]) continue;
         tb->in_p[r] = 1;
+        tb->lastP[tb->nlastP++] = r;
         if (tb->in_r[r] || tb->in_m[r]) {
 #if ORACLE_MUTANT == 3 /* planted: prefetch overwrites the score */
             tb->s[r] = pscore;
@@ -281,8 +295,10 @@ static void place_table(oracle_t *o, int32_t t, const int32_t *P, int64_t nP, co
 
     tb->plc[0] = evicted; tb->plc[1] = adm_miss; tb->plc[2] = fill; tb->plc[3] = p_res;
     tb->plc[4] = p_drop; tb->plc[5] = m_drop; tb->plc[6] = tb->nres; tb->plc[7] = fill * tb->row_bytes;
+    tb->plc[8] = tb->nlastP;
     tb->digest = dig;
     tb->have_fwd = 0;
+    tb->have_plc = 1;
     free(K);
     free(pnew);
 }
@@ -315,8 +331,21 @@ static void forward_table(oracle_t *o, int32_t t, const int32_t *idx, const int6
     }
     for (int64_t k = 0; k < nU; ++k) tb->in_u[tb->U[k]] = 0;
     tb->nU = nU; tb->nM = nM; tb->have_fwd = 1;
+    /* coverage numerator: distinct rows of this batch in set(P) of the
+     * placement just before it (none if another forward came between) */
+    int64_t covered = 0;
+    if (tb->have_plc) {
+        for (int64_t k = 0; k < tb->nlastP; ++k) tb->in_p[tb->lastP[k]] = 1;
+#if ORACLE_MUTANT == 10 /* planted: lookups counted with their repeats */
+        for (int64_t i = s0; i < s1; ++i) covered += tb->in_p[idx[i]];
+#else
+        for (int64_t k = 0; k < nU; ++k) covered += tb->in_p[tb->U[k]];
+#endif
+        for (int64_t k = 0; k < tb->nlastP; ++k) tb->in_p[tb->lastP[k]] = 0;
+    }
+    tb->have_plc = 0;
     tb->fwd[0] = L; tb->fwd[1] = nU; tb->fwd[2] = hits; tb->fwd[3] = hits_pf; tb->fwd[4] = nM;
-    tb->fwd[5] = nM * tb->row_bytes;
+    tb->fwd[5] = nM * tb->row_bytes; tb->fwd[6] = covered;
     /* pooled sums, double accumulation, one rounding to float */
     for (int32_t j = 0; j < B; ++j) {
         int64_t a = bo[j], e = bo[j + 1];
@@ -416,9 +445,11 @@ int32_t oracle_forward(void *h, const int32_t *idx, const int64_t *off, int32_t 
     return O_OK;
 }
 
-/* fwd[6]: lookups, unique, hits, hits_prefetch, misses, ondemand_bytes.
- * plc[8]: evicted, admitted_miss, prefetch_fill, prefetch_resident,
- *         prefetch_dropped, miss_dropped, resident, prefetch_bytes. */
+/* fwd[7]: lookups, unique, hits, hits_prefetch, misses, ondemand_bytes,
+ *         prefetch_covered.
+ * plc[9]: evicted, admitted_miss, prefetch_fill, prefetch_resident,
+ *         prefetch_dropped, miss_dropped, resident, prefetch_bytes,
+ *         prefetch_distinct. */
 void oracle_table_stats(void *h, int32_t t, int64_t *fwd, int64_t *plc, uint64_t *digest) {
     oracle_t *o = (oracle_t *)h;
     otab *tb = &o->t[t];

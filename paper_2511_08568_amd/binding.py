@@ -25,9 +25,9 @@ DTYPE_CODES = {"f32": RECMG_F32, "f16": RECMG_F16, "bf16": RECMG_BF16}
 POLICY_CODES = {"lru": RECMG_LRU_BATCH, "priority": RECMG_PRIORITY}
 MISS_CODES = {"zero_copy": RECMG_ZERO_COPY, "staged": RECMG_STAGED}
 
-STAT_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand_bytes", "evicted",
-               "admitted_miss", "prefetch_fill", "prefetch_resident", "prefetch_dropped", "miss_dropped",
-               "resident", "prefetch_bytes")
+STAT_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand_bytes", "prefetch_covered",
+               "evicted", "admitted_miss", "prefetch_fill", "prefetch_resident", "prefetch_dropped", "miss_dropped",
+               "resident", "prefetch_bytes", "prefetch_distinct")
 
 EXPORTED = ("recmg_query_workspace", "recmg_cache_init", "recmg_apply_placement", "recmg_embbag_forward",
             "recmg_stats", "recmg_stage_times", "recmg_set_timing", "recmg_cache_destroy", "recmg_last_error")

@@ -222,6 +222,7 @@ struct recmg_cache {
     bool have_fwd = false;
     hipStream_t last_stream = nullptr;
     int32_t pool_B = -1;
+    int64_t plc_np = -1;  // prefetch ids of the placement since the last forward (-1: none)
     char *stage[2] = {nullptr, nullptr};  // staging buffers, alternating between forwards
     int cur = 0;                          // buffer of the latest forward
     bool fill_pending = false;            // a prefetch fill runs on the side stream
@@ -773,6 +774,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     launch_plc_finalize(g, s);
     HIP_TRY(hipGetLastError());
     c->placements++;
+    c->plc_np = num_prefetch;
     c->have_fwd = false;
     c->last_stream = s;
     return RECMG_OK;
@@ -825,6 +827,7 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
                          (int)(sizeof(TState) / 4), stamp, s);
             launch_fwd_probe(g, stamp, n, s);
             launch_fwd_src(g, indices, n, s);
+            if (c->plc_np >= 0) launch_fwd_cover(g, stamp, c->plc_np, s);
         }
     }
     if (n > 0) {
@@ -859,11 +862,14 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
     launch_fwd_finalize(g, s);
     HIP_TRY(hipGetLastError());
     c->forwards++;
+    c->plc_np = -1;  // coverage counts against the placement just before a forward only
     c->have_fwd = true;
     c->last_n = n;
     c->last_stream = s;
     return RECMG_OK;
 }
+
+static_assert(sizeof(recmg_table_stats_t) == 8 * (kNumStats + 1), "counter layout of recmg_table_stats_t");
 
 int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_stats_t *total, int32_t *resident_dump,
                     int64_t dump_capacity, int64_t *resident_counts) {
@@ -887,7 +893,7 @@ int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_sta
             if (!o) continue;
             const int64_t *v = which == 0 ? st[t].last : st[t].total;
             int64_t *dst = &o[t].lookups;
-            for (int k = 0; k < 14; ++k) dst[k] = v[k];
+            for (int k = 0; k < kNumStats; ++k) dst[k] = v[k];
             o[t].digest = st[t].digest;
         }
     }

@@ -31,6 +31,36 @@ __global__ void __launch_bounds__(kBlock) k_fwd_prep(DGlobal g, const int64_t *_
         st.mcount = 0;
         st.hits = 0;
         st.hits_pf = 0;
+        st.covered = 0;
+    }
+}
+
+// Coverage (Eq. coverage): how many distinct rows of the last placement's
+// prefetch list (PU, still in place) this batch touches.  A row is in the
+// batch iff its rank word carries this forward's stamp and its bit.
+__global__ void __launch_bounds__(kBlock) k_fwd_cover(DGlobal g, int32_t stamp, int64_t np) {
+    if (*g.err) return;
+    __shared__ int64_t s_pstart[RECMG_MAX_TABLES + 1];
+    __shared__ int32_t s_pc[RECMG_MAX_TABLES];
+    for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
+        s_pstart[t] = g.pstart[t];
+        if (t < g.T) s_pc[t] = g.st[t].pcount;
+    }
+    __syncthreads();
+    const int stride_st = (int)(sizeof(TState) / 4);
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < np; base += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = base + threadIdx.x;
+        int t = 0;
+        bool hit = false;
+        if (i < np) {
+            t = find_seg(s_pstart, g.T, i);
+            if (i - s_pstart[t] < s_pc[t]) {
+                const int32_t row = g.PU[i];
+                const uint4 rk = g.tabs[t].rank[row >> 5];
+                hit = (int32_t)rk.z == stamp && (rk.y & (1u << (row & 31)));
+            }
+        }
+        (void)wave_append(hit, t, &g.st[0].covered, stride_st);  // counts only
     }
 }
 
@@ -651,14 +681,15 @@ __global__ void k_fwd_finalize(DGlobal g) {
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         TState &st = g.st[t];
         const DTable &tb = g.tabs[t];
-        int64_t v[6];
+        int64_t v[kFwdStats];
         v[0] = g.tstart[t + 1] - g.tstart[t];
         v[1] = st.ucount;
         v[2] = st.hits;
         v[3] = st.hits_pf;
         v[4] = st.mcount;
         v[5] = (int64_t)st.mcount * tb.row_bytes;
-        for (int k = 0; k < 6; ++k) {
+        v[6] = st.covered;
+        for (int k = 0; k < kFwdStats; ++k) {
             st.last[k] = v[k];
             st.total[k] += v[k];
         }
@@ -682,6 +713,11 @@ void launch_fwd_prep(const DGlobal &g, const int64_t *offsets, int32_t B, int64_
 void launch_fwd_probe(const DGlobal &g, int32_t stamp, int64_t n, hipStream_t s) {
     if (n <= 0) return;
     k_fwd_probe<<<grid_for(n, kBlock, 8192), kBlock, 0, s>>>(g, stamp, n);
+}
+
+void launch_fwd_cover(const DGlobal &g, int32_t stamp, int64_t np, hipStream_t s) {
+    if (np <= 0) return;
+    k_fwd_cover<<<grid_for(np, kBlock, 4096), kBlock, 0, s>>>(g, stamp, np);
 }
 
 void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStream_t s) {

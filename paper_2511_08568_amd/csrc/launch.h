@@ -16,6 +16,7 @@ void launch_dedup(const DGlobal &g, int mode, int32_t *counts, int count_stride,
 void launch_fwd_prep(const DGlobal &g, const int64_t *offsets, int32_t B, int64_t n, hipStream_t s);
 void launch_fwd_probe(const DGlobal &g, int32_t stamp, int64_t n, hipStream_t s);
 void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStream_t s);
+void launch_fwd_cover(const DGlobal &g, int32_t stamp, int64_t np, hipStream_t s);
 void launch_fetch(const DGlobal &g, hipStream_t s);
 // Pooled-sum kernels: kinds [0, kPoolKindsGroup) are the group-per-bag kernel
 // (dtype * 2 + vec), the rest the wave-per-bag kernel per (dtype, wlw, wr).

@@ -504,7 +504,7 @@ __global__ void k_plc_finalize(DGlobal g) {
         st.free_top -= st.popped;  // popped stays: the fill may still read it
         st.n_res = tb.cap - st.free_top;
         st.rebuild = 0;
-        int64_t v[8];
+        int64_t v[kPlcStats];
         v[0] = st.evicted;
         v[1] = st.adm_miss;
         v[2] = st.p_fill;
@@ -513,9 +513,10 @@ __global__ void k_plc_finalize(DGlobal g) {
         v[5] = st.m_drop;
         v[6] = st.n_res;
         v[7] = (int64_t)st.p_fill * tb.row_bytes;
-        for (int k = 0; k < 8; ++k) {
-            st.last[6 + k] = v[k];
-            st.total[6 + k] += v[k];
+        v[8] = st.pcount;
+        for (int k = 0; k < kPlcStats; ++k) {
+            st.last[kFwdStats + k] = v[k];
+            st.total[kFwdStats + k] += v[k];
         }
         st.digest = st.digest_acc;
     }

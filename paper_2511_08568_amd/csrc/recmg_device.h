@@ -31,7 +31,9 @@ constexpr int32_t ERR_OFFSETS = 2;
 #endif
 constexpr int kWaveBags = RECMG_WPOOL_BAGS;  // consecutive bags per wave in the wave-per-bag pooled kernel
 constexpr int kRaddrPad = 64;  // entries past the batch in the per-index row-address array (read, never used)
-constexpr int32_t ERR_INTERNAL = 4;  // a slot-accounting invariant failed (never expected)
+constexpr int32_t ERR_INTERNAL = 4;
+// int64 counters of recmg_table_stats_t: kFwdStats of a forward, then the placement's
+constexpr int kFwdStats = 7, kPlcStats = 9, kNumStats = kFwdStats + kPlcStats;  // a slot-accounting invariant failed (never expected)
 
 // outcome of the top-Cap ranking of one table
 constexpr int32_t SEL_SELECT = 0;  // keep keys >= threshold
@@ -78,14 +80,14 @@ struct TState {
     int32_t rebuild, sel_mode, need, plc_nm;  // plc_nm: misses the current placement ranks
     uint64_t prefix;  // radix-select prefix; the threshold key after the last pass
     uint32_t pad0;
-    int32_t pad1;
+    int32_t covered;  // accumulator: distinct prefetch rows of the last placement found in this batch
     // accumulators of the call in flight
     int32_t hits, hits_pf, p_res, evicted, adm_miss, p_fill, p_drop, m_drop;
     unsigned long long digest_acc;
     // published counters, in recmg_table_stats_t order
-    int64_t last[14];
+    int64_t last[kNumStats];
     unsigned long long digest;
-    int64_t total[14];
+    int64_t total[kNumStats];
 };
 
 // Device pointers into the workspace, passed by value to every kernel.

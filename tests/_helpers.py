@@ -132,8 +132,8 @@ class GpuRunner:
 
 
 PLACE_KEYS = ("evicted", "admitted_miss", "prefetch_fill", "prefetch_resident", "prefetch_dropped",
-              "miss_dropped", "resident", "prefetch_bytes", "digest")
-FWD_KEYS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand_bytes")
+              "miss_dropped", "resident", "prefetch_bytes", "prefetch_distinct", "digest")
+FWD_KEYS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand_bytes", "prefetch_covered")
 
 
 def compare_runs(w, tabs, ora, gpu, label=""):

@@ -240,5 +240,41 @@ def pin_invariants(mutant=0, seeds=range(40)):
                 prev[t] = p["resident"]
 
 
+def pin_prefetch_quality(mutant=0, seeds=range(30)):
+    """Sec. IV's coverage (Eq. coverage) counts unique vectors: brute force of
+    |set(P_b) ∩ set(I_b)| and |set(P_b)| on tiny traces; exact lookahead covers
+    every distinct row; a forward with no placement before it covers nothing."""
+    for s in seeds:
+        w = tg.random_tiny(s, batches=5, policy=("lru", "priority")[s % 2])
+        if s % 3 == 0:
+            w.prefetch = ("exact",)
+        _, recs = run_oracle(w, mutant=mutant, want64=False)
+        for b, r in enumerate(recs):
+            for t, (a, e) in enumerate(segments(w, r["off"])):
+                P = set(r["P"][r["poff"][t]:r["poff"][t + 1]].tolist())
+                U = set(r["idx"][a:e].tolist())
+                assert r["place"][t]["prefetch_distinct"] == len(P), f"seed {s} batch {b} table {t}"
+                assert r["fwd"][t]["prefetch_covered"] == len(P & U), f"seed {s} batch {b} table {t}"
+                if s % 3 == 0 and b + 1 < len(recs):
+                    # exact lookahead: P_{b+1} = U_{b+1}
+                    nxt = recs[b + 1]
+                    a2, e2 = w.table_segment(nxt["off"], t)
+                    assert nxt["fwd"][t]["prefetch_covered"] == np.unique(nxt["idx"][a2:e2]).size
+    # a second forward with no placement in between covers nothing
+    w = tg.random_tiny(7, batches=3)
+    tabs = [w.table_values(t) for t in range(w.num_tables)]
+    o = oracle.for_workload(w, tabs, mutant=mutant)
+    P, poff = w.prefetch_list(0)
+    assert o.placement(P, poff, None) == 0
+    idx, off = w.batch(0)
+    for rep in range(2):
+        assert o.forward(idx, off, w.bags)[0] == 0
+        for t in range(w.num_tables):
+            a, e = w.table_segment(off, t)
+            want = len(set(P[poff[t]:poff[t + 1]].tolist()) & set(idx[a:e].tolist())) if rep == 0 else 0
+            assert o.stats(t)["prefetch_covered"] == want
+    o.close()
+
+
 ALL_PINS = (pin_hand_examples, pin_embedding_bag, pin_splitmix, pin_lru_history, pin_unbounded_cache,
-            pin_zero_capacity, pin_priority_es0, pin_invariants)
+            pin_zero_capacity, pin_priority_es0, pin_invariants, pin_prefetch_quality)

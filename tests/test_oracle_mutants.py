@@ -15,6 +15,7 @@ MUTANTS = {
     7: "LRU prefetch scored like a touch",
     8: "digest forgets the table id",
     9: "aging does not saturate at 0",
+    10: "coverage counts lookups with their repeats",
 }
 
 
