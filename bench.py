@@ -78,6 +78,89 @@ def huge_page_tensor(shape, dtype):
     return torch.from_numpy(arr).view(dtype).view(shape)
 
 
+def buffer_sweep(args, dev):
+    """Hit rate against buffer size on one configuration's trace (Sec. VII-D's
+    sweep, on synthetic traces): every point runs the HIP path and the oracle
+    on the same batches and checks that their counters agree."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import tracegen as tg
+    from paper_2511_08568_amd import TieredEmbeddingCache
+
+    base = tg.make_config(args.config)
+    NB = min(args.sweep_batches, base.batches)
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.uint16}
+    host = [torch.empty((tb.rows, tb.dim), dtype=tdt[tb.dtype], pin_memory=True) for tb in base.tables]
+    for t in range(base.num_tables):
+        base.table_values(t, out=host[t].numpy())
+    tabs_np = [h.numpy() for h in host]
+    batches = [base.batch(b) for b in range(NB)]
+    seen = [np.unique(np.concatenate([base.uniques(b)[t] for b in range(NB)])).size for t in range(base.num_tables)]
+    uniq_total = sum(int(base.uniques(b)[t].size) for b in range(NB) for t in range(base.num_tables))
+    recipe = base.prefetch if base.prefetch[0] != "none" else ("exact",)
+    variants = {"lru": ("lru", ("none",)), "caching_model": ("priority", ("none",)),
+                "caching_and_prefetch": ("priority", recipe)}
+    points = []
+    for frac in (0.01, 0.02, 0.05, 0.10, 0.15, 0.20, 0.30):
+        caps = [max(1, int(round(frac * n))) for n in seen]
+        pt = {"buffer_frac_of_touched_rows": frac, "cache_rows": sum(caps)}
+        # Belady bound for a demand-filled buffer of Cap rows (no prefetch)
+        opt = 0
+        for t in range(base.num_tables):
+            lab = tg.optgen_labels([base.uniques(b)[t] for b in range(NB)], caps[t])
+            opt += sum(int(x.sum()) for x in lab)
+        pt["belady_bound"] = opt / uniq_total
+        parity = True
+        for name, (policy, pf) in variants.items():
+            w = tg.make_config(args.config)
+            w.policy, w.prefetch = policy, pf
+            w.bits = ("optgen", 0.8, NB)
+            for tb, c in zip(w.tables, caps):
+                tb.cap = c
+            pre = [w.prefetch_list(b) for b in range(NB)]
+            bits = [w.cache_bits(b - 1) if b > 0 else None for b in range(NB)]
+            max_idx = max(i.size for i, _ in batches)
+            max_pf = max(max(P.size for P, _ in pre), 1)
+            cache = TieredEmbeddingCache(host, [tb.dtype for tb in w.tables], caps, policy=policy,
+                                         eviction_speed=w.eviction_speed, max_bags_per_table=w.bags,
+                                         max_indices=max_idx, max_prefetch=max_pf)
+            o = oracle.for_workload(w, tabs_np)
+            out = torch.empty(w.bags * sum(tb.dim for tb in w.tables), dtype=torch.float32, device=dev)
+            osum = {"hits": 0, "misses": 0, "evicted": 0, "prefetch_fill": 0}
+            for b in range(NB):
+                P, po = pre[b]
+                cache.placement(torch.from_numpy(P).to(dev) if P.size else None, torch.from_numpy(po).to(dev),
+                                None if bits[b] is None else torch.from_numpy(bits[b]).to(dev))
+                i, off = batches[b]
+                cache.forward(torch.from_numpy(i).to(dev), torch.from_numpy(off).to(dev), w.bags, out=out)
+                assert o.placement(P, po, bits[b]) == 0
+                for t in range(w.num_tables):
+                    st = o.stats(t)
+                    osum["evicted"] += st["evicted"]
+                    osum["prefetch_fill"] += st["prefetch_fill"]
+                assert o.forward(i, off, w.bags)[0] == 0
+                for t in range(w.num_tables):
+                    st = o.stats(t)
+                    osum["hits"] += st["hits"]
+                    osum["misses"] += st["misses"]
+            _, tot = cache.stats()
+            cache.close()
+            o.close()
+            gsum = {k: sum(tot[t][k] for t in range(w.num_tables)) for k in osum}
+            parity &= gsum == osum
+            pt[name] = gsum["hits"] / uniq_total
+            pt[name + "_prefetch_fills"] = gsum["prefetch_fill"]
+        pt["counters_equal_oracle"] = parity
+        points.append(pt)
+        log(f"buffer {frac:.2f}: " + json.dumps({k: round(v, 4) for k, v in pt.items() if isinstance(v, float)}))
+    print(json.dumps({"metric": "hit rate (hits / distinct rows per batch, summed) vs buffer size",
+                      "workload": describe_workload(args.config, base), "batches": NB,
+                      "caching_bits": "OPTgen labels for a buffer of 0.8 x Cap over the same batches",
+                      "prefetch_recipe": list(recipe), "points": points}), flush=True)
+
+
 def describe_workload(cid, w):
     """One line naming the configuration by its shapes."""
     tabs = w.tables
@@ -114,6 +197,14 @@ def main():
                     help="steps after the timed ones with every stage timed (stage split, host-link rate)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-link-peak", action="store_true")
+    ap.add_argument("--bits", default=None, choices=["lookahead", "optgen"],
+                    help="caching-bit source of PRIORITY configurations (optgen: Belady-optimal labels for a "
+                         "buffer of 0.8 x Cap over the run's batches)")
+    ap.add_argument("--buffer-sweep", action="store_true",
+                    help="instead of the benchmark: hit rate against buffer size (1-30%% of the rows the trace "
+                         "touches) for LRU, the caching policy with OPTgen bits, that policy with the "
+                         "configuration's prefetch list, and the Belady bound; one JSON line")
+    ap.add_argument("--sweep-batches", type=int, default=60)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 3 device-to-device copies of MIB MiB (scale for HBM byte counters) and exit")
     args = ap.parse_args()
@@ -140,6 +231,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "copies": 3}), flush=True)
         return
+    if args.buffer_sweep:
+        buffer_sweep(args, dev)
+        return
     if args.row_scale < 1.0:
         w = tg.scaled_config(args.config, row_scale=args.row_scale)
     else:
@@ -152,6 +246,8 @@ def main():
     # after the timed steps, a few more with every stage timed (the breakdown)
     KB = min(args.breakdown_steps, w.batches - W - K)
     nb = W + K + KB
+    if args.bits == "optgen":
+        w.bits = ("optgen", 0.8, nb + 1)  # labels over the batches this run plays
     T = w.num_tables
 
     # -- tables in pinned host memory -------------------------------------------------------------

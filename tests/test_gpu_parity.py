@@ -115,6 +115,15 @@ def test_pool_kernel_shapes(dtypes, seed, policy):
     _parity(_kinds_workload(dtypes, seed, policy), label=f"kinds-{'-'.join(dtypes)}")
 
 
+@pytest.mark.parametrize("cid,scale,tables", [(3, 0.01, 6), (5, 0.005, 8)])
+def test_optgen_caching_bits(cid, scale, tables):
+    """PRIORITY placement fed OPTgen's Belady-optimal labels (the caching
+    model's ground truth, Sec. VI-A) instead of the noisy lookahead bits."""
+    w = tg.scaled_config(cid, row_scale=scale, batches=6, bags=256, max_tables=tables)
+    w.bits = ("optgen", 0.8, w.batches)
+    _parity(w, label=f"c{cid}-optgen")
+
+
 def test_config4_no_prefetch_scaled():
     w = tg.scaled_config(4, row_scale=0.0005, batches=6, bags=512, max_tables=2, prefetch=("none",))
     _parity(w, label="c4-noprefetch")

@@ -81,3 +81,77 @@ def test_cache_bits_shape():
     idx, off = w.batch(1)
     bits = w.cache_bits(1)
     assert bits.shape == idx.shape and set(np.unique(bits)) <= {0, 1}
+
+
+# ----------------------------------------------------------------------------- OPTgen labels
+
+def _optimal_hits(uniq, capacity):
+    """Most hits any demand-filled buffer of `capacity` rows can score on the
+    batch sequence (a row hits in batch b if the buffer held it across the
+    boundary before b), by exhaustive search over every buffer content."""
+    rows = sorted(set().union(*[set(u.tolist()) for u in uniq]))
+    idx = {r: i for i, r in enumerate(rows)}
+    best = {0: 0}  # buffer content (bit mask) after the previous batch -> hits so far
+    for u in uniq:
+        used = 0
+        for r in u.tolist():
+            used |= 1 << idx[r]
+        nxt = {}
+        for buf, h in best.items():
+            h2 = h + bin(buf & used).count("1")
+            avail = buf | used  # a row may stay if it was held or was just used
+            sub = avail
+            while True:  # every subset of avail of at most `capacity` rows
+                if bin(sub).count("1") <= capacity and nxt.get(sub, -1) < h2:
+                    nxt[sub] = h2
+                if sub == 0:
+                    break
+                sub = (sub - 1) & avail
+        best = nxt
+    return max(best.values())
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_optgen_is_optimal_on_tiny_traces(seed):
+    g = np.random.default_rng(seed)
+    nrows, nb = int(g.integers(2, 7)), int(g.integers(2, 7))
+    uniq = [np.unique(g.integers(0, nrows, int(g.integers(0, nrows + 1)))) for _ in range(nb)]
+    for cap in range(0, nrows + 1):
+        labels = tg.optgen_labels(uniq, cap)
+        assert all(l.shape == u.shape for l, u in zip(labels, uniq))
+        # a granted request is a hit at the row's next use: the count must be
+        # the optimum of an exhaustive search over buffer contents
+        assert sum(int(l.sum()) for l in labels) == _optimal_hits(uniq, cap), (seed, cap)
+        # the buffer never holds more than cap rows across a boundary
+        for k in range(nb - 1):
+            held = 0
+            for b in range(k + 1):
+                for r, lab in zip(uniq[b].tolist(), labels[b].tolist()):
+                    nxt = next((bb for bb in range(b + 1, nb) if r in set(uniq[bb].tolist())), None)
+                    if lab and nxt is not None and b <= k < nxt:
+                        held += 1
+            assert held <= cap
+
+
+def test_optgen_large_and_zero_buffer():
+    g = np.random.default_rng(5)
+    uniq = [np.unique(g.integers(0, 50, 30)) for _ in range(8)]
+    # a buffer that holds every row keeps every row until its next use
+    labels = tg.optgen_labels(uniq, 50)
+    for b, (u, l) in enumerate(zip(uniq, labels)):
+        later = set().union(*[set(x.tolist()) for x in uniq[b + 1:]]) if b + 1 < len(uniq) else set()
+        assert l.tolist() == [int(r in later) for r in u.tolist()]
+    assert all(int(l.sum()) == 0 for l in tg.optgen_labels(uniq, 0))
+
+
+def test_optgen_bits_expand_to_accesses():
+    w = tg.random_tiny(3, batches=5, policy="priority")
+    w.bits = ("optgen", 0.8, 5)
+    for b in range(5):
+        bits = w.cache_bits(b)
+        idx, off = w.batch(b)
+        assert bits.shape == idx.shape and bits.dtype == np.uint8
+        for t in range(w.num_tables):
+            s, e = w.table_segment(off, t)
+            for r in np.unique(idx[s:e]):
+                assert np.unique(bits[s:e][idx[s:e] == r]).size == 1  # one label per distinct row

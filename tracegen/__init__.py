@@ -218,6 +218,10 @@ class Workload:
     drift: Optional[Tuple[int, float]] = None   # (period in batches, fraction of lookups)
     bit_flip: float = 0.17                      # caching-bit noise (PRIORITY configs)
     integer_values: bool = False
+    # caching-bit source: ("lookahead",) = reuse in the next two batches with
+    # noise; ("optgen", frac, horizon) = Belady-optimal labels (optgen_labels)
+    # for a buffer of frac * Cap rows over the first `horizon` batches
+    bits: Tuple = ("lookahead",)
 
     def __post_init__(self):
         self._cache: dict = {}
@@ -380,10 +384,14 @@ class Workload:
     # -- caching bits ----------------------------------------------------------------
     def cache_bits(self, b: int) -> Optional[np.ndarray]:
         """One byte per access of batch b: the stand-in for the caching model's
-        1-bit output (Sec. V-A).  c(r) = [r reused in batch b+1 or b+2], flipped
-        per distinct row with probability ``bit_flip``.  None for LRU configs."""
+        1-bit output (Sec. V-A).  ("lookahead",): c(r) = [r reused in batch b+1
+        or b+2], flipped per distinct row with probability ``bit_flip``.
+        ("optgen", frac, horizon): the model's ground truth, OPTgen's label for
+        a buffer of frac * Cap rows (Sec. VI-A).  None for LRU configs."""
         if self.policy != "priority":
             return None
+        if self.bits[0] == "optgen":
+            return self._optgen_bits(b)
         idx, off = self.batch(b)
         fut1, fut2 = self.uniques(b + 1), self.uniques(b + 2)
         out = np.zeros(idx.size, dtype=np.uint8)
@@ -396,6 +404,73 @@ class Workload:
             out[s:e] = (reuse ^ flip).astype(np.uint8)[inv]
         _pmap(one, range(self.num_tables))
         return out
+
+
+    def _optgen_bits(self, b: int) -> np.ndarray:
+        _, frac, horizon = self.bits
+        key = ("optgen", frac, horizon)
+        labels = self._cache.get(key)
+        if labels is None:
+            seqs = [[] for _ in self.tables]
+            for bb in range(min(horizon, self.batches)):
+                for t, u in enumerate(self.uniques(bb)):
+                    seqs[t].append(u)
+            labels = [optgen_labels(seqs[t], int(math.floor(frac * tb.cap))) for t, tb in enumerate(self.tables)]
+            self._cache[key] = labels
+        idx, off = self.batch(b)
+        out = np.zeros(idx.size, dtype=np.uint8)
+        if b >= len(labels[0]):
+            return out
+        for t in range(self.num_tables):
+            s, e = self.table_segment(off, t)
+            _, inv = np.unique(idx[s:e], return_inverse=True)
+            out[s:e] = labels[t][b][inv]
+        return out
+
+
+def optgen_labels(uniq: List[np.ndarray], capacity: int) -> List[np.ndarray]:
+    """Belady-optimal caching labels at batch granularity, after OPTgen (Jain &
+    Lin, ISCA 2016), the labeller the paper trains its caching model on
+    (Sec. VI-A).
+
+    ``uniq[b]`` holds the sorted distinct rows of batch b of one table.  A row
+    used in batch b and next in batch b' asks to stay in the buffer over the
+    boundaries b .. b'-1 (boundary k lies between batches k and k+1).  Requests
+    are taken in order of b' (the time the reuse happens), and among the same
+    b' the shorter ones first, then by row; a request is granted iff every
+    boundary it spans still holds fewer than ``capacity`` rows, and then it
+    occupies them.  Label 1 marks a granted request: the row should stay until
+    its next use (a hit there under the optimal policy); rows with no later
+    use in the trace get 0.  Returns one uint8 array per batch, aligned with
+    ``uniq[b]``."""
+    H = len(uniq)
+    labels = [np.zeros(u.size, dtype=np.uint8) for u in uniq]
+    if H == 0 or capacity <= 0:
+        return labels
+    rows = np.concatenate(uniq).astype(np.int64) if H else np.zeros(0, np.int64)
+    bats = np.concatenate([np.full(u.size, b, np.int64) for b, u in enumerate(uniq)])
+    pos = np.concatenate([np.arange(u.size, dtype=np.int64) for u in uniq])
+    order = np.lexsort((bats, rows))  # by row, then batch
+    r_s, b_s, p_s = rows[order], bats[order], pos[order]
+    same = r_s[1:] == r_s[:-1]  # consecutive uses of one row
+    start, end, row, at = b_s[:-1][same], b_s[1:][same], r_s[:-1][same], p_s[:-1][same]
+    # requests by (end asc, start desc, row asc)
+    o = np.lexsort((row, -start, end))
+    start, end, at = start[o], end[o], at[o]
+    occ = np.zeros(H, dtype=np.int64)
+    i, n = 0, start.size
+    while i < n:
+        j = i
+        while j < n and start[j] == start[i] and end[j] == end[i]:
+            j += 1
+        a, e = int(start[i]), int(end[i])
+        k = min(j - i, max(capacity - int(occ[a:e].max()), 0))
+        if k > 0:
+            occ[a:e] += k
+            lb = labels[a]
+            lb[at[i:i + k]] = 1
+        i = j
+    return labels
 
 
 # ----------------------------------------------------------------------------
