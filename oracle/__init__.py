@@ -55,7 +55,8 @@ def load(mutant: int = 0) -> ctypes.CDLL:
     lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     lib.oracle_create.restype = P
-    lib.oracle_create.argtypes = [ctypes.c_int32, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
+    lib.oracle_create.argtypes = [ctypes.c_int32, P, P, P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                  ctypes.c_int32]
     lib.oracle_destroy.argtypes = [P]
     lib.oracle_placement.restype = ctypes.c_int32
     lib.oracle_placement.argtypes = [P, P, P, P]
@@ -80,10 +81,13 @@ class Oracle:
     """The tiered lookup and cache-state machine on the CPU.
 
     ``tables`` are numpy arrays [rows, dim] in storage type (float32, float16,
-    or uint16 bfloat16 bits); they must stay alive as long as the oracle."""
+    or uint16 bfloat16 bits); they must stay alive as long as the oracle.
+    ``ways`` = 0: fully associative caches; W > 0: W-way set-associative
+    caches with Alg. 2 run inside each set."""
 
     def __init__(self, tables: Sequence[np.ndarray], dtypes: Sequence[str], caps: Sequence[int],
-                 policy: str = "lru", eviction_speed: int = 4, nthreads: int = 1, mutant: int = 0):
+                 policy: str = "lru", eviction_speed: int = 4, nthreads: int = 1, mutant: int = 0,
+                 ways: int = 0):
         self.lib = load(mutant)
         self.T = len(tables)
         self._tables = [np.ascontiguousarray(t) for t in tables]
@@ -95,7 +99,7 @@ class Oracle:
         caps_a = np.array(caps, dtype=np.int64)
         self.h = self.lib.oracle_create(self.T, rows.ctypes.data, dims.ctypes.data, dts.ctypes.data,
                                         ctypes.cast(ptrs, ctypes.c_void_p), caps_a.ctypes.data,
-                                        POLICIES[policy], int(eviction_speed), int(nthreads))
+                                        POLICIES[policy], int(eviction_speed), int(nthreads), int(ways))
         if not self.h:
             raise ValueError("oracle_create rejected the configuration")
 
@@ -160,4 +164,4 @@ def splitmix64_mix(z: int, mutant: int = 0) -> int:
 def for_workload(w, tables: Sequence[np.ndarray], nthreads: int = 1, mutant: int = 0) -> Oracle:
     """An oracle configured like workload ``w`` (a ``tracegen.Workload``)."""
     return Oracle(tables, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables], policy=w.policy,
-                  eviction_speed=w.eviction_speed, nthreads=nthreads, mutant=mutant)
+                  eviction_speed=w.eviction_speed, nthreads=nthreads, mutant=mutant, ways=w.ways)

@@ -11,8 +11,8 @@
  * indexed by row id; placement sorts the whole candidate set by key; pooled
  * sums are accumulated in double and rounded once to float.
  *
- * What it computes, per table t (caches are partitioned per table and fully
- * associative):
+ * What it computes, per table t (caches are partitioned per table; fully
+ * associative unless `ways` > 0, see the set-associative placement below):
  *
  * Forward on one batch (Sec. II, pooling by summation; Sec. VII-E for the
  * three-way split of accesses into cache hits, prefetch hits and on-demand
@@ -46,6 +46,28 @@
  *   prefetch_dropped, miss_dropped, resident, prefetch_bytes,
  *   prefetch_distinct = |set(P)|, and the digest
  *   sum over R' of SplitMix64's output mix of ((t << 40) | r), mod 2^64.
+ *
+ * Set-associative placement (ways W > 0; Sec. VI-B: the buffer is TorchRec's
+ * software cache, whose production form is W-way set-associative, Sec. VII-B
+ * and VII-E).  Per table, S = floor(Cap / W) sets of W ways; row r belongs to
+ * set r mod S (no sets when S = 0: nothing is ever resident).  Alg. 1 and
+ * Alg. 2 run literally inside each set, one event at a time:
+ *   A. rows of U that are resident lose their prefetch flag and take the touch
+ *      score (as in step 3 above; no aging here);
+ *   B. every miss of M, in ascending row order, is inserted with its touch
+ *      score;
+ *   C. every row of set(P), in ascending row order: if resident, its score
+ *      becomes max(score, b or ES); otherwise it is inserted with score b
+ *      (LRU_BATCH) or ES (PRIORITY).
+ *   insert(r, v) in r's set: the lowest free way if there is one; otherwise
+ *   Alg. 2 on the set: the victim is the lowest way holding the minimum score
+ *   (scores before this scan's aging), then, under PRIORITY only, every way
+ *   of the set ages by one, saturating at 0; r takes the victim's way.
+ *   A row whose way at the end differs from its way at the start (newly
+ *   admitted, or evicted and brought back into another way) gets
+ *   pf(r) = [r in P]; other residents keep their flag.  Counters are those of
+ *   the fully associative form, except that prefetch_fill counts every row
+ *   read from the host: rows of (R' \ R) \ M and rows of R ∩ R' that moved.
  *
  * Compile-time ORACLE_MUTANT = k (k > 0) plants one known mistake; the test
  * suite builds those variants on the CPU to show that its pins catch them.
@@ -90,10 +112,14 @@ typedef struct {
     int64_t fwd[7];
     int64_t plc[9];
     uint64_t digest;
+    /* set-associative form: nsets sets of `ways` rows each (-1 = free way) */
+    int64_t nsets;
+    int32_t *way_row, *way_row0;
+    uint8_t *in_r0;
 } otab;
 
 typedef struct {
-    int32_t T, policy, es, nthreads;
+    int32_t T, policy, es, nthreads, ways;
     int64_t placements, forwards;
     otab *t;
 } oracle_t;
@@ -141,6 +167,7 @@ void oracle_destroy(void *h) {
         free(tb->last_idx); free(tb->U); free(tb->M);
         free(tb->in_u); free(tb->in_m); free(tb->in_p); free(tb->c);
         free(tb->lastP);
+        free(tb->way_row); free(tb->way_row0); free(tb->in_r0);
     }
     free(o->t);
     free(o);
@@ -148,11 +175,12 @@ void oracle_destroy(void *h) {
 
 void *oracle_create(int32_t T, const int64_t *rows, const int32_t *dims, const int32_t *dtypes,
                     const void *const *tables, const int64_t *caps, int32_t policy, int32_t es,
-                    int32_t nthreads) {
+                    int32_t nthreads, int32_t ways) {
     if (T <= 0 || !rows || !dims || !dtypes || !tables || !caps) return NULL;
     if (policy != O_LRU_BATCH && policy != O_PRIORITY) return NULL;
+    if (ways < 0) return NULL;
     oracle_t *o = (oracle_t *)calloc(1, sizeof(oracle_t));
-    o->T = T; o->policy = policy; o->es = es; o->nthreads = nthreads > 0 ? nthreads : 1;
+    o->T = T; o->policy = policy; o->es = es; o->nthreads = nthreads > 0 ? nthreads : 1; o->ways = ways;
     o->t = (otab *)calloc((size_t)T, sizeof(otab));
     for (int32_t t = 0; t < T; ++t) {
         otab *tb = &o->t[t];
@@ -169,6 +197,14 @@ void *oracle_create(int32_t T, const int64_t *rows, const int32_t *dims, const i
         tb->res = (int32_t *)malloc(sizeof(int32_t) * (size_t)(tb->cap + 1));
         tb->in_u = (uint8_t *)calloc(n, 1); tb->in_m = (uint8_t *)calloc(n, 1);
         tb->in_p = (uint8_t *)calloc(n, 1); tb->c = (uint8_t *)calloc(n, 1);
+        if (ways > 0) {
+            tb->nsets = tb->cap / ways;
+            size_t nw = (size_t)(tb->nsets * ways) + 1;
+            tb->way_row = (int32_t *)malloc(sizeof(int32_t) * nw);
+            tb->way_row0 = (int32_t *)malloc(sizeof(int32_t) * nw);
+            for (size_t k = 0; k < nw; ++k) tb->way_row[k] = -1;
+            tb->in_r0 = (uint8_t *)calloc(n, 1);
+        }
     }
     return o;
 }
@@ -189,6 +225,8 @@ static int key_desc(const void *a, const void *b) {
     return 0;
 }
 
+static void place_table_sa(oracle_t *o, int32_t t, const int32_t *P, int64_t nP);
+
 static void place_table(oracle_t *o, int32_t t, const int32_t *P, int64_t nP, const uint8_t *bits) {
     otab *tb = &o->t[t];
     const int64_t b = o->placements;
@@ -204,6 +242,10 @@ static void place_table(oracle_t *o, int32_t t, const int32_t *P, int64_t nP, co
             if (bits[tb->last_base + i]) tb->c[tb->last_idx[i]] = 1;
 #endif
         }
+    }
+    if (o->ways > 0) {
+        place_table_sa(o, t, P, nP);
+        return;
     }
     /* 1. aging (PRIORITY) */
 #if ORACLE_MUTANT != 2 /* planted (2): no aging */
@@ -301,6 +343,157 @@ static void place_table(oracle_t *o, int32_t t, const int32_t *P, int64_t nP, co
     tb->have_plc = 1;
     free(K);
     free(pnew);
+}
+
+/* --------------------------------------------------- set-associative placement */
+
+static int cmp_row(const void *a, const void *b) {
+    int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+#if ORACLE_MUTANT == 14 /* planted: events of a set taken in descending row order */
+    return (x < y) - (x > y);
+#else
+    return (x > y) - (x < y);
+#endif
+}
+
+static int64_t set_of(const otab *tb, int32_t r, int32_t ways) {
+#if ORACLE_MUTANT == 16 /* planted: the set index taken modulo the ways */
+    return ((int64_t)r % ways) % tb->nsets;
+#else
+    (void)ways;
+    return (int64_t)r % tb->nsets;
+#endif
+}
+
+/* Put row r with score v into its set (Alg. 1's fetch; Alg. 2 when the set is full). */
+static void sa_insert(oracle_t *o, otab *tb, int32_t r, int64_t v) {
+    const int32_t W = o->ways;
+    if (tb->nsets == 0) return; /* no sets: r is dropped */
+    int32_t *set = tb->way_row + set_of(tb, r, W) * W;
+    int32_t w = -1;
+    for (int32_t k = 0; k < W && w < 0; ++k)
+        if (set[k] < 0) w = k;
+    if (w < 0) {
+        /* Alg. 2: scan the set for the lowest score; a later way replaces the
+         * incumbent only if strictly lower */
+#if ORACLE_MUTANT == 12 /* planted: the set ages before the victim is chosen */
+        if (o->policy == O_PRIORITY)
+            for (int32_t k = 0; k < W; ++k) tb->s[set[k]] = tb->s[set[k]] > 0 ? tb->s[set[k]] - 1 : 0;
+#endif
+        w = 0;
+        for (int32_t k = 1; k < W; ++k)
+#if ORACLE_MUTANT == 11 /* planted: among equal scores the last way is the victim */
+            if (tb->s[set[k]] <= tb->s[set[w]]) w = k;
+#else
+            if (tb->s[set[k]] < tb->s[set[w]]) w = k;
+#endif
+#if ORACLE_MUTANT != 12 && ORACLE_MUTANT != 15
+        if (o->policy == O_PRIORITY)
+            for (int32_t k = 0; k < W; ++k) tb->s[set[k]] = tb->s[set[k]] > 0 ? tb->s[set[k]] - 1 : 0;
+#endif
+        tb->in_r[set[w]] = 0;
+    }
+    set[w] = r;
+    tb->in_r[r] = 1;
+    tb->s[r] = v;
+}
+
+static void place_table_sa(oracle_t *o, int32_t t, const int32_t *P, int64_t nP) {
+    otab *tb = &o->t[t];
+    const int64_t b = o->placements;
+    const int lru = o->policy == O_LRU_BATCH;
+    const int32_t W = o->ways;
+    const int64_t nslot = tb->nsets * W;
+    int64_t nU = tb->have_fwd ? tb->nU : 0, nM = tb->have_fwd ? tb->nM : 0;
+
+    memcpy(tb->way_row0, tb->way_row, sizeof(int32_t) * (size_t)(nslot + 1));
+    for (int64_t k = 0; k < nslot; ++k)
+        if (tb->way_row0[k] >= 0) tb->in_r0[tb->way_row0[k]] = 1;
+#if ORACLE_MUTANT == 15 /* planted: every resident ages once per placement instead of per scan */
+    if (!lru)
+        for (int64_t k = 0; k < nslot; ++k)
+            if (tb->way_row[k] >= 0) {
+                int32_t r = tb->way_row[k];
+                tb->s[r] = tb->s[r] > 0 ? tb->s[r] - 1 : 0;
+            }
+#endif
+    /* A. accessed residents: prefetch flag cleared, touch score */
+    for (int64_t k = 0; k < nU; ++k) {
+        int32_t r = tb->U[k];
+        if (tb->in_r[r]) {
+            tb->pf[r] = 0;
+            tb->s[r] = lru ? b - 1 : (int64_t)tb->c[r] + o->es;
+        }
+    }
+    /* distinct prefetch rows, ascending */
+    int64_t pscore = lru ? b : o->es;
+    int32_t *pd = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nP + 1));
+    int64_t npd = 0;
+    for (int64_t k = 0; k < nP; ++k)
+        if (!tb->in_p[P[k]]) { tb->in_p[P[k]] = 1; pd[npd++] = P[k]; }
+    free(tb->lastP);
+    tb->lastP = (int32_t *)malloc(sizeof(int32_t) * (size_t)(npd + 1));
+    memcpy(tb->lastP, pd, sizeof(int32_t) * (size_t)npd);
+    tb->nlastP = npd;
+    qsort(pd, (size_t)npd, sizeof(int32_t), cmp_row);
+    int32_t *ms = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nM + 1));
+    memcpy(ms, tb->M, sizeof(int32_t) * (size_t)nM);
+    qsort(ms, (size_t)nM, sizeof(int32_t), cmp_row);
+#if ORACLE_MUTANT == 13 /* planted: prefetch events before the misses */
+    for (int64_t k = 0; k < npd; ++k) {
+        int32_t r = pd[k];
+        if (tb->in_r[r]) { if (pscore > tb->s[r]) tb->s[r] = pscore; }
+        else sa_insert(o, tb, r, pscore);
+    }
+    for (int64_t k = 0; k < nM; ++k) if (!tb->in_r[ms[k]]) sa_insert(o, tb, ms[k], lru ? b - 1 : (int64_t)tb->c[ms[k]] + o->es);
+#else
+    /* B. misses, ascending */
+    for (int64_t k = 0; k < nM; ++k) sa_insert(o, tb, ms[k], lru ? b - 1 : (int64_t)tb->c[ms[k]] + o->es);
+    /* C. prefetch rows, ascending */
+    for (int64_t k = 0; k < npd; ++k) {
+        int32_t r = pd[k];
+        if (tb->in_r[r]) {
+            if (pscore > tb->s[r]) tb->s[r] = pscore;
+        } else {
+            sa_insert(o, tb, r, pscore);
+        }
+    }
+#endif
+    /* counters and prefetch flags */
+    int64_t evicted = 0, adm_miss = 0, fill = 0, p_res = 0, p_drop = 0, m_drop = 0;
+    for (int64_t k = 0; k < nslot; ++k)
+        if (tb->way_row0[k] >= 0 && !tb->in_r[tb->way_row0[k]]) ++evicted;
+    uint64_t dig = 0;
+    tb->nres = 0;
+    for (int64_t k = 0; k < nslot; ++k) {
+        int32_t r = tb->way_row[k];
+        if (r < 0) continue;
+        if (tb->way_row0[k] != r) { /* newly admitted, or moved to another way */
+            if (tb->in_m[r]) ++adm_miss; else ++fill;
+            tb->pf[r] = tb->in_p[r];
+        }
+        tb->res[tb->nres++] = r;
+        dig += oracle_splitmix64_mix(((uint64_t)t << 40) | (uint64_t)r);
+    }
+    for (int64_t k = 0; k < nM; ++k) if (!tb->in_r[ms[k]]) ++m_drop;
+    for (int64_t k = 0; k < npd; ++k) {
+        if (tb->in_r0[pd[k]]) ++p_res;
+        else if (!tb->in_r[pd[k]]) ++p_drop;
+    }
+    /* clear scratch marks */
+    for (int64_t k = 0; k < nslot; ++k)
+        if (tb->way_row0[k] >= 0) tb->in_r0[tb->way_row0[k]] = 0;
+    for (int64_t k = 0; k < npd; ++k) tb->in_p[pd[k]] = 0;
+    for (int64_t k = 0; k < nU; ++k) { tb->in_m[tb->U[k]] = 0; tb->c[tb->U[k]] = 0; }
+
+    tb->plc[0] = evicted; tb->plc[1] = adm_miss; tb->plc[2] = fill; tb->plc[3] = p_res;
+    tb->plc[4] = p_drop; tb->plc[5] = m_drop; tb->plc[6] = tb->nres; tb->plc[7] = fill * tb->row_bytes;
+    tb->plc[8] = tb->nlastP;
+    tb->digest = dig;
+    tb->have_fwd = 0;
+    tb->have_plc = 1;
+    free(pd);
+    free(ms);
 }
 
 /* ----------------------------------------------------------------- forward */

@@ -17,6 +17,13 @@ Sources of truth used here:
     eviction_speed 0 the priority policy reduces to ranking by row id;
   * invariants: hits + misses = distinct rows, |R| <= Cap, resident-count
     conservation, digest = sum of SplitMix64 mixes over the resident dump.
+Set-associative caches (ways W > 0) are pinned by three hand-worked traces and:
+  * a direct-mapped cache (W = 1) holds, per set, the largest prefetched row of
+    the set if any, else the largest missed row, else what it held;
+  * LRU_BATCH with one event per set per batch keeps, per set, the W rows with
+    the latest events (no ties, so the closed form is exact);
+  * when every set can hold all of its rows, nothing is evicted;
+  * invariants: at most W residents per set, digest over the dump.
 """
 import numpy as np
 import torch
@@ -25,7 +32,8 @@ import oracle
 import tracegen as tg
 from _helpers import golden_table, load_golden, splitmix64_mix_py
 
-GOLDEN_FILES = ("hand_lru.json", "hand_priority_es4.json", "hand_priority_es1.json", "hand_priority_es0.json")
+GOLDEN_FILES = ("hand_lru.json", "hand_priority_es4.json", "hand_priority_es1.json", "hand_priority_es0.json",
+                "hand_sa_lru_w2.json", "hand_sa_priority_w2.json", "hand_sa_priority_es1.json")
 
 
 # ----------------------------------------------------------------------------- drivers
@@ -63,7 +71,7 @@ def pin_hand_examples(mutant=0):
         g = load_golden(name)
         tab = golden_table(g)
         o = oracle.Oracle([tab], ["f32"], [g["cap"]], policy=g["policy"], eviction_speed=g["eviction_speed"],
-                          mutant=mutant)
+                          mutant=mutant, ways=g.get("ways", 0))
         for b, step in enumerate(g["steps"]):
             P = np.array(step["prefetch"], np.int32)
             bits = None if step["bits"] is None else np.array(step["bits"], np.uint8)
@@ -276,5 +284,123 @@ def pin_prefetch_quality(mutant=0, seeds=range(30)):
     o.close()
 
 
+# ----------------------------------------------------------------------------- set-associative
+
+def pin_sa_direct_mapped(mutant=0, seeds=range(30)):
+    """W = 1: every insertion replaces the set's only row, so after a placement
+    a set holds its largest row of set(P) if it has one, else its largest miss
+    of the last batch, else its previous row (misses first, then prefetches,
+    each ascending; Alg. 1 inserts unconditionally)."""
+    for s in seeds:
+        w = tg.random_tiny(s, max_rows=24, max_cap=8, batches=6)
+        w.ways = 1
+        _, recs = run_oracle(w, mutant=mutant, want64=False)
+        T = w.num_tables
+        held = [dict() for _ in range(T)]  # set -> row
+        M_prev = [set() for _ in range(T)]
+        for b, r in enumerate(recs):
+            for t in range(T):
+                S = min(w.tables[t].cap, w.tables[t].rows)
+                P = set(r["P"][r["poff"][t]:r["poff"][t + 1]].tolist())
+                if S > 0:
+                    for st in range(S):
+                        ps = [x for x in P if x % S == st]
+                        ms = [x for x in M_prev[t] if x % S == st]
+                        if ps:
+                            held[t][st] = max(ps)
+                        elif ms:
+                            held[t][st] = max(ms)
+                assert r["resident"][t].tolist() == sorted(held[t].values()), f"seed {s} batch {b} table {t}"
+            for t, (a, e) in enumerate(segments(w, r["off"])):
+                U = set(r["idx"][a:e].tolist())
+                R = set(held[t].values())
+                M_prev[t] = U - R
+                assert r["fwd"][t]["misses"] == len(U - R) and r["fwd"][t]["hits"] == len(U & R)
+
+
+def pin_sa_lru_distinct_events(mutant=0, seeds=range(30)):
+    """LRU_BATCH in W-way sets when every batch touches at most one row per set
+    and the placement before it prefetches at most one row per set, in sets the
+    batch does not touch (a prefetch before forward p and an access in forward
+    p carry the same stamp p): stamps within a set never tie, and the cache
+    keeps, per set, the W rows whose latest event is most recent."""
+    for s in seeds:
+        g = np.random.Generator(np.random.Philox(np.random.SeedSequence(4242, spawn_key=(s,))))
+        S = int(g.integers(1, 5))
+        W = int(g.integers(1, 4))
+        per = int(g.integers(W + 1, W + 5))  # rows per set
+        n = S * per
+        cap = S * W + int(g.integers(0, W))  # leftover slots stay unused
+        tab = np.arange(n, dtype=np.float32)[:, None]
+        o = oracle.Oracle([tab], ["f32"], [cap], policy="lru", ways=W, mutant=mutant)
+        last = {}
+        for b in range(8):
+            sets = [x for x in range(S) if g.random() < 0.7]
+            P = np.array([x + S * int(g.integers(0, per)) for x in range(S) if x not in sets and g.random() < 0.6],
+                         np.int32)
+            assert o.placement(P, np.array([0, P.size], np.int64), None) == 0
+            for x in P.tolist():
+                last[x] = b
+            R = set()
+            for st in range(S):
+                rows = sorted((x for x in last if x % S == st), key=lambda x: last[x], reverse=True)
+                R |= set(rows[:W])
+            assert o.resident(0).tolist() == sorted(R), f"seed {s} placement {b}"
+            idx = np.array([x + S * int(g.integers(0, per)) for x in sets], np.int32)
+            assert o.forward(idx, np.array([0, idx.size], np.int64), 1)[0] == 0
+            st = o.stats(0)
+            U = set(idx.tolist())
+            assert st["hits"] == len(U & R) and st["misses"] == len(U - R)
+            for x in U:
+                last[x] = b
+        o.close()
+
+
+def pin_sa_no_eviction(mutant=0, seeds=range(12)):
+    """Cap = N with W dividing N: each of the N / W sets owns exactly W rows, so
+    no set overflows; the cache holds every row offered so far."""
+    for s in seeds:
+        w = tg.random_tiny(s, max_rows=12, batches=5)
+        for tb in w.tables:
+            tb.rows = 12
+            tb.cap = 12
+        w.ways = (1, 2, 3, 4, 6, 12)[s % 6]
+        _, recs = run_oracle(w, mutant=mutant, want64=False)
+        seen = [set() for _ in w.tables]
+        for b, r in enumerate(recs):
+            for t in range(w.num_tables):
+                seen[t] |= set(r["P"][r["poff"][t]:r["poff"][t + 1]].tolist())
+                assert r["resident"][t].tolist() == sorted(seen[t]), f"seed {s} batch {b} table {t}"
+                assert r["place"][t]["evicted"] == 0
+            for t, (a, e) in enumerate(segments(w, r["off"])):
+                U = set(r["idx"][a:e].tolist())
+                assert r["fwd"][t]["misses"] == len(U - seen[t])
+                seen[t] |= U
+
+
+def pin_sa_invariants(mutant=0, seeds=range(30)):
+    for s in seeds:
+        w = tg.random_tiny(s, max_rows=30, max_cap=12, batches=6)
+        w.ways = 1 + s % 4
+        _, recs = run_oracle(w, mutant=mutant, want64=False)
+        prev = [0] * w.num_tables
+        for r in recs:
+            for t, (a, e) in enumerate(segments(w, r["off"])):
+                f, p = r["fwd"][t], r["place"][t]
+                S = min(w.tables[t].cap, w.tables[t].rows) // w.ways
+                res = r["resident"][t]
+                assert f["hits"] + f["misses"] == f["unique"] == np.unique(r["idx"][a:e]).size
+                assert p["resident"] == res.size <= S * w.ways
+                if S:
+                    assert np.bincount(res % S, minlength=S).max(initial=0) <= w.ways
+                else:
+                    assert res.size == 0
+                assert p["resident"] <= prev[t] - p["evicted"] + p["admitted_miss"] + p["prefetch_fill"]
+                dig = sum(splitmix64_mix_py((t << 40) | int(x)) for x in res) & ((1 << 64) - 1)
+                assert p["digest"] == dig
+                prev[t] = p["resident"]
+
+
 ALL_PINS = (pin_hand_examples, pin_embedding_bag, pin_splitmix, pin_lru_history, pin_unbounded_cache,
-            pin_zero_capacity, pin_priority_es0, pin_invariants, pin_prefetch_quality)
+            pin_zero_capacity, pin_priority_es0, pin_invariants, pin_prefetch_quality, pin_sa_direct_mapped,
+            pin_sa_lru_distinct_events, pin_sa_no_eviction, pin_sa_invariants)

@@ -16,6 +16,12 @@ MUTANTS = {
     8: "digest forgets the table id",
     9: "aging does not saturate at 0",
     10: "coverage counts lookups with their repeats",
+    11: "set-associative: ties evict the last way",
+    12: "set-associative: the set ages before the victim is chosen",
+    13: "set-associative: prefetch rows inserted before the misses",
+    14: "set-associative: events of a set in descending row order",
+    15: "set-associative: aging once per placement instead of per eviction",
+    16: "set-associative: set index taken modulo the ways",
 }
 
 

@@ -222,6 +222,8 @@ class Workload:
     # noise; ("optgen", frac, horizon) = Belady-optimal labels (optgen_labels)
     # for a buffer of frac * Cap rows over the first `horizon` batches
     bits: Tuple = ("lookahead",)
+    # 0: fully associative caches; W > 0: W-way set-associative caches
+    ways: int = 0
 
     def __post_init__(self):
         self._cache: dict = {}
@@ -531,7 +533,8 @@ def scaled_config(cid: int, row_scale: float = 1.0, batches: Optional[int] = Non
         new.append(dataclasses.replace(tb, rows=rows, cap=cap))
     w2 = Workload(config_id if config_id is not None else 100 + cid, w.name + "_scaled", new,
                   batches=batches or w.batches, bags=bags or w.bags, policy=w.policy,
-                  eviction_speed=w.eviction_speed, prefetch=w.prefetch, drift=w.drift, bit_flip=w.bit_flip)
+                  eviction_speed=w.eviction_speed, prefetch=w.prefetch, drift=w.drift, bit_flip=w.bit_flip,
+                  ways=w.ways)
     for k, v in overrides.items():
         setattr(w2, k, v)
     return w2
