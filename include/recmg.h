@@ -11,7 +11,8 @@
  * the end of each batch" by Alg. 1 (load_embeddings) and Alg. 2
  * (gpu_buffer_populate).
  *
- * Cache semantics, per table t (fully associative, one cache per table):
+ * Cache semantics, per table t (fully associative, one cache per table;
+ * config.ways selects the set-associative form below):
  *   keys are (score, row); the cache keeps the min(Cap_t, |K|) largest keys of
  *   K = resident ∪ last batch's misses ∪ set(prefetch list); among equal
  *   scores the lower row id is evicted first.
@@ -21,6 +22,20 @@
  *   placement; a touched row scores bit + eviction_speed, with bit the OR of
  *   its caching bits in the last batch; a prefetched row scores
  *   max(its score, eviction_speed).
+ *
+ * Set-associative form (config.ways = W > 0; the production buffer of Sec.
+ * VI-B is a W-way set-associative software cache, Sec. VII-B and VII-E): a
+ * table has S = floor(Cap_t / W) sets of W slots (Cap_t mod W slots unused; S
+ * = 0 caches nothing) and row r belongs to set r mod S.  Alg. 1 and Alg. 2
+ * run literally inside each set: rows the last batch touched take the touch
+ * score (no aging); then the set's misses, ascending by row, and the set's
+ * distinct prefetch rows, ascending, are inserted (a resident prefetched row
+ * only keeps max(score, prefetch score)).  An insertion takes the lowest free
+ * slot of the set; in a full set, the lowest slot holding the minimum score
+ * is the victim and, under PRIORITY, every slot of the set then ages by one
+ * (saturating at 0).  A row that ends in a slot other than the one it started
+ * in has prefetch flag [row in P]; such a row, when it was resident before and
+ * moved, is read from the host again and counts in prefetch_fill.
  *
  * Call order:  recmg_cache_init -> { recmg_apply_placement ->
  *              recmg_embbag_forward }* -> recmg_stats -> recmg_cache_destroy.
@@ -101,6 +116,8 @@ typedef struct {
                                            compute stream */
     int32_t timing;                     /* initial timing level (see recmg_set_timing): 0 none,
                                            1 the pooled kernel only, 2 every stage */
+    int32_t ways;                       /* 0: fully associative caches.  1 .. 64: W-way
+                                           set-associative caches (see below) */
 } recmg_config_t;
 
 /* Stages timed at timing level 2 (RECMG_STAGE_FWD_POOL from level 1 on). */

@@ -55,6 +55,7 @@ class recmg_config_t(ctypes.Structure):
         ("host_staging_bytes", ctypes.c_size_t),
         ("copy_stream", ctypes.c_void_p),
         ("timing", ctypes.c_int32),
+        ("ways", ctypes.c_int32),
     ]
 
 
@@ -163,12 +164,13 @@ class TieredEmbeddingCache:
 
     host_tables: CPU tensors [rows, dim], float32 / float16 / bfloat16 (or
     uint16 holding bfloat16 bits), pinned for miss_mode="zero_copy".  They must
-    outlive the cache."""
+    outlive the cache.  ways = 0: fully associative caches; W in 1..64: W-way
+    set-associative caches (Alg. 2 inside each set)."""
 
     def __init__(self, host_tables: Sequence, dtypes: Sequence[str], cache_rows: Sequence[int], *,
                  policy: str = "lru", eviction_speed: int = 4, miss_mode: str = "zero_copy",
                  max_bags_per_table: int, max_indices: int, max_prefetch: int, validate: bool = False,
-                 timing: int = 0, overlap: bool = True, workspace=None, device: int = 0):
+                 timing: int = 0, overlap: bool = True, workspace=None, device: int = 0, ways: int = 0):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", device)
@@ -195,6 +197,7 @@ class TieredEmbeddingCache:
         cfg.miss_mode = MISS_CODES[miss_mode]
         cfg.validate = int(bool(validate))
         cfg.timing = 2 if timing is True else int(timing)  # 0 off, 1 pooled kernel, 2 every stage
+        cfg.ways = int(ways)  # 0 fully associative, W > 0 W-way set-associative
         cfg.max_bags_per_table = int(max_bags_per_table)
         cfg.max_indices = int(max_indices)
         cfg.max_prefetch = int(max_prefetch)

@@ -54,11 +54,13 @@ struct Geom {
     int64_t map_cap = 0, bm_words = 0;
     int32_t bm_nblk = 0, gsz = 0, nchunk = 0, vec = 0, bpb = 0, copy_unit = 0;
     int32_t wlw = 0, wr = 0, wnch = 0, kind = 0;
+    int32_t ways = 0, nsets = 0, qbits = 0;  // set-associative form (ways > 0)
 };
 
 struct Layout {
     size_t total = 0, host_total = 0;
-    std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, slot_cbit, free_stack, map, bitmap, rank;
+    std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, slot_cbit, free_stack, map, bitmap, rank,
+        seg;
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, raddr = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
     size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, pool_btab = 0, ftstart = 0;
@@ -81,6 +83,7 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
         return fail(RECMG_E_INVALID, "eviction_speed out of [0, 2^20]");
     if (cfg->miss_mode != RECMG_ZERO_COPY && cfg->miss_mode != RECMG_STAGED) return fail(RECMG_E_INVALID, "bad miss_mode");
     if (cfg->timing < 0 || cfg->timing > 2) return fail(RECMG_E_INVALID, "timing must be 0, 1 or 2");
+    if (cfg->ways < 0 || cfg->ways > 64) return fail(RECMG_E_INVALID, "ways out of [0, 64]");
     if (cfg->max_bags_per_table < 0 || cfg->max_indices < 0 || cfg->max_indices >= (int64_t(1) << 31) ||
         cfg->max_prefetch < 0 || cfg->max_prefetch >= (int64_t(1) << 31))
         return fail(RECMG_E_INVALID, "max_* sizes out of range");
@@ -99,8 +102,21 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
         g.esz = g.dtype == RECMG_F32 ? 4 : 2;
         g.row_bytes = g.dim * g.esz;
         g.cap = (int32_t)std::min<int64_t>(cfg->cache_rows[t], g.rows);
-        g.map_cap = pow2ceil(std::max<int64_t>(64, 4 * (int64_t)g.cap));  // load <= 1/4
-        const int64_t words = (g.rows + 31) / 32;
+        int64_t bm_bits = g.rows;
+        if (cfg->ways > 0) {
+            // floor(Cap / W) sets of W ways; the Cap mod W slots left over stay
+            // unused, and a table with no set caches nothing (the fully
+            // associative path with Cap 0 does exactly that)
+            g.nsets = g.cap / cfg->ways;
+            g.cap = g.nsets * cfg->ways;
+            if (g.nsets > 0) {
+                g.ways = cfg->ways;
+                g.qbits = bitlen((uint64_t)((g.rows - 1) / g.nsets));
+                bm_bits = (int64_t)g.nsets << g.qbits;  // < 2 N_t
+            }
+        }
+        g.map_cap = g.ways ? 64 : pow2ceil(std::max<int64_t>(64, 4 * (int64_t)g.cap));  // load <= 1/4
+        const int64_t words = (bm_bits + 31) / 32;
         g.bm_nblk = (int32_t)((words + kWordsPerBlock - 1) / kWordsPerBlock);
         g.bm_words = (int64_t)g.bm_nblk * kWordsPerBlock;
         g.vec = g.row_bytes % 16 == 0;
@@ -153,6 +169,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
         L->map.push_back(take((size_t)g.map_cap * 8));
         L->bitmap.push_back(take((size_t)g.bm_words * 4));
         L->rank.push_back(take((size_t)g.bm_words * 16));
+        L->seg.push_back(take((size_t)g.nsets * 16));
         L->total_bm_blocks += g.bm_nblk;
         L->sum_cap += g.cap;
     }
@@ -214,7 +231,8 @@ struct recmg_cache {
     Layout L;
     DGlobal g{};
     std::vector<const char *> host;  // host tables (host pointers)
-    int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1;
+    int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1, max_sets = 0;
+    bool has_fa = false, has_sa = false;  // tables of each form present
     std::vector<int32_t> pool_order;  // table ids ordered by pooled-kernel kind
     std::vector<PoolLaunch> pool_launches;
     int64_t max_rows = 0;
@@ -624,6 +642,13 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         d.wlw = ge.wlw;
         d.wr = ge.wr;
         d.wnch = ge.wnch;
+        d.ways = ge.ways;
+        d.nsets = ge.ways ? ge.nsets : 0;
+        d.qbits = ge.qbits;
+        d.seg = reinterpret_cast<int4 *>(ws + L.seg[t]);
+        if (ge.ways) c->has_sa = true;
+        else c->has_fa = true;
+        if (ge.ways) c->max_sets = std::max(c->max_sets, ge.nsets);
         bstart[t + 1] = bstart[t] + ge.bm_nblk;
         out_off += ge.dim;
         cap_off += ge.cap;
@@ -650,6 +675,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         HIP_TRY(hipMemsetAsync(ws + L.map[t], 0xff, (size_t)ge.map_cap * 8, s0));
         HIP_TRY(hipMemsetAsync(ws + L.bitmap[t], 0, (size_t)ge.bm_words * 4, s0));
         HIP_TRY(hipMemsetAsync(ws + L.rank[t], 0xff, (size_t)ge.bm_words * 16, s0));  // stamp -1
+        HIP_TRY(hipMemsetAsync(ws + L.seg[t], 0, (size_t)ge.nsets * 16, s0));
     }
     HIP_TRY(hipMemsetAsync(ws + L.st, 0, sizeof(TState) * T, s0));
     HIP_TRY(hipMemsetAsync(ws + L.tstart, 0, 8 * (T + 1), s0));
@@ -735,13 +761,14 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     const int64_t cand = (c->have_fwd ? c->last_n : 0) + num_prefetch;
     const int64_t per_table = c->max_cap + (cand + c->T - 1) / c->T;
     const int64_t cand_grid = std::min<int64_t>(std::max<int64_t>(cand / c->T, 1024), cand + 1);
-    {
+    if (c->has_fa) {
         StageTimer tm(c, RECMG_STAGE_PLC_RANK, s);
         launch_plc_rank(g, p, per_table, s);
     }
     {
         StageTimer tm(c, RECMG_STAGE_PLC_APPLY, s);
-        launch_plc_apply(g, p, c->max_cap, c->max_map, cand_grid, s);
+        if (c->has_fa) launch_plc_apply(g, p, c->max_cap, c->max_map, cand_grid, s);
+        if (c->has_sa) launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->max_sets, s);
     }
     if (c->cfg.miss_mode == RECMG_STAGED) {
         // host-staged prefetch rows; the fill overlaps the next forward when a copy stream is given

@@ -11,6 +11,11 @@
 // O(ids + N_t / 32) with no comparison passes, which suits ids drawn from a
 // bounded domain; the emit clears the bitmap behind it.
 //
+// Set-associative tables mark row r at bm_pos(r) = (set << qbits) | (r / nsets)
+// instead of r, so U and PU come out grouped by set and ascending within each
+// set (the order in which a set takes its events); the resident dump keeps
+// plain row positions.
+//
 // Marking: Zipf-popular rows make many threads set the same bit.  Each block
 // first deduplicates its ids in a small LDS hash set, so a popular row costs
 // one global atomic per block instead of one per occurrence.
@@ -27,12 +32,15 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
     __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
     __shared__ int64_t s_rows[RECMG_MAX_TABLES];
     __shared__ uint32_t *s_bm[RECMG_MAX_TABLES];
+    __shared__ int32_t s_ns[RECMG_MAX_TABLES], s_qb[RECMG_MAX_TABLES];
     __shared__ unsigned long long s_set[kLdsSet];
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         s_start[t] = starts[t];
         if (t < g.T) {
             s_rows[t] = g.tabs[t].rows;
             s_bm[t] = g.tabs[t].bitmap;
+            s_ns[t] = g.tabs[t].nsets;
+            s_qb[t] = g.tabs[t].qbits;
         }
     }
     for (int k = threadIdx.x; k < kLdsSet; k += blockDim.x) s_set[k] = ~0ull;
@@ -62,8 +70,9 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
             h = (h + 1) & (kLdsSet - 1);
         }
         if (mine) {
-            uint32_t *w = s_bm[t] + (r >> 5);
-            const uint32_t bit = 1u << (r & 31);
+            const uint32_t pos = bm_pos(s_ns[t], s_qb[t], r);
+            uint32_t *w = s_bm[t] + (pos >> 5);
+            const uint32_t bit = 1u << (pos & 31);
             if (!(__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit)) atomicOr(w, bit);
         }
     }
@@ -149,7 +158,8 @@ __global__ void __launch_bounds__(kBlock) k_bm_emit(DGlobal g, int32_t stamp) {
         while (bits) {
             const int b = __ffs(bits) - 1;
             bits &= bits - 1;
-            out[u++] = (int32_t)(word * 32 + b);
+            const uint32_t pos = (uint32_t)(word * 32 + b);
+            out[u++] = MODE == EMIT_DUMP ? (int32_t)pos : bm_row(tb, pos);
         }
     }
 }

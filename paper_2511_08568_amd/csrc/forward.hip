@@ -55,16 +55,18 @@ __global__ void __launch_bounds__(kBlock) k_fwd_cover(DGlobal g, int32_t stamp, 
         if (i < np) {
             t = find_seg(s_pstart, g.T, i);
             if (i - s_pstart[t] < s_pc[t]) {
-                const int32_t row = g.PU[i];
-                const uint4 rk = g.tabs[t].rank[row >> 5];
-                hit = (int32_t)rk.z == stamp && (rk.y & (1u << (row & 31)));
+                const DTable &tb = g.tabs[t];
+                const uint32_t pos = bm_pos(tb, g.PU[i]);
+                const uint4 rk = tb.rank[pos >> 5];
+                hit = (int32_t)rk.z == stamp && (rk.y & (1u << (pos & 31)));
             }
         }
         (void)wave_append(hit, t, &g.st[0].covered, stride_st);  // counts only
     }
 }
 
-// Cache probe of every distinct row (row -> slot map): hits are stamped and
+// Cache probe of every distinct row (row -> slot map, or a scan of the row's
+// set in a set-associative table): hits are stamped and
 // counted, misses are numbered (their staging row).  One thread per slot of
 // the index space; table t's distinct rows occupy [tstart[t], + ucount).
 __global__ void __launch_bounds__(kBlock) k_fwd_probe(DGlobal g, int32_t stamp, int64_t n) {
@@ -90,7 +92,7 @@ __global__ void __launch_bounds__(kBlock) k_fwd_probe(DGlobal g, int32_t stamp, 
         if (valid) {
             const DTable &tb = g.tabs[t];
             row = g.U[i];
-            const int32_t slot = map_find(tb, row);
+            const int32_t slot = find_slot(tb, row);
             if (slot >= 0) {
                 g.slotU[i] = slot;
                 tb.slot_touch[slot] = stamp;
@@ -119,22 +121,24 @@ __global__ void __launch_bounds__(kBlock) k_fwd_src(DGlobal g, const int32_t *__
     __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
     __shared__ const uint4 *s_rank[RECMG_MAX_TABLES];
     __shared__ const char *s_pool[RECMG_MAX_TABLES];
-    __shared__ int32_t s_rb[RECMG_MAX_TABLES];
+    __shared__ int32_t s_rb[RECMG_MAX_TABLES], s_ns[RECMG_MAX_TABLES], s_qb[RECMG_MAX_TABLES];
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         s_start[t] = g.tstart[t];
         if (t < g.T) {
             s_rank[t] = g.tabs[t].rank;
             s_pool[t] = g.tabs[t].pool;
             s_rb[t] = g.tabs[t].row_bytes;
+            s_ns[t] = g.tabs[t].nsets;
+            s_qb[t] = g.tabs[t].qbits;
         }
     }
     __syncthreads();
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
         const int t = find_seg(s_start, g.T, i);
-        const int32_t r = indices[i];
-        const uint4 rk = s_rank[t][r >> 5];
-        const int32_t u = (int32_t)rk.x + __popc(rk.y & ((1u << (r & 31)) - 1u));
+        const uint32_t pos = bm_pos(s_ns[t], s_qb[t], indices[i]);
+        const uint4 rk = s_rank[t][pos >> 5];
+        const int32_t u = (int32_t)rk.x + __popc(rk.y & ((1u << (pos & 31)) - 1u));
         const int32_t sl = g.slotU[s_start[t] + u];
         g.src[i] = sl;
         g.raddr[i] = sl >= 0 ? (uint64_t)(s_pool[t] + (int64_t)sl * s_rb[t])

@@ -46,7 +46,8 @@ __global__ void k_plc_prep(DGlobal g, const int64_t *__restrict__ poff, int64_t 
             st.p_fill = 0;
             st.p_drop = 0;
             st.m_drop = 0;
-            st.digest_acc = 0ull;
+            // set-associative tables update the digest by the rows that come and go
+            st.digest_acc = g.tabs[t].ways ? st.digest : 0ull;
         }
     }
 }
@@ -95,14 +96,15 @@ __global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last
         if (valid) {
             const DTable &tb = g.tabs[t];
             row = g.PU[i];
-            const int32_t slot = map_find(tb, row);
+            const int32_t slot = find_slot(tb, row);
             if (slot >= 0) {
                 atomicOr(&tb.slot_flags[slot], F_INP);
                 resident = true;
             } else {
                 // distinct rows of the last batch carry its stamp in the rank word
-                const uint4 rk = tb.rank[row >> 5];
-                const uint32_t bit = 1u << (row & 31);
+                const uint32_t pos = bm_pos(tb, row);
+                const uint4 rk = tb.rank[pos >> 5];
+                const uint32_t bit = 1u << (pos & 31);
                 if ((int32_t)rk.z == last_stamp && (rk.y & bit)) {
                     const int64_t ts = g.tstart[t];
                     const int32_t u = (int32_t)rk.x + __popc(rk.y & (bit - 1u));
@@ -212,9 +214,10 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
     TState &st = g.st[t];
     const Counts c = table_counts(tb, st, p);
     if (blockIdx.x == 0 && threadIdx.x == 0) {
-        st.sel_mode = c.mode;
+        st.sel_mode = tb.ways ? SEL_NONE : c.mode;  // set-associative tables place in setassoc.hip
         st.plc_nm = c.nm;
     }
+    if (tb.ways) return;
     const bool sel = c.mode == SEL_SELECT;
     if (sel)
         for (int b = threadIdx.x; b < kRadix; b += blockDim.x) s_hist[b] = 0;
@@ -318,6 +321,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_evict(DGlobal g, PlcParams p) {
     __shared__ int s_base;
     const int t = blockIdx.y;
     const DTable &tb = g.tabs[t];
+    if (tb.ways) return;
     TState &st = g.st[t];
     const int mode = st.sel_mode;
     const uint64_t thr = st.prefix;
@@ -366,6 +370,7 @@ __global__ void __launch_bounds__(kBlock) k_map_clear(DGlobal g) {
     if (*g.err) return;
     const int t = blockIdx.y;
     const DTable &tb = g.tabs[t];
+    if (tb.ways) return;
     TState &st = g.st[t];
     const int64_t mcap = (int64_t)tb.map_mask + 1;
     if ((int64_t)st.tomb * 4 <= mcap) return;
@@ -378,6 +383,7 @@ __global__ void __launch_bounds__(kBlock) k_map_refill(DGlobal g) {
     if (*g.err) return;
     const int t = blockIdx.y;
     const DTable &tb = g.tabs[t];
+    if (tb.ways) return;
     TState &st = g.st[t];
     if (!st.rebuild) return;
     for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < tb.cap; k += (int64_t)gridDim.x * blockDim.x) {
@@ -393,6 +399,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
     __shared__ int s_base;
     const int t = blockIdx.y;
     const DTable &tb = g.tabs[t];
+    if (tb.ways) return;
     TState &st = g.st[t];
     const Counts c = table_counts(tb, st, p);
     const int mode = st.sel_mode;
@@ -501,8 +508,10 @@ __global__ void k_plc_finalize(DGlobal g) {
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         TState &st = g.st[t];
         const DTable &tb = g.tabs[t];
-        st.free_top -= st.popped;  // popped stays: the fill may still read it
-        st.n_res = tb.cap - st.free_top;
+        if (!tb.ways) {  // set-associative tables count residents as they place
+            st.free_top -= st.popped;  // popped stays: the fill may still read it
+            st.n_res = tb.cap - st.free_top;
+        }
         st.rebuild = 0;
         int64_t v[kPlcStats];
         v[0] = st.evicted;

@@ -68,6 +68,14 @@ struct DTable {
     // load instruction reads wr rows of 64 / wr lanes x wlw bytes; a row is
     // wnch such chunks
     int32_t wlw, wr, wnch;
+    // set-associative form (ways > 0): nsets sets of `ways` slots, row r in set
+    // r mod nsets at slots [set * ways, + ways).  Dedup bitmaps index row r at
+    // position (set << qbits) | (r / nsets), so sorted distinct rows come out
+    // grouped by set, ascending within a set.  ways == 0: fully associative
+    // (the map above), bitmap position = row.
+    int32_t ways, nsets, qbits, pad_sa;
+    int4 *seg;  // [nsets] (U begin, U end, PU begin, PU end) of each set in the
+                // current placement, relative to the table's lists; zero between uses
 };
 
 // Mutable per-table state and counters, resident in the workspace.
@@ -223,6 +231,30 @@ __device__ __forceinline__ void map_delete(const DTable &tb, int32_t row) {
     }
 }
 
+// Bitmap position of row r (see DTable::qbits) and its inverse.
+__device__ __forceinline__ uint32_t bm_pos(int32_t nsets, int32_t qbits, int32_t r) {
+    if (!nsets) return (uint32_t)r;
+    const uint32_t u = (uint32_t)r, n = (uint32_t)nsets;
+    return ((u % n) << qbits) | (u / n);
+}
+__device__ __forceinline__ uint32_t bm_pos(const DTable &tb, int32_t r) { return bm_pos(tb.nsets, tb.qbits, r); }
+__device__ __forceinline__ int32_t bm_row(const DTable &tb, uint32_t pos) {
+    if (!tb.nsets) return (int32_t)pos;
+    return (int32_t)((pos & ((1u << tb.qbits) - 1u)) * (uint32_t)tb.nsets + (pos >> tb.qbits));
+}
+
+// Slot of `row` in its set, or -1.
+__device__ __forceinline__ int32_t set_find(const DTable &tb, int32_t row) {
+    const int32_t base = (int32_t)((uint32_t)row % (uint32_t)tb.nsets) * tb.ways;
+    for (int32_t k = 0; k < tb.ways; ++k)
+        if ((int32_t)gload4(tb.slot_row + base + k) == row) return base + k;
+    return -1;
+}
+
+__device__ __forceinline__ int32_t find_slot(const DTable &tb, int32_t row) {
+    return tb.ways ? set_find(tb, row) : map_find(tb, row);
+}
+
 // SplitMix64 output mix (Steele, Lea & Flood, OOPSLA 2014).
 __device__ __forceinline__ unsigned long long mix64(unsigned long long z) {
     z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ULL;
@@ -299,6 +331,12 @@ __device__ __forceinline__ long long block_excl_scan64(long long v, long long *t
     __syncthreads();
     *total = tot;
     return pre + x - v;
+}
+
+__device__ __forceinline__ int wave_min(int v) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) v = min(v, __shfl_xor(v, d, 64));
+    return v;
 }
 
 __device__ __forceinline__ int wave_sum(int v) {

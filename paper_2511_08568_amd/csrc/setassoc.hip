@@ -1,0 +1,254 @@
+// Placement in W-way set-associative tables: Alg. 1 (load_embeddings) and
+// Alg. 2 (gpu_buffer_populate) of Sec. VI-B run literally inside each set.
+//
+// Row r lives in set r mod S, slots [set * W, + W).  Sets are independent, so
+// one wave takes one set, lane w holding way w (row, score, flags) in
+// registers, and plays the set's events in order:
+//   A. rows the last batch touched (slot_touch = its stamp) lose their
+//      prefetch flag and take the touch score: LRU_BATCH the batch stamp,
+//      PRIORITY the OR of their caching bits + eviction_speed;
+//   B. the set's misses of the last batch, ascending by row, are inserted with
+//      their touch score;
+//   C. the set's distinct prefetch rows, ascending by row: a resident one keeps
+//      max(score, prefetch score), any other is inserted with the prefetch score.
+// Insert: the lowest free way, else Alg. 2 over the set: the victim is the
+// lowest way holding the minimum score (scores before this scan), then under
+// PRIORITY every way of the set ages by one, saturating at 0.
+//
+// The events of a set come from the dedup lists: U (the last forward's
+// distinct rows) and PU (this placement's distinct prefetch rows) are emitted
+// grouped by set and ascending within a set (bm_pos), so each set's events are
+// two contiguous segments, found by k_sa_heads and kept in DTable::seg.
+//
+// A way whose row at the end differs from its row at the start gets a fill
+// entry (misses of the last batch from HBM staging, every other row from the
+// host) and the prefetch flag [row in P]; the fill itself is k_plc_fill's.
+// Counters follow the set definitions: evicted |R \ R'|, admitted_miss
+// |(R' \ R) ∩ M|, prefetch_fill = rows read from the host (new rows and rows
+// moved to another way), prefetch_dropped |P \ (R ∪ R')|, miss_dropped
+// |M \ R'|; the digest and the resident count change by what came and went.
+#include "launch.h"
+
+namespace recmg {
+
+// Segment bounds of every set that has events.  Index space: the last
+// forward's distinct rows (all tables, nu), then this placement's distinct
+// prefetch rows (np).  A first element of its set in its table's list writes
+// the begin, a last element the end.
+__global__ void __launch_bounds__(kBlock) k_sa_heads(DGlobal g, int64_t nu, int64_t np, int32_t have_fwd) {
+    if (*g.err) return;
+    __shared__ int64_t s_ts[RECMG_MAX_TABLES + 1], s_ps[RECMG_MAX_TABLES + 1];
+    __shared__ int32_t s_uc[RECMG_MAX_TABLES], s_pc[RECMG_MAX_TABLES];
+    for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
+        s_ts[t] = g.tstart[t];
+        s_ps[t] = g.pstart[t];
+        if (t < g.T) {
+            s_uc[t] = have_fwd ? g.st[t].ucount : 0;
+            s_pc[t] = g.st[t].pcount;
+        }
+    }
+    __syncthreads();
+    const int64_t n = nu + np;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const bool is_u = i < nu;
+        const int64_t k = is_u ? i : i - nu;
+        const int64_t *starts = is_u ? s_ts : s_ps;
+        const int t = find_seg(starts, g.T, k);
+        const DTable &tb = g.tabs[t];
+        const int64_t loc = k - starts[t];
+        const int32_t cnt = is_u ? s_uc[t] : s_pc[t];
+        if (!tb.ways || loc >= cnt) continue;
+        const int32_t *list = (is_u ? g.U : g.PU) + starts[t];
+        const uint32_t ns = (uint32_t)tb.nsets;
+        const uint32_t set = (uint32_t)list[loc] % ns;
+        int *sg = reinterpret_cast<int *>(tb.seg + set);
+        if (loc == 0 || (uint32_t)list[loc - 1] % ns != set) sg[is_u ? 0 : 2] = (int)loc;
+        if (loc + 1 == cnt || (uint32_t)list[loc + 1] % ns != set) sg[is_u ? 1 : 3] = (int)(loc + 1);
+    }
+}
+
+// One wave per set (lane w = way w); sets without events return at once.
+__global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p) {
+    if (*g.err) return;
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    const int W = tb.ways;
+    if (!W) return;
+    const int64_t set = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+    if (set >= tb.nsets) return;  // wave-uniform
+    const int lane = threadIdx.x & 63;
+    const int4 sg = tb.seg[set];
+    if (sg.x == sg.y && sg.z == sg.w) return;
+    if (lane == 0) tb.seg[set] = make_int4(0, 0, 0, 0);
+    TState &st = g.st[t];
+    const bool way = lane < W;
+    const int64_t slot = set * W + lane;
+
+    // A. this set's ways; rows the last batch touched take the touch score
+    int32_t row0 = -1, score = 0;
+    uint32_t flags = 0;
+    if (way) {
+        row0 = tb.slot_row[slot];
+        score = tb.slot_score[slot];
+        flags = tb.slot_flags[slot] & F_PF;
+        if (row0 >= 0 && tb.slot_touch[slot] == p.last_stamp) {
+            const int cb = tb.slot_cbit[slot];
+            if (cb) tb.slot_cbit[slot] = 0;
+            flags = 0;
+            score = p.prio ? cb + p.es : p.lru_touch;
+        }
+    }
+    int32_t row = row0;
+    int32_t src = -1;  // this lane's last insertion: staging index of a miss, or -1 (host)
+    bool inp = false;  // this lane's row is named by the prefetch list
+
+    auto insert = [&](int32_t r, int32_t v, int32_t from) {
+        const uint64_t fr = __ballot(way && row < 0);
+        int victim;
+        if (fr) {
+            victim = __ffsll((unsigned long long)fr) - 1;
+        } else {
+            const int m = wave_min(way ? score : INT32_MAX);
+            victim = __ffsll((unsigned long long)__ballot(way && score == m)) - 1;
+            if (p.prio && way) score = score > 0 ? score - 1 : 0;
+        }
+        if (lane == victim) {
+            row = r;
+            score = v;
+            src = from;
+            inp = false;
+        }
+    };
+
+    // B. misses of the last batch, ascending
+    const int64_t ub = g.tstart[t];
+    int nmiss = 0;
+    for (int32_t i0 = sg.x; i0 < sg.y; i0 += 64) {
+        const int32_t i = i0 + lane;
+        int32_t r = 0, su = 0;
+        if (i < sg.y) {
+            r = g.U[ub + i];
+            su = g.slotU[ub + i];
+        }
+        uint64_t mm = __ballot(i < sg.y && su < 0);
+        nmiss += __popcll(mm);
+        while (mm) {
+            const int j = __ffsll((unsigned long long)mm) - 1;
+            mm &= mm - 1;
+            const int32_t rr = __shfl(r, j, 64), m = -__shfl(su, j, 64) - 1;
+            const int32_t v = p.prio ? (int32_t)g.mcbit[ub + m] + p.es : p.lru_touch;
+            insert(rr, v, m);
+        }
+    }
+
+    // C. distinct prefetch rows, ascending
+    const int64_t pb = g.pstart[t];
+    for (int32_t i0 = sg.z; i0 < sg.w; i0 += 64) {
+        const int32_t i = i0 + lane;
+        const int32_t r = i < sg.w ? g.PU[pb + i] : 0;
+        const int cnt = min(64, sg.w - i0);
+        for (int j = 0; j < cnt; ++j) {
+            const int32_t rr = __shfl(r, j, 64);
+            const uint64_t h = __ballot(way && row == rr);
+            if (h) {
+                if (lane == __ffsll((unsigned long long)h) - 1) {
+                    if (score < p.pscore) score = p.pscore;
+                    inp = true;
+                }
+                continue;
+            }
+            // a miss of the last batch (its row is still in staging)?
+            int32_t from = -1;
+            if (p.have_fwd) {
+                const uint32_t pos = bm_pos(tb, rr);
+                const uint4 rk = tb.rank[pos >> 5];
+                const uint32_t bit = 1u << (pos & 31);
+                if ((int32_t)rk.z == p.last_stamp && (rk.y & bit)) {
+                    const int32_t su = g.slotU[ub + (int32_t)rk.x + __popc(rk.y & (bit - 1u))];
+                    if (su < 0) from = -su - 1;
+                }
+            }
+            insert(rr, p.pscore, from);
+            if (lane == __ffsll((unsigned long long)__ballot(way && row == rr)) - 1) inp = true;
+        }
+    }
+
+    // counters: compare the set's rows at the start and at the end
+    bool kept0 = false, was = false;
+    for (int k = 0; k < W; ++k) {
+        const int32_t fk = __shfl(row, k, 64), ik = __shfl(row0, k, 64);
+        kept0 |= fk == row0;
+        was |= ik == row;
+    }
+    const bool evicted = way && row0 >= 0 && !kept0;
+    const bool changed = way && row >= 0 && row != row0;
+    const bool fresh = way && row >= 0 && !was;  // in R' \ R
+    const bool from_m = changed && src >= 0;
+    unsigned long long dig = 0;
+    if (fresh) dig += mix64(((unsigned long long)t << 40) | (unsigned long long)row);
+    if (evicted) dig -= mix64(((unsigned long long)t << 40) | (unsigned long long)row0);
+    const int d_res = (way && row >= 0 ? 1 : 0) - (way && row0 >= 0 ? 1 : 0);
+
+    // prefetch rows in neither R nor R'
+    int pdrop = 0;
+    for (int32_t i0 = sg.z; i0 < sg.w; i0 += 64) {
+        const int32_t i = i0 + lane;
+        const int32_t r = i < sg.w ? g.PU[pb + i] : -1;
+        bool in = false;
+        for (int k = 0; k < W; ++k) {
+            // both shuffles in every lane: a lane reading from a lane that
+            // skipped the shuffle would see 0, not the row
+            const int32_t fk = __shfl(row, k, 64), ik = __shfl(row0, k, 64);
+            in |= (fk == r) | (ik == r);
+        }
+        pdrop += (i < sg.w && !in) ? 1 : 0;
+    }
+
+    // fill list and write-back
+    const int stride_st = (int)(sizeof(TState) / 4);
+    const int32_t k = wave_append(changed, t, &g.st[0].popped, stride_st);
+    if (changed) {
+        const int64_t fj = g.ftstart[t] + pb + k;
+        if (fj < 0 || fj >= g.fill_cap) {
+            atomicOr(g.err, ERR_INTERNAL);
+        } else {
+            g.fill_src[fj] = from_m ? src : -(row + 1);
+            g.fill_slot[fj] = (int32_t)slot;
+        }
+    }
+    if (way) {
+        tb.slot_row[slot] = row;
+        tb.slot_score[slot] = score;
+        tb.slot_flags[slot] = changed ? (inp ? F_PF : 0u) : flags;
+        if (changed) tb.slot_touch[slot] = -1;
+    }
+    const int n_ev = wave_sum(evicted ? 1 : 0), n_am = wave_sum(from_m ? 1 : 0);
+    const int n_fill = wave_sum(changed && !from_m ? 1 : 0), n_pd = wave_sum(pdrop), n_res = wave_sum(d_res);
+    const unsigned long long dsum = wave_sum64(dig);
+    if (lane == 0) {
+        if (n_ev) atomicAdd(&st.evicted, n_ev);
+        if (n_am) atomicAdd(&st.adm_miss, n_am);
+        if (n_fill) atomicAdd(&st.p_fill, n_fill);
+        if (n_pd) atomicAdd(&st.p_drop, n_pd);
+        if (nmiss - n_am) atomicAdd(&st.m_drop, nmiss - n_am);
+        if (n_res) atomicAdd(&st.n_res, n_res);
+        if (dsum) atomicAdd(&st.digest_acc, dsum);
+    }
+}
+
+static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
+    int64_t b = (n + per_block - 1) / per_block;
+    if (b < 1) b = 1;
+    if (b > (int64_t)cap) b = cap;
+    return (unsigned)b;
+}
+
+void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t max_sets, hipStream_t s) {
+    if (nu + np > 0) k_sa_heads<<<grid_for(nu + np, kBlock, 8192), kBlock, 0, s>>>(g, nu, np, p.have_fwd);
+    if (max_sets > 0) {
+        const dim3 grid((unsigned)((max_sets + kBlock / 64 - 1) / (kBlock / 64)), g.T);
+        k_sa_place<<<grid, kBlock, 0, s>>>(g, p);
+    }
+}
+
+}  // namespace recmg

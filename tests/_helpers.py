@@ -98,7 +98,7 @@ class GpuRunner:
         self.cache = TieredEmbeddingCache(self.host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables],
                                           policy=w.policy, eviction_speed=w.eviction_speed, miss_mode=miss_mode,
                                           max_bags_per_table=w.bags, max_indices=max_indices,
-                                          max_prefetch=max_prefetch, validate=validate)
+                                          max_prefetch=max_prefetch, validate=validate, ways=w.ways)
 
     def to_dev(self, a):
         return self.torch.from_numpy(np.ascontiguousarray(a)).to(self.dev)

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def _cfg(rows=(1000,), dims=(64,), dtypes=(0,), caps=(100,), policy=0, miss=0, max_idx=5000, max_pf=5000,
-         bags=256, es=4):
+         bags=256, es=4, ways=0):
     T = len(rows)
     keep = []
     cfg = bd.recmg_config_t()
@@ -48,6 +48,7 @@ def _cfg(rows=(1000,), dims=(64,), dtypes=(0,), caps=(100,), policy=0, miss=0, m
     cfg.host_tables = ptrs
     cfg.policy, cfg.miss_mode, cfg.eviction_speed = policy, miss, es
     cfg.max_indices, cfg.max_prefetch, cfg.max_bags_per_table = max_idx, max_pf, bags
+    cfg.ways = ways
     cfg._keep = keep
     return cfg
 
@@ -71,12 +72,21 @@ def test_query_scales_with_capacity():
 
 @pytest.mark.parametrize("kw", [dict(rows=(0,)), dict(dims=(0,)), dict(dtypes=(7,)), dict(caps=(-1,)),
                                 dict(policy=5), dict(miss=9), dict(max_idx=-1), dict(es=-1),
-                                dict(max_idx=1 << 31)])
+                                dict(max_idx=1 << 31), dict(ways=-1), dict(ways=65)])
 def test_query_rejects_bad_configs(kw):
     with pytest.raises(bd.RecmgError) as e:
         bd.recmg_query_workspace(_cfg(**kw))
     assert e.value.code == bd.RECMG_E_INVALID
     assert pk.recmg_last_error()
+
+
+def test_set_associative_slots():
+    """W-way sets use floor(Cap / W) * W slots: Cap 96, 100 and 127 all give 3
+    sets of 32 (the same workspace), Cap 128 gives 4."""
+    q = lambda cap: bd.recmg_query_workspace(_cfg(caps=(cap,), rows=(100000,), ways=32))[0]
+    assert q(100) == q(96) == q(127) != q(128)
+    # a table with fewer slots than ways has no set
+    assert q(31) == q(0)
 
 
 def test_null_handle_is_rejected():

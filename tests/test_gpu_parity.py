@@ -28,13 +28,14 @@ def test_hand_examples(name):
     gd = load_golden(name)
     tab = golden_table(gd)
     w = tg.Workload(0, name, [tg.Table(gd["rows"], gd["dim"], "f32", gd["cap"], 1.0, ("fixed", 1))],
-                    batches=len(gd["steps"]), bags=1, policy=gd["policy"], eviction_speed=gd["eviction_speed"])
+                    batches=len(gd["steps"]), bags=1, policy=gd["policy"], eviction_speed=gd["eviction_speed"],
+                    ways=gd.get("ways", 0))
     import torch as th
     from paper_2511_08568_amd import TieredEmbeddingCache
     dev = th.device("cuda", 0)
     cache = TieredEmbeddingCache([th.from_numpy(tab).pin_memory()], ["f32"], [gd["cap"]], policy=gd["policy"],
                                  eviction_speed=gd["eviction_speed"], max_bags_per_table=4, max_indices=16,
-                                 max_prefetch=16)
+                                 max_prefetch=16, ways=w.ways)
     for b, step in enumerate(gd["steps"]):
         P = np.array(step["prefetch"], np.int32)
         bits = None if step["bits"] is None else th.tensor(step["bits"], dtype=th.uint8, device=dev)
@@ -212,6 +213,51 @@ def test_run_twice_is_deterministic():
         g.close()
     for a, b in zip(*res):
         assert np.array_equal(a["out"], b["out"]) and a["fwd"] == b["fwd"] and a["place"] == b["place"]
+
+
+# ----------------------------------------------------------------------------- set-associative
+
+@pytest.mark.parametrize("seed", range(16))
+def test_sa_tiny_random(seed):
+    """W-way sets (W = 1..5) on tiny tables: few sets, many evictions per set."""
+    w = tg.random_tiny(seed, max_rows=40, max_cap=12, max_dim=9, batches=6, bags=5)
+    w.ways = 1 + seed % 5
+    _parity(w, label=f"sa-tiny{seed}-w{w.ways}")
+
+
+@pytest.mark.parametrize("seed,ways", [(0, 2), (1, 4), (2, 8), (3, 3)])
+def test_sa_crowded_sets(seed, ways):
+    """Hundreds of events per set (more than one wave's worth of misses and of
+    prefetch rows), sets that never fill, and tables with no set at all
+    (Cap < W) next to set-associative ones."""
+    w = tg.random_tiny(200 + seed, max_rows=3000, max_cap=40, max_dim=33, batches=5, bags=60,
+                       integer_values=False)
+    w.ways = ways
+    w.tables[0].cap = ways - 1  # no set: nothing is cached
+    _parity(w, label=f"sa-crowded{seed}-w{ways}")
+
+
+@pytest.mark.parametrize("cid,scale,bags,tables,ways", [(2, 0.02, 256, 3, 32), (3, 0.01, 256, 6, 32),
+                                                        (5, 0.01, 256, 8, 32), (4, 0.0005, 512, 2, 32),
+                                                        (3, 0.01, 256, 4, 4), (2, 0.02, 256, 2, 64)])
+def test_sa_configs_scaled(cid, scale, bags, tables, ways):
+    """The scaled configurations with W-way set-associative caches (32 ways:
+    the production default the paper compares against)."""
+    w = tg.scaled_config(cid, row_scale=scale, batches=6, bags=bags, max_tables=tables, ways=ways)
+    _parity(w, label=f"c{cid}-sa{ways}")
+
+
+def test_sa_staged():
+    w = tg.scaled_config(3, row_scale=0.01, batches=5, bags=256, max_tables=5, ways=32)
+    _parity(w, miss_mode="staged", label="c3-sa32-staged")
+
+
+def test_sa_config1_full():
+    """Configuration 1 at full size with a 32-way cache (10,000 slots: 312 sets
+    of 32, 16 slots unused), first 30 batches."""
+    w = tg.make_config(1)
+    w.ways = 32
+    _parity(w, nbatches=30, label="c1-sa32")
 
 
 @pytest.mark.parametrize("fill", [0xFF, 0x5A])
