@@ -100,8 +100,11 @@ def buffer_sweep(args, dev):
     seen = [np.unique(np.concatenate([base.uniques(b)[t] for b in range(NB)])).size for t in range(base.num_tables)]
     uniq_total = sum(int(base.uniques(b)[t].size) for b in range(NB) for t in range(base.num_tables))
     recipe = base.prefetch if base.prefetch[0] != "none" else ("exact",)
-    variants = {"lru": ("lru", ("none",)), "caching_model": ("priority", ("none",)),
-                "caching_and_prefetch": ("priority", recipe)}
+    # (policy, prefetch recipe, ways): fully associative, and 32-way sets as in
+    # the production buffer the paper compares against
+    variants = {"lru": ("lru", ("none",), 0), "caching_model": ("priority", ("none",), 0),
+                "caching_and_prefetch": ("priority", recipe, 0), "lru_32way": ("lru", ("none",), 32),
+                "caching_and_prefetch_32way": ("priority", recipe, 32)}
     points = []
     for frac in (0.01, 0.02, 0.05, 0.10, 0.15, 0.20, 0.30):
         caps = [max(1, int(round(frac * n))) for n in seen]
@@ -113,9 +116,9 @@ def buffer_sweep(args, dev):
             opt += sum(int(x.sum()) for x in lab)
         pt["belady_bound"] = opt / uniq_total
         parity = True
-        for name, (policy, pf) in variants.items():
+        for name, (policy, pf, ways) in variants.items():
             w = tg.make_config(args.config)
-            w.policy, w.prefetch = policy, pf
+            w.policy, w.prefetch, w.ways = policy, pf, ways
             w.bits = ("optgen", 0.8, NB)
             for tb, c in zip(w.tables, caps):
                 tb.cap = c
@@ -125,7 +128,7 @@ def buffer_sweep(args, dev):
             max_pf = max(max(P.size for P, _ in pre), 1)
             cache = TieredEmbeddingCache(host, [tb.dtype for tb in w.tables], caps, policy=policy,
                                          eviction_speed=w.eviction_speed, max_bags_per_table=w.bags,
-                                         max_indices=max_idx, max_prefetch=max_pf)
+                                         max_indices=max_idx, max_prefetch=max_pf, ways=ways)
             o = oracle.for_workload(w, tabs_np)
             out = torch.empty(w.bags * sum(tb.dim for tb in w.tables), dtype=torch.float32, device=dev)
             osum = {"hits": 0, "misses": 0, "evicted": 0, "prefetch_fill": 0}
@@ -175,7 +178,8 @@ def describe_workload(cid, w):
             f"{span([tb.rows for tb in tabs])} rows x dim {'/'.join(map(str, dims))}, "
             f"HBM cache {sum(tb.cap for tb in tabs):,} rows in all, {w.bags:,} bags/table, "
             f"pooling {'/'.join(pools)} (table 0: {tabs[0].pooling}), "
-            f"Zipf {span([tb.alpha for tb in tabs], '{:.2f}')}, prefetch {w.prefetch}, policy {w.policy}")
+            f"Zipf {span([tb.alpha for tb in tabs], '{:.2f}')}, prefetch {w.prefetch}, policy {w.policy}"
+            + (f", {w.ways}-way sets" if w.ways else ""))
 
 
 def log(msg):
@@ -205,6 +209,9 @@ def main():
                          "touches) for LRU, the caching policy with OPTgen bits, that policy with the "
                          "configuration's prefetch list, and the Belady bound; one JSON line")
     ap.add_argument("--sweep-batches", type=int, default=60)
+    ap.add_argument("--ways", type=int, default=0,
+                    help="W > 0: W-way set-associative caches (Alg. 2 inside each set) instead of fully "
+                         "associative ones")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 3 device-to-device copies of MIB MiB (scale for HBM byte counters) and exit")
     args = ap.parse_args()
@@ -240,6 +247,7 @@ def main():
         w = tg.make_config(args.config)
     if args.prefetch is not None:
         w.prefetch = (args.prefetch,)
+    w.ways = args.ways
     W, K = args.warmup, args.steps
     if W + K > w.batches:
         raise SystemExit(f"warmup + steps must be at most the workload's {w.batches} batches")
@@ -285,7 +293,8 @@ def main():
 
     cache = TieredEmbeddingCache(host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables], policy=w.policy,
                                  eviction_speed=w.eviction_speed, miss_mode=args.miss_mode,
-                                 max_bags_per_table=w.bags, max_indices=max_idx, max_prefetch=max_pf, timing=1)
+                                 max_bags_per_table=w.bags, max_indices=max_idx, max_prefetch=max_pf, timing=1,
+                                 ways=w.ways)
     log(f"cache ready: workspace {cache.workspace_bytes / 1e9:.2f} GB")
 
     def step(b, marks=None):

@@ -64,6 +64,7 @@ struct Layout {
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, raddr = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
     size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, pool_btab = 0, ftstart = 0;
+    size_t sa_bstart = 0, sa_btab = 0;
     size_t fstage = 0;
     // pinned host staging (STAGED): miss ids, miss rows, fill sources, prefetch rows
     size_t h_mrows = 0, h_rows = 0, h_fsrc = 0, h_frows = 0;
@@ -200,6 +201,8 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->pool_bstart = take(4 * (T + 1));
     L->pool_btab = take(4 * T);
     L->ftstart = take(8 * (T + 1));
+    L->sa_bstart = take(4 * (T + 1));
+    L->sa_btab = take(4 * T);
     L->staging[0] = take(mi * (size_t)L->stage_stride);
     L->staging[1] = take(mi * (size_t)L->stage_stride);
     const bool staged = cfg->miss_mode == RECMG_STAGED;
@@ -231,7 +234,8 @@ struct recmg_cache {
     Layout L;
     DGlobal g{};
     std::vector<const char *> host;  // host tables (host pointers)
-    int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1, max_sets = 0;
+    int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1, nsa = 0;
+    int64_t sa_blocks = 0;  // blocks of the set-associative placement kernel
     bool has_fa = false, has_sa = false;  // tables of each form present
     std::vector<int32_t> pool_order;  // table ids ordered by pooled-kernel kind
     std::vector<PoolLaunch> pool_launches;
@@ -604,6 +608,8 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.stage_stride = L.stage_stride;
     g.T = T;
     g.total_bm_blocks = L.total_bm_blocks;
+    g.sa_bstart = reinterpret_cast<int32_t *>(ws + L.sa_bstart);
+    g.sa_btab = reinterpret_cast<int32_t *>(ws + L.sa_btab);
 
     std::vector<DTable> tabs(T);
     std::vector<int32_t> bstart(T + 1, 0);
@@ -648,7 +654,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         d.seg = reinterpret_cast<int4 *>(ws + L.seg[t]);
         if (ge.ways) c->has_sa = true;
         else c->has_fa = true;
-        if (ge.ways) c->max_sets = std::max(c->max_sets, ge.nsets);
+
         bstart[t + 1] = bstart[t] + ge.bm_nblk;
         out_off += ge.dim;
         cap_off += ge.cap;
@@ -662,6 +668,14 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     for (int t = 0; t < T; ++t) c->pool_order[t] = t;
     std::stable_sort(c->pool_order.begin(), c->pool_order.end(),
                      [&](int x, int y) { return geo[x].kind < geo[y].kind; });
+    // set-associative placement: tables with the fewest sets first, four sets per block
+    std::vector<int32_t> sa_tab, sa_bs(1, 0);
+    for (int t = 0; t < T; ++t)
+        if (geo[t].ways) sa_tab.push_back(t);
+    std::stable_sort(sa_tab.begin(), sa_tab.end(), [&](int x, int y) { return geo[x].nsets < geo[y].nsets; });
+    for (int t : sa_tab) sa_bs.push_back(sa_bs.back() + (geo[t].nsets + kBlock / 64 - 1) / (kBlock / 64));
+    c->nsa = (int32_t)sa_tab.size();
+    c->sa_blocks = sa_bs.back();
 
     // clear the metadata (not the slot pool or staging), set "free" markers
     hipStream_t s0 = nullptr;
@@ -686,6 +700,8 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     HIP_TRY(hipMemcpy(ws + L.tabs, tabs.data(), sizeof(DTable) * T, hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(ws + L.bm_block_start, bstart.data(), 4 * (T + 1), hipMemcpyHostToDevice));
     HIP_TRY(hipMemcpy(ws + L.pool_btab, c->pool_order.data(), 4 * T, hipMemcpyHostToDevice));
+    HIP_TRY(hipMemcpy(ws + L.sa_bstart, sa_bs.data(), 4 * sa_bs.size(), hipMemcpyHostToDevice));
+    if (!sa_tab.empty()) HIP_TRY(hipMemcpy(ws + L.sa_btab, sa_tab.data(), 4 * sa_tab.size(), hipMemcpyHostToDevice));
     launch_init_state(g, c->max_cap, s0);
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipDeviceSynchronize());
@@ -768,7 +784,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     {
         StageTimer tm(c, RECMG_STAGE_PLC_APPLY, s);
         if (c->has_fa) launch_plc_apply(g, p, c->max_cap, c->max_map, cand_grid, s);
-        if (c->has_sa) launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->max_sets, s);
+        if (c->has_sa) launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks, s);
     }
     if (c->cfg.miss_mode == RECMG_STAGED) {
         // host-staged prefetch rows; the fill overlaps the next forward when a copy stream is given

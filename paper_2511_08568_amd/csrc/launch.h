@@ -44,7 +44,9 @@ void launch_plc_finalize(const DGlobal &g, hipStream_t s);
 void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s);
 
 // setassoc.hip: placement of the set-associative tables (nu: index space of
-// the last forward's distinct rows, np: of this placement's prefetch rows)
-void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t max_sets, hipStream_t s);
+// the last forward's distinct rows, np: of this placement's prefetch rows;
+// nsa tables, blocks = sa_bstart[nsa], four sets per block)
+void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks,
+                     hipStream_t s);
 
 }  // namespace recmg

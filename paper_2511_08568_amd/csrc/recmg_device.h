@@ -134,6 +134,8 @@ struct DGlobal {
     int64_t stage_stride;
     int32_t T;
     int32_t total_bm_blocks;
+    int32_t *sa_bstart;  // [nsa + 1] first placement block of each set-associative table
+    int32_t *sa_btab;    // [nsa] those tables, fewest sets first
 };
 
 // Parameters of one placement.
@@ -331,12 +333,6 @@ __device__ __forceinline__ long long block_excl_scan64(long long v, long long *t
     __syncthreads();
     *total = tot;
     return pre + x - v;
-}
-
-__device__ __forceinline__ int wave_min(int v) {
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) v = min(v, __shfl_xor(v, d, 64));
-    return v;
 }
 
 __device__ __forceinline__ int wave_sum(int v) {

@@ -67,19 +67,39 @@ __global__ void __launch_bounds__(kBlock) k_sa_heads(DGlobal g, int64_t nu, int6
     }
 }
 
+// Minimum of v over the wave, returned as a scalar: DPP within rows of 16
+// lanes, row broadcasts into the last row, one read of lane 63.  Every lane
+// must be active.
+__device__ __forceinline__ int wave_min_dpp(int v) {
+    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));   // quad_perm [1,0,3,2]
+    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));   // quad_perm [2,3,0,1]
+    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false));  // row_half_mirror
+    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false));  // row_mirror
+    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x142, 0xA, 0xF, false));  // row_bcast:15 into rows 1, 3
+    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x143, 0xC, 0xF, false));  // row_bcast:31 into rows 2, 3
+    return __builtin_amdgcn_readlane(v, 63);
+}
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+
 // One wave per set (lane w = way w); sets without events return at once.
-__global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p) {
+// Blocks run table by table, tables with the fewest sets first: their sets
+// take the most events each, and the longest waves should start first.
+__global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p, int32_t nsa) {
     if (*g.err) return;
-    const int t = blockIdx.y;
+    const int kt = find_seg32(g.sa_bstart, nsa, (int32_t)blockIdx.x);
+    const int t = g.sa_btab[kt];
     const DTable &tb = g.tabs[t];
     const int W = tb.ways;
-    if (!W) return;
-    const int64_t set = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+    const int64_t set = (int64_t)(blockIdx.x - g.sa_bstart[kt]) * (kBlock / 64) + (threadIdx.x >> 6);
     if (set >= tb.nsets) return;  // wave-uniform
     const int lane = threadIdx.x & 63;
     const int4 sg = tb.seg[set];
     if (sg.x == sg.y && sg.z == sg.w) return;
     if (lane == 0) tb.seg[set] = make_int4(0, 0, 0, 0);
+    // A set's events are played one after another: a set with many of them is
+    // the kernel's critical path, so its wave takes issue slots first.
+    if ((sg.y - sg.x) + (sg.w - sg.z) > 256) __builtin_amdgcn_s_setprio(3);
     TState &st = g.st[t];
     const bool way = lane < W;
     const int64_t slot = set * W + lane;
@@ -102,14 +122,18 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p) {
     int32_t src = -1;  // this lane's last insertion: staging index of a miss, or -1 (host)
     bool inp = false;  // this lane's row is named by the prefetch list
 
-    auto insert = [&](int32_t r, int32_t v, int32_t from) {
-        const uint64_t fr = __ballot(way && row < 0);
+    // insert row r with score v (from: its staging index, or -1); returns the
+    // way.  Ways are never freed, so once no way is free the set stays full.
+    bool full = ballot(way && row < 0) == 0;
+    auto insert = [&](int32_t r, int32_t v, int32_t from) -> int {
         int victim;
-        if (fr) {
+        if (!full) {
+            const uint64_t fr = ballot(way && row < 0);
             victim = __ffsll((unsigned long long)fr) - 1;
+            full = (fr & (fr - 1)) == 0;
         } else {
-            const int m = wave_min(way ? score : INT32_MAX);
-            victim = __ffsll((unsigned long long)__ballot(way && score == m)) - 1;
+            const int m = wave_min_dpp(way ? score : INT32_MAX);
+            victim = __ffsll((unsigned long long)ballot(way && score == m)) - 1;
             if (p.prio && way) score = score > 0 ? score - 1 : 0;
         }
         if (lane == victim) {
@@ -118,49 +142,42 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p) {
             src = from;
             inp = false;
         }
+        return victim;
     };
 
-    // B. misses of the last batch, ascending
+    // B. misses of the last batch, ascending.  Each chunk of 64 distinct rows
+    // is loaded lane-parallel with the misses' touch scores, then played one
+    // miss at a time from registers.
     const int64_t ub = g.tstart[t];
     int nmiss = 0;
     for (int32_t i0 = sg.x; i0 < sg.y; i0 += 64) {
         const int32_t i = i0 + lane;
-        int32_t r = 0, su = 0;
+        int32_t r = 0, su = 0, v = 0;
         if (i < sg.y) {
             r = g.U[ub + i];
             su = g.slotU[ub + i];
+            if (su < 0) v = p.prio ? (int32_t)g.mcbit[ub + (-su - 1)] + p.es : p.lru_touch;
         }
-        uint64_t mm = __ballot(i < sg.y && su < 0);
+        uint64_t mm = ballot(i < sg.y && su < 0);
         nmiss += __popcll(mm);
         while (mm) {
             const int j = __ffsll((unsigned long long)mm) - 1;
             mm &= mm - 1;
-            const int32_t rr = __shfl(r, j, 64), m = -__shfl(su, j, 64) - 1;
-            const int32_t v = p.prio ? (int32_t)g.mcbit[ub + m] + p.es : p.lru_touch;
-            insert(rr, v, m);
+            insert(__builtin_amdgcn_readlane(r, j), __builtin_amdgcn_readlane(v, j),
+                   -__builtin_amdgcn_readlane(su, j) - 1);
         }
     }
 
-    // C. distinct prefetch rows, ascending
+    // C. distinct prefetch rows, ascending.  Each lane first finds whether its
+    // row missed in the last batch (then it is still in staging).
     const int64_t pb = g.pstart[t];
     for (int32_t i0 = sg.z; i0 < sg.w; i0 += 64) {
         const int32_t i = i0 + lane;
-        const int32_t r = i < sg.w ? g.PU[pb + i] : 0;
-        const int cnt = min(64, sg.w - i0);
-        for (int j = 0; j < cnt; ++j) {
-            const int32_t rr = __shfl(r, j, 64);
-            const uint64_t h = __ballot(way && row == rr);
-            if (h) {
-                if (lane == __ffsll((unsigned long long)h) - 1) {
-                    if (score < p.pscore) score = p.pscore;
-                    inp = true;
-                }
-                continue;
-            }
-            // a miss of the last batch (its row is still in staging)?
-            int32_t from = -1;
+        int32_t r = -1, from = -1;
+        if (i < sg.w) {
+            r = g.PU[pb + i];
             if (p.have_fwd) {
-                const uint32_t pos = bm_pos(tb, rr);
+                const uint32_t pos = bm_pos(tb, r);
                 const uint4 rk = tb.rank[pos >> 5];
                 const uint32_t bit = 1u << (pos & 31);
                 if ((int32_t)rk.z == p.last_stamp && (rk.y & bit)) {
@@ -168,15 +185,27 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p) {
                     if (su < 0) from = -su - 1;
                 }
             }
-            insert(rr, p.pscore, from);
-            if (lane == __ffsll((unsigned long long)__ballot(way && row == rr)) - 1) inp = true;
+        }
+        const int cnt = min(64, sg.w - i0);
+        for (int j = 0; j < cnt; ++j) {
+            const int32_t rr = __builtin_amdgcn_readlane(r, j);
+            const uint64_t h = ballot(way && row == rr);
+            if (h) {
+                if (lane == __ffsll((unsigned long long)h) - 1) {
+                    if (score < p.pscore) score = p.pscore;
+                    inp = true;
+                }
+                continue;
+            }
+            const int w = insert(rr, p.pscore, __builtin_amdgcn_readlane(from, j));
+            if (lane == w) inp = true;
         }
     }
 
     // counters: compare the set's rows at the start and at the end
     bool kept0 = false, was = false;
     for (int k = 0; k < W; ++k) {
-        const int32_t fk = __shfl(row, k, 64), ik = __shfl(row0, k, 64);
+        const int32_t fk = __builtin_amdgcn_readlane(row, k), ik = __builtin_amdgcn_readlane(row0, k);
         kept0 |= fk == row0;
         was |= ik == row;
     }
@@ -195,12 +224,8 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p) {
         const int32_t i = i0 + lane;
         const int32_t r = i < sg.w ? g.PU[pb + i] : -1;
         bool in = false;
-        for (int k = 0; k < W; ++k) {
-            // both shuffles in every lane: a lane reading from a lane that
-            // skipped the shuffle would see 0, not the row
-            const int32_t fk = __shfl(row, k, 64), ik = __shfl(row0, k, 64);
-            in |= (fk == r) | (ik == r);
-        }
+        for (int k = 0; k < W; ++k)
+            in |= (__builtin_amdgcn_readlane(row, k) == r) | (__builtin_amdgcn_readlane(row0, k) == r);
         pdrop += (i < sg.w && !in) ? 1 : 0;
     }
 
@@ -243,12 +268,10 @@ static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
     return (unsigned)b;
 }
 
-void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t max_sets, hipStream_t s) {
+void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks,
+                     hipStream_t s) {
     if (nu + np > 0) k_sa_heads<<<grid_for(nu + np, kBlock, 8192), kBlock, 0, s>>>(g, nu, np, p.have_fwd);
-    if (max_sets > 0) {
-        const dim3 grid((unsigned)((max_sets + kBlock / 64 - 1) / (kBlock / 64)), g.T);
-        k_sa_place<<<grid, kBlock, 0, s>>>(g, p);
-    }
+    if (blocks > 0) k_sa_place<<<(unsigned)blocks, kBlock, 0, s>>>(g, p, nsa);
 }
 
 }  // namespace recmg
