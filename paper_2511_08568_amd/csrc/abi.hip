@@ -64,7 +64,7 @@ struct Layout {
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, raddr = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
     size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, pool_btab = 0, ftstart = 0;
-    size_t sa_bstart = 0, sa_btab = 0;
+    size_t sa_bstart = 0, sa_btab = 0, fdesc = 0;
     size_t fstage = 0;
     // pinned host staging (STAGED): miss ids, miss rows, fill sources, prefetch rows
     size_t h_mrows = 0, h_rows = 0, h_fsrc = 0, h_frows = 0;
@@ -193,8 +193,9 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->mscore = take(4 * mi);
     L->NP = take(4 * mp);
     L->PU = take(4 * mp);
-    L->fill_src = take(4 * (mi + mp));
-    L->fill_slot = take(4 * (mi + mp));
+    L->fill_src = take(4 * 2 * (mi + mp));   // two fill lists: a placement's fill may still
+    L->fill_slot = take(4 * 2 * (mi + mp));  // read one while the next placement writes the other
+    L->fdesc = take(8 * 4 * 2 * (size_t)T);
     L->hist = take(4 * (size_t)kRadix * T);
     L->dump = take(4 * (size_t)L->sum_cap);
     L->dump_count = take(4 * T);
@@ -243,12 +244,25 @@ struct recmg_cache {
     int64_t placements = 0, forwards = 0, last_n = 0;
     bool have_fwd = false;
     hipStream_t last_stream = nullptr;
+    // Calls may come on different streams (e.g. the next placement on its own
+    // stream while the last forward still runs): each call waits for what it
+    // needs from the latest call of the other kind through these events.
+    hipStream_t fwd_stream = nullptr, plc_stream = nullptr;
+    bool fwd_ev = false, plc_ev = false;  // the events below were recorded
+    hipEvent_t ev_src = nullptr;   // latest forward: after its dedup, probe, sources and coverage
+    hipEvent_t ev_pool = nullptr;  // latest forward: after its pooled kernel
+    hipEvent_t ev_fwd = nullptr;   // latest forward: after all its kernels
+    hipEvent_t ev_plc = nullptr;   // latest placement: after all its kernels but the fill
+    hipEvent_t ev_fill[2] = {nullptr, nullptr};  // fill of the latest placement of each parity
+    bool fill_rec[2] = {false, false};
+    int fill_last = -1;  // parity of the latest fill no forward has waited for yet
+    int32_t *fill_src_buf[2] = {nullptr, nullptr}, *fill_slot_buf[2] = {nullptr, nullptr};
+    int64_t *fdesc_buf[2] = {nullptr, nullptr};
     int32_t pool_B = -1;
     int64_t plc_np = -1;  // prefetch ids of the placement since the last forward (-1: none)
     char *stage[2] = {nullptr, nullptr};  // staging buffers, alternating between forwards
     int cur = 0;                          // buffer of the latest forward
-    bool fill_pending = false;            // a prefetch fill runs on the side stream
-    hipEvent_t ev_admit = nullptr, ev_fill = nullptr;
+
     int64_t pool_blocks = 0;
     std::vector<int32_t> pool_bstart;
     // STAGED
@@ -315,6 +329,16 @@ int32_t check_handle(recmg_cache_t *c) {
     if (!c) return fail(RECMG_E_INVALID, "handle is NULL");
     if (c->magic != kMagic) return fail(RECMG_E_STATE, "handle is not live");
     return RECMG_OK;
+}
+
+// Waits for every stream the handle's calls used.
+hipError_t sync_all(recmg_cache_t *c) {
+    hipError_t e = hipStreamSynchronize(c->last_stream);
+    if (e == hipSuccess && c->fwd_ev) e = hipStreamSynchronize(c->fwd_stream);
+    if (e == hipSuccess && c->plc_ev) e = hipStreamSynchronize(c->plc_stream);
+    if (e == hipSuccess && c->copy_stream) e = hipStreamSynchronize(c->copy_stream);
+    if (e == hipSuccess) c->fill_last = -1;
+    return e;
 }
 
 int32_t set_device(recmg_cache_t *c) {
@@ -594,8 +618,13 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.NP = reinterpret_cast<int32_t *>(ws + L.NP);
     g.PU = reinterpret_cast<int32_t *>(ws + L.PU);
     g.ftstart = reinterpret_cast<int64_t *>(ws + L.ftstart);
-    g.fill_src = reinterpret_cast<int32_t *>(ws + L.fill_src);
-    g.fill_slot = reinterpret_cast<int32_t *>(ws + L.fill_slot);
+    for (int k = 0; k < 2; ++k) {
+        c->fill_src_buf[k] = reinterpret_cast<int32_t *>(ws + L.fill_src) + k * (cfg->max_indices + cfg->max_prefetch);
+        c->fill_slot_buf[k] = reinterpret_cast<int32_t *>(ws + L.fill_slot) + k * (cfg->max_indices + cfg->max_prefetch);
+        c->fdesc_buf[k] = reinterpret_cast<int64_t *>(ws + L.fdesc) + k * 4 * T;
+    }
+    g.fill_src = c->fill_src_buf[0];
+    g.fill_slot = c->fill_slot_buf[0];
     g.fill_cap = cfg->max_indices + cfg->max_prefetch;
     g.fstage = ws + L.fstage;
     g.staged_fill = cfg->miss_mode == RECMG_STAGED ? 1 : 0;
@@ -707,10 +736,8 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     HIP_TRY(hipDeviceSynchronize());
 
     c->copy_stream = static_cast<hipStream_t>(cfg->copy_stream);
-    if (c->copy_stream) {
-        HIP_TRY(hipEventCreateWithFlags(&c->ev_admit, hipEventDisableTiming));
-        HIP_TRY(hipEventCreateWithFlags(&c->ev_fill, hipEventDisableTiming));
-    }
+    for (hipEvent_t *e : {&c->ev_src, &c->ev_pool, &c->ev_fwd, &c->ev_plc, &c->ev_fill[0], &c->ev_fill[1]})
+        HIP_TRY(hipEventCreateWithFlags(e, hipEventDisableTiming));
     if (cfg->miss_mode == RECMG_STAGED) {
         char *hs = static_cast<char *>(cfg->host_staging);
         c->h_mrows = reinterpret_cast<int32_t *>(hs + L.h_mrows);
@@ -741,11 +768,19 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (c->cfg.validate && (rc = host_check_ids(prefetch_rows, prefetch_offsets, c->T + 1, 1, num_prefetch, c->geo, s)))
         return rc;
-    if (c->fill_pending) {  // two placements in a row: the earlier fill must finish first
-        HIP_TRY(hipStreamWaitEvent(s, c->ev_fill, 0));
-        c->fill_pending = false;
-    }
+    // what this placement reads from calls on other streams: the latest
+    // forward's distinct rows, misses and sources; the latest placement's state
+    if (c->fwd_ev && c->fwd_stream != s) HIP_TRY(hipStreamWaitEvent(s, c->ev_src, 0));
+    if (c->plc_ev && c->plc_stream != s) HIP_TRY(hipStreamWaitEvent(s, c->ev_plc, 0));
+    const int q = (int)(c->placements & 1);
+    if (c->fill_rec[q]) HIP_TRY(hipStreamWaitEvent(s, c->ev_fill[q], 0));  // it read this parity's fill list
+    // STAGED: the host rewrites its staging of fill sources and rows, which
+    // the previous fill's copies may still read
+    if (c->cfg.miss_mode == RECMG_STAGED && c->fill_rec[q ^ 1]) HIP_TRY(hipStreamWaitEvent(s, c->ev_fill[q ^ 1], 0));
     c->g.staging = c->stage[c->cur];  // misses of the latest forward
+    c->g.fill_src = c->fill_src_buf[q];
+    c->g.fill_slot = c->fill_slot_buf[q];
+    int64_t *fdesc = c->fdesc_buf[q];
     const DGlobal &g = c->g;
     const int64_t b = c->placements;
     if (b + 2 >= (int64_t(1) << 31)) return fail(RECMG_E_STATE, "placement count exhausted");
@@ -786,40 +821,31 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         if (c->has_fa) launch_plc_apply(g, p, c->max_cap, c->max_map, cand_grid, s);
         if (c->has_sa) launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks, s);
     }
-    if (c->cfg.miss_mode == RECMG_STAGED) {
-        // host-staged prefetch rows; the fill overlaps the next forward when a copy stream is given
-        hipStream_t cs = c->copy_stream ? c->copy_stream : s;
-        if (cs != s) {
-            HIP_TRY(hipEventRecord(c->ev_admit, s));
-            HIP_TRY(hipStreamWaitEvent(cs, c->ev_admit, 0));
-        }
-        StageTimer tm(c, RECMG_STAGE_PLC_FILL, cs);
-        if ((rc = staged_fill(c, s, cs))) return rc;
-        launch_plc_fill(g, cs);
-        if (cs != s) {
-            HIP_TRY(hipEventRecord(c->ev_fill, cs));
-            c->fill_pending = true;
-        }
-    } else if (c->copy_stream) {
-        // the fill overlaps the next forward's dedup; that forward's pooling waits for it
-        HIP_TRY(hipEventRecord(c->ev_admit, s));
-        HIP_TRY(hipStreamWaitEvent(c->copy_stream, c->ev_admit, 0));
-        {
-            StageTimer tm(c, RECMG_STAGE_PLC_FILL, c->copy_stream);
-            launch_plc_fill(g, c->copy_stream);
-        }
-        HIP_TRY(hipEventRecord(c->ev_fill, c->copy_stream));
-        c->fill_pending = true;
-    } else {
-        StageTimer tm(c, RECMG_STAGE_PLC_FILL, s);
-        launch_plc_fill(g, s);
+    launch_plc_finalize(g, fdesc, s);
+    HIP_TRY(hipEventRecord(c->ev_plc, s));
+    // The fill overwrites the slots of evicted rows: it waits for the latest
+    // forward's pooled kernel, which may read them, and for this placement.
+    // On the copy stream it overlaps the next forward's dedup and probe (and a
+    // placement on a stream of its own overlaps the previous fill); that
+    // forward's pooled kernel waits for it.
+    hipStream_t fs = c->copy_stream ? c->copy_stream : s;
+    if (fs != s) HIP_TRY(hipStreamWaitEvent(fs, c->ev_plc, 0));
+    if (c->fwd_ev && c->fwd_stream != fs) HIP_TRY(hipStreamWaitEvent(fs, c->ev_pool, 0));
+    {
+        StageTimer tm(c, RECMG_STAGE_PLC_FILL, fs);
+        if (c->cfg.miss_mode == RECMG_STAGED && (rc = staged_fill(c, s, fs))) return rc;  // host-staged rows
+        launch_plc_fill(g, fdesc, fs);
     }
-    launch_plc_finalize(g, s);
+    HIP_TRY(hipEventRecord(c->ev_fill[q], fs));
+    c->fill_rec[q] = true;
+    c->fill_last = q;
     HIP_TRY(hipGetLastError());
     c->placements++;
     c->plc_np = num_prefetch;
     c->have_fwd = false;
     c->last_stream = s;
+    c->plc_stream = s;
+    c->plc_ev = true;
     return RECMG_OK;
 }
 
@@ -836,6 +862,11 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
     if ((rc = set_device(c))) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (c->cfg.validate && (rc = host_check_ids(indices, offsets, (int64_t)c->T * B + 1, B, n, c->geo, s))) return rc;
+    // what this forward needs from calls on other streams: the latest
+    // placement's state (its fill is waited for before the pooled kernel) and
+    // the end of the latest forward, whose per-index arrays this one rewrites
+    if (c->plc_ev && c->plc_stream != s) HIP_TRY(hipStreamWaitEvent(s, c->ev_plc, 0));
+    if (c->fwd_ev && c->fwd_stream != s) HIP_TRY(hipStreamWaitEvent(s, c->ev_fwd, 0));
     const DGlobal &g = c->g;
     if (c->pool_B != (int32_t)B) {
         // blocks of the pooled kernels: tables grouped by kernel kind, one
@@ -873,6 +904,7 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
             if (c->plc_np >= 0) launch_fwd_cover(g, stamp, c->plc_np, s);
         }
     }
+    HIP_TRY(hipEventRecord(c->ev_src, s));  // a placement on another stream may start here
     if (n > 0) {
         StageTimer tm(c, RECMG_STAGE_FWD_FETCH, s);
         if (c->cfg.miss_mode == RECMG_ZERO_COPY) {
@@ -881,9 +913,9 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
             return rc;
         }
     }
-    if (c->fill_pending) {
-        HIP_TRY(hipStreamWaitEvent(s, c->ev_fill, 0));
-        c->fill_pending = false;
+    if (c->fill_last >= 0) {  // rows the latest placement admitted
+        HIP_TRY(hipStreamWaitEvent(s, c->ev_fill[c->fill_last], 0));
+        c->fill_last = -1;
     }
     {
         // the pooled kernel is timed by events its own dispatch records
@@ -902,13 +934,17 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
                     (int)c->pool_launches.size(), a, b, s);
         if (a) c->marks.push_back({RECMG_STAGE_FWD_POOL, a, b});
     }
+    HIP_TRY(hipEventRecord(c->ev_pool, s));  // the next fill may overwrite slots from here on
     launch_fwd_finalize(g, s);
+    HIP_TRY(hipEventRecord(c->ev_fwd, s));
     HIP_TRY(hipGetLastError());
     c->forwards++;
     c->plc_np = -1;  // coverage counts against the placement just before a forward only
     c->have_fwd = true;
     c->last_n = n;
     c->last_stream = s;
+    c->fwd_stream = s;
+    c->fwd_ev = true;
     return RECMG_OK;
 }
 
@@ -920,11 +956,7 @@ int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_sta
     if (rc) return rc;
     if ((rc = set_device(c))) return rc;
     hipStream_t s = c->last_stream;
-    if (c->fill_pending) {
-        HIP_TRY(hipStreamWaitEvent(s, c->ev_fill, 0));
-        c->fill_pending = false;
-    }
-    HIP_TRY(hipStreamSynchronize(s));
+    HIP_TRY(sync_all(c));
     const int T = c->T;
     std::vector<TState> st(T);
     int32_t err = 0;
@@ -1027,11 +1059,9 @@ int32_t recmg_cache_destroy(recmg_cache_t *c) {
     if (c->magic != kMagic) return fail(RECMG_E_STATE, "handle is not live");
     (void)set_device(c);
     int32_t rc = RECMG_OK;
-    if (hipStreamSynchronize(c->last_stream) != hipSuccess) rc = fail(RECMG_E_HIP, "synchronize failed at destroy");
-    if (c->copy_stream && hipStreamSynchronize(c->copy_stream) != hipSuccess)
-        rc = fail(RECMG_E_HIP, "synchronize failed at destroy");
-    if (c->ev_admit) (void)hipEventDestroy(c->ev_admit);
-    if (c->ev_fill) (void)hipEventDestroy(c->ev_fill);
+    if (sync_all(c) != hipSuccess) rc = fail(RECMG_E_HIP, "synchronize failed at destroy");
+    for (hipEvent_t e : {c->ev_src, c->ev_pool, c->ev_fwd, c->ev_plc, c->ev_fill[0], c->ev_fill[1]})
+        if (e) (void)hipEventDestroy(e);
     for (auto &m : c->marks) {
         c->ev_free.push_back(m.a);
         c->ev_free.push_back(m.b);

@@ -729,7 +729,13 @@ void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStre
     k_fwd_src<<<grid_for(n, kBlock * 4, 16384), kBlock, 0, s>>>(g, indices, n);
 }
 
-void launch_fetch(const DGlobal &g, hipStream_t s) { k_fetch<<<1024, kBlock, 0, s>>>(g); }
+#ifndef RECMG_FETCH_BLOCKS
+#define RECMG_FETCH_BLOCKS 256
+#endif
+
+// As for the prefetch fill, which runs at the same time on the copy stream: a
+// modest grid fills the host link and leaves most CUs' L1s to other kernels.
+void launch_fetch(const DGlobal &g, hipStream_t s) { k_fetch<<<RECMG_FETCH_BLOCKS, kBlock, 0, s>>>(g); }
 
 int pool_kind(int dtype, int vec, int wlw, int wr) {
     if (wlw == 0) return dtype * 2 + vec;

@@ -39,8 +39,9 @@ void launch_plc_classify(const DGlobal &g, int32_t last_stamp, int64_t np, hipSt
 void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s);
 void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,
                       hipStream_t s);
-void launch_plc_fill(const DGlobal &g, hipStream_t s);
-void launch_plc_finalize(const DGlobal &g, hipStream_t s);
+// fdesc: this placement's fill descriptor, [T][4] int64 (written by finalize, read by fill)
+void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s);
+void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, hipStream_t s);
 void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s);
 
 // setassoc.hip: placement of the set-associative tables (nu: index space of

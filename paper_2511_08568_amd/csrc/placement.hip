@@ -475,39 +475,42 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
 
 // Copy admitted rows into their slots: misses from HBM staging, prefetch
 // fills from pinned host memory over the host link (ZERO_COPY) or from rows the
-// host staged and copied in (STAGED).  May run on a side
-// stream, concurrently with the next forward's dedup: it reads only
-// placement-owned state (popped, ftstart, pstart, the fill list) and the
-// staging buffer of the previous forward, which the next forward does not use.
-__global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g) {
+// host staged and copied in (STAGED).  May run on a side stream, concurrently
+// with the next forward and with the next placement: it reads only its own
+// placement's fill list and descriptor (both double-buffered, see
+// k_plc_finalize) and the staging buffer of the forward before that placement,
+// which the next forward does not use.
+__global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, const int64_t *__restrict__ fdesc) {
     if (*g.err) return;
     __shared__ int32_t s_cnt[RECMG_MAX_TABLES];
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
-        const int64_t base = g.ftstart[t] + g.pstart[t];
-        const int32_t n = g.st[t].popped;
+        const int64_t base = fdesc[4 * t], n = fdesc[4 * t + 1];
         // admit wrote entries [base, base + n) and checked them against fill_cap
-        s_cnt[t] = (base >= 0 && n >= 0 && base + n <= g.fill_cap) ? n : 0;
+        s_cnt[t] = (base >= 0 && n >= 0 && base + n <= g.fill_cap) ? (int32_t)n : 0;
     }
     __syncthreads();
     copy_flat(
         g, s_cnt,
         [&](int t, const DTable &tb, int64_t j) -> const char * {
-            const int64_t fts = g.ftstart[t];
-            const int32_t src = g.fill_src[fts + g.pstart[t] + j];
-            if (src >= 0) return g.staging + (fts + src) * g.stage_stride;  // admitted miss
+            const int32_t src = g.fill_src[fdesc[4 * t] + j];
+            if (src >= 0) return g.staging + (fdesc[4 * t + 2] + src) * g.stage_stride;  // admitted miss
             return g.staged_fill ? g.fstage + (int64_t)(-src - 1) * g.stage_stride  // prefetch row, host-staged
                                  : tb.host + (int64_t)(-src - 1) * tb.row_bytes;    // prefetch row, zero-copy
         },
-        [&](int t, const DTable &tb, int64_t j) {
-            return tb.pool + (int64_t)g.fill_slot[g.ftstart[t] + g.pstart[t] + j] * tb.row_bytes;
-        });
+        [&](int t, const DTable &tb, int64_t j) { return tb.pool + (int64_t)g.fill_slot[fdesc[4 * t] + j] * tb.row_bytes; });
 }
 
-__global__ void k_plc_finalize(DGlobal g) {
+// Publishes the counters and writes the fill descriptor of this placement
+// (per table: first fill-list entry, entry count, base of its admitted misses
+// in staging), which the fill reads instead of state the next placement resets.
+__global__ void k_plc_finalize(DGlobal g, int64_t *fdesc) {
     if (*g.err) return;
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         TState &st = g.st[t];
         const DTable &tb = g.tabs[t];
+        fdesc[4 * t] = g.ftstart[t] + g.pstart[t];
+        fdesc[4 * t + 1] = st.popped;
+        fdesc[4 * t + 2] = g.ftstart[t];
         if (!tb.ways) {  // set-associative tables count residents as they place
             st.free_top -= st.popped;  // popped stays: the fill may still read it
             st.n_res = tb.cap - st.free_top;
@@ -587,13 +590,22 @@ void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int
     k_plc_admit<<<dim3(grid_for(cand_bound, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
 }
 
-void launch_plc_fill(const DGlobal &g, hipStream_t s) {
-    // The host link saturates with a few hundred waves of 4-deep 16-byte loads;
-    // a modest grid leaves the other CUs to the forward that runs alongside.
-    k_plc_fill<<<512, kBlock, 0, s>>>(g);
+#ifndef RECMG_FILL_BLOCKS
+#define RECMG_FILL_BLOCKS 128
+#endif
+
+void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s) {
+    // 128 blocks of 4-deep 16-byte loads keep the host link full (about 2 MB
+    // in flight).  Host reads hold a CU's L1 miss slots for microseconds, so a
+    // larger grid slows every kernel that shares its CUs: with 512 blocks the
+    // next forward's dedup, running alongside, took 0.88 ms on configuration 2
+    // instead of 0.28 ms.
+    k_plc_fill<<<RECMG_FILL_BLOCKS, kBlock, 0, s>>>(g, fdesc);
 }
 
-void launch_plc_finalize(const DGlobal &g, hipStream_t s) { k_plc_finalize<<<1, kBlock, 0, s>>>(g); }
+void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, hipStream_t s) {
+    k_plc_finalize<<<1, kBlock, 0, s>>>(g, fdesc);
+}
 
 void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s) {
     k_init_state<<<dim3(grid_for(max_cap, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g);

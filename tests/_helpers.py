@@ -81,7 +81,7 @@ class GpuRunner:
     """Drives the HIP path through a workload (test helper; marshalling only)."""
 
     def __init__(self, w, tabs, miss_mode="zero_copy", validate=False, max_indices=None, max_prefetch=None,
-                 nbatches=None, pin=True):
+                 nbatches=None, pin=True, pipeline=False):
         import torch
         from paper_2511_08568_amd import TieredEmbeddingCache
         self.torch = torch
@@ -99,13 +99,21 @@ class GpuRunner:
                                           policy=w.policy, eviction_speed=w.eviction_speed, miss_mode=miss_mode,
                                           max_bags_per_table=w.bags, max_indices=max_indices,
                                           max_prefetch=max_prefetch, validate=validate, ways=w.ways)
+        # pipelined placement: placements on a stream of their own, whose
+        # inputs are copied on that stream too
+        self.pstream = torch.cuda.Stream(device=self.dev) if pipeline else None
 
     def to_dev(self, a):
         return self.torch.from_numpy(np.ascontiguousarray(a)).to(self.dev)
 
     def placement(self, P, poff, bits=None):
-        self.cache.placement(self.to_dev(P) if P.size else None, self.to_dev(poff),
-                             None if bits is None else self.to_dev(bits))
+        if self.pstream is None:
+            self.cache.placement(self.to_dev(P) if P.size else None, self.to_dev(poff),
+                                 None if bits is None else self.to_dev(bits))
+            return
+        with self.torch.cuda.stream(self.pstream):
+            self.cache.placement(self.to_dev(P) if P.size else None, self.to_dev(poff),
+                                 None if bits is None else self.to_dev(bits), stream=self.pstream)
 
     def forward(self, idx, off):
         return self.cache.forward(self.to_dev(idx), self.to_dev(off), self.w.bags).cpu().numpy()

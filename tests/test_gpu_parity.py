@@ -4,7 +4,7 @@ import numpy as np
 import pytest
 
 import tracegen as tg
-from _helpers import GpuRunner, compare_runs, golden_table, load_golden
+from _helpers import GpuRunner, check_pooled, compare_runs, golden_table, load_golden
 from oracle_pins import GOLDEN_FILES, run_oracle
 
 torch = pytest.importorskip("torch")
@@ -274,7 +274,7 @@ def test_workspace_contents_do_not_matter(fill):
     probe.close()
     ws = th.full((nbytes,), fill, dtype=th.uint8, device="cuda")
     g = GpuRunner.__new__(GpuRunner)
-    g.torch, g.w, g.dev = th, w, th.device("cuda", 0)
+    g.torch, g.w, g.dev, g.pstream = th, w, th.device("cuda", 0), None
     g.host = [th.from_numpy(np.ascontiguousarray(a)).pin_memory() for a in tabs]
     g.cache = TieredEmbeddingCache(g.host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables],
                                    policy=w.policy, eviction_speed=w.eviction_speed,
@@ -287,3 +287,100 @@ def test_workspace_contents_do_not_matter(fill):
     finally:
         g.close()
     compare_runs(w, tabs, ora, gpu, label=f"garbage-workspace-{fill:#x}")
+
+
+# ----------------------------------------------------------------------------- pipelined placement
+
+def _device_inputs(w, nb, dev):
+    import torch as th
+    ins = []
+    for b in range(nb):
+        P, poff = w.prefetch_list(b)
+        bits = w.cache_bits(b - 1) if b > 0 else None
+        idx, off = w.batch(b)
+        ins.append(dict(P=th.from_numpy(P).to(dev) if P.size else None, poff=th.from_numpy(poff).to(dev),
+                        bits=None if bits is None else th.from_numpy(bits).to(dev),
+                        idx=th.from_numpy(idx).to(dev), off=th.from_numpy(off).to(dev)))
+    th.cuda.synchronize()
+    return ins
+
+
+@pytest.mark.parametrize("cid,scale,tables,ways", [(2, 0.02, 3, 0), (3, 0.01, 6, 0), (5, 0.01, 6, 32),
+                                                   (4, 0.0005, 2, 0)])
+def test_pipelined_placement_matches_oracle(cid, scale, tables, ways):
+    """Placements on a stream of their own, all calls issued back to back with
+    no synchronisation in between: placement b+1 runs while forward b still
+    waits for its fill or pools, and the fill of b+1 while forward b+1
+    deduplicates.  Totals of every counter, the final resident set and digest,
+    and every batch's pooled sums must equal the oracle's."""
+    import torch as th
+    w = tg.scaled_config(cid, row_scale=scale, batches=8, bags=256, max_tables=tables, ways=ways)
+    nb = w.batches
+    tabs, ora = run_oracle(w, nbatches=nb)
+    g = GpuRunner(w, tabs, nbatches=nb, pipeline=True)
+    try:
+        ins = _device_inputs(w, nb, g.dev)
+        outs = [th.empty(w.bags * sum(tb.dim for tb in w.tables), dtype=th.float32, device=g.dev) for _ in range(nb)]
+        for b in range(nb):
+            x = ins[b]
+            g.cache.placement(x["P"], x["poff"], x["bits"], stream=g.pstream)
+            g.cache.forward(x["idx"], x["off"], w.bags, out=outs[b])
+        last, tot, res = g.cache.stats(dump=True)
+    finally:
+        g.close()
+    from _helpers import FWD_KEYS, PLACE_KEYS
+    import tracegen
+    f64 = [tracegen.storage_to_f64(a, tb.dtype) for a, tb in zip(tabs, w.tables)]
+    for t in range(w.num_tables):
+        for k in PLACE_KEYS:
+            if k == "digest":
+                continue
+            assert tot[t][k] == sum(r["place"][t][k] for r in ora), f"table {t} total {k}"
+        for k in FWD_KEYS:
+            assert tot[t][k] == sum(r["fwd"][t][k] for r in ora), f"table {t} total {k}"
+        assert np.array_equal(res[t], ora[-1]["resident"][t]), f"table {t}: final resident set"
+        assert last[t]["digest"] == ora[-1]["place"][t]["digest"]
+    for b in range(nb):
+        check_pooled(w, f64, ora[b]["idx"], ora[b]["off"], outs[b].cpu().numpy(), ora[b]["out64"], f"batch {b}")
+
+
+@pytest.mark.parametrize("pipeline", [False, True])
+@pytest.mark.parametrize("ways", [0, 16])
+def test_skipped_placements(pipeline, ways):
+    """Placements the caller skips (the models were late, Sec. VI-C): the
+    next placement sees only the most recent forward's rows and misses, and
+    the batches in between run on the cache as it stands."""
+    import oracle
+    w = tg.scaled_config(3, row_scale=0.01, batches=9, bags=256, max_tables=5, ways=ways)
+    tabs = [w.table_values(t) for t in range(w.num_tables)]
+    o = oracle.for_workload(w, tabs)
+    g = GpuRunner(w, tabs, pipeline=pipeline)
+    try:
+        for b in range(w.batches):
+            if b % 3 != 2:
+                P, poff = w.prefetch_list(b)
+                bits = w.cache_bits(b - 1) if b > 0 else None
+                g.placement(P, poff, bits)
+                assert o.placement(P, poff, bits) == 0
+                last, _, res = g.cache.stats(dump=True)
+                for t in range(w.num_tables):
+                    ref = o.stats(t)
+                    for k in PLACE_KEYS_ALL:
+                        assert last[t][k] == ref[k], f"batch {b} table {t} placement {k}"
+                    assert np.array_equal(res[t], o.resident(t))
+            idx, off = w.batch(b)
+            out = g.forward(idx, off)
+            st, ref32, ref64 = o.forward(idx, off, w.bags, want64=True)
+            last, _ = g.cache.stats()
+            for t in range(w.num_tables):
+                ref = o.stats(t)
+                for k in ("lookups", "unique", "hits", "hits_prefetch", "misses", "prefetch_covered"):
+                    assert last[t][k] == ref[k], f"batch {b} table {t} forward {k}"
+            assert np.allclose(out, ref32, rtol=2e-2, atol=1e-3)
+    finally:
+        g.close()
+        o.close()
+
+
+PLACE_KEYS_ALL = ("evicted", "admitted_miss", "prefetch_fill", "prefetch_resident", "prefetch_dropped",
+                  "miss_dropped", "resident", "prefetch_distinct", "digest")
