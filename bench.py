@@ -46,7 +46,7 @@ def measured_traffic(args):
     """(bytes per launch, record) when the committed counter record matches
     this workload and the current kernel source, else (None, reason)."""
     default = (args.config == 2 and args.row_scale == 1.0 and args.prefetch is None
-               and args.miss_mode == "zero_copy")
+               and args.miss_mode == "zero_copy" and args.ways == 0 and args.bits is None)
     if not default:
         return None, "counters recorded for the default workload only"
     try:
