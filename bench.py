@@ -289,14 +289,15 @@ def main():
     d_bits = [None if cb is None else torch.from_numpy(cb).to(dev) for cb in bits]
     max_idx = max(i.size for i, _ in batches)
     max_pf = max(max(P.size for P, _ in prefetch), 1)
-    outs = [torch.empty(w.bags * sum(tb.dim for tb in w.tables), dtype=torch.float32, device=dev) for _ in range(2)]
+    # one output buffer per batch, so that every batch can be checked against the oracle afterwards
+    outs = [torch.empty(w.bags * sum(tb.dim for tb in w.tables), dtype=torch.float32, device=dev) for _ in range(nb)]
     torch.cuda.synchronize()
     log(f"{nb} batches staged in {time.time() - t0:.1f}s (max {max_idx} indices)")
 
     cache = TieredEmbeddingCache(host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables], policy=w.policy,
                                  eviction_speed=w.eviction_speed, miss_mode=args.miss_mode,
                                  max_bags_per_table=w.bags, max_indices=max_idx, max_prefetch=max_pf, timing=1,
-                                 ways=w.ways)
+                                 ways=w.ways, stats_log_calls=2 * nb)
     log(f"cache ready: workspace {cache.workspace_bytes / 1e9:.2f} GB")
 
     # Pipelined placement: placements run on a stream of their own, so that
@@ -311,7 +312,7 @@ def main():
         if marks is not None:
             marks[b].record(pstream if pstream is not None else torch.cuda.current_stream())
         i, o = d_batches[b]
-        cache.forward(i, o, w.bags, out=outs[b & 1])
+        cache.forward(i, o, w.bags, out=outs[b])
 
     for b in range(W):
         step(b)
@@ -461,14 +462,23 @@ def main():
         "stage_split_over": f"{KB} breakdown steps (every stage timed) after the timed ones",
     }
 
-    last_out = outs[(nb - 1) & 1].cpu().numpy()
-    last_digest = [tot2[t]["digest"] for t in range(T)]
+    # what the oracle replay checks: every call's counters (the device log),
+    # the final resident sets, and the pooled sums of every batch, or of a
+    # fixed subset (every 5th, the first and the last) where checking all would
+    # take the host too long
+    call_log = cache.stats_log()
+    _, _, final_res = cache.stats(dump=True)
+    work = sum(int(batches[b][0].size) for b in range(nb)) * (sum(tb.dim for tb in w.tables) / T)
+    check = list(range(nb)) if work <= 1e10 else sorted({0, nb - 1, *range(0, nb, 5)})
+    gpu_out = {b: outs[b].cpu().numpy() for b in check}
+    del outs
     cache.close()
 
     if not args.no_cpu_baseline:
         # The oracle replays the same batches on the host: timed as the CPU
-        # baseline, and compared with the GPU run (all counters summed over
-        # every batch, the final resident digests, the last batch's sums).
+        # baseline, and compared with the GPU run (every call's counters and
+        # digest, the totals, the final resident sets, the checked batches'
+        # pooled sums against rtol x L1 mass).
         import oracle
         cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
         nth = max(1, min(cores, T))
@@ -478,7 +488,9 @@ def main():
         # The timed sample is the replay of the GPU's batches, continued with
         # the workload's next batches (generated outside the timed intervals)
         # until about --cpu-seconds of oracle time.
-        done, n_lookups, secs, ref64 = 0, 0, 0.0, None
+        done, n_lookups, secs = 0, 0, 0.0
+        calls_equal, digests_equal, res_equal, pooled_ok, worst = True, True, None, True, 0.0
+        rtol = {"f32": 1e-5, "f16": 2e-2, "bf16": 2e-2}
         last_log = time.time()
         for b in range(w.batches):
             if time.time() - last_log > 15:
@@ -494,12 +506,32 @@ def main():
                 idx, off = w.batch(b)
             t_start = time.time()
             assert o.placement(P, poff, cb) == 0
+            secs += time.time() - t_start
             plc = [o.stats(t) for t in range(T)] if b < nb else None
-            st, _, r64 = o.forward(idx, off, w.bags, want64=(b == nb - 1))
+            t_start = time.time()
+            st, _, r64 = o.forward(idx, off, w.bags, want64=(b in gpu_out))
             secs += time.time() - t_start
             assert st == 0
-            if b == nb - 1:
-                ref64 = r64
+            if b < nb:
+                # this batch's two calls against the device log: placement 2b, forward 2b + 1
+                for t in range(T):
+                    fw = o.stats(t)
+                    for k in oracle.PLC_FIELDS:
+                        calls_equal &= call_log[2 * b][t][k] == plc[t][k]
+                    for k in oracle.FWD_FIELDS:
+                        calls_equal &= call_log[2 * b + 1][t][k] == fw[k]
+                    digests_equal &= call_log[2 * b][t]["digest"] == plc[t]["digest"]
+                if b in gpu_out:
+                    mass = o.pooled_abs(idx, off, w.bags)  # the tolerance scale, outside the timed intervals
+                    err = np.abs(gpu_out[b].astype(np.float64) - r64)
+                    at = 0
+                    for t, tb in enumerate(w.tables):
+                        n = w.bags * tb.dim
+                        pooled_ok &= bool(np.all(err[at:at + n] <= rtol[tb.dtype] * mass[at:at + n]))
+                        at += n
+                    worst = max(worst, float((err / np.maximum(mass, 1e-300)).max()) if err.size else 0.0)
+                if b == nb - 1:
+                    res_equal = all(np.array_equal(final_res[t], o.resident(t)) for t in range(T))
             if b < nb:
                 for t in range(T):
                     fw = o.stats(t)
@@ -531,26 +563,17 @@ def main():
                       f"usable core)",
             "cpu_model": cpu_model,
         }
-        if done >= nb and ref64 is not None:
-            counters_equal = all(sums[t][k] == tot2[t][k] for t in range(T) for k in sums[t] if k != "digest")
-            digest_equal = all(sums[t]["digest"] == last_digest[t] for t in range(T))
-            idx, off = batches[nb - 1]
-            rtol = {"f32": 1e-5, "f16": 2e-2, "bf16": 2e-2}
-            worst, ok, at = 0.0, True, 0
-            for t, tb in enumerate(w.tables):
-                s, e = w.table_segment(off, t)
-                rows = np.abs(tg.storage_to_f64(host[t].numpy()[idx[s:e]], tb.dtype))  # only the rows used
-                lens = np.diff(off[t * w.bags:(t + 1) * w.bags + 1])
-                seg = np.repeat(np.arange(w.bags), lens)
-                mass = np.zeros((w.bags, tb.dim))
-                np.add.at(mass, seg, rows)
-                n = w.bags * tb.dim
-                err = np.abs(last_out[at:at + n].astype(np.float64) - ref64[at:at + n]).reshape(w.bags, tb.dim)
-                ok &= bool(np.all(err <= rtol[tb.dtype] * mass))
-                worst = max(worst, float((err / np.maximum(mass, 1e-300)).max()))
-                at += n
-            result["parity"] = {"batches": nb, "counters_equal": counters_equal, "digest_equal": digest_equal,
-                                "last_batch_pooled_within_tol": ok, "last_batch_max_err_over_l1": worst}
+        if done >= nb:
+            totals_equal = all(sums[t][k] == tot2[t][k] for t in range(T) for k in sums[t] if k != "digest")
+            result["parity"] = {
+                "batches": nb,
+                "counters_equal_every_call": bool(calls_equal and totals_equal),
+                "digest_equal_every_placement": bool(digests_equal),
+                "final_resident_sets_equal": bool(res_equal),
+                "pooled_batches_checked": len(check) if len(check) < nb else "all",
+                "pooled_within_tol": bool(pooled_ok),
+                "pooled_max_err_over_l1": worst,
+            }
     print(json.dumps(result), flush=True)
 
 

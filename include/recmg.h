@@ -118,6 +118,8 @@ typedef struct {
                                            1 the pooled kernel only, 2 every stage */
     int32_t ways;                       /* 0: fully associative caches.  1 .. 64: W-way
                                            set-associative caches (see below) */
+    int32_t stats_log_calls;            /* >= 0: the counters of the latest this many calls
+                                           are kept on the device (recmg_stats_log) */
 } recmg_config_t;
 
 /* Stages timed at timing level 2 (RECMG_STAGE_FWD_POOL from level 1 on). */
@@ -209,6 +211,20 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
  * too small, RECMG_E_RANGE if the device error flag is set. */
 int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_stats_t *total,
                     int32_t *resident_dump, int64_t dump_capacity, int64_t *resident_counts);
+
+/* Counters of individual calls, in call order (placements and forwards
+ * numbered together from 0), from the device log of the latest
+ * config.stats_log_calls calls (the per-batch log a6 of the stats row: Sec.
+ * VII-E's access split per batch).  Synchronises.
+ *   out         host [n_calls][num_tables]: record of call first_call + k, table t
+ *               at out[k * num_tables + t].  A placement's record holds its
+ *               placement counters and the digest after it, a forward's record
+ *               its forward counters; the other group and a forward's digest are 0.
+ *   calls_made  host, or NULL: number of calls so far.
+ * RECMG_E_INVALID if a requested call is not (or no longer) in the log;
+ * n_calls = 0 only reports calls_made. */
+int32_t recmg_stats_log(recmg_cache_t *c, recmg_table_stats_t *out, int64_t first_call, int64_t n_calls,
+                        int64_t *calls_made);
 
 /* Device time per stage, summed over the calls since the last reset, in
  * milliseconds (ms[RECMG_NUM_STAGES]), and how many times each stage ran

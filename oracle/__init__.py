@@ -67,6 +67,8 @@ def load(mutant: int = 0) -> ctypes.CDLL:
     lib.oracle_resident.argtypes = [P, ctypes.c_int32, P, ctypes.c_int64]
     lib.oracle_row_state.restype = ctypes.c_int32
     lib.oracle_row_state.argtypes = [P, ctypes.c_int32, ctypes.c_int32, P, P]
+    lib.oracle_pooled_abs.restype = ctypes.c_int32
+    lib.oracle_pooled_abs.argtypes = [P, P, P, ctypes.c_int32, P]
     lib.oracle_splitmix64_mix.restype = ctypes.c_uint64
     lib.oracle_splitmix64_mix.argtypes = [ctypes.c_uint64]
     _LIBS[mutant] = lib
@@ -133,6 +135,20 @@ class Oracle:
         out64 = np.zeros(max(n, 1), dtype=np.float64) if want64 else None
         st = int(self.lib.oracle_forward(self.h, _ptr(indices), _ptr(offsets), int(bags), _ptr(out32), _ptr(out64)))
         return st, out32[:n], (out64[:n] if want64 else None)
+
+    def pooled_abs(self, indices: np.ndarray, offsets: np.ndarray, bags: int) -> np.ndarray:
+        """Per pooled output element, the sum of |x_i| over its bag (float64,
+        table-major like forward's output): the tolerance scale.  Stateless."""
+        indices = np.ascontiguousarray(indices, dtype=np.int32)
+        offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+        if indices.size == 0:
+            indices = np.zeros(1, np.int32)
+        n = bags * sum(self.dims)
+        out = np.zeros(max(n, 1), dtype=np.float64)
+        st = int(self.lib.oracle_pooled_abs(self.h, _ptr(indices), _ptr(offsets), int(bags), _ptr(out)))
+        if st != 0:
+            raise ValueError(f"oracle_pooled_abs returned {st}")
+        return out[:n]
 
     def stats(self, t: int) -> dict:
         fwd = np.zeros(len(FWD_FIELDS), np.int64)

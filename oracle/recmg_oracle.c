@@ -638,6 +638,30 @@ int32_t oracle_forward(void *h, const int32_t *idx, const int64_t *off, int32_t 
     return O_OK;
 }
 
+/* L1 mass of every pooled output element: out[t][j][k] = sum over bag j of
+ * |E_t[I[i]][k]|, in double (the scale of the pooled-sum tolerance).  Reads
+ * only the tables: no cache state, no counters. */
+int32_t oracle_pooled_abs(void *h, const int32_t *idx, const int64_t *off, int32_t B, double *out) {
+    oracle_t *o = (oracle_t *)h;
+    if (!o || !off || !out || B < 0) return O_E_INVALID;
+    int64_t base = 0;
+    for (int32_t t = 0; t < o->T; ++t) {
+        const otab *tb = &o->t[t];
+        const int64_t *bo = off + (int64_t)t * B;
+        for (int32_t j = 0; j < B; ++j)
+            for (int32_t k = 0; k < tb->d; ++k) {
+                double acc = 0.0;
+                for (int64_t i = bo[j]; i < bo[j + 1]; ++i) {
+                    if (idx[i] < 0 || idx[i] >= tb->n) return O_E_RANGE;
+                    acc += fabs(elem(tb, idx[i], k));
+                }
+                out[base + (int64_t)j * tb->d + k] = acc;
+            }
+        base += (int64_t)B * tb->d;
+    }
+    return O_OK;
+}
+
 /* fwd[7]: lookups, unique, hits, hits_prefetch, misses, ondemand_bytes,
  *         prefetch_covered.
  * plc[9]: evicted, admitted_miss, prefetch_fill, prefetch_resident,

@@ -21,5 +21,6 @@ from .binding import (  # noqa: F401
     recmg_set_timing,
     recmg_stage_times,
     recmg_stats,
+    recmg_stats_log,
     recmg_table_stats_t,
 )

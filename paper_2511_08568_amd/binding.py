@@ -30,7 +30,8 @@ STAT_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand
                "resident", "prefetch_bytes", "prefetch_distinct")
 
 EXPORTED = ("recmg_query_workspace", "recmg_cache_init", "recmg_apply_placement", "recmg_embbag_forward",
-            "recmg_stats", "recmg_stage_times", "recmg_set_timing", "recmg_cache_destroy", "recmg_last_error")
+            "recmg_stats", "recmg_stats_log", "recmg_stage_times", "recmg_set_timing", "recmg_cache_destroy",
+            "recmg_last_error")
 STAGES = ("fwd_dedup", "fwd_fetch", "fwd_pool", "plc_classify", "plc_rank", "plc_apply", "plc_fill", "host_link")
 
 
@@ -56,6 +57,7 @@ class recmg_config_t(ctypes.Structure):
         ("copy_stream", ctypes.c_void_p),
         ("timing", ctypes.c_int32),
         ("ways", ctypes.c_int32),
+        ("stats_log_calls", ctypes.c_int32),
     ]
 
 
@@ -89,6 +91,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.recmg_embbag_forward.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32, P, P]
     lib.recmg_stats.argtypes = [P, ctypes.POINTER(recmg_table_stats_t), ctypes.POINTER(recmg_table_stats_t), P,
                                 ctypes.c_int64, P]
+    lib.recmg_stats_log.argtypes = [P, P, ctypes.c_int64, ctypes.c_int64, P]
     lib.recmg_stage_times.argtypes = [P, P, P, ctypes.c_int32]
     lib.recmg_set_timing.argtypes = [P, ctypes.c_int32]
     lib.recmg_cache_destroy.argtypes = [P]
@@ -143,6 +146,10 @@ def recmg_stage_times(handle: int, ms: int, calls: int, reset: int) -> int:
     return int(load_library().recmg_stage_times(handle, ms or None, calls or None, int(reset)))
 
 
+def recmg_stats_log(handle: int, out, first_call: int, n_calls: int, calls_made) -> int:
+    return int(load_library().recmg_stats_log(handle, out, int(first_call), int(n_calls), calls_made))
+
+
 def recmg_set_timing(handle: int, level: int) -> int:
     return int(load_library().recmg_set_timing(handle, int(level)))
 
@@ -170,7 +177,8 @@ class TieredEmbeddingCache:
     def __init__(self, host_tables: Sequence, dtypes: Sequence[str], cache_rows: Sequence[int], *,
                  policy: str = "lru", eviction_speed: int = 4, miss_mode: str = "zero_copy",
                  max_bags_per_table: int, max_indices: int, max_prefetch: int, validate: bool = False,
-                 timing: int = 0, overlap: bool = True, workspace=None, device: int = 0, ways: int = 0):
+                 timing: int = 0, overlap: bool = True, workspace=None, device: int = 0, ways: int = 0,
+                 stats_log_calls: int = 0):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", device)
@@ -198,6 +206,7 @@ class TieredEmbeddingCache:
         cfg.validate = int(bool(validate))
         cfg.timing = 2 if timing is True else int(timing)  # 0 off, 1 pooled kernel, 2 every stage
         cfg.ways = int(ways)  # 0 fully associative, W > 0 W-way set-associative
+        cfg.stats_log_calls = int(stats_log_calls)  # counters of the latest calls, kept on the device
         cfg.max_bags_per_table = int(max_bags_per_table)
         cfg.max_indices = int(max_indices)
         cfg.max_prefetch = int(max_prefetch)
@@ -267,6 +276,20 @@ class TieredEmbeddingCache:
             res.append(buf[at:at + counts[t]].copy())
             at += int(counts[t])
         return (L, Tt, res, code) if not strict else (L, Tt, res)
+
+    def stats_log(self, first_call: int = 0, n_calls: int = None):
+        """Counters of calls first_call .. first_call + n_calls - 1 (placements and
+        forwards numbered together), each a list over tables of dicts; default:
+        every call still in the log.  Synchronises."""
+        made = ctypes.c_int64(0)
+        _check(recmg_stats_log(self.handle, None, 0, 0, ctypes.byref(made)), "recmg_stats_log")
+        if n_calls is None:
+            first_call = max(first_call, made.value - int(self.cfg.stats_log_calls))
+            n_calls = made.value - first_call
+        buf = (recmg_table_stats_t * (self.T * max(n_calls, 1)))()
+        _check(recmg_stats_log(self.handle, buf, first_call, n_calls, ctypes.byref(made)), "recmg_stats_log")
+        conv = lambda s: {**{f: int(getattr(s, f)) for f in STAT_FIELDS}, "digest": int(s.digest)}
+        return [[conv(buf[k * self.T + t]) for t in range(self.T)] for k in range(n_calls)]
 
     def set_timing(self, level: int):
         """0 off, 1 the pooled kernel only (no stream commands added), 2 every stage."""

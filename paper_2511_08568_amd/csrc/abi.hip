@@ -64,7 +64,7 @@ struct Layout {
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, raddr = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
     size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, pool_btab = 0, ftstart = 0;
-    size_t sa_bstart = 0, sa_btab = 0, fdesc = 0;
+    size_t sa_bstart = 0, sa_btab = 0, fdesc = 0, stat_log = 0;
     size_t fstage = 0;
     // pinned host staging (STAGED): miss ids, miss rows, fill sources, prefetch rows
     size_t h_mrows = 0, h_rows = 0, h_fsrc = 0, h_frows = 0;
@@ -85,6 +85,7 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
     if (cfg->miss_mode != RECMG_ZERO_COPY && cfg->miss_mode != RECMG_STAGED) return fail(RECMG_E_INVALID, "bad miss_mode");
     if (cfg->timing < 0 || cfg->timing > 2) return fail(RECMG_E_INVALID, "timing must be 0, 1 or 2");
     if (cfg->ways < 0 || cfg->ways > 64) return fail(RECMG_E_INVALID, "ways out of [0, 64]");
+    if (cfg->stats_log_calls < 0) return fail(RECMG_E_INVALID, "negative stats_log_calls");
     if (cfg->max_bags_per_table < 0 || cfg->max_indices < 0 || cfg->max_indices >= (int64_t(1) << 31) ||
         cfg->max_prefetch < 0 || cfg->max_prefetch >= (int64_t(1) << 31))
         return fail(RECMG_E_INVALID, "max_* sizes out of range");
@@ -202,6 +203,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->pool_bstart = take(4 * (T + 1));
     L->pool_btab = take(4 * T);
     L->ftstart = take(8 * (T + 1));
+    L->stat_log = take((size_t)cfg->stats_log_calls * T * sizeof(recmg_table_stats_t));
     L->sa_bstart = take(4 * (T + 1));
     L->sa_btab = take(4 * T);
     L->staging[0] = take(mi * (size_t)L->stage_stride);
@@ -242,6 +244,7 @@ struct recmg_cache {
     std::vector<PoolLaunch> pool_launches;
     int64_t max_rows = 0;
     int64_t placements = 0, forwards = 0, last_n = 0;
+    int64_t calls = 0;  // placements + forwards so far (the stats log's call index)
     bool have_fwd = false;
     hipStream_t last_stream = nullptr;
     // Calls may come on different streams (e.g. the next placement on its own
@@ -637,6 +640,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.stage_stride = L.stage_stride;
     g.T = T;
     g.total_bm_blocks = L.total_bm_blocks;
+    g.stat_log = reinterpret_cast<int64_t *>(ws + L.stat_log);
     g.sa_bstart = reinterpret_cast<int32_t *>(ws + L.sa_bstart);
     g.sa_btab = reinterpret_cast<int32_t *>(ws + L.sa_btab);
 
@@ -821,7 +825,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         if (c->has_fa) launch_plc_apply(g, p, c->max_cap, c->max_map, cand_grid, s);
         if (c->has_sa) launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks, s);
     }
-    launch_plc_finalize(g, fdesc, s);
+    launch_plc_finalize(g, fdesc, c->cfg.stats_log_calls ? c->calls % c->cfg.stats_log_calls : -1, s);
     HIP_TRY(hipEventRecord(c->ev_plc, s));
     // The fill overwrites the slots of evicted rows: it waits for the latest
     // forward's pooled kernel, which may read them, and for this placement.
@@ -841,6 +845,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     c->fill_last = q;
     HIP_TRY(hipGetLastError());
     c->placements++;
+    c->calls++;
     c->plc_np = num_prefetch;
     c->have_fwd = false;
     c->last_stream = s;
@@ -935,10 +940,11 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
         if (a) c->marks.push_back({RECMG_STAGE_FWD_POOL, a, b});
     }
     HIP_TRY(hipEventRecord(c->ev_pool, s));  // the next fill may overwrite slots from here on
-    launch_fwd_finalize(g, s);
+    launch_fwd_finalize(g, c->cfg.stats_log_calls ? c->calls % c->cfg.stats_log_calls : -1, s);
     HIP_TRY(hipEventRecord(c->ev_fwd, s));
     HIP_TRY(hipGetLastError());
     c->forwards++;
+    c->calls++;
     c->plc_np = -1;  // coverage counts against the placement just before a forward only
     c->have_fwd = true;
     c->last_n = n;
@@ -993,6 +999,28 @@ int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_sta
             coff += c->geo[t].cap;
         }
     }
+    g_last_error.clear();
+    return RECMG_OK;
+}
+
+int32_t recmg_stats_log(recmg_cache_t *c, recmg_table_stats_t *out, int64_t first_call, int64_t n_calls,
+                        int64_t *calls_made) {
+    int32_t rc = check_handle(c);
+    if (rc) return rc;
+    if (calls_made) *calls_made = c->calls;
+    if (n_calls == 0) return RECMG_OK;
+    const int64_t cap = c->cfg.stats_log_calls;
+    if (!out || n_calls < 0 || first_call < 0 || first_call + n_calls > c->calls || first_call < c->calls - cap)
+        return fail(RECMG_E_INVALID, "calls outside the stats log (the latest stats_log_calls calls are kept)");
+    if ((rc = set_device(c))) return rc;
+    HIP_TRY(sync_all(c));
+    const size_t rec = sizeof(recmg_table_stats_t) * (size_t)c->T;
+    for (int64_t k = first_call; k < first_call + n_calls; ++k)
+        HIP_TRY(hipMemcpy(reinterpret_cast<char *>(out) + (k - first_call) * rec,
+                          reinterpret_cast<const char *>(c->g.stat_log) + (k % cap) * rec, rec, hipMemcpyDeviceToHost));
+    int32_t err = 0;
+    HIP_TRY(hipMemcpy(&err, c->g.err, 4, hipMemcpyDeviceToHost));
+    if (err) return fail(RECMG_E_RANGE, "device error flag set (row id out of range or malformed offsets)");
     g_last_error.clear();
     return RECMG_OK;
 }

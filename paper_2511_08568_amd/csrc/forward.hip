@@ -680,7 +680,9 @@ __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(REC
     else pool_wave_v<DT, LW, R>(raddr, ob, nbags, D, ob_out);
 }
 
-__global__ void k_fwd_finalize(DGlobal g) {
+// Publishes the forward's counters; log_slot >= 0: also as that call's record
+// of the stats log (the placement group of the record stays zero).
+__global__ void k_fwd_finalize(DGlobal g, int64_t log_slot) {
     if (*g.err) return;
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         TState &st = g.st[t];
@@ -696,6 +698,10 @@ __global__ void k_fwd_finalize(DGlobal g) {
         for (int k = 0; k < kFwdStats; ++k) {
             st.last[k] = v[k];
             st.total[k] += v[k];
+        }
+        if (log_slot >= 0) {
+            int64_t *rec = g.stat_log + (log_slot * g.T + t) * (kNumStats + 1);
+            for (int k = 0; k <= kNumStats; ++k) rec[k] = k < kFwdStats ? v[k] : 0;
         }
     }
 }
@@ -785,6 +791,8 @@ void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out
     }
 }
 
-void launch_fwd_finalize(const DGlobal &g, hipStream_t s) { k_fwd_finalize<<<1, kBlock, 0, s>>>(g); }
+void launch_fwd_finalize(const DGlobal &g, int64_t log_slot, hipStream_t s) {
+    k_fwd_finalize<<<1, kBlock, 0, s>>>(g, log_slot);
+}
 
 }  // namespace recmg

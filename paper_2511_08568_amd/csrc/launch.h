@@ -30,7 +30,8 @@ struct PoolLaunch {
 void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, const int32_t *bstart,
                  const int32_t *btab, int32_t nt, const PoolLaunch *ls, int nl, hipEvent_t ev0, hipEvent_t ev1,
                  hipStream_t s);
-void launch_fwd_finalize(const DGlobal &g, hipStream_t s);
+// log_slot: record of this call in the stats log, or -1
+void launch_fwd_finalize(const DGlobal &g, int64_t log_slot, hipStream_t s);
 
 // placement.hip
 void launch_plc_prep(const DGlobal &g, const int64_t *poff, int64_t np, int32_t have_fwd, hipStream_t s);
@@ -41,7 +42,7 @@ void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int
                       hipStream_t s);
 // fdesc: this placement's fill descriptor, [T][4] int64 (written by finalize, read by fill)
 void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s);
-void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, hipStream_t s);
+void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, int64_t log_slot, hipStream_t s);
 void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s);
 
 // setassoc.hip: placement of the set-associative tables (nu: index space of

@@ -503,7 +503,9 @@ __global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, const int64_t *_
 // Publishes the counters and writes the fill descriptor of this placement
 // (per table: first fill-list entry, entry count, base of its admitted misses
 // in staging), which the fill reads instead of state the next placement resets.
-__global__ void k_plc_finalize(DGlobal g, int64_t *fdesc) {
+// log_slot >= 0: the counters also go to that call's record of the stats log
+// (the forward group of the record stays zero).
+__global__ void k_plc_finalize(DGlobal g, int64_t *fdesc, int64_t log_slot) {
     if (*g.err) return;
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         TState &st = g.st[t];
@@ -531,6 +533,11 @@ __global__ void k_plc_finalize(DGlobal g, int64_t *fdesc) {
             st.total[kFwdStats + k] += v[k];
         }
         st.digest = st.digest_acc;
+        if (log_slot >= 0) {
+            int64_t *rec = g.stat_log + (log_slot * g.T + t) * (kNumStats + 1);
+            for (int k = 0; k < kNumStats; ++k) rec[k] = k < kFwdStats ? 0 : v[k - kFwdStats];
+            rec[kNumStats] = (int64_t)st.digest_acc;
+        }
     }
 }
 
@@ -604,8 +611,8 @@ void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s) {
     k_plc_fill<<<g.staged_fill ? 1024 : RECMG_FILL_BLOCKS, kBlock, 0, s>>>(g, fdesc);
 }
 
-void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, hipStream_t s) {
-    k_plc_finalize<<<1, kBlock, 0, s>>>(g, fdesc);
+void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, int64_t log_slot, hipStream_t s) {
+    k_plc_finalize<<<1, kBlock, 0, s>>>(g, fdesc, log_slot);
 }
 
 void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s) {

@@ -136,6 +136,7 @@ struct DGlobal {
     int32_t total_bm_blocks;
     int32_t *sa_bstart;  // [nsa + 1] first placement block of each set-associative table
     int32_t *sa_btab;    // [nsa] those tables, fewest sets first
+    int64_t *stat_log;   // [log calls][T][kNumStats + 1]: the counters of each call (see recmg_stats_log)
 };
 
 // Parameters of one placement.

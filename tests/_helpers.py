@@ -81,7 +81,7 @@ class GpuRunner:
     """Drives the HIP path through a workload (test helper; marshalling only)."""
 
     def __init__(self, w, tabs, miss_mode="zero_copy", validate=False, max_indices=None, max_prefetch=None,
-                 nbatches=None, pin=True, pipeline=False):
+                 nbatches=None, pin=True, pipeline=False, stats_log_calls=0):
         import torch
         from paper_2511_08568_amd import TieredEmbeddingCache
         self.torch = torch
@@ -98,7 +98,8 @@ class GpuRunner:
         self.cache = TieredEmbeddingCache(self.host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables],
                                           policy=w.policy, eviction_speed=w.eviction_speed, miss_mode=miss_mode,
                                           max_bags_per_table=w.bags, max_indices=max_indices,
-                                          max_prefetch=max_prefetch, validate=validate, ways=w.ways)
+                                          max_prefetch=max_prefetch, validate=validate, ways=w.ways,
+                                          stats_log_calls=stats_log_calls)
         # pipelined placement: placements on a stream of their own, whose
         # inputs are copied on that stream too
         self.pstream = torch.cuda.Stream(device=self.dev) if pipeline else None

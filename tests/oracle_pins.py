@@ -109,6 +109,18 @@ def pin_embedding_bag(mutant=0):
                     torch.from_numpy(r["idx"][s:e].astype(np.int64)), torch.from_numpy(f64[t]), o_t,
                     mode="sum", include_last_offset=True).numpy().reshape(-1))
             ref = np.concatenate(ref) if ref else np.zeros(0)
+            # the L1 mass (tolerance scale) is the pooled sum of |table|
+            o2 = oracle.for_workload(w, tabs, mutant=mutant)
+            absref = []
+            for t in range(w.num_tables):
+                s, e = w.table_segment(r["off"], t)
+                o_t = torch.from_numpy(r["off"][t * w.bags:(t + 1) * w.bags + 1] - s)
+                absref.append(torch.nn.functional.embedding_bag(
+                    torch.from_numpy(r["idx"][s:e].astype(np.int64)), torch.from_numpy(np.abs(f64[t])), o_t,
+                    mode="sum", include_last_offset=True).numpy().reshape(-1))
+            absref = np.concatenate(absref) if absref else np.zeros(0)
+            assert np.allclose(o2.pooled_abs(r["idx"], r["off"], w.bags), absref, rtol=1e-12, atol=1e-12)
+            o2.close()
             if w.integer_values:
                 assert np.array_equal(r["out64"], ref), "integer-valued pooled sums must be exact"
                 assert np.array_equal(r["out32"], ref.astype(np.float32))

@@ -317,7 +317,7 @@ def test_pipelined_placement_matches_oracle(cid, scale, tables, ways):
     w = tg.scaled_config(cid, row_scale=scale, batches=8, bags=256, max_tables=tables, ways=ways)
     nb = w.batches
     tabs, ora = run_oracle(w, nbatches=nb)
-    g = GpuRunner(w, tabs, nbatches=nb, pipeline=True)
+    g = GpuRunner(w, tabs, nbatches=nb, pipeline=True, stats_log_calls=2 * nb)
     try:
         ins = _device_inputs(w, nb, g.dev)
         outs = [th.empty(w.bags * sum(tb.dim for tb in w.tables), dtype=th.float32, device=g.dev) for _ in range(nb)]
@@ -326,9 +326,19 @@ def test_pipelined_placement_matches_oracle(cid, scale, tables, ways):
             g.cache.placement(x["P"], x["poff"], x["bits"], stream=g.pstream)
             g.cache.forward(x["idx"], x["off"], w.bags, out=outs[b])
         last, tot, res = g.cache.stats(dump=True)
+        log = g.cache.stats_log()
     finally:
         g.close()
     from _helpers import FWD_KEYS, PLACE_KEYS
+    # every call's own counters, from the device log
+    assert len(log) == 2 * nb
+    for b in range(nb):
+        for t in range(w.num_tables):
+            for k in PLACE_KEYS:
+                assert log[2 * b][t][k] == ora[b]["place"][t][k], f"placement {b} table {t} {k}"
+            for k in FWD_KEYS:
+                assert log[2 * b][t][k] == 0 and log[2 * b + 1][t][k] == ora[b]["fwd"][t][k], f"forward {b} {t} {k}"
+            assert all(log[2 * b + 1][t][k] == 0 for k in PLACE_KEYS)
     import tracegen
     f64 = [tracegen.storage_to_f64(a, tb.dtype) for a, tb in zip(tabs, w.tables)]
     for t in range(w.num_tables):
@@ -384,3 +394,37 @@ def test_skipped_placements(pipeline, ways):
 
 PLACE_KEYS_ALL = ("evicted", "admitted_miss", "prefetch_fill", "prefetch_resident", "prefetch_dropped",
                   "miss_dropped", "resident", "prefetch_distinct", "digest")
+
+
+def test_stats_log_window():
+    """The log keeps the latest stats_log_calls calls; older ones are refused."""
+    from paper_2511_08568_amd import RecmgError
+    w = tg.scaled_config(1, row_scale=0.05, batches=5, bags=64)
+    tabs = [w.table_values(t) for t in range(w.num_tables)]
+    import oracle
+    o = oracle.for_workload(w, tabs)
+    g = GpuRunner(w, tabs, stats_log_calls=3)
+    try:
+        recs = []
+        for b in range(w.batches):
+            P, poff = w.prefetch_list(b)
+            g.placement(P, poff)
+            assert o.placement(P, poff) == 0
+            recs.append([o.stats(t) for t in range(w.num_tables)])
+            idx, off = w.batch(b)
+            g.forward(idx, off)
+            assert o.forward(idx, off, w.bags)[0] == 0
+            recs.append([o.stats(t) for t in range(w.num_tables)])
+        log = g.cache.stats_log()
+        assert len(log) == 3  # calls 7, 8, 9
+        assert log[0][0]["hits"] == recs[7][0]["hits"]      # call 7 = forward 3
+        assert log[1][0]["digest"] == recs[8][0]["digest"]  # call 8 = placement 4
+        assert log[1][0]["resident"] == recs[8][0]["resident"]
+        assert log[2][0]["hits"] == recs[9][0]["hits"]      # call 9 = forward 4
+        with pytest.raises(RecmgError):
+            g.cache.stats_log(first_call=0, n_calls=4)
+        with pytest.raises(RecmgError):
+            g.cache.stats_log(first_call=8, n_calls=3)  # call 10 not made yet
+    finally:
+        g.close()
+        o.close()
