@@ -598,16 +598,18 @@ void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int
 }
 
 #ifndef RECMG_FILL_BLOCKS
-#define RECMG_FILL_BLOCKS 128
+#define RECMG_FILL_BLOCKS 112
 #endif
 
 void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s) {
-    // Zero-copy fills read the host: 128 blocks of 4-deep 16-byte loads keep
-    // the host link full (about 2 MB in flight).  Host reads hold a CU's L1
-    // miss slots for microseconds, so a larger grid slows every kernel that
-    // shares its CUs: with 512 blocks the next forward's dedup, running
-    // alongside, took 0.88 ms on configuration 2 instead of 0.28 ms.  STAGED
-    // fills copy within HBM and take a full grid.
+    // Zero-copy fills read the host: about a hundred blocks of 4-deep 16-byte
+    // loads keep the host link full (about 2 MB in flight).  Host reads hold a
+    // CU's L1 miss slots for microseconds, so a larger grid slows every kernel
+    // that shares its CUs: with 512 blocks the next forward's dedup, running
+    // alongside, took 0.88 ms on configuration 2 instead of 0.28 ms.  Measured
+    // on configuration 2: 80-96 blocks leave the link short, 160 and more slow
+    // the placement that runs beside the fill.  STAGED fills copy within HBM
+    // and take a full grid.
     k_plc_fill<<<g.staged_fill ? 1024 : RECMG_FILL_BLOCKS, kBlock, 0, s>>>(g, fdesc);
 }
 
