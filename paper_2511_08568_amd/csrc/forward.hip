@@ -736,11 +736,14 @@ void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStre
 }
 
 #ifndef RECMG_FETCH_BLOCKS
-#define RECMG_FETCH_BLOCKS 256
+#define RECMG_FETCH_BLOCKS 96
 #endif
 
 // As for the prefetch fill, which runs at the same time on the copy stream: a
-// modest grid fills the host link and leaves most CUs' L1s to other kernels.
+// modest grid fills the host link and leaves most CUs' L1s to other kernels
+// (the next placement runs beside it).  Measured on configuration 3 (64-256
+// blocks): 96 is best with 32-way sets (k_sa_place's critical path runs
+// alongside), within 1% of the best without prefetch and on configuration 5.
 void launch_fetch(const DGlobal &g, hipStream_t s) { k_fetch<<<RECMG_FETCH_BLOCKS, kBlock, 0, s>>>(g); }
 
 int pool_kind(int dtype, int vec, int wlw, int wr) {
