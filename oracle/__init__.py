@@ -124,15 +124,23 @@ class Oracle:
             prefetch = np.zeros(1, np.int32)
         return int(self.lib.oracle_placement(self.h, _ptr(prefetch), _ptr(poff), _ptr(bits)))
 
-    def forward(self, indices: np.ndarray, offsets: np.ndarray, bags: int, want64: bool = False):
-        """Returns (status, out32 [sum_t B*D_t], out64 or None)."""
+    def forward(self, indices: np.ndarray, offsets: np.ndarray, bags: int, want64: bool = False,
+                out32: Optional[np.ndarray] = None, out64: Optional[np.ndarray] = None):
+        """Returns (status, out32 [sum_t B*D_t], out64 or None).  out32 / out64:
+        caller-allocated outputs (float32 / float64, at least that size) to write
+        instead of new arrays; out64 given implies want64."""
         indices = np.ascontiguousarray(indices, dtype=np.int32)
         offsets = np.ascontiguousarray(offsets, dtype=np.int64)
         if indices.size == 0:
             indices = np.zeros(1, np.int32)
         n = bags * sum(self.dims)
-        out32 = np.zeros(max(n, 1), dtype=np.float32)
-        out64 = np.zeros(max(n, 1), dtype=np.float64) if want64 else None
+        want64 = want64 or out64 is not None
+        if out32 is None:
+            out32 = np.zeros(max(n, 1), dtype=np.float32)
+        if out64 is None and want64:
+            out64 = np.zeros(max(n, 1), dtype=np.float64)
+        assert out32.dtype == np.float32 and out32.size >= n and out32.flags.c_contiguous
+        assert not want64 or (out64.dtype == np.float64 and out64.size >= n and out64.flags.c_contiguous)
         st = int(self.lib.oracle_forward(self.h, _ptr(indices), _ptr(offsets), int(bags), _ptr(out32), _ptr(out64)))
         return st, out32[:n], (out64[:n] if want64 else None)
 
