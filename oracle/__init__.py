@@ -21,7 +21,7 @@ FWD_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand_
 PLC_FIELDS = ("evicted", "admitted_miss", "prefetch_fill", "prefetch_resident",
               "prefetch_dropped", "miss_dropped", "resident", "prefetch_bytes", "prefetch_distinct")
 DTYPES = {"f32": 0, "f16": 1, "bf16": 2}
-POLICIES = {"lru": 0, "priority": 1}
+POLICIES = {"lru": 0, "priority": 1, "lfu": 2}
 
 
 def lib_path(mutant: int = 0) -> str:

@@ -35,9 +35,13 @@
  *   2. rows of U that are resident lose their prefetch flag.
  *   3. touch: for r in U, s(r) <- b-1 under LRU_BATCH (b = index of this
  *      placement, so b-1 is the batch just run), or c(r) + ES under PRIORITY
- *      (Alg. 1's priority = C + eviction_speed), with c(r) the OR of r's bits.
+ *      (Alg. 1's priority = C + eviction_speed), with c(r) the OR of r's bits,
+ *      or f(r) under LFU_BATCH, f(r) being the number of batches that have
+ *      accessed r so far (counted for every row, resident or not; the 32-way
+ *      LFU baseline of Sec. VII-B at batch granularity).
  *   4. prefetch: for r in set(P), s(r) <- max(s(r) if r in R or M, else -inf,
- *      b under LRU_BATCH or ES under PRIORITY) (Alg. 1's prefetch priority).
+ *      b under LRU_BATCH or ES under PRIORITY) (Alg. 1's prefetch priority);
+ *      under LFU_BATCH a prefetched row keeps its frequency f(r).
  *   5. K = R ∪ M ∪ set(P); R' = the min(Cap, |K|) members with the largest
  *      key (s(r), r): the lowest score is evicted first, and among equal
  *      scores the lower row id goes first (Alg. 2's minimum-priority victim).
@@ -83,7 +87,7 @@
 #endif
 
 enum { O_F32 = 0, O_F16 = 1, O_BF16 = 2 };
-enum { O_LRU_BATCH = 0, O_PRIORITY = 1 };
+enum { O_LRU_BATCH = 0, O_PRIORITY = 1, O_LFU_BATCH = 2 };
 enum { O_OK = 0, O_E_RANGE = -1, O_E_INVALID = -2 };
 
 typedef struct {
@@ -112,6 +116,8 @@ typedef struct {
     int64_t fwd[7];
     int64_t plc[9];
     uint64_t digest;
+    /* LFU_BATCH: number of batches that accessed each row (kept for every row) */
+    int64_t *freq;
     /* set-associative form: nsets sets of `ways` rows each (-1 = free way) */
     int64_t nsets;
     int32_t *way_row, *way_row0;
@@ -167,7 +173,7 @@ void oracle_destroy(void *h) {
         free(tb->last_idx); free(tb->U); free(tb->M);
         free(tb->in_u); free(tb->in_m); free(tb->in_p); free(tb->c);
         free(tb->lastP);
-        free(tb->way_row); free(tb->way_row0); free(tb->in_r0);
+        free(tb->way_row); free(tb->way_row0); free(tb->in_r0); free(tb->freq);
     }
     free(o->t);
     free(o);
@@ -177,7 +183,7 @@ void *oracle_create(int32_t T, const int64_t *rows, const int32_t *dims, const i
                     const void *const *tables, const int64_t *caps, int32_t policy, int32_t es,
                     int32_t nthreads, int32_t ways) {
     if (T <= 0 || !rows || !dims || !dtypes || !tables || !caps) return NULL;
-    if (policy != O_LRU_BATCH && policy != O_PRIORITY) return NULL;
+    if (policy != O_LRU_BATCH && policy != O_PRIORITY && policy != O_LFU_BATCH) return NULL;
     if (ways < 0) return NULL;
     oracle_t *o = (oracle_t *)calloc(1, sizeof(oracle_t));
     o->T = T; o->policy = policy; o->es = es; o->nthreads = nthreads > 0 ? nthreads : 1; o->ways = ways;
@@ -197,6 +203,7 @@ void *oracle_create(int32_t T, const int64_t *rows, const int32_t *dims, const i
         tb->res = (int32_t *)malloc(sizeof(int32_t) * (size_t)(tb->cap + 1));
         tb->in_u = (uint8_t *)calloc(n, 1); tb->in_m = (uint8_t *)calloc(n, 1);
         tb->in_p = (uint8_t *)calloc(n, 1); tb->c = (uint8_t *)calloc(n, 1);
+        if (policy == O_LFU_BATCH) tb->freq = (int64_t *)calloc(n, sizeof(int64_t));
         if (ways > 0) {
             tb->nsets = tb->cap / ways;
             size_t nw = (size_t)(tb->nsets * ways) + 1;
@@ -227,14 +234,48 @@ static int key_desc(const void *a, const void *b) {
 
 static void place_table_sa(oracle_t *o, int32_t t, const int32_t *P, int64_t nP);
 
+/* Score of a row the last batch touched, in placement b. */
+static int64_t touch_score(const oracle_t *o, const otab *tb, int32_t r, int64_t b) {
+    if (o->policy == O_LRU_BATCH) return b - 1;
+    if (o->policy == O_PRIORITY) return (int64_t)tb->c[r] + o->es;
+    return tb->freq[r];
+}
+
+/* Score a prefetch gives a row not resident and not missed (the prefetch
+ * score); a resident or missed row keeps the larger of its score and this.
+ * LFU_BATCH ranks a prefetched row by its frequency and gives no floor. */
+static int64_t prefetch_score(const oracle_t *o, const otab *tb, int32_t r, int64_t b) {
+    if (o->policy == O_LRU_BATCH) {
+#if ORACLE_MUTANT == 7 /* planted: prefetch scored like a touch */
+        return b - 1;
+#else
+        return b;
+#endif
+    }
+    if (o->policy == O_PRIORITY) return o->es;
+    return tb->freq[r];
+}
+
+static int64_t prefetch_floor(const oracle_t *o, const otab *tb, int32_t r, int64_t b) {
+    return o->policy == O_LFU_BATCH ? 0 : prefetch_score(o, tb, r, b);
+}
+
 static void place_table(oracle_t *o, int32_t t, const int32_t *P, int64_t nP, const uint8_t *bits) {
     otab *tb = &o->t[t];
     const int64_t b = o->placements;
-    const int lru = o->policy == O_LRU_BATCH;
+    const int prio = o->policy == O_PRIORITY;
     int64_t nU = tb->have_fwd ? tb->nU : 0, nM = tb->have_fwd ? tb->nM : 0;
 
+    /* LFU_BATCH: one more batch for every row the last batch accessed */
+    if (o->policy == O_LFU_BATCH && tb->have_fwd) {
+#if ORACLE_MUTANT == 17 /* planted: frequency counts every access, not every batch */
+        for (int64_t i = 0; i < tb->nlast; ++i) tb->freq[tb->last_idx[i]] += 1;
+#else
+        for (int64_t k = 0; k < nU; ++k) tb->freq[tb->U[k]] += 1;
+#endif
+    }
     /* c(r): OR of the caching bits over r's accesses in the last batch. */
-    if (!lru && bits && tb->have_fwd) {
+    if (prio && bits && tb->have_fwd) {
         for (int64_t i = 0; i < tb->nlast; ++i) {
 #if ORACLE_MUTANT == 4 /* planted: the last access's bit wins */
             tb->c[tb->last_idx[i]] = bits[tb->last_base + i] != 0;
@@ -249,7 +290,7 @@ static void place_table(oracle_t *o, int32_t t, const int32_t *P, int64_t nP, co
     }
     /* 1. aging (PRIORITY) */
 #if ORACLE_MUTANT != 2 /* planted (2): no aging */
-    if (!lru)
+    if (prio)
         for (int64_t k = 0; k < tb->nres; ++k) {
             int32_t r = tb->res[k];
 #if ORACLE_MUTANT == 9 /* planted: the decrement does not saturate at 0 */
@@ -265,13 +306,9 @@ static void place_table(oracle_t *o, int32_t t, const int32_t *P, int64_t nP, co
 #if ORACLE_MUTANT != 6 /* planted (6): prefetch flag survives an access */
         if (tb->in_r[r]) tb->pf[r] = 0;
 #endif
-        tb->s[r] = lru ? b - 1 : (int64_t)tb->c[r] + o->es;
+        tb->s[r] = touch_score(o, tb, r, b);
     }
     /* 4. prefetch scores over set(P) */
-    int64_t pscore = lru ? b : o->es;
-#if ORACLE_MUTANT == 7 /* planted: prefetch scored like a touch */
-    if (lru) pscore = b - 1;
-#endif
     int64_t np_new = 0, p_res = 0;
     int32_t *pnew = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nP + 1));
     free(tb->lastP);
@@ -284,13 +321,13 @@ static void place_table(oracle_t *o, int32_t t, const int32_t *P, int64_t nP, co
         tb->lastP[tb->nlastP++] = r;
         if (tb->in_r[r] || tb->in_m[r]) {
 #if ORACLE_MUTANT == 3 /* planted: prefetch overwrites the score */
-            tb->s[r] = pscore;
+            tb->s[r] = prefetch_floor(o, tb, r, b);
 #else
-            if (pscore > tb->s[r]) tb->s[r] = pscore;
+            if (prefetch_floor(o, tb, r, b) > tb->s[r]) tb->s[r] = prefetch_floor(o, tb, r, b);
 #endif
             if (tb->in_r[r]) ++p_res;
         } else {
-            tb->s[r] = pscore;
+            tb->s[r] = prefetch_score(o, tb, r, b);
             pnew[np_new++] = r;
         }
     }
@@ -401,7 +438,6 @@ static void sa_insert(oracle_t *o, otab *tb, int32_t r, int64_t v) {
 static void place_table_sa(oracle_t *o, int32_t t, const int32_t *P, int64_t nP) {
     otab *tb = &o->t[t];
     const int64_t b = o->placements;
-    const int lru = o->policy == O_LRU_BATCH;
     const int32_t W = o->ways;
     const int64_t nslot = tb->nsets * W;
     int64_t nU = tb->have_fwd ? tb->nU : 0, nM = tb->have_fwd ? tb->nM : 0;
@@ -410,7 +446,7 @@ static void place_table_sa(oracle_t *o, int32_t t, const int32_t *P, int64_t nP)
     for (int64_t k = 0; k < nslot; ++k)
         if (tb->way_row0[k] >= 0) tb->in_r0[tb->way_row0[k]] = 1;
 #if ORACLE_MUTANT == 15 /* planted: every resident ages once per placement instead of per scan */
-    if (!lru)
+    if (o->policy == O_PRIORITY)
         for (int64_t k = 0; k < nslot; ++k)
             if (tb->way_row[k] >= 0) {
                 int32_t r = tb->way_row[k];
@@ -422,11 +458,10 @@ static void place_table_sa(oracle_t *o, int32_t t, const int32_t *P, int64_t nP)
         int32_t r = tb->U[k];
         if (tb->in_r[r]) {
             tb->pf[r] = 0;
-            tb->s[r] = lru ? b - 1 : (int64_t)tb->c[r] + o->es;
+            tb->s[r] = touch_score(o, tb, r, b);
         }
     }
     /* distinct prefetch rows, ascending */
-    int64_t pscore = lru ? b : o->es;
     int32_t *pd = (int32_t *)malloc(sizeof(int32_t) * (size_t)(nP + 1));
     int64_t npd = 0;
     for (int64_t k = 0; k < nP; ++k)
@@ -442,20 +477,20 @@ static void place_table_sa(oracle_t *o, int32_t t, const int32_t *P, int64_t nP)
 #if ORACLE_MUTANT == 13 /* planted: prefetch events before the misses */
     for (int64_t k = 0; k < npd; ++k) {
         int32_t r = pd[k];
-        if (tb->in_r[r]) { if (pscore > tb->s[r]) tb->s[r] = pscore; }
-        else sa_insert(o, tb, r, pscore);
+        if (tb->in_r[r]) { if (prefetch_floor(o, tb, r, b) > tb->s[r]) tb->s[r] = prefetch_floor(o, tb, r, b); }
+        else sa_insert(o, tb, r, prefetch_score(o, tb, r, b));
     }
-    for (int64_t k = 0; k < nM; ++k) if (!tb->in_r[ms[k]]) sa_insert(o, tb, ms[k], lru ? b - 1 : (int64_t)tb->c[ms[k]] + o->es);
+    for (int64_t k = 0; k < nM; ++k) if (!tb->in_r[ms[k]]) sa_insert(o, tb, ms[k], touch_score(o, tb, ms[k], b));
 #else
     /* B. misses, ascending */
-    for (int64_t k = 0; k < nM; ++k) sa_insert(o, tb, ms[k], lru ? b - 1 : (int64_t)tb->c[ms[k]] + o->es);
+    for (int64_t k = 0; k < nM; ++k) sa_insert(o, tb, ms[k], touch_score(o, tb, ms[k], b));
     /* C. prefetch rows, ascending */
     for (int64_t k = 0; k < npd; ++k) {
         int32_t r = pd[k];
         if (tb->in_r[r]) {
-            if (pscore > tb->s[r]) tb->s[r] = pscore;
+            if (prefetch_floor(o, tb, r, b) > tb->s[r]) tb->s[r] = prefetch_floor(o, tb, r, b);
         } else {
-            sa_insert(o, tb, r, pscore);
+            sa_insert(o, tb, r, prefetch_score(o, tb, r, b));
         }
     }
 #endif

@@ -12,7 +12,8 @@ Sources of truth used here:
     (the textbook pooled lookup, Sec. II);
   * the published first outputs of SplitMix64 seeded with 0;
   * closed forms that hold for special cases: an LRU cache keeps the Cap rows
-    with the most recent events (global history), an unbounded cache keeps
+    with the most recent events (global history), an LFU cache the Cap rows
+    with the most batches accessed (among rows ever offered), an unbounded cache keeps
     everything it was offered, a zero-capacity cache never hits, and with
     eviction_speed 0 the priority policy reduces to ranking by row id;
   * invariants: hits + misses = distinct rows, |R| <= Cap, resident-count
@@ -33,7 +34,8 @@ import tracegen as tg
 from _helpers import golden_table, load_golden, splitmix64_mix_py
 
 GOLDEN_FILES = ("hand_lru.json", "hand_priority_es4.json", "hand_priority_es1.json", "hand_priority_es0.json",
-                "hand_sa_lru_w2.json", "hand_sa_priority_w2.json", "hand_sa_priority_es1.json")
+                "hand_sa_lru_w2.json", "hand_sa_priority_w2.json", "hand_sa_priority_es1.json",
+                "hand_sa_lfu_w2.json")
 
 
 # ----------------------------------------------------------------------------- drivers
@@ -177,6 +179,31 @@ def pin_lru_history(mutant=0, seeds=range(40)):
                         pf_live[t][x] = False
 
 
+def pin_lfu_history(mutant=0, seeds=range(40)):
+    """LFU_BATCH keeps the Cap rows with the largest (f, row), f = number of
+    batches that accessed the row before this placement, over every row ever
+    accessed or prefetched: a row leaves only for Cap rows of larger key, and
+    keys never decrease, so it can come back only through a new event."""
+    for s in seeds:
+        w = tg.random_tiny(s, policy="lfu", batches=6)
+        _, recs = run_oracle(w, mutant=mutant, want64=False)
+        T = w.num_tables
+        f = [dict() for _ in range(T)]
+        offered = [set() for _ in range(T)]
+        for b, r in enumerate(recs):
+            for t in range(T):
+                offered[t] |= set(r["P"][r["poff"][t]:r["poff"][t + 1]].tolist())
+                ranked = sorted(offered[t], key=lambda x: (f[t].get(x, 0), x), reverse=True)
+                R = set(ranked[: w.tables[t].cap])
+                assert sorted(R) == r["resident"][t].tolist(), f"seed {s} batch {b} table {t}"
+            for t, (a, e) in enumerate(segments(w, r["off"])):
+                U = set(r["idx"][a:e].tolist())
+                assert r["fwd"][t]["misses"] == len(U - set(r["resident"][t].tolist()))
+                for x in U:
+                    f[t][x] = f[t].get(x, 0) + 1
+                offered[t] |= U
+
+
 def pin_unbounded_cache(mutant=0, seeds=range(20)):
     """Cap >= N: nothing is ever evicted; the cache holds every row accessed or
     prefetched so far, and the misses of a batch are its never-seen rows."""
@@ -240,7 +267,7 @@ def pin_priority_es0(mutant=0, seeds=range(30)):
 
 def pin_invariants(mutant=0, seeds=range(40)):
     for s in seeds:
-        w = tg.random_tiny(s, batches=6)
+        w = tg.random_tiny(s, batches=6, policy=("lru", "priority", "lfu")[s % 3])
         _, recs = run_oracle(w, mutant=mutant, want64=False)
         prev = [0] * w.num_tables
         for r in recs:
@@ -304,7 +331,7 @@ def pin_sa_direct_mapped(mutant=0, seeds=range(30)):
     of the last batch, else its previous row (misses first, then prefetches,
     each ascending; Alg. 1 inserts unconditionally)."""
     for s in seeds:
-        w = tg.random_tiny(s, max_rows=24, max_cap=8, batches=6)
+        w = tg.random_tiny(s, max_rows=24, max_cap=8, batches=6, policy=("lru", "priority", "lfu")[s % 3])
         w.ways = 1
         _, recs = run_oracle(w, mutant=mutant, want64=False)
         T = w.num_tables
@@ -392,7 +419,7 @@ def pin_sa_no_eviction(mutant=0, seeds=range(12)):
 
 def pin_sa_invariants(mutant=0, seeds=range(30)):
     for s in seeds:
-        w = tg.random_tiny(s, max_rows=30, max_cap=12, batches=6)
+        w = tg.random_tiny(s, max_rows=30, max_cap=12, batches=6, policy=("lru", "priority", "lfu")[s % 3])
         w.ways = 1 + s % 4
         _, recs = run_oracle(w, mutant=mutant, want64=False)
         prev = [0] * w.num_tables
@@ -413,6 +440,7 @@ def pin_sa_invariants(mutant=0, seeds=range(30)):
                 prev[t] = p["resident"]
 
 
-ALL_PINS = (pin_hand_examples, pin_embedding_bag, pin_splitmix, pin_lru_history, pin_unbounded_cache,
+ALL_PINS = (pin_hand_examples, pin_embedding_bag, pin_splitmix, pin_lru_history, pin_lfu_history,
+            pin_unbounded_cache,
             pin_zero_capacity, pin_priority_es0, pin_invariants, pin_prefetch_quality, pin_sa_direct_mapped,
             pin_sa_lru_distinct_events, pin_sa_no_eviction, pin_sa_invariants)

@@ -22,6 +22,7 @@ MUTANTS = {
     14: "set-associative: events of a set in descending row order",
     15: "set-associative: aging once per placement instead of per eviction",
     16: "set-associative: set index taken modulo the ways",
+    17: "LFU counts every access instead of every batch",
 }
 
 
