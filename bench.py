@@ -46,7 +46,7 @@ def measured_traffic(args):
     """(bytes per launch, record) when the committed counter record matches
     this workload and the current kernel source, else (None, reason)."""
     default = (args.config == 2 and args.row_scale == 1.0 and args.prefetch is None
-               and args.miss_mode == "zero_copy" and args.ways == 0 and args.bits is None)
+               and args.miss_mode == "zero_copy" and args.ways == 0 and args.bits is None and args.policy is None)
     if not default:
         return None, "counters recorded for the default workload only"
     try:
@@ -104,7 +104,7 @@ def buffer_sweep(args, dev):
     # the production buffer the paper compares against
     variants = {"lru": ("lru", ("none",), 0), "caching_model": ("priority", ("none",), 0),
                 "caching_and_prefetch": ("priority", recipe, 0), "lru_32way": ("lru", ("none",), 32),
-                "caching_and_prefetch_32way": ("priority", recipe, 32)}
+                "lfu_32way": ("lfu", ("none",), 32), "caching_and_prefetch_32way": ("priority", recipe, 32)}
     points = []
     for frac in (0.01, 0.02, 0.05, 0.10, 0.15, 0.20, 0.30):
         caps = [max(1, int(round(frac * n))) for n in seen]
@@ -211,6 +211,8 @@ def main():
     ap.add_argument("--sweep-batches", type=int, default=60)
     ap.add_argument("--no-pipeline", dest="pipeline", action="store_false",
                     help="run placements on the forward's stream (no overlap of placement b+1 with forward b)")
+    ap.add_argument("--policy", default=None, choices=["lru", "priority", "lfu"],
+                    help="override the configuration's placement policy")
     ap.add_argument("--ways", type=int, default=0,
                     help="W > 0: W-way set-associative caches (Alg. 2 inside each set) instead of fully "
                          "associative ones")
@@ -250,6 +252,8 @@ def main():
     if args.prefetch is not None:
         w.prefetch = (args.prefetch,)
     w.ways = args.ways
+    if args.policy is not None:
+        w.policy = args.policy
     W, K = args.warmup, args.steps
     if W + K > w.batches:
         raise SystemExit(f"warmup + steps must be at most the workload's {w.batches} batches")

@@ -22,6 +22,10 @@
  *   placement; a touched row scores bit + eviction_speed, with bit the OR of
  *   its caching bits in the last batch; a prefetched row scores
  *   max(its score, eviction_speed).
+ *   LFU_BATCH (the LFU baseline of Sec. VII-B, per batch): a row's score is
+ *   the number of batches that have accessed it, counted for every row
+ *   whether cached or not (a device array of N_t counters); a prefetch does
+ *   not change it.
  *
  * Set-associative form (config.ways = W > 0; the production buffer of Sec.
  * VI-B is a W-way set-associative software cache, Sec. VII-B and VII-E): a
@@ -77,7 +81,7 @@ typedef enum {
 } recmg_status_t;
 
 typedef enum { RECMG_F32 = 0, RECMG_F16 = 1, RECMG_BF16 = 2 } recmg_dtype_t;
-typedef enum { RECMG_LRU_BATCH = 0, RECMG_PRIORITY = 1 } recmg_policy_t;
+typedef enum { RECMG_LRU_BATCH = 0, RECMG_PRIORITY = 1, RECMG_LFU_BATCH = 2 } recmg_policy_t;
 typedef enum {
     RECMG_ZERO_COPY = 0, /* misses are read from host memory by a GPU kernel over the host link */
     RECMG_STAGED = 1     /* miss ids (and the placement's prefetch fills) go to the host, a

@@ -17,12 +17,12 @@ LIB_PATH = os.environ.get("RECMG_LIBRARY") or os.path.join(HERE, "librecmg.so")
 
 RECMG_OK, RECMG_E_INVALID, RECMG_E_RANGE, RECMG_E_STATE, RECMG_E_HIP, RECMG_E_NOMEM = range(6)
 RECMG_F32, RECMG_F16, RECMG_BF16 = range(3)
-RECMG_LRU_BATCH, RECMG_PRIORITY = range(2)
+RECMG_LRU_BATCH, RECMG_PRIORITY, RECMG_LFU_BATCH = range(3)
 RECMG_ZERO_COPY, RECMG_STAGED = range(2)
 RECMG_MAX_TABLES = 256
 
 DTYPE_CODES = {"f32": RECMG_F32, "f16": RECMG_F16, "bf16": RECMG_BF16}
-POLICY_CODES = {"lru": RECMG_LRU_BATCH, "priority": RECMG_PRIORITY}
+POLICY_CODES = {"lru": RECMG_LRU_BATCH, "priority": RECMG_PRIORITY, "lfu": RECMG_LFU_BATCH}
 MISS_CODES = {"zero_copy": RECMG_ZERO_COPY, "staged": RECMG_STAGED}
 
 STAT_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand_bytes", "prefetch_covered",

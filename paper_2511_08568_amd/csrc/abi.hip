@@ -60,7 +60,7 @@ struct Geom {
 struct Layout {
     size_t total = 0, host_total = 0;
     std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, slot_cbit, free_stack, map, bitmap, rank,
-        seg;
+        seg, freq;
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, raddr = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
     size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, pool_btab = 0, ftstart = 0;
@@ -79,7 +79,8 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
     if (T < 1 || T > RECMG_MAX_TABLES) return fail(RECMG_E_INVALID, "num_tables out of [1, RECMG_MAX_TABLES]");
     if (!cfg->rows || !cfg->dims || !cfg->dtypes || !cfg->host_tables || !cfg->cache_rows)
         return fail(RECMG_E_INVALID, "a per-table array is NULL");
-    if (cfg->policy != RECMG_LRU_BATCH && cfg->policy != RECMG_PRIORITY) return fail(RECMG_E_INVALID, "bad policy");
+    if (cfg->policy != RECMG_LRU_BATCH && cfg->policy != RECMG_PRIORITY && cfg->policy != RECMG_LFU_BATCH)
+        return fail(RECMG_E_INVALID, "bad policy");
     if (cfg->eviction_speed < 0 || cfg->eviction_speed > (1 << 20))
         return fail(RECMG_E_INVALID, "eviction_speed out of [0, 2^20]");
     if (cfg->miss_mode != RECMG_ZERO_COPY && cfg->miss_mode != RECMG_STAGED) return fail(RECMG_E_INVALID, "bad miss_mode");
@@ -172,6 +173,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
         L->bitmap.push_back(take((size_t)g.bm_words * 4));
         L->rank.push_back(take((size_t)g.bm_words * 16));
         L->seg.push_back(take((size_t)g.nsets * 16));
+        L->freq.push_back(take(cfg->policy == RECMG_LFU_BATCH ? (size_t)g.rows * 4 : 0));
         L->total_bm_blocks += g.bm_nblk;
         L->sum_cap += g.cap;
     }
@@ -685,6 +687,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         d.nsets = ge.ways ? ge.nsets : 0;
         d.qbits = ge.qbits;
         d.seg = reinterpret_cast<int4 *>(ws + L.seg[t]);
+        d.freq = cfg->policy == RECMG_LFU_BATCH ? reinterpret_cast<int32_t *>(ws + L.freq[t]) : nullptr;
         if (ge.ways) c->has_sa = true;
         else c->has_fa = true;
 
@@ -723,6 +726,7 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         HIP_TRY(hipMemsetAsync(ws + L.bitmap[t], 0, (size_t)ge.bm_words * 4, s0));
         HIP_TRY(hipMemsetAsync(ws + L.rank[t], 0xff, (size_t)ge.bm_words * 16, s0));  // stamp -1
         HIP_TRY(hipMemsetAsync(ws + L.seg[t], 0, (size_t)ge.nsets * 16, s0));
+        if (cfg->policy == RECMG_LFU_BATCH) HIP_TRY(hipMemsetAsync(ws + L.freq[t], 0, (size_t)ge.rows * 4, s0));
     }
     HIP_TRY(hipMemsetAsync(ws + L.st, 0, sizeof(TState) * T, s0));
     HIP_TRY(hipMemsetAsync(ws + L.tstart, 0, 8 * (T + 1), s0));
@@ -790,9 +794,10 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     if (b + 2 >= (int64_t(1) << 31)) return fail(RECMG_E_STATE, "placement count exhausted");
     PlcParams p{};
     p.prio = c->cfg.policy == RECMG_PRIORITY;
+    p.lfu = c->cfg.policy == RECMG_LFU_BATCH;
     p.es = c->cfg.eviction_speed;
     p.lru_touch = (int32_t)b;
-    p.pscore = p.prio ? p.es : (int32_t)(b + 1);
+    p.pscore = p.prio ? p.es : p.lfu ? 0 : (int32_t)(b + 1);
     p.have_fwd = c->have_fwd ? 1 : 0;
     p.last_stamp = c->have_fwd ? (int32_t)(c->forwards - 1) : -2;
     p.rowbits = c->rowbits;
@@ -805,6 +810,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         StageTimer tm(c, RECMG_STAGE_PLC_CLASSIFY, s);
         launch_plc_prep(g, prefetch_offsets, num_prefetch, p.have_fwd, s);
         if (p.prio && cache_bits && c->have_fwd) launch_plc_bits(g, cache_bits, c->last_n, s);
+        if (p.lfu && c->have_fwd) launch_plc_freq(g, c->last_n, s);
         if (num_prefetch > 0) {
             launch_mark(g, prefetch_rows, g.pstart, num_prefetch, s);
             launch_dedup(g, EMIT_PREFETCH,

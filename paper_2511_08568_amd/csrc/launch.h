@@ -36,6 +36,7 @@ void launch_fwd_finalize(const DGlobal &g, int64_t log_slot, hipStream_t s);
 // placement.hip
 void launch_plc_prep(const DGlobal &g, const int64_t *poff, int64_t np, int32_t have_fwd, hipStream_t s);
 void launch_plc_bits(const DGlobal &g, const uint8_t *bits, int64_t n_last, hipStream_t s);
+void launch_plc_freq(const DGlobal &g, int64_t n_last, hipStream_t s);
 void launch_plc_classify(const DGlobal &g, int32_t last_stamp, int64_t np, hipStream_t s);
 void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s);
 void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,

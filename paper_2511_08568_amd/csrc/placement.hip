@@ -13,6 +13,8 @@
 //
 // Scores:  LRU_BATCH  touched by the last batch: lru_touch; prefetched:
 //                     max(score, pscore) with pscore = lru_touch + 1
+//          LFU_BATCH  every row's score is its batch count (k_plc_freq adds
+//                     the last batch); a prefetch does not change it
 //          PRIORITY   residents first age by one, saturating at 0 (Alg. 2);
 //                     touched: caching bit + ES (Alg. 1); prefetched:
 //                     max(score, ES); a touched resident loses its prefetch flag.
@@ -67,6 +69,23 @@ __global__ void __launch_bounds__(kBlock) k_plc_bits(DGlobal g, const uint8_t *_
         const int32_t s = g.src[i];
         uint8_t *f = s >= 0 ? &g.tabs[t].slot_cbit[s] : &g.mcbit[s_start[t] + (-(int64_t)s - 1)];
         if (!*f) *f = 1;
+    }
+}
+
+// LFU_BATCH: one more batch for every distinct row of the last forward (rows
+// of U are distinct, so plain increments suffice).
+__global__ void __launch_bounds__(kBlock) k_plc_freq(DGlobal g, int64_t n) {
+    if (*g.err) return;
+    __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
+    __shared__ int32_t s_uc[RECMG_MAX_TABLES];
+    for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
+        s_start[t] = g.tstart[t];
+        if (t < g.T) s_uc[t] = g.st[t].ucount;
+    }
+    __syncthreads();
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int t = find_seg(s_start, g.T, i);
+        if (i - s_start[t] < s_uc[t]) g.tabs[t].freq[g.U[i]] += 1;
     }
 }
 
@@ -239,9 +258,9 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
             const int cb = tb.slot_cbit[k];
             if (cb) tb.slot_cbit[k] = 0;
             if (p.prio) s = s > 0 ? s - 1 : 0;
-            if (tb.slot_touch[k] == p.last_stamp) {
+            if (row >= 0 && tb.slot_touch[k] == p.last_stamp) {
                 f &= ~F_PF;
-                s = p.prio ? cb + p.es : p.lru_touch;
+                s = touch_score(p, tb, row, cb);
             }
             if ((f & F_INP) && s < p.pscore) s = p.pscore;
             if (row >= 0) {
@@ -252,12 +271,12 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
             const int64_t m = ts + (k - c.cap);
             row = g.M[m];
             const uint32_t f = g.mflags[m];
-            s = p.prio ? (int32_t)g.mcbit[m] + p.es : p.lru_touch;
+            s = touch_score(p, tb, row, g.mcbit[m]);
             if ((f & F_INP) && s < p.pscore) s = p.pscore;
             g.mscore[m] = s;
         } else {
             row = g.NP[ps + (k - c.cap - c.nm)];
-            s = p.pscore;
+            s = new_prefetch_score(p, tb, row);
         }
         if (sel) hist_add(s_hist, row >= 0, (uint32_t)(make_key(s, row < 0 ? 0 : row, p.rowbits) >> shift) & dmask);
     }
@@ -278,7 +297,7 @@ __device__ __forceinline__ bool item_key(const DGlobal &g, const DTable &tb, con
         s = g.mscore[m];
     } else {
         row = g.NP[ps + (k - c.cap - c.nm)];
-        s = p.pscore;
+        s = new_prefetch_score(p, tb, row);
     }
     *key = make_key(s, row, p.rowbits);
     return true;
@@ -422,7 +441,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
                 inp = (g.mflags[ts + k] & F_INP) != 0;
             } else {
                 row = g.NP[ps + (k - c.nm)];
-                s = p.pscore;
+                s = new_prefetch_score(p, tb, row);
                 inp = true;
             }
             adm = kept(mode, make_key(s, row, p.rowbits), thr) ? 1 : 0;
@@ -566,6 +585,11 @@ void launch_plc_prep(const DGlobal &g, const int64_t *poff, int64_t np, int32_t 
 void launch_plc_bits(const DGlobal &g, const uint8_t *bits, int64_t n_last, hipStream_t s) {
     if (n_last <= 0) return;
     k_plc_bits<<<grid_for(n_last, kBlock * 4, 16384), kBlock, 0, s>>>(g, bits, n_last);
+}
+
+void launch_plc_freq(const DGlobal &g, int64_t n_last, hipStream_t s) {
+    if (n_last <= 0) return;
+    k_plc_freq<<<grid_for(n_last, kBlock * 4, 8192), kBlock, 0, s>>>(g, n_last);
 }
 
 void launch_plc_classify(const DGlobal &g, int32_t last_stamp, int64_t np, hipStream_t s) {

@@ -76,6 +76,7 @@ struct DTable {
     int32_t ways, nsets, qbits, pad_sa;
     int4 *seg;  // [nsets] (U begin, U end, PU begin, PU end) of each set in the
                 // current placement, relative to the table's lists; zero between uses
+    int32_t *freq;  // LFU_BATCH: [rows] batches that accessed each row (every row, cached or not)
 };
 
 // Mutable per-table state and counters, resident in the workspace.
@@ -141,15 +142,28 @@ struct DGlobal {
 
 // Parameters of one placement.
 struct PlcParams {
-    int32_t prio;        // 1: PRIORITY, 0: LRU_BATCH
+    int32_t prio;        // 1: PRIORITY
     int32_t es;          // eviction_speed
     int32_t lru_touch;   // LRU score of a row touched by the last batch
-    int32_t pscore;      // score of a prefetched row
+    int32_t pscore;      // score of a prefetched row (LFU: 0, a floor that changes nothing)
     int32_t last_stamp;  // stamp of the last forward, -2 if none since the last placement
     int32_t have_fwd;
     int32_t rowbits, total_bits, passes;
-    int32_t pad;
+    int32_t lfu;         // 1: LFU_BATCH (scores are the rows' batch counts)
 };
+
+// Score of a row the last batch touched: LRU_BATCH the batch stamp, PRIORITY
+// its caching bit + eviction_speed (Alg. 1), LFU_BATCH its batch count.
+__device__ __forceinline__ int32_t touch_score(const PlcParams &p, const DTable &tb, int32_t row, int cbit) {
+    if (p.prio) return cbit + p.es;
+    if (p.lfu) return tb.freq[row];
+    return p.lru_touch;
+}
+
+// Score a prefetch gives a row neither resident nor missed.
+__device__ __forceinline__ int32_t new_prefetch_score(const PlcParams &p, const DTable &tb, int32_t row) {
+    return p.lfu ? tb.freq[row] : p.pscore;
+}
 
 // -------------------------------------------------------------------- helpers
 

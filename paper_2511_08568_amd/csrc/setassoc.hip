@@ -6,11 +6,13 @@
 // registers, and plays the set's events in order:
 //   A. rows the last batch touched (slot_touch = its stamp) lose their
 //      prefetch flag and take the touch score: LRU_BATCH the batch stamp,
-//      PRIORITY the OR of their caching bits + eviction_speed;
+//      PRIORITY the OR of their caching bits + eviction_speed, LFU_BATCH the
+//      row's batch count;
 //   B. the set's misses of the last batch, ascending by row, are inserted with
 //      their touch score;
 //   C. the set's distinct prefetch rows, ascending by row: a resident one keeps
-//      max(score, prefetch score), any other is inserted with the prefetch score.
+//      max(score, prefetch score), any other is inserted with the prefetch score
+//      (LFU_BATCH: its batch count).
 // Insert: the lowest free way, else Alg. 2 over the set: the victim is the
 // lowest way holding the minimum score (scores before this scan), then under
 // PRIORITY every way of the set ages by one, saturating at 0.
@@ -115,7 +117,7 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p, int
             const int cb = tb.slot_cbit[slot];
             if (cb) tb.slot_cbit[slot] = 0;
             flags = 0;
-            score = p.prio ? cb + p.es : p.lru_touch;
+            score = touch_score(p, tb, row0, cb);
         }
     }
     int32_t row = row0;
@@ -156,7 +158,7 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p, int
         if (i < sg.y) {
             r = g.U[ub + i];
             su = g.slotU[ub + i];
-            if (su < 0) v = p.prio ? (int32_t)g.mcbit[ub + (-su - 1)] + p.es : p.lru_touch;
+            if (su < 0) v = touch_score(p, tb, r, g.mcbit[ub + (-su - 1)]);
         }
         uint64_t mm = ballot(i < sg.y && su < 0);
         nmiss += __popcll(mm);
@@ -173,9 +175,10 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p, int
     const int64_t pb = g.pstart[t];
     for (int32_t i0 = sg.z; i0 < sg.w; i0 += 64) {
         const int32_t i = i0 + lane;
-        int32_t r = -1, from = -1;
+        int32_t r = -1, from = -1, v = 0;
         if (i < sg.w) {
             r = g.PU[pb + i];
+            v = new_prefetch_score(p, tb, r);
             if (p.have_fwd) {
                 const uint32_t pos = bm_pos(tb, r);
                 const uint4 rk = tb.rank[pos >> 5];
@@ -197,7 +200,7 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p, int
                 }
                 continue;
             }
-            const int w = insert(rr, p.pscore, __builtin_amdgcn_readlane(from, j));
+            const int w = insert(rr, __builtin_amdgcn_readlane(v, j), __builtin_amdgcn_readlane(from, j));
             if (lane == w) inp = true;
         }
     }

@@ -64,6 +64,13 @@ def test_query_workspace_sizes():
     assert dev2 - dev >= 5000 * 256 - 256 and host2 >= 2 * 5000 * 256
 
 
+def test_lfu_keeps_a_counter_per_row():
+    """LFU_BATCH counts batches for every row: 4 bytes per row more workspace."""
+    lru, _ = bd.recmg_query_workspace(_cfg(rows=(100000,)))
+    lfu, _ = bd.recmg_query_workspace(_cfg(rows=(100000,), policy=2))
+    assert lfu - lru >= 4 * 100000 - 1024  # up to a few 256-byte alignments
+
+
 def test_query_scales_with_capacity():
     a, _ = bd.recmg_query_workspace(_cfg(caps=(100,)))
     b, _ = bd.recmg_query_workspace(_cfg(caps=(1000,)))
@@ -71,7 +78,7 @@ def test_query_scales_with_capacity():
 
 
 @pytest.mark.parametrize("kw", [dict(rows=(0,)), dict(dims=(0,)), dict(dtypes=(7,)), dict(caps=(-1,)),
-                                dict(policy=5), dict(miss=9), dict(max_idx=-1), dict(es=-1),
+                                dict(policy=5), dict(policy=3), dict(miss=9), dict(max_idx=-1), dict(es=-1),
                                 dict(max_idx=1 << 31), dict(ways=-1), dict(ways=65)])
 def test_query_rejects_bad_configs(kw):
     with pytest.raises(bd.RecmgError) as e:

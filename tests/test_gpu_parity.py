@@ -428,3 +428,21 @@ def test_stats_log_window():
     finally:
         g.close()
         o.close()
+
+
+# ----------------------------------------------------------------------------- LFU
+
+@pytest.mark.parametrize("seed", range(8))
+def test_lfu_tiny_random(seed):
+    w = tg.random_tiny(300 + seed, max_rows=40, max_cap=12, max_dim=9, batches=6, bags=5, policy="lfu")
+    w.ways = (0, 0, 1, 2, 3, 4, 0, 8)[seed]
+    _parity(w, label=f"lfu-tiny{seed}-w{w.ways}")
+
+
+@pytest.mark.parametrize("cid,scale,tables,ways", [(2, 0.02, 3, 0), (3, 0.01, 6, 0), (3, 0.01, 6, 32),
+                                                   (5, 0.01, 6, 32)])
+def test_lfu_configs_scaled(cid, scale, tables, ways):
+    """LFU_BATCH (the LFU baseline) on the scaled configurations, fully
+    associative and 32-way."""
+    w = tg.scaled_config(cid, row_scale=scale, batches=6, bags=256, max_tables=tables, ways=ways, policy="lfu")
+    _parity(w, label=f"c{cid}-lfu-w{ways}")
