@@ -24,8 +24,9 @@
  *   max(its score, eviction_speed).
  *   LFU_BATCH (the LFU baseline of Sec. VII-B, per batch): a row's score is
  *   the number of batches that have accessed it, counted for every row
- *   whether cached or not (a device array of N_t counters); a prefetch does
- *   not change it.
+ *   whether cached or not (a device array of N_t counters) by the placement
+ *   that consumes the batch (a batch no placement follows is not counted);
+ *   a prefetch does not change it.
  *
  * Set-associative form (config.ways = W > 0; the production buffer of Sec.
  * VI-B is a W-way set-associative software cache, Sec. VII-B and VII-E): a

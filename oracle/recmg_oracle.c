@@ -37,8 +37,9 @@
  *      placement, so b-1 is the batch just run), or c(r) + ES under PRIORITY
  *      (Alg. 1's priority = C + eviction_speed), with c(r) the OR of r's bits,
  *      or f(r) under LFU_BATCH, f(r) being the number of batches that have
- *      accessed r so far (counted for every row, resident or not; the 32-way
- *      LFU baseline of Sec. VII-B at batch granularity).
+ *      accessed r so far (counted for every row, resident or not, by the
+ *      placement that consumes the batch; the 32-way LFU baseline of
+ *      Sec. VII-B at batch granularity).
  *   4. prefetch: for r in set(P), s(r) <- max(s(r) if r in R or M, else -inf,
  *      b under LRU_BATCH or ES under PRIORITY) (Alg. 1's prefetch priority);
  *      under LFU_BATCH a prefetched row keeps its frequency f(r).

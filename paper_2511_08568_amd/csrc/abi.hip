@@ -801,6 +801,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     p.have_fwd = c->have_fwd ? 1 : 0;
     p.last_stamp = c->have_fwd ? (int32_t)(c->forwards - 1) : -2;
     p.rowbits = c->rowbits;
+    // largest score a key can hold (an LFU count grows by at most one per placement)
     const int64_t maxscore = p.prio ? (int64_t)p.es + 1 : b + 1;
     p.total_bits = bitlen((uint64_t)maxscore) + p.rowbits;
     if (p.total_bits < 1) p.total_bits = 1;

@@ -355,13 +355,14 @@ def test_pipelined_placement_matches_oracle(cid, scale, tables, ways):
 
 
 @pytest.mark.parametrize("pipeline", [False, True])
-@pytest.mark.parametrize("ways", [0, 16])
-def test_skipped_placements(pipeline, ways):
+@pytest.mark.parametrize("ways,policy", [(0, "priority"), (16, "priority"), (0, "lfu"), (16, "lfu")])
+def test_skipped_placements(pipeline, ways, policy):
     """Placements the caller skips (the models were late, Sec. VI-C): the
     next placement sees only the most recent forward's rows and misses, and
-    the batches in between run on the cache as it stands."""
+    the batches in between run on the cache as it stands (and do not count
+    for LFU)."""
     import oracle
-    w = tg.scaled_config(3, row_scale=0.01, batches=9, bags=256, max_tables=5, ways=ways)
+    w = tg.scaled_config(3, row_scale=0.01, batches=9, bags=256, max_tables=5, ways=ways, policy=policy)
     tabs = [w.table_values(t) for t in range(w.num_tables)]
     o = oracle.for_workload(w, tabs)
     g = GpuRunner(w, tabs, pipeline=pipeline)
