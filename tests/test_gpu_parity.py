@@ -447,3 +447,79 @@ def test_lfu_configs_scaled(cid, scale, tables, ways):
     associative and 32-way."""
     w = tg.scaled_config(cid, row_scale=scale, batches=6, bags=256, max_tables=tables, ways=ways, policy="lfu")
     _parity(w, label=f"c{cid}-lfu-w{ways}")
+
+
+# ----------------------------------------------------------------------------- random call sequences
+
+@pytest.mark.parametrize("seed", range(9))
+def test_random_call_sequences(seed):
+    """Random interleavings of placements and forwards on three streams (two
+    placements or two forwards in a row, batches out of order, calls on a
+    stream other than the previous call's), checked against the oracle
+    replaying the same calls: totals, resident sets and digests at random
+    check points, every forward's pooled sums at the end.  The library orders
+    calls across streams by events; nothing here synchronises between calls."""
+    import torch as th
+    import oracle
+    rng = np.random.default_rng(7000 + seed)
+    policy = ("lru", "priority", "lfu")[seed % 3]
+    w = tg.random_tiny(700 + seed, max_rows=3000, max_cap=300, max_dim=33, batches=10, bags=40,
+                       integer_values=False, policy=policy)
+    w.ways = (0, 4, 32)[(seed // 3) % 3]
+    tabs = [w.table_values(t) for t in range(w.num_tables)]
+    o = oracle.for_workload(w, tabs)
+    g = GpuRunner(w, tabs)
+    f64 = [tg.storage_to_f64(a, tb.dtype) for a, tb in zip(tabs, w.tables)]
+    streams = [th.cuda.current_stream(), th.cuda.Stream(), th.cuda.Stream()]
+    T = w.num_tables
+    tot = [dict() for _ in range(T)]
+    outs = []
+    last_fwd = None
+    from _helpers import FWD_KEYS, PLACE_KEYS
+
+    def add(group, keys):
+        for t in range(T):
+            st = o.stats(t)
+            for k in keys:
+                if k != "digest":
+                    tot[t][k] = tot[t].get(k, 0) + st[k]
+
+    try:
+        for step in range(40):
+            op = rng.choice(["plc", "fwd", "plc", "fwd", "check"])
+            s = streams[int(rng.integers(3))]
+            k = int(rng.integers(w.batches))
+            if op == "plc":
+                P, poff = w.prefetch_list(k)
+                bits = w.cache_bits(last_fwd) if last_fwd is not None else None
+                with th.cuda.stream(s):
+                    g.cache.placement(g.to_dev(P) if P.size else None, g.to_dev(poff),
+                                      None if bits is None else g.to_dev(bits), stream=s)
+                assert o.placement(P, poff, bits) == 0
+                add("plc", PLACE_KEYS)
+            elif op == "fwd":
+                idx, off = w.batch(k)
+                with th.cuda.stream(s):
+                    out = g.cache.forward(g.to_dev(idx), g.to_dev(off), w.bags, stream=s)
+                st, _, r64 = o.forward(idx, off, w.bags, want64=True)
+                assert st == 0
+                add("fwd", FWD_KEYS)
+                outs.append((out, r64.copy(), idx, off, step))
+                last_fwd = k
+            else:
+                _, gt, res = g.cache.stats(dump=True)
+                for t in range(T):
+                    for key, v in tot[t].items():
+                        assert gt[t][key] == v, f"step {step} table {t} total {key}"
+                    assert np.array_equal(res[t], o.resident(t)), f"step {step} table {t}: resident set"
+                    assert gt[t]["digest"] == o.stats(t)["digest"]
+        _, gt, res = g.cache.stats(dump=True)
+        for t in range(T):
+            for key, v in tot[t].items():
+                assert gt[t][key] == v, f"end table {t} total {key}"
+            assert np.array_equal(res[t], o.resident(t))
+        for out, r64, idx, off, step in outs:
+            check_pooled(w, f64, idx, off, out.cpu().numpy(), r64, f"forward at step {step}")
+    finally:
+        g.close()
+        o.close()
