@@ -1,0 +1,150 @@
+"""HIP path vs the CPU oracle at the full sizes of configurations 2-5, in the
+launch configuration bench.py times: placements on a stream of their own,
+calls issued back to back with no synchronisation between them.
+
+Checked: every call's counters and every placement's digest (the device stats
+log) against the oracle replaying the same calls, the final resident sets row
+by row, and the pooled sums of sampled bags of the first and last batch, each
+bag summed on the host in fp64 from the tables (the oracle's definition, one
+output at a time) and compared within rtol x its L1 mass.  Configurations 4
+and 5 run in STAGED mode (their 102 and 61 GB of tables stay pageable).
+Configuration 1 at full size is in test_gpu_parity.py."""
+import gc
+import os
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import tracegen as tg
+
+torch = pytest.importorskip("torch")
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+RTOL = {"f32": 1e-5, "f16": 2e-2, "bf16": 2e-2}
+TDT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.uint16}
+
+
+def _say(msg):
+    print(f"[fullsize] {msg}", file=sys.stderr, flush=True)
+
+
+def _run(cid, nb, miss_mode="zero_copy", ways=0, nsample=128):
+    import oracle
+    from paper_2511_08568_amd import TieredEmbeddingCache
+    w = tg.make_config(cid)
+    w.ways = ways
+    dev = torch.device("cuda", 0)
+    t0 = time.time()
+    pin = miss_mode == "zero_copy"
+    host = [torch.empty((tb.rows, tb.dim), dtype=TDT[tb.dtype], pin_memory=pin) for tb in w.tables]
+    for t in range(w.num_tables):
+        w.table_values(t, out=host[t].numpy())
+    _say(f"config {cid}: tables ready in {time.time() - t0:.1f}s")
+    batches = [w.batch(b) for b in range(nb)]
+    pre = [w.prefetch_list(b) for b in range(nb)]
+    bits = [w.cache_bits(b - 1) if b > 0 else None for b in range(nb)]
+    d_in = []
+    for b in range(nb):
+        (idx, off), (P, po) = batches[b], pre[b]
+        d_in.append((torch.from_numpy(P).to(dev) if P.size else None, torch.from_numpy(po).to(dev),
+                     None if bits[b] is None else torch.from_numpy(bits[b]).to(dev),
+                     torch.from_numpy(idx).to(dev), torch.from_numpy(off).to(dev)))
+    cache = TieredEmbeddingCache(host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables], policy=w.policy,
+                                 eviction_speed=w.eviction_speed, miss_mode=miss_mode, max_bags_per_table=w.bags,
+                                 max_indices=max(i.size for i, _ in batches),
+                                 max_prefetch=max(max(P.size for P, _ in pre), 1), ways=ways,
+                                 stats_log_calls=2 * nb)
+    outs = [torch.empty(w.bags * sum(tb.dim for tb in w.tables), dtype=torch.float32, device=dev) for _ in range(nb)]
+    pstream = torch.cuda.Stream(device=dev)
+    torch.cuda.synchronize()
+    try:
+        for b in range(nb):
+            P, po, cb, idx, off = d_in[b]
+            cache.placement(P, po, cb, stream=pstream)
+            cache.forward(idx, off, w.bags, out=outs[b])
+        log = cache.stats_log()
+        _, _, res = cache.stats(dump=True)
+    finally:
+        cache.close()
+    del cache, d_in
+    _say(f"config {cid}: {nb} steps on the GPU done")
+    host_np = [h.numpy() for h in host]
+    nth = max(1, min(16, len(os.sched_getaffinity(0)), w.num_tables))
+    o = oracle.for_workload(w, host_np, nthreads=nth)
+    try:
+        for b in range(nb):
+            (idx, off), (P, po) = batches[b], pre[b]
+            assert o.placement(P, po, bits[b]) == 0
+            for t in range(w.num_tables):
+                st = o.stats(t)
+                for k in oracle.PLC_FIELDS + ("digest",):
+                    assert log[2 * b][t][k] == st[k], f"config {cid} placement {b} table {t} {k}"
+            assert o.forward(idx, off, w.bags)[0] == 0
+            for t in range(w.num_tables):
+                st = o.stats(t)
+                for k in oracle.FWD_FIELDS:
+                    assert log[2 * b + 1][t][k] == st[k], f"config {cid} forward {b} table {t} {k}"
+        for t in range(w.num_tables):
+            assert np.array_equal(res[t], o.resident(t)), f"config {cid} table {t}: final resident set"
+    finally:
+        o.close()
+    _say(f"config {cid}: counters and resident sets equal the oracle's")
+    # sampled bags of the first and last batch, each summed in fp64 on the host
+    rng = np.random.default_rng(1000 + cid)
+    for b in sorted({0, nb - 1}):
+        idx, off = batches[b]
+        got = outs[b].cpu().numpy()
+        base = 0
+        for t, tb in enumerate(w.tables):
+            for j in rng.choice(w.bags, size=min(nsample, w.bags), replace=False):
+                a, e = off[t * w.bags + j], off[t * w.bags + j + 1]
+                rows = tg.storage_to_f64(host_np[t][idx[a:e]], tb.dtype)
+                ref = rows.sum(axis=0) if e > a else np.zeros(tb.dim)
+                mass = np.abs(rows).sum(axis=0) if e > a else np.zeros(tb.dim)
+                g = got[base + j * tb.dim: base + (j + 1) * tb.dim].astype(np.float64)
+                assert np.all(np.abs(g - ref) <= RTOL[tb.dtype] * mass), f"config {cid} batch {b} table {t} bag {j}"
+            base += w.bags * tb.dim
+    _say(f"config {cid}: sampled pooled sums within tolerance")
+
+
+def _release():
+    """Give back device memory and pinned host memory that torch keeps cached:
+    the box caps pinned memory, and these tests pin tens of GB each."""
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    torch._C._host_emptyCache()
+
+
+@pytest.fixture(autouse=True)
+def _free_between_tests():
+    _release()
+    yield
+    _release()
+
+
+def test_config2_fullsize():
+    """8 x 1,000,000 x 128 fp32, cache 50,000/table, 2,048 bags: 8 steps."""
+    _run(2, 8)
+
+
+def test_config2_fullsize_32way():
+    _run(2, 6, ways=32)
+
+
+def test_config3_fullsize():
+    """26 fp16 tables (1e3..2e7 rows), cache 2%, 4,096 bags: 5 steps."""
+    _run(3, 5)
+
+
+def test_config4_fullsize_staged():
+    """4 x 1e8 x 128 bf16 (102 GB, pageable), 20 GB cache, 16,384 bags of 80: 3 steps."""
+    _run(4, 3, miss_mode="staged", nsample=64)
+
+
+def test_config5_fullsize_staged():
+    """64 x 2,000,000 fp32 (dims 32..256, 61 GB, pageable), cache 10%, 8,192 bags: 4 steps."""
+    _run(5, 4, miss_mode="staged", nsample=32)
