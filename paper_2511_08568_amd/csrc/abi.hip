@@ -640,8 +640,6 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     c->stage[1] = ws + L.staging[1];
     g.staging = c->stage[0];
     g.stage_stride = L.stage_stride;
-    g.stage_rows = cfg->max_indices;
-    g.fstage_rows = cfg->miss_mode == RECMG_STAGED ? cfg->max_prefetch : 0;
     g.T = T;
     g.total_bm_blocks = L.total_bm_blocks;
     g.stat_log = reinterpret_cast<int64_t *>(ws + L.stat_log);

@@ -508,30 +508,16 @@ __global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, const int64_t *_
         s_cnt[t] = (base >= 0 && n >= 0 && base + n <= g.fill_cap) ? (int32_t)n : 0;
     }
     __syncthreads();
+    // entries were checked where admit and the set-associative placement wrote them
     copy_flat(
         g, s_cnt,
-        // every source and slot is checked against its buffer (an entry outside
-        // it would be a broken invariant: flagged, and the row skipped)
         [&](int t, const DTable &tb, int64_t j) -> const char * {
             const int32_t src = g.fill_src[fdesc[4 * t] + j];
-            const int64_t k = src >= 0 ? fdesc[4 * t + 2] + src : -(int64_t)src - 1;
-            const int64_t lim = src >= 0 ? g.stage_rows : (g.staged_fill ? g.fstage_rows : tb.rows);
-            if (k < 0 || k >= lim) {
-                atomicOr(g.err, ERR_INTERNAL);
-                return nullptr;
-            }
-            if (src >= 0) return g.staging + k * g.stage_stride;             // admitted miss
-            return g.staged_fill ? g.fstage + k * g.stage_stride            // prefetch row, host-staged
-                                 : tb.host + k * (int64_t)tb.row_bytes;     // prefetch row, zero-copy
+            if (src >= 0) return g.staging + (fdesc[4 * t + 2] + src) * g.stage_stride;  // admitted miss
+            return g.staged_fill ? g.fstage + (int64_t)(-src - 1) * g.stage_stride  // prefetch row, host-staged
+                                 : tb.host + (int64_t)(-src - 1) * tb.row_bytes;    // prefetch row, zero-copy
         },
-        [&](int t, const DTable &tb, int64_t j) -> char * {
-            const int32_t slot = g.fill_slot[fdesc[4 * t] + j];
-            if ((uint32_t)slot >= (uint32_t)tb.cap) {
-                atomicOr(g.err, ERR_INTERNAL);
-                return nullptr;
-            }
-            return tb.pool + (int64_t)slot * tb.row_bytes;
-        });
+        [&](int t, const DTable &tb, int64_t j) { return tb.pool + (int64_t)g.fill_slot[fdesc[4 * t] + j] * tb.row_bytes; });
 }
 
 // Publishes the counters and writes the fill descriptor of this placement

@@ -133,8 +133,6 @@ struct DGlobal {
     char *fstage;             // [max_prefetch][stage_stride] prefetch rows staged by the host (STAGED)
     int32_t staged_fill;      // 1: a fill source -(k + 1) is fstage row k, not host row k
     int64_t stage_stride;
-    int64_t stage_rows;       // rows of each staging buffer (max_indices) and of fstage (max_prefetch)
-    int64_t fstage_rows;
     int32_t T;
     int32_t total_bm_blocks;
     int32_t *sa_bstart;  // [nsa + 1] first placement block of each set-associative table
@@ -411,7 +409,7 @@ __device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
 
 // Copy `count[t]` rows of every table in 16/4/2-byte units, the tables' work
 // laid end to end so every table gets its share of the grid.  src_of / dst_of
-// give the byte addresses of item j of table t (null: skip the item).
+// give the byte addresses of item j of table t.
 template <class Src, class Dst>
 __device__ __forceinline__ void copy_flat(const DGlobal &g, const int32_t *count, Src src_of, Dst dst_of) {
     __shared__ int64_t s_pre[RECMG_MAX_TABLES + 1];
@@ -445,16 +443,12 @@ __device__ __forceinline__ void copy_flat(const DGlobal &g, const int32_t *count
                 const int64_t loc = it - s_pre[t];
                 const int64_t j = loc / nunit;
                 const int64_t vo = (loc - j * nunit) * u;
-                const char *sp = src_of(t, tb, j);
-                char *dp = dst_of(t, tb, j);
-                if (sp && dp) {  // a null address marks an item the caller found invalid
-                    sp += vo;
-                    dst[q] = dp + vo;
-                    unit[q] = u;
-                    if (u == 16) v16[q] = gload16(sp);
-                    else if (u == 4) v4[q] = gload4(sp);
-                    else v2[q] = gload2(sp);
-                }
+                const char *sp = src_of(t, tb, j) + vo;
+                dst[q] = dst_of(t, tb, j) + vo;
+                unit[q] = u;
+                if (u == 16) v16[q] = gload16(sp);
+                else if (u == 4) v4[q] = gload4(sp);
+                else v2[q] = gload2(sp);
             }
         }
 #pragma unroll
