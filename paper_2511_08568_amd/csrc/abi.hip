@@ -704,12 +704,12 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     for (int t = 0; t < T; ++t) c->pool_order[t] = t;
     std::stable_sort(c->pool_order.begin(), c->pool_order.end(),
                      [&](int x, int y) { return geo[x].kind < geo[y].kind; });
-    // set-associative placement: tables with the fewest sets first, four sets per block
+    // set-associative placement: tables with the fewest sets first, kSaWaves sets per block
     std::vector<int32_t> sa_tab, sa_bs(1, 0);
     for (int t = 0; t < T; ++t)
         if (geo[t].ways) sa_tab.push_back(t);
     std::stable_sort(sa_tab.begin(), sa_tab.end(), [&](int x, int y) { return geo[x].nsets < geo[y].nsets; });
-    for (int t : sa_tab) sa_bs.push_back(sa_bs.back() + (geo[t].nsets + kBlock / 64 - 1) / (kBlock / 64));
+    for (int t : sa_tab) sa_bs.push_back(sa_bs.back() + (geo[t].nsets + kSaWaves - 1) / kSaWaves);
     c->nsa = (int32_t)sa_tab.size();
     c->sa_blocks = sa_bs.back();
 

@@ -48,7 +48,8 @@ void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s);
 
 // setassoc.hip: placement of the set-associative tables (nu: index space of
 // the last forward's distinct rows, np: of this placement's prefetch rows;
-// nsa tables, blocks = sa_bstart[nsa], four sets per block)
+// nsa tables, blocks = sa_bstart[nsa], kSaWaves sets per block)
+constexpr int kSaWaves = 16, kSaBlock = 64 * kSaWaves;
 void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks,
                      hipStream_t s);
 

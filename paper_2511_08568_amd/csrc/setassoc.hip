@@ -84,27 +84,40 @@ __device__ __forceinline__ int wave_min_dpp(int v) {
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 
-// One wave per set (lane w = way w); sets without events return at once.
-// Blocks run table by table, tables with the fewest sets first: their sets
-// take the most events each, and the longest waves should start first.
-__global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p, int32_t nsa) {
-    if (*g.err) return;
+// One wave per set (lane w = way w), kSaWaves sets per block.  Blocks run
+// table by table, tables with the fewest sets first: their sets take the most
+// events each, and the longest waves should start first.  The counters and
+// the fill-list space of a block's sets are added up in LDS and taken with one
+// atomic each per block (a wave per set would queue hundreds of thousands of
+// atomics on the same few words of a table with many sets).
+__global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, int32_t nsa) {
+    __shared__ int s_cnt[kSaWaves][8];
+    __shared__ unsigned long long s_dig[kSaWaves];
+    __shared__ int s_off[kSaWaves];
+    if (*g.err) return;  // block-uniform
     const int kt = find_seg32(g.sa_bstart, nsa, (int32_t)blockIdx.x);
     const int t = g.sa_btab[kt];
     const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
     const int W = tb.ways;
-    const int64_t set = (int64_t)(blockIdx.x - g.sa_bstart[kt]) * (kBlock / 64) + (threadIdx.x >> 6);
-    if (set >= tb.nsets) return;  // wave-uniform
-    const int lane = threadIdx.x & 63;
-    const int4 sg = tb.seg[set];
-    if (sg.x == sg.y && sg.z == sg.w) return;
+    const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int64_t set = (int64_t)(blockIdx.x - g.sa_bstart[kt]) * kSaWaves + wid;
+    int4 sg = make_int4(0, 0, 0, 0);
+    if (set < tb.nsets) sg = tb.seg[set];
+    const bool active = sg.x != sg.y || sg.z != sg.w;  // wave-uniform
+    const bool way = lane < W;
+    const int64_t slot = set * W + lane;
+    const int64_t pb = g.pstart[t];
+    // results of this lane's way, and of the wave
+    int32_t row = -1, src = -1;
+    bool changed = false, from_m = false;
+    int c_ev = 0, c_am = 0, c_fill = 0, c_pd = 0, c_md = 0, c_res = 0;
+    unsigned long long dsum = 0;
+    if (active) {
     if (lane == 0) tb.seg[set] = make_int4(0, 0, 0, 0);
     // A set's events are played one after another: a set with many of them is
     // the kernel's critical path, so its wave takes issue slots first.
     if ((sg.y - sg.x) + (sg.w - sg.z) > 256) __builtin_amdgcn_s_setprio(3);
-    TState &st = g.st[t];
-    const bool way = lane < W;
-    const int64_t slot = set * W + lane;
 
     // A. this set's ways; rows the last batch touched take the touch score
     int32_t row0 = -1, score = 0;
@@ -120,8 +133,7 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p, int
             score = touch_score(p, tb, row0, cb);
         }
     }
-    int32_t row = row0;
-    int32_t src = -1;  // this lane's last insertion: staging index of a miss, or -1 (host)
+    row = row0;        // src: this lane's last insertion, staging index of a miss or -1 (host)
     bool inp = false;  // this lane's row is named by the prefetch list
 
     // insert row r with score v (from: its staging index, or -1); returns the
@@ -172,7 +184,6 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p, int
 
     // C. distinct prefetch rows, ascending.  Each lane first finds whether its
     // row missed in the last batch (then it is still in staging).
-    const int64_t pb = g.pstart[t];
     for (int32_t i0 = sg.z; i0 < sg.w; i0 += 64) {
         const int32_t i = i0 + lane;
         int32_t r = -1, from = -1, v = 0;
@@ -213,9 +224,9 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p, int
         was |= ik == row;
     }
     const bool evicted = way && row0 >= 0 && !kept0;
-    const bool changed = way && row >= 0 && row != row0;
+    changed = way && row >= 0 && row != row0;
     const bool fresh = way && row >= 0 && !was;  // in R' \ R
-    const bool from_m = changed && src >= 0;
+    from_m = changed && src >= 0;
     unsigned long long dig = 0;
     if (fresh) dig += mix64(((unsigned long long)t << 40) | (unsigned long long)row);
     if (evicted) dig -= mix64(((unsigned long long)t << 40) | (unsigned long long)row0);
@@ -232,35 +243,63 @@ __global__ void __launch_bounds__(kBlock) k_sa_place(DGlobal g, PlcParams p, int
         pdrop += (i < sg.w && !in) ? 1 : 0;
     }
 
-    // fill list and write-back
-    const int stride_st = (int)(sizeof(TState) / 4);
-    const int32_t k = wave_append(changed, t, &g.st[0].popped, stride_st);
-    if (changed) {
-        const int64_t fj = g.ftstart[t] + pb + k;
-        if (fj < 0 || fj >= g.fill_cap) {
-            atomicOr(g.err, ERR_INTERNAL);
-        } else {
-            g.fill_src[fj] = from_m ? src : -(row + 1);
-            g.fill_slot[fj] = (int32_t)slot;
-        }
-    }
     if (way) {
         tb.slot_row[slot] = row;
         tb.slot_score[slot] = score;
         tb.slot_flags[slot] = changed ? (inp ? F_PF : 0u) : flags;
         if (changed) tb.slot_touch[slot] = -1;
     }
-    const int n_ev = wave_sum(evicted ? 1 : 0), n_am = wave_sum(from_m ? 1 : 0);
-    const int n_fill = wave_sum(changed && !from_m ? 1 : 0), n_pd = wave_sum(pdrop), n_res = wave_sum(d_res);
-    const unsigned long long dsum = wave_sum64(dig);
+    c_ev = wave_sum(evicted ? 1 : 0);
+    c_am = wave_sum(from_m ? 1 : 0);
+    c_fill = wave_sum(changed && !from_m ? 1 : 0);
+    c_pd = wave_sum(pdrop);
+    c_md = nmiss - c_am;
+    c_res = wave_sum(d_res);
+    dsum = wave_sum64(dig);
+    }  // active
+
+    // the block's totals: one atomic per counter, one for the fill-list space
+    const uint64_t chm = ballot(changed);
     if (lane == 0) {
-        if (n_ev) atomicAdd(&st.evicted, n_ev);
-        if (n_am) atomicAdd(&st.adm_miss, n_am);
-        if (n_fill) atomicAdd(&st.p_fill, n_fill);
-        if (n_pd) atomicAdd(&st.p_drop, n_pd);
-        if (nmiss - n_am) atomicAdd(&st.m_drop, nmiss - n_am);
-        if (n_res) atomicAdd(&st.n_res, n_res);
-        if (dsum) atomicAdd(&st.digest_acc, dsum);
+        s_cnt[wid][0] = __popcll(chm);
+        s_cnt[wid][1] = c_ev;
+        s_cnt[wid][2] = c_am;
+        s_cnt[wid][3] = c_fill;
+        s_cnt[wid][4] = c_pd;
+        s_cnt[wid][5] = c_md;
+        s_cnt[wid][6] = c_res;
+        s_dig[wid] = dsum;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int tot[7] = {0, 0, 0, 0, 0, 0, 0};
+        unsigned long long d = 0;
+#pragma unroll 1  // unrolled, the loads of every wave's counts would be held in registers at once
+        for (int w = 0; w < kSaWaves; ++w) {
+            s_off[w] = tot[0];
+            for (int k = 0; k < 7; ++k) tot[k] += s_cnt[w][k];
+            d += s_dig[w];
+        }
+        const int base = tot[0] ? atomicAdd(&st.popped, tot[0]) : 0;
+#pragma unroll 1
+        for (int w = 0; w < kSaWaves; ++w) s_off[w] += base;
+        if (tot[1]) atomicAdd(&st.evicted, tot[1]);
+        if (tot[2]) atomicAdd(&st.adm_miss, tot[2]);
+        if (tot[3]) atomicAdd(&st.p_fill, tot[3]);
+        if (tot[4]) atomicAdd(&st.p_drop, tot[4]);
+        if (tot[5]) atomicAdd(&st.m_drop, tot[5]);
+        if (tot[6]) atomicAdd(&st.n_res, tot[6]);
+        if (d) atomicAdd(&st.digest_acc, d);
+    }
+    __syncthreads();
+    if (changed) {
+        const int64_t fj = g.ftstart[t] + pb + s_off[wid] + __popcll(chm & ((1ull << lane) - 1ull));
+        if (fj < 0 || fj >= g.fill_cap) {
+            atomicOr(g.err, ERR_INTERNAL);
+        } else {
+            g.fill_src[fj] = from_m ? src : -(row + 1);
+            g.fill_slot[fj] = (int32_t)slot;
+        }
     }
 }
 
@@ -274,7 +313,7 @@ static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
 void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks,
                      hipStream_t s) {
     if (nu + np > 0) k_sa_heads<<<grid_for(nu + np, kBlock, 8192), kBlock, 0, s>>>(g, nu, np, p.have_fwd);
-    if (blocks > 0) k_sa_place<<<(unsigned)blocks, kBlock, 0, s>>>(g, p, nsa);
+    if (blocks > 0) k_sa_place<<<(unsigned)blocks, kSaBlock, 0, s>>>(g, p, nsa);
 }
 
 }  // namespace recmg
