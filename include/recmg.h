@@ -152,7 +152,9 @@ typedef struct {
     int64_t lookups;           /* indices of this table in the batch */
     int64_t unique;            /* distinct rows U */
     int64_t hits;              /* |U ∩ R| */
-    int64_t hits_prefetch;     /* hits on rows still flagged as prefetched */
+    int64_t hits_prefetch;     /* hits on rows still flagged as prefetched: admitted through a
+                                  prefetch (read from the host, not a miss of the batch before)
+                                  and not accessed since the placement that admitted them */
     int64_t misses;            /* |U \ R| = on-demand fetches, each row fetched once */
     int64_t ondemand_bytes;    /* misses * row bytes */
     int64_t prefetch_covered;  /* |set(P) ∩ U|, P of the placement just before this forward
