@@ -450,11 +450,12 @@ def main():
                                    "each breakdown placement starts after the previous forward, so the two "
                                    "do not overlap there)"},
         "ondemand_fetches_per_batch": delta["misses"] / K,
-        # Sec. IV Eq. coverage (unique vectors) and Sec. VII-E prefetch accuracy
-        # (useful prefetches over prefetches issued), over the timed steps
+        # Sec. IV Eq. coverage (unique vectors of the batch the list names) and
+        # prefetch accuracy (of the distinct rows prefetched, those the batch
+        # uses), over the timed steps
         "prefetch_quality": {"coverage": delta["prefetch_covered"] / max(delta["unique"], 1),
-                             "accuracy": (delta["hits_prefetch"] / delta["prefetch_fill"]
-                                          if delta["prefetch_fill"] else None),
+                             "accuracy": (delta["prefetch_covered"] / delta["prefetch_distinct"]
+                                          if delta["prefetch_distinct"] else None),
                              "prefetch_distinct_per_batch": delta["prefetch_distinct"] / K},
         "prefetch_fills_per_batch": delta["prefetch_fill"] / K,
         "host_link": {"bytes_per_batch": link_bytes / max(KB, 1), "achieved_GBs": link_gbs,

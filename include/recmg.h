@@ -145,16 +145,17 @@ typedef enum {
  * placement (Sec. VII-E splits accesses into hits from caching, hits from
  * prefetching and on-demand fetches).  Prefetch quality (Sec. IV, Eq. coverage;
  * Sec. VII-E): coverage = prefetch_covered / unique of a forward, with P the
- * prefetch list of the placement just before it; prefetch accuracy (useful
- * prefetches over prefetches issued) = hits_prefetch / prefetch_fill summed
- * over calls. */
+ * prefetch list of the placement just before it; prefetch accuracy (the
+ * prefetched rows the next batch uses, over the rows prefetched) =
+ * prefetch_covered / prefetch_distinct, summed over placement + forward pairs.
+ * Both depend only on the lists and the batches, not on the cache. */
 typedef struct {
     int64_t lookups;           /* indices of this table in the batch */
     int64_t unique;            /* distinct rows U */
     int64_t hits;              /* |U ∩ R| */
-    int64_t hits_prefetch;     /* hits on rows still flagged as prefetched: admitted through a
-                                  prefetch (read from the host, not a miss of the batch before)
-                                  and not accessed since the placement that admitted them */
+    int64_t hits_prefetch;     /* hits on rows still flagged as prefetched: admitted while the
+                                  prefetch list named them (from the host, or from staging as a
+                                  miss of the batch before) and not accessed since */
     int64_t misses;            /* |U \ R| = on-demand fetches, each row fetched once */
     int64_t ondemand_bytes;    /* misses * row bytes */
     int64_t prefetch_covered;  /* |set(P) ∩ U|, P of the placement just before this forward

@@ -359,12 +359,12 @@ static void place_table(oracle_t *o, int32_t t, const int32_t *P, int64_t nP, co
         if (!tb->in_r[r]) {
             if (tb->in_m[r]) ++adm_miss; else ++fill;
             tb->in_r[r] = 1;
-            /* R16: only a row admitted through a prefetch (read from the host for
-               it) is flagged; a miss that P also names is admitted as a miss */
-#if ORACLE_MUTANT == 18 /* planted: an admitted miss that P names is flagged */
-            tb->pf[r] = tb->in_p[r];
-#else
+            /* every admitted row that P names is flagged, a miss of the last
+               batch included (R16) */
+#if ORACLE_MUTANT == 18 /* planted: an admitted miss that P names is not flagged */
             tb->pf[r] = tb->in_p[r] && !tb->in_m[r];
+#else
+            tb->pf[r] = tb->in_p[r];
 #endif
         }
         tb->res[tb->nres++] = r;
@@ -513,9 +513,9 @@ static void place_table_sa(oracle_t *o, int32_t t, const int32_t *P, int64_t nP)
         if (tb->way_row0[k] != r) { /* newly admitted, or moved to another way */
             if (tb->in_m[r]) ++adm_miss; else ++fill;
 #if ORACLE_MUTANT == 18
-            tb->pf[r] = tb->in_p[r];
+            tb->pf[r] = tb->in_p[r] && !tb->in_m[r];
 #else
-            tb->pf[r] = tb->in_p[r] && !tb->in_m[r]; /* R16, as in the fully associative form */
+            tb->pf[r] = tb->in_p[r]; /* R16, as in the fully associative form */
 #endif
         }
         tb->res[tb->nres++] = r;

@@ -463,7 +463,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
                 slot = tb.free_stack[fi];
                 tb.slot_row[slot] = row;
                 tb.slot_score[slot] = s;
-                tb.slot_flags[slot] = inp && !is_miss ? F_PF : 0u;  // admitted through a prefetch
+                tb.slot_flags[slot] = inp ? F_PF : 0u;
                 tb.slot_touch[slot] = -1;
                 n_reuse += map_insert(tb, row, slot);
                 // the fill list: admitted row j of this table, its source and slot

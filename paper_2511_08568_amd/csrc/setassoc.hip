@@ -24,8 +24,7 @@
 //
 // A way whose row at the end differs from its row at the start gets a fill
 // entry (misses of the last batch from HBM staging, every other row from the
-// host) and the prefetch flag [row in P and read from the host]; the fill
-// itself is k_plc_fill's.
+// host) and the prefetch flag [row in P]; the fill itself is k_plc_fill's.
 // Counters follow the set definitions: evicted |R \ R'|, admitted_miss
 // |(R' \ R) ∩ M|, prefetch_fill = rows read from the host (new rows and rows
 // moved to another way), prefetch_dropped |P \ (R ∪ R')|, miss_dropped
@@ -247,7 +246,7 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     if (way) {
         tb.slot_row[slot] = row;
         tb.slot_score[slot] = score;
-        tb.slot_flags[slot] = changed ? (inp && !from_m ? F_PF : 0u) : flags;
+        tb.slot_flags[slot] = changed ? (inp ? F_PF : 0u) : flags;
         if (changed) tb.slot_touch[slot] = -1;
     }
     c_ev = wave_sum(evicted ? 1 : 0);

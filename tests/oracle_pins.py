@@ -144,8 +144,8 @@ def pin_splitmix(mutant=0):
 def pin_lru_history(mutant=0, seeds=range(40)):
     """LRU_BATCH keeps the Cap rows whose most recent event (access in forward f
     -> f, prefetch before forward p -> p) is latest, ties to the higher id.  A
-    row admitted through a prefetch (named by P and not a miss of the last
-    batch) is flagged until it is accessed (R16)."""
+    row admitted while P names it (a miss of the last batch included) is
+    flagged until it is accessed (R16)."""
     for s in seeds:
         w = tg.random_tiny(s, policy="lru", batches=6)
         _, recs = run_oracle(w, mutant=mutant, want64=False)
@@ -153,7 +153,6 @@ def pin_lru_history(mutant=0, seeds=range(40)):
         last = [dict() for _ in range(T)]
         R = [set() for _ in range(T)]
         pf_live = [dict() for _ in range(T)]
-        M_prev = [set() for _ in range(T)]  # misses of the last forward
         for b, r in enumerate(recs):
             dig_t = []
             for t in range(T):
@@ -163,7 +162,7 @@ def pin_lru_history(mutant=0, seeds=range(40)):
                 ranked = sorted(last[t], key=lambda x: (last[t][x], x), reverse=True)
                 newR = set(ranked[: w.tables[t].cap])
                 for x in newR - R[t]:
-                    pf_live[t][x] = x in P and x not in M_prev[t]
+                    pf_live[t][x] = x in P
                 for x in R[t] - newR:
                     pf_live[t].pop(x, None)
                 R[t] = newR
@@ -176,7 +175,6 @@ def pin_lru_history(mutant=0, seeds=range(40)):
                 assert r["fwd"][t]["misses"] == len(U - R[t])
                 assert r["fwd"][t]["hits"] == len(U & R[t])
                 assert r["fwd"][t]["hits_prefetch"] == sum(1 for x in U & R[t] if pf_live[t].get(x))
-                M_prev[t] = U - R[t]
                 for x in U:
                     last[t][x] = b
                     if x in R[t]:
@@ -274,7 +272,7 @@ def pin_invariants(mutant=0, seeds=range(40)):
         w = tg.random_tiny(s, batches=6, policy=("lru", "priority", "lfu")[s % 3])
         _, recs = run_oracle(w, mutant=mutant, want64=False)
         prev = [0] * w.num_tables
-        hpf, fills = [0] * w.num_tables, [0] * w.num_tables
+        hpf, adm = [0] * w.num_tables, [0] * w.num_tables
         for r in recs:
             for t, (a, e) in enumerate(segments(w, r["off"])):
                 f, p = r["fwd"][t], r["place"][t]
@@ -282,10 +280,10 @@ def pin_invariants(mutant=0, seeds=range(40)):
                 assert f["unique"] == np.unique(r["idx"][a:e]).size
                 assert f["hits"] + f["misses"] == f["unique"]
                 assert 0 <= f["hits_prefetch"] <= f["hits"]
-                # a flagged row was read from the host once, and its first access ends the flag
-                fills[t] += p["prefetch_fill"]
+                # a flag is set by one admission and ended by the row's first access
+                adm[t] += p["prefetch_fill"] + p["admitted_miss"]
                 hpf[t] += f["hits_prefetch"]
-                assert hpf[t] <= fills[t], "prefetch accuracy above 1"
+                assert hpf[t] <= adm[t]
                 cap = w.tables[t].cap
                 assert p["resident"] <= cap and p["resident"] == r["resident"][t].size
                 assert p["resident"] == prev[t] - p["evicted"] + p["admitted_miss"] + p["prefetch_fill"]
@@ -432,13 +430,13 @@ def pin_sa_invariants(mutant=0, seeds=range(30)):
         w.ways = 1 + s % 4
         _, recs = run_oracle(w, mutant=mutant, want64=False)
         prev = [0] * w.num_tables
-        hpf, fills = [0] * w.num_tables, [0] * w.num_tables
+        hpf, adm = [0] * w.num_tables, [0] * w.num_tables
         for r in recs:
             for t, (a, e) in enumerate(segments(w, r["off"])):
                 f, p = r["fwd"][t], r["place"][t]
-                fills[t] += p["prefetch_fill"]
+                adm[t] += p["prefetch_fill"] + p["admitted_miss"]
                 hpf[t] += f["hits_prefetch"]
-                assert hpf[t] <= fills[t], "prefetch accuracy above 1"
+                assert hpf[t] <= adm[t]
                 S = min(w.tables[t].cap, w.tables[t].rows) // w.ways
                 res = r["resident"][t]
                 assert f["hits"] + f["misses"] == f["unique"] == np.unique(r["idx"][a:e]).size

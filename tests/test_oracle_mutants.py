@@ -23,7 +23,7 @@ MUTANTS = {
     15: "set-associative: aging once per placement instead of per eviction",
     16: "set-associative: set index taken modulo the ways",
     17: "LFU counts every access instead of every batch",
-    18: "an admitted miss that the prefetch list names is flagged as prefetched",
+    18: "an admitted miss that the prefetch list names is not flagged as prefetched",
 }
 
 
