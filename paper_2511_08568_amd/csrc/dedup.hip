@@ -28,7 +28,10 @@ constexpr int kLdsProbes = 8;
 
 __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__restrict__ keys,
                                                  const int64_t *__restrict__ starts, int64_t n) {
-    if (*g.err) return;
+    // The error word is read once per block: another block of this kernel may
+    // set it meanwhile, and the waves of a block must agree before its barriers.
+    __shared__ int s_err;
+    if (threadIdx.x == 0) s_err = *g.err;
     __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
     __shared__ int64_t s_rows[RECMG_MAX_TABLES];
     __shared__ uint32_t *s_bm[RECMG_MAX_TABLES];
@@ -45,6 +48,7 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
     }
     for (int k = threadIdx.x; k < kLdsSet; k += blockDim.x) s_set[k] = ~0ull;
     __syncthreads();
+    if (s_err) return;  // block-uniform
     // each block takes a contiguous chunk, so repeats within the chunk meet in LDS
     const int64_t chunk = (n + gridDim.x - 1) / gridDim.x;
     const int64_t lo = (int64_t)blockIdx.x * chunk;

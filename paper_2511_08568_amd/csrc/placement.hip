@@ -334,8 +334,18 @@ __device__ __forceinline__ bool kept(int mode, uint64_t key, uint64_t thr) {
 
 // ----------------------------------------------------------------- evict / admit
 
+// The error word read once per block.  Evict and admit may set it (a broken
+// invariant) while other blocks of the same kernel start, and the waves of a
+// block must agree before the block's barriers.
+__device__ __forceinline__ bool block_err(const DGlobal &g) {
+    __shared__ int s_err;
+    if (threadIdx.x == 0) s_err = *g.err;
+    __syncthreads();
+    return s_err != 0;
+}
+
 __global__ void __launch_bounds__(kBlock) k_plc_evict(DGlobal g, PlcParams p) {
-    if (*g.err) return;
+    if (block_err(g)) return;
     __shared__ int tmp[16];
     __shared__ int s_base;
     const int t = blockIdx.y;
@@ -413,7 +423,7 @@ __global__ void __launch_bounds__(kBlock) k_map_refill(DGlobal g) {
 }
 
 __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
-    if (*g.err) return;
+    if (block_err(g)) return;
     __shared__ int tmp[16];
     __shared__ int s_base;
     const int t = blockIdx.y;

@@ -94,7 +94,9 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     __shared__ int s_cnt[kSaWaves][8];
     __shared__ unsigned long long s_dig[kSaWaves];
     __shared__ int s_off[kSaWaves];
-    if (*g.err) return;  // block-uniform
+    // No early return: every wave reaches the block's barriers.  A wave that
+    // finds the error word set (another block may set it meanwhile) does no work.
+    const bool err = *g.err != 0;
     const int kt = find_seg32(g.sa_bstart, nsa, (int32_t)blockIdx.x);
     const int t = g.sa_btab[kt];
     const DTable &tb = g.tabs[t];
@@ -103,7 +105,7 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int64_t set = (int64_t)(blockIdx.x - g.sa_bstart[kt]) * kSaWaves + wid;
     int4 sg = make_int4(0, 0, 0, 0);
-    if (set < tb.nsets) sg = tb.seg[set];
+    if (!err && set < tb.nsets) sg = tb.seg[set];
     const bool active = sg.x != sg.y || sg.z != sg.w;  // wave-uniform
     const bool way = lane < W;
     const int64_t slot = set * W + lane;
