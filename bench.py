@@ -221,8 +221,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the tables of a configuration are one "
-                                   "GPU's share; --gpus must be 1"}), flush=True)
+        print(json.dumps({"error": "the library runs on one GPU: each configuration's tables are one GPU's "
+                                   "share (sharding by table is described, not built); --gpus must be 1"}), flush=True)
         sys.exit(2)
 
     import numpy as np

@@ -101,3 +101,16 @@ def test_null_handle_is_rejected():
     assert lib.recmg_embbag_forward(None, None, None, 0, 0, None, None) == bd.RECMG_E_INVALID
     assert lib.recmg_apply_placement(None, None, None, 0, None, None) == bd.RECMG_E_INVALID
     assert lib.recmg_cache_destroy(None) == bd.RECMG_OK
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py --gpus N > 1 stops before touching a GPU, with a JSON error line and status 2."""
+    import json
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120, cwd=root)
+    assert r.returncode == 2
+    msg = json.loads(r.stdout.strip().splitlines()[-1])
+    assert "one GPU" in msg["error"]
