@@ -218,12 +218,15 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
         }
     }
 
-    // counters: compare the set's rows at the start and at the end
-    bool kept0 = false, was = false;
-    for (int k = 0; k < W; ++k) {
-        const int32_t fk = __builtin_amdgcn_readlane(row, k), ik = __builtin_amdgcn_readlane(row0, k);
-        kept0 |= fk == row0;
-        was |= ik == row;
+    // counters: compare the set's rows at the start and at the end.  A set's
+    // rows are distinct at every point, so a row that left an unchanged way
+    // can only be found in a changed one, and the search runs over those.
+    const uint64_t dm = ballot(way && row != row0);
+    bool kept0 = (dm >> lane & 1ull) == 0, was = kept0;
+    for (uint64_t m = dm; m; m &= m - 1) {
+        const int k = __ffsll((unsigned long long)m) - 1;
+        kept0 |= __builtin_amdgcn_readlane(row, k) == row0;
+        was |= __builtin_amdgcn_readlane(row0, k) == row;
     }
     const bool evicted = way && row0 >= 0 && !kept0;
     changed = way && row >= 0 && row != row0;
@@ -239,9 +242,9 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     for (int32_t i0 = sg.z; i0 < sg.w; i0 += 64) {
         const int32_t i = i0 + lane;
         const int32_t r = i < sg.w ? g.PU[pb + i] : -1;
-        bool in = false;
-        for (int k = 0; k < W; ++k)
-            in |= (__builtin_amdgcn_readlane(row, k) == r) | (__builtin_amdgcn_readlane(row0, k) == r);
+        bool in = false;  // R ∪ R' = the rows at the start and the rows of the changed ways
+        for (int k = 0; k < W; ++k) in |= __builtin_amdgcn_readlane(row0, k) == r;
+        for (uint64_t m = dm; m; m &= m - 1) in |= __builtin_amdgcn_readlane(row, __ffsll((unsigned long long)m) - 1) == r;
         pdrop += (i < sg.w && !in) ? 1 : 0;
     }
 
