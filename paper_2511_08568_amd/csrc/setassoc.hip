@@ -84,6 +84,8 @@ __device__ __forceinline__ int wave_min_dpp(int v) {
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 
+static_assert(kSaWaves == 16, "the block's counts are added up over one DPP row of 16 lanes");
+
 // One wave per set (lane w = way w), kSaWaves sets per block.  Blocks run
 // table by table, tables with the fewest sets first: their sets take the most
 // events each, and the longest waves should start first.  The counters and
@@ -276,25 +278,39 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
         s_dig[wid] = dsum;
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-        int tot[7] = {0, 0, 0, 0, 0, 0, 0};
-        unsigned long long d = 0;
-#pragma unroll 1  // unrolled, the loads of every wave's counts would be held in registers at once
-        for (int w = 0; w < kSaWaves; ++w) {
-            s_off[w] = tot[0];
-            for (int k = 0; k < 7; ++k) tot[k] += s_cnt[w][k];
-            d += s_dig[w];
+    // Wave 0 adds them up, lane w holding wave w's counts: inclusive scans
+    // over the 16 lanes of the first row by DPP row shifts (lanes past the row
+    // edge read 0), the totals in lane 15.
+    if (wid == 0) {
+        auto row_scan = [&](int v) {
+            v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true);  // row_shr:1
+            v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, true);  // row_shr:2
+            v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, true);  // row_shr:4
+            v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, true);  // row_shr:8
+            return v;
+        };
+        const bool mine = lane < kSaWaves;
+        const int c0 = mine ? s_cnt[lane][0] : 0;
+        const int sc0 = row_scan(c0);
+        const int tot0 = __builtin_amdgcn_readlane(sc0, kSaWaves - 1);
+        int tot[7];
+        tot[0] = tot0;
+#pragma unroll
+        for (int k = 1; k < 7; ++k) tot[k] = __builtin_amdgcn_readlane(row_scan(mine ? s_cnt[lane][k] : 0), kSaWaves - 1);
+        const unsigned long long d = wave_sum64(mine ? s_dig[lane] : 0ull);
+        int base = 0;
+        if (lane == 0 && tot0) base = atomicAdd(&st.popped, tot0);
+        base = __builtin_amdgcn_readfirstlane(base);
+        if (mine) s_off[lane] = base + sc0 - c0;
+        if (lane == 0) {
+            if (tot[1]) atomicAdd(&st.evicted, tot[1]);
+            if (tot[2]) atomicAdd(&st.adm_miss, tot[2]);
+            if (tot[3]) atomicAdd(&st.p_fill, tot[3]);
+            if (tot[4]) atomicAdd(&st.p_drop, tot[4]);
+            if (tot[5]) atomicAdd(&st.m_drop, tot[5]);
+            if (tot[6]) atomicAdd(&st.n_res, tot[6]);
+            if (d) atomicAdd(&st.digest_acc, d);
         }
-        const int base = tot[0] ? atomicAdd(&st.popped, tot[0]) : 0;
-#pragma unroll 1
-        for (int w = 0; w < kSaWaves; ++w) s_off[w] += base;
-        if (tot[1]) atomicAdd(&st.evicted, tot[1]);
-        if (tot[2]) atomicAdd(&st.adm_miss, tot[2]);
-        if (tot[3]) atomicAdd(&st.p_fill, tot[3]);
-        if (tot[4]) atomicAdd(&st.p_drop, tot[4]);
-        if (tot[5]) atomicAdd(&st.m_drop, tot[5]);
-        if (tot[6]) atomicAdd(&st.n_res, tot[6]);
-        if (d) atomicAdd(&st.digest_acc, d);
     }
     __syncthreads();
     if (changed) {
