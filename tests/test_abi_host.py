@@ -114,3 +114,15 @@ def test_bench_refuses_more_than_one_gpu():
     assert r.returncode == 2
     msg = json.loads(r.stdout.strip().splitlines()[-1])
     assert "one GPU" in msg["error"]
+
+
+def test_missing_library_fails_loudly():
+    """With no built library the binding raises: there is no other path."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("import paper_2511_08568_amd as p\n"
+            "try:\n    p.load_library()\nexcept RuntimeError as e:\n    print('raised', e)\n")
+    env = dict(os.environ, RECMG_LIBRARY=os.path.join(root, "no_such_librecmg.so"))
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120, cwd=root, env=env)
+    assert r.returncode == 0 and r.stdout.startswith("raised"), r.stdout + r.stderr
