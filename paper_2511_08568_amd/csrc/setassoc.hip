@@ -89,9 +89,9 @@ static_assert(kSaWaves == 16, "the block's counts are added up over one DPP row 
 // One wave per set (lane w = way w), kSaWaves sets per block.  Blocks run
 // table by table, tables with the fewest sets first: their sets take the most
 // events each, and the longest waves should start first.  The counters and
-// the fill-list space of a block's sets are added up in LDS and taken with one
-// atomic each per block (a wave per set would queue hundreds of thousands of
-// atomics on the same few words of a table with many sets).
+// the fill-list space of a block's sets are added up by its first wave and
+// taken with one atomic each per block (a wave per set would queue hundreds of
+// thousands of atomics on the same few words of a table with many sets).
 __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, int32_t nsa) {
     __shared__ int s_cnt[kSaWaves][8];
     __shared__ unsigned long long s_dig[kSaWaves];
