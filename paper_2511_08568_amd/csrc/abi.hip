@@ -290,6 +290,19 @@ struct recmg_cache {
     std::vector<Mark> marks;
     double stage_ms[RECMG_NUM_STAGES] = {0};
     int64_t stage_calls[RECMG_NUM_STAGES] = {0};
+
+    // Every event the handle created, also when init stops half way.  The
+    // caller of delete has synchronised (or nothing was enqueued).
+    ~recmg_cache() {
+        for (hipEvent_t e : {ev_src, ev_pool, ev_fwd, ev_plc, ev_fill[0], ev_fill[1], ev_ready, ev_copied})
+            if (e) (void)hipEventDestroy(e);
+        for (const Mark &m : marks) {
+            if (m.a) (void)hipEventDestroy(m.a);
+            if (m.b) (void)hipEventDestroy(m.b);
+        }
+        for (hipEvent_t e : ev_free)
+            if (e) (void)hipEventDestroy(e);
+    }
 };
 
 namespace {
@@ -1095,17 +1108,8 @@ int32_t recmg_cache_destroy(recmg_cache_t *c) {
     (void)set_device(c);
     int32_t rc = RECMG_OK;
     if (sync_all(c) != hipSuccess) rc = fail(RECMG_E_HIP, "synchronize failed at destroy");
-    for (hipEvent_t e : {c->ev_src, c->ev_pool, c->ev_fwd, c->ev_plc, c->ev_fill[0], c->ev_fill[1]})
-        if (e) (void)hipEventDestroy(e);
-    for (auto &m : c->marks) {
-        c->ev_free.push_back(m.a);
-        c->ev_free.push_back(m.b);
-    }
-    for (hipEvent_t e : c->ev_free) (void)hipEventDestroy(e);
-    if (c->ev_ready) (void)hipEventDestroy(c->ev_ready);
-    if (c->ev_copied) (void)hipEventDestroy(c->ev_copied);
     c->magic = 0;
-    delete c;
+    delete c;  // destroys the handle's events
     return rc;
 }
 
