@@ -156,7 +156,7 @@ __global__ void __launch_bounds__(kBlock) k_fetch(DGlobal g) {
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) s_cnt[t] = g.st[t].mcount;
     __syncthreads();
     copy_flat(
-        g, s_cnt,
+        g, s_cnt, gridDim.x,
         [&](int t, const DTable &tb, int64_t j) {
             return tb.host + (int64_t)g.M[g.tstart[t] + j] * tb.row_bytes;
         },

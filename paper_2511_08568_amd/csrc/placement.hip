@@ -511,6 +511,9 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
 // which the next forward does not use.
 __global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, const int64_t *__restrict__ fdesc) {
     if (*g.err) return;
+    // the blocks that copy, chosen by k_plc_finalize (fdesc[3])
+    const int64_t nb = fdesc[3] < 1 ? 1 : fdesc[3] > (int64_t)gridDim.x ? (int64_t)gridDim.x : fdesc[3];
+    if ((int64_t)blockIdx.x >= nb) return;  // block-uniform
     __shared__ int32_t s_cnt[RECMG_MAX_TABLES];
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         const int64_t base = fdesc[4 * t], n = fdesc[4 * t + 1];
@@ -520,7 +523,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, const int64_t *_
     __syncthreads();
     // entries were checked where admit and the set-associative placement wrote them
     copy_flat(
-        g, s_cnt,
+        g, s_cnt, nb,
         [&](int t, const DTable &tb, int64_t j) -> const char * {
             const int32_t src = g.fill_src[fdesc[4 * t] + j];
             if (src >= 0) return g.staging + (fdesc[4 * t + 2] + src) * g.stage_stride;  // admitted miss
@@ -530,13 +533,41 @@ __global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, const int64_t *_
         [&](int t, const DTable &tb, int64_t j) { return tb.pool + (int64_t)g.fill_slot[fdesc[4 * t] + j] * tb.row_bytes; });
 }
 
+#ifndef RECMG_FILL_BLOCKS
+#define RECMG_FILL_BLOCKS 112  // zero-copy fill alone on the host link
+#endif
+#ifndef RECMG_FILL_BLOCKS_SHARED
+#define RECMG_FILL_BLOCKS_SHARED 256  // zero-copy fill beside the next forward's on-demand fetch
+#endif
+constexpr int kStagedFillBlocks = 1024;
+// on-demand fetch bytes above which the next fetch is taken to share the link
+// with the fill (below it, the fetch takes a few microseconds of link time)
+constexpr unsigned long long kSharedFetchBytes = 1ull << 20;
+
 // Publishes the counters and writes the fill descriptor of this placement
 // (per table: first fill-list entry, entry count, base of its admitted misses
 // in staging), which the fill reads instead of state the next placement resets.
+// fdesc[3] (a spare word of table 0's entry) is the number of blocks the fill
+// copies with: zero-copy fills take more when the last forward fetched at
+// least 1 MB on demand, since the next forward's fetch will then share the
+// host link (with fewer waves of its own the fill gets less of it), and fewer
+// when the fill has the link to itself, so that it takes no more CUs than it
+// needs from the kernels beside it.
 // log_slot >= 0: the counters also go to that call's record of the stats log
 // (the forward group of the record stays zero).
 __global__ void k_plc_finalize(DGlobal g, int64_t *fdesc, int64_t log_slot) {
-    if (*g.err) return;
+    if (*g.err) return;  // one block; nothing sets the word while it runs
+    __shared__ unsigned long long s_mbytes;  // bytes of the last forward's on-demand misses
+    if (threadIdx.x == 0) s_mbytes = 0;
+    __syncthreads();
+    unsigned long long mb = 0;
+    for (int t = threadIdx.x; t < g.T; t += blockDim.x)
+        mb += (unsigned long long)(g.st[t].mcount > 0 ? g.st[t].mcount : 0) * (unsigned long long)g.tabs[t].row_bytes;
+    if (mb) atomicAdd(&s_mbytes, mb);
+    __syncthreads();
+    if (threadIdx.x == 0)
+        fdesc[3] = g.staged_fill ? kStagedFillBlocks
+                                 : s_mbytes >= kSharedFetchBytes ? RECMG_FILL_BLOCKS_SHARED : RECMG_FILL_BLOCKS;
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         TState &st = g.st[t];
         const DTable &tb = g.tabs[t];
@@ -632,20 +663,23 @@ void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int
     k_plc_admit<<<dim3(grid_for(cand_bound, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
 }
 
-#ifndef RECMG_FILL_BLOCKS
-#define RECMG_FILL_BLOCKS 112
-#endif
-
 void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s) {
     // Zero-copy fills read the host: about a hundred blocks of 4-deep 16-byte
-    // loads keep the host link full (about 2 MB in flight).  Host reads hold a
-    // CU's L1 miss slots for microseconds, so a larger grid slows every kernel
-    // that shares its CUs: with 512 blocks the next forward's dedup, running
-    // alongside, took 0.88 ms on configuration 2 instead of 0.28 ms.  Measured
-    // on configuration 2: 80-96 blocks leave the link short, 160 and more slow
-    // the placement that runs beside the fill.  STAGED fills copy within HBM
-    // and take a full grid.
-    k_plc_fill<<<g.staged_fill ? 1024 : RECMG_FILL_BLOCKS, kBlock, 0, s>>>(g, fdesc);
+    // loads keep the host link full (about 2 MB in flight) when the fill has
+    // it to itself.  Host reads hold a CU's L1 miss slots for microseconds, so
+    // a larger grid slows every kernel that shares its CUs: with 512 blocks the
+    // next forward's dedup, running alongside, took 0.88 ms on configuration 2
+    // instead of 0.28 ms.  Measured on configuration 2 (no on-demand misses):
+    // 80-96 blocks leave the link short, 160 and more slow the placement that
+    // runs beside the fill (192: -8% lookups/s).  On configuration 3 the fill
+    // shares the link with the next forward's fetch of about 330,000 misses,
+    // and 256 blocks gave +4%.  The grid holds the larger count; k_plc_finalize
+    // writes how many of its blocks copy.  STAGED fills copy within HBM and
+    // take a full grid.
+    const int blocks = g.staged_fill ? kStagedFillBlocks
+                                     : (RECMG_FILL_BLOCKS > RECMG_FILL_BLOCKS_SHARED ? RECMG_FILL_BLOCKS
+                                                                                     : RECMG_FILL_BLOCKS_SHARED);
+    k_plc_fill<<<blocks, kBlock, 0, s>>>(g, fdesc);
 }
 
 void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, int64_t log_slot, hipStream_t s) {

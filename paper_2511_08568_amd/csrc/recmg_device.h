@@ -408,10 +408,12 @@ __device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
 }
 
 // Copy `count[t]` rows of every table in 16/4/2-byte units, the tables' work
-// laid end to end so every table gets its share of the grid.  src_of / dst_of
-// give the byte addresses of item j of table t.
+// laid end to end so every table gets its share of the first `nblocks` blocks
+// of the grid (the others copy nothing).  src_of / dst_of give the byte
+// addresses of item j of table t.
 template <class Src, class Dst>
-__device__ __forceinline__ void copy_flat(const DGlobal &g, const int32_t *count, Src src_of, Dst dst_of) {
+__device__ __forceinline__ void copy_flat(const DGlobal &g, const int32_t *count, int64_t nblocks, Src src_of,
+                                          Dst dst_of) {
     __shared__ int64_t s_pre[RECMG_MAX_TABLES + 1];
     __shared__ long long tmp[16];
     // per-table unit counts, scanned (T <= 256 = blockDim)
@@ -423,8 +425,8 @@ __device__ __forceinline__ void copy_flat(const DGlobal &g, const int32_t *count
     if (t0 < g.T) s_pre[t0] = ex;
     if (t0 == 0) s_pre[g.T] = tot;
     __syncthreads();
-    const int64_t items = s_pre[g.T];
-    const int64_t S = (int64_t)gridDim.x * blockDim.x;
+    const int64_t items = (int64_t)blockIdx.x < nblocks ? s_pre[g.T] : 0;
+    const int64_t S = nblocks * blockDim.x;
     for (int64_t base = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; base < items; base += 4 * S) {
         uint4 v16[4];
         uint32_t v4[4];
