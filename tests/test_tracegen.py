@@ -155,3 +155,29 @@ def test_optgen_bits_expand_to_accesses():
             s, e = w.table_segment(off, t)
             for r in np.unique(idx[s:e]):
                 assert np.unique(bits[s:e][idx[s:e] == r]).size == 1  # one label per distinct row
+
+
+def test_configuration_shapes():
+    """The five workloads' tables, caches, batches and policies as their recipes state them."""
+    w = tg.make_config(1)
+    assert [(t.rows, t.dim, t.dtype, t.cap) for t in w.tables] == [(100_000, 64, "f32", 10_000)]
+    assert (w.bags, w.batches, w.policy) == (256, 100, "lru")
+    w = tg.make_config(2)
+    assert w.num_tables == 8 and all((t.rows, t.dim, t.dtype, t.cap) == (1_000_000, 128, "f32", 50_000)
+                                     for t in w.tables)
+    assert (w.bags, w.batches, w.policy, w.prefetch) == (2048, 500, "lru", ("exact",))
+    w = tg.make_config(3)
+    assert w.num_tables == 26 and w.tables[0].rows == 20_000_000
+    assert all(1_000 <= t.rows <= 20_000_000 and t.dim == 128 and t.dtype == "f16" and t.cap == int(0.02 * t.rows)
+               for t in w.tables)
+    assert (w.bags, w.batches, w.policy, w.eviction_speed) == (4096, 1000, "priority", 4)
+    w = tg.make_config(4)
+    # 20 GB of HBM cache over 4 tables of 256-byte rows
+    assert w.num_tables == 4 and all((t.rows, t.dim, t.dtype, t.cap) == (100_000_000, 128, "bf16", 19_531_250)
+                                     for t in w.tables)
+    assert (w.bags, w.batches, w.policy) == (16_384, 200, "lru")
+    w = tg.make_config(5)
+    assert w.num_tables == 64
+    assert [t.dim for t in w.tables[:8]] == [32, 64, 128, 256] * 2
+    assert all((t.rows, t.dtype, t.cap) == (2_000_000, "f32", 200_000) for t in w.tables)
+    assert (w.bags, w.batches, w.policy) == (8192, 300, "priority")
