@@ -239,7 +239,8 @@ def test_sa_crowded_sets(seed, ways):
 
 @pytest.mark.parametrize("cid,scale,bags,tables,ways", [(2, 0.02, 256, 3, 32), (3, 0.01, 256, 6, 32),
                                                         (5, 0.01, 256, 8, 32), (4, 0.0005, 512, 2, 32),
-                                                        (3, 0.01, 256, 4, 4), (2, 0.02, 256, 2, 64)])
+                                                        (3, 0.01, 256, 4, 4), (2, 0.02, 256, 2, 64),
+                                                        (3, 0.01, 256, 4, 48), (2, 0.02, 256, 2, 17)])
 def test_sa_configs_scaled(cid, scale, bags, tables, ways):
     """The scaled configurations with W-way set-associative caches (32 ways:
     the production default the paper compares against)."""
