@@ -3,16 +3,18 @@
 
 One step = one placement (prefetch list + caching bits applied to the HBM
 cache) followed by one pooled lookup of a batch, i.e. every row of the hot
-path.  Default workload: configuration 2 -- 8 fp32 tables x 1,000,000 rows x
-128 dims in pinned host memory, a 50,000-row HBM cache per table, 2,048 bags per
-table with Poisson(40) pooling clipped to [1, 200], Zipf(1.1) rows through a
-per-table permutation, prefetch list = the next batch's exact distinct rows,
-LRU-by-batch ranking.  Inputs are synthetic (tracegen) and resident in HBM
-before the timed region.
+path.  Default workload: configuration 5, the one with the most work per batch
+-- 64 fp32 tables x 2,000,000 rows with dims 32/64/128/256 (61.4 GB in pinned
+host memory), a 200,000-row HBM cache per table, 8,192 bags per table with
+geometric(mean 25) pooling (one-hot for the last 16 tables), Zipf exponents
+0.8/1.0/1.2, a prefetch list of twice the cache headroom with half of it
+precise, PRIORITY ranking (eviction speed 4).  Inputs are synthetic (tracegen)
+and resident in HBM before the timed region.
 
-Prints one JSON line: pooled lookups/s (value), the pooled kernel's achieved
-HBM bandwidth against the 8 TB/s peak (roofline), host-link traffic, on-demand
-fetches per batch, and the CPU oracle timed on the host (cpu_baseline).
+Prints one JSON line: pooled lookups/s (value); the roofline of the kernel
+that dominates the step (the fill or the miss fetch, host-link bound) and of
+the pooled kernel (HBM bound); host-link traffic; on-demand fetches per batch;
+and the CPU oracle timed on the host (cpu_baseline).
 """
 import argparse
 import hashlib
@@ -26,37 +28,48 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-PCIE5_X16_GBS = 64.0
-# HBM bytes per pooled launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs of the
-# default workload, scaled by a copy-kernel calibration; valid only for the
-# kernel source it was measured on (sha256 of the files below)
-TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_pool_w_config2_traffic.json")
-KERNEL_SOURCES = ("forward.hip", "recmg_device.h")
+PCIE5_X16_GBS = 64.0  # PCIe Gen5 x16, one direction, published
+DEFAULT_CONFIG = 5
+# HBM bytes per launch of each kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE
+# runs of a workload's bench.py command, scaled by a copy-kernel calibration;
+# valid only for the kernel source they were measured on (sha256 of the file
+# that holds the kernel and of the shared device headers)
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "traffic_config{}.json")
+CSRC = os.path.join(ROOT, "paper_2511_08568_amd", "csrc")
+KERNEL_FILES = {"pooled": "forward.hip", "k_fetch": "forward.hip", "k_plc_fill": "placement.hip"}
+SHARED_HEADERS = ("recmg_device.h", "launch.h")
 
 
-def kernel_source_sha256():
+def kernel_source_sha256(kernel):
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, "paper_2511_08568_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    for f in (KERNEL_FILES[kernel],) + SHARED_HEADERS:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()
 
 
-def measured_traffic(args):
-    """(bytes per launch, record) when the committed counter record matches
-    this workload and the current kernel source, else (None, reason)."""
-    default = (args.config == 2 and args.row_scale == 1.0 and args.prefetch is None
-               and args.miss_mode == "zero_copy" and args.ways == 0 and args.bits is None and args.policy is None)
+def measured_traffic(args, kernel):
+    """(bytes per launch, source) of `kernel` when the committed counter record
+    matches this workload and the current kernel sources, else (None, reason)."""
+    default = (args.row_scale == 1.0 and args.prefetch is None and args.miss_mode == "zero_copy" and args.ways == 0
+               and args.bits is None and args.policy is None)
     if not default:
-        return None, "counters recorded for the default workload only"
+        return None, "counters recorded for the configurations' own settings only"
+    path = TRAFFIC_RECORD.format(args.config)
     try:
-        with open(TRAFFIC_RECORD) as fh:
+        with open(path) as fh:
             rec = json.load(fh)
     except (OSError, ValueError):
-        return None, "no counter record"
-    if rec.get("source_sha256") != kernel_source_sha256():
+        return None, "no counter record for this configuration"
+    k = rec["kernels"].get(kernel)
+    if k is None:
+        return None, f"{kernel} not in the counter record"
+    if k.get("source_sha256") != kernel_source_sha256(kernel):
         return None, "kernel source changed since the counters were taken"
-    return rec["read_bytes_per_launch"] + rec["write_bytes_per_launch"], rec
+    return (k["read_bytes_per_launch"] + k["write_bytes_per_launch"],
+            f"{os.path.relpath(path, ROOT)}: FETCH_SIZE x {rec['fetch_scale']:.2f} + WRITE_SIZE x "
+            f"{rec['write_scale']:.2f}, bytes per launch ({k['read_bytes_per_launch'] / 1e6:.1f} MB read, "
+            f"{k['write_bytes_per_launch'] / 1e6:.1f} MB written)")
 
 
 def huge_page_tensor(shape, dtype):
@@ -189,9 +202,9 @@ def log(msg):
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="configuration id (1..5)")
+    ap.add_argument("--config", type=int, default=DEFAULT_CONFIG, help="configuration id (1..5)")
     ap.add_argument("--row-scale", type=float, default=1.0, help="<1 shrinks rows and caches (debug only)")
     ap.add_argument("--miss-mode", default="zero_copy", choices=["zero_copy", "staged"])
     ap.add_argument("--prefetch", default=None, choices=["none", "exact"],
@@ -337,7 +350,9 @@ def main():
     elapsed_ms = ev0.elapsed_time(ev1)
     timed_stages = cache.stage_times(reset=True)  # the pooled kernel only (timing level 1)
     _, tot1 = cache.stats()
-    log(f"timed {K} steps: {elapsed_ms:.3f} ms; pooled kernel {timed_stages['fwd_pool'][0]:.3f} ms")
+    log(f"timed {K} steps: {elapsed_ms:.3f} ms; kernels (ms): pooled {timed_stages['fwd_pool'][0]:.3f}, "
+        f"fill {timed_stages['plc_fill'][0]:.3f}, fetch {timed_stages['fwd_fetch'][0]:.3f}, "
+        f"host-link union {timed_stages['host_link'][0]:.3f}")
     # breakdown: every stage timed (each stage adds two stream commands, so
     # these steps are slower and stay out of the headline figure)
     # Events before each placement and between it and its forward also split
@@ -382,6 +397,18 @@ def main():
     bytes_per_launch = alg_bytes / K
     pool_s = pool_ms / max(pool_calls, 1) / 1e3
     achieved = bytes_per_launch / pool_s / 1e9 if pool_s > 0 else 0.0
+    # The host-link kernels over the timed steps, by the events their own
+    # dispatches record (timing level 1): the placement's fill (prefetch rows
+    # read from pinned host memory; admitted misses come from HBM staging) and
+    # the forward's zero-copy miss fetch.  They run at the same time on two
+    # streams, so each kernel's own rate is its share of the link; the union
+    # of their intervals gives the link's rate.
+    fill_ms, fill_calls = timed_stages["plc_fill"]
+    fetch_ms, fetch_calls = timed_stages["fwd_fetch"]
+    union_ms = timed_stages["host_link"][0]
+    host_bytes = {"k_plc_fill": delta["prefetch_bytes"], "k_fetch": delta["ondemand_bytes"]}
+    link_times = {"k_plc_fill": (fill_ms, fill_calls), "k_fetch": (fetch_ms, fetch_calls)}
+    zero_copy = args.miss_mode == "zero_copy"
     # host link over the breakdown steps: bytes moved there / the union of the
     # miss-fetch and fill intervals (they overlap on two streams)
     bdelta = {k: sum(tot2[t][k] - tot1[t][k] for t in range(T)) for k in tot2[0] if k != "digest"}
@@ -389,7 +416,7 @@ def main():
     link_ms = stages["host_link"][0]
     link_gbs = link_bytes / (link_ms / 1e3) / 1e9 if link_ms > 0 else 0.0
 
-    traffic, trec = measured_traffic(args)
+    pool_traffic, pool_tsrc = measured_traffic(args, "pooled")
 
     link_peak = None
     if not args.no_link_peak:
@@ -427,17 +454,15 @@ def main():
             "pipelined_placement": bool(args.pipeline),
             "row_scale": args.row_scale,
         },
-        "roofline": {
-            "kernel": "k_pool_w (pooled gather + sum)",
+        "hit_path_roofline": {
+            "kernel": "k_pool_w (pooled gather + sum; one launch per row-size kind, timed together per forward)",
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": traffic,
-            "traffic_source": (f"{os.path.relpath(TRAFFIC_RECORD, ROOT)}: FETCH_SIZE x {trec['fetch_scale']:.2f} + "
-                               f"WRITE_SIZE x {trec['write_scale']:.2f}, bytes per launch")
-            if traffic is not None else trec,
+            "traffic": pool_traffic,
+            "traffic_source": pool_tsrc,
             "alg_bytes_per_launch": bytes_per_launch,
             "avg_launch_us": pool_s * 1e6,
             "logical_bytes_per_launch": logical_bytes / K,
@@ -467,6 +492,42 @@ def main():
         "stage_split_over": f"{KB} breakdown steps (every stage timed) after the timed ones",
     }
 
+    # The roofline object describes the kernel that takes most of the timed
+    # steps' kernel time.  With zero-copy misses that is the fill or the miss
+    # fetch whenever either moves more than a few MB per batch: they are bound
+    # by the host link (PCIe Gen5 x16), not by HBM, and are priced against it.
+    link_kernel = max(link_times, key=lambda k: link_times[k][0])
+    if zero_copy and link_times[link_kernel][0] > pool_ms:
+        ms, calls = link_times[link_kernel]
+        avg_s = ms / max(calls, 1) / 1e3
+        per_launch = host_bytes[link_kernel] / max(calls, 1)
+        ach = per_launch / avg_s / 1e9 if avg_s > 0 else 0.0
+        traffic, tsrc = measured_traffic(args, link_kernel)
+        union_gbs = sum(host_bytes.values()) / (union_ms / 1e3) / 1e9 if union_ms > 0 else 0.0
+        result["roofline"] = {
+            "kernel": link_kernel + (" (prefetch fill: host rows into HBM slots)" if link_kernel == "k_plc_fill"
+                                     else " (zero-copy on-demand miss fetch)"),
+            "bound": "host_link",
+            "achieved": ach,
+            "peak": PCIE5_X16_GBS,
+            "unit": "GB/s",
+            "frac": ach / PCIE5_X16_GBS,
+            "traffic": traffic,
+            "traffic_source": tsrc,
+            "alg_bytes_per_launch": per_launch,
+            "avg_launch_us": avg_s * 1e6,
+            "frac_of_measured_peak": ach / link_peak if link_peak else None,
+            "measured_h2d_peak_GBs": link_peak,
+            "link_shared_with": ("k_fetch" if link_kernel == "k_plc_fill" else "k_plc_fill") + " on the other stream",
+            "link_union": {"bytes_per_step": sum(host_bytes.values()) / K,
+                           "ms_per_step": union_ms / K,
+                           "achieved_GBs": union_gbs,
+                           "frac": union_gbs / PCIE5_X16_GBS,
+                           "frac_of_measured_peak": union_gbs / link_peak if link_peak else None},
+        }
+    else:
+        result["roofline"] = dict(result["hit_path_roofline"])
+
     # what the oracle replay checks: every call's counters (the device log),
     # the final resident sets, and the pooled sums of every batch, or of a
     # fixed subset (every 5th, the first and the last) where checking all would
@@ -490,9 +551,10 @@ def main():
         tabs_np = [h.numpy() for h in host]
         o = oracle.for_workload(w, tabs_np, nthreads=nth)
         sums = [dict.fromkeys(tot1[0], 0) for _ in range(T)]
-        # The timed sample is the replay of the GPU's batches, continued with
-        # the workload's next batches (generated outside the timed intervals)
-        # until about --cpu-seconds of oracle time.
+        # The timed sample is the replay of the GPU's batches (always whole, for
+        # the parity check), continued with the workload's next batches
+        # (generated outside the timed intervals) until about --cpu-seconds of
+        # oracle time.
         done, n_lookups, secs = 0, 0, 0.0
         calls_equal, digests_equal, res_equal, pooled_ok, worst = True, True, None, True, 0.0
         # output buffers allocated once, outside the timed intervals
@@ -552,8 +614,6 @@ def main():
                             sums[t][k] += plc[t][k]
             n_lookups += idx.size
             done += 1
-            if b < nb and secs > args.cpu_seconds and b < nb - 1:
-                break  # the replay alone exceeds the budget: no parity check
         o.close()
         cpu_model = ""
         try:

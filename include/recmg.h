@@ -53,10 +53,14 @@
  * path synchronise with the host.
  *
  * Errors: every entry point returns a recmg_status_t.  Argument errors found
- * on the host leave the cache state unchanged.  Out-of-range rows found on
- * the device (validate = 0) latch a device error flag: that call and every
- * later call become no-ops on the device, and the next recmg_stats returns
- * RECMG_E_RANGE.  With validate = 1 the host copies the ids back and checks
+ * on the host leave the cache state unchanged.  An error returned after a
+ * placement or forward has begun enqueuing device work (RECMG_E_HIP, or
+ * RECMG_E_STATE from the STAGED host path) leaves the device state ahead of
+ * the handle's own bookkeeping: the handle is then broken, every later call
+ * but recmg_cache_destroy returns RECMG_E_STATE, and it must be destroyed.
+ * Out-of-range rows found on the device (validate = 0) latch a device error
+ * flag: that call and every later call become no-ops on the device, and the
+ * next recmg_stats returns RECMG_E_RANGE.  With validate = 1 the host copies the ids back and checks
  * them before anything is launched (synchronous; for debugging).
  * recmg_last_error() gives a message for the calling thread's last error.
  */
@@ -76,7 +80,7 @@ typedef enum {
     RECMG_OK = 0,
     RECMG_E_INVALID = 1, /* null, inconsistent or over-size argument */
     RECMG_E_RANGE = 2,   /* a row id outside [0, rows_t) or malformed offsets */
-    RECMG_E_STATE = 3,   /* call on a destroyed handle or after a device error */
+    RECMG_E_STATE = 3,   /* call on a destroyed or broken handle, or a broken invariant */
     RECMG_E_HIP = 4,     /* HIP runtime error (message via recmg_last_error) */
     RECMG_E_NOMEM = 5    /* workspace or staging buffer smaller than queried */
 } recmg_status_t;
@@ -117,17 +121,18 @@ typedef struct {
     size_t device_workspace_bytes;
     void *host_staging;                 /* caller-owned pinned host memory, STAGED only */
     size_t host_staging_bytes;
-    void *copy_stream;                  /* hipStream_t for STAGED copies; NULL = the
-                                           compute stream */
+    void *copy_stream;                  /* hipStream_t for STAGED copies and the placement's
+                                           fill; NULL = the stream of each call */
     int32_t timing;                     /* initial timing level (see recmg_set_timing): 0 none,
-                                           1 the pooled kernel only, 2 every stage */
+                                           1 the pooled, fetch and fill kernels, 2 every stage */
     int32_t ways;                       /* 0: fully associative caches.  1 .. 64: W-way
                                            set-associative caches (see below) */
     int32_t stats_log_calls;            /* >= 0: the counters of the latest this many calls
                                            are kept on the device (recmg_stats_log) */
 } recmg_config_t;
 
-/* Stages timed at timing level 2 (RECMG_STAGE_FWD_POOL from level 1 on). */
+/* Stages timed at timing level 2 (at level 1: the kernels named in
+ * recmg_set_timing). */
 typedef enum {
     RECMG_STAGE_FWD_DEDUP = 0,  /* offsets check, dedup + sort, map probe, inverse map */
     RECMG_STAGE_FWD_FETCH = 1,  /* on-demand miss fetch (zero-copy kernel or staged copy) */
@@ -243,9 +248,11 @@ int32_t recmg_stage_times(recmg_cache_t *c, double *ms, int64_t *calls, int32_t 
 
 /* Timing level for later calls:
  *   0  none;
- *   1  the pooled kernels only, by events their own dispatches record (no
- *      command is added to the stream; the first pooled dispatch of a call
- *      starts a little later, by a few microseconds);
+ *   1  the kernels of the pooled sum, of the zero-copy miss fetch and of the
+ *      placement's fill (RECMG_STAGE_FWD_POOL, _FWD_FETCH, _PLC_FILL, and
+ *      their host-link union), by events their own dispatches record (no
+ *      command is added to the stream; such a dispatch starts a little later,
+ *      by a few microseconds);
  *   2  every stage: an event pair per stage per call around the stage's
  *      commands (two extra stream commands per stage, a few microseconds each).
  * Returns RECMG_E_INVALID for another level.  Not thread-safe with calls in

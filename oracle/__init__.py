@@ -65,8 +65,6 @@ def load(mutant: int = 0) -> ctypes.CDLL:
     lib.oracle_table_stats.argtypes = [P, ctypes.c_int32, P, P, P]
     lib.oracle_resident.restype = ctypes.c_int64
     lib.oracle_resident.argtypes = [P, ctypes.c_int32, P, ctypes.c_int64]
-    lib.oracle_row_state.restype = ctypes.c_int32
-    lib.oracle_row_state.argtypes = [P, ctypes.c_int32, ctypes.c_int32, P, P]
     lib.oracle_pooled_abs.restype = ctypes.c_int32
     lib.oracle_pooled_abs.argtypes = [P, P, P, ctypes.c_int32, P]
     lib.oracle_splitmix64_mix.restype = ctypes.c_uint64
@@ -173,12 +171,6 @@ class Oracle:
         out = np.zeros(max(n, 1), np.int32)
         self.lib.oracle_resident(self.h, int(t), _ptr(out), n)
         return out[:n]
-
-    def row_state(self, t: int, r: int):
-        s = np.zeros(1, np.int64)
-        p = np.zeros(1, np.int32)
-        ok = self.lib.oracle_row_state(self.h, int(t), int(r), _ptr(s), _ptr(p))
-        return (int(s[0]), int(p[0])) if ok else None
 
 
 def splitmix64_mix(z: int, mutant: int = 0) -> int:

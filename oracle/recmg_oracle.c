@@ -731,13 +731,3 @@ int64_t oracle_resident(void *h, int32_t t, int32_t *rows_out, int64_t capacity)
         if (tb->in_r[r]) { if (q < capacity && rows_out) rows_out[q] = (int32_t)r; ++q; }
     return q;
 }
-
-/* Score and prefetch flag of a resident row (for tests); returns 0 if not resident. */
-int32_t oracle_row_state(void *h, int32_t t, int32_t r, int64_t *score, int32_t *pf) {
-    oracle_t *o = (oracle_t *)h;
-    otab *tb = &o->t[t];
-    if (r < 0 || r >= tb->n || !tb->in_r[r]) return 0;
-    if (score) *score = tb->s[r];
-    if (pf) *pf = tb->pf[r];
-    return 1;
-}

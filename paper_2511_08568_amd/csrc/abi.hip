@@ -260,7 +260,11 @@ struct recmg_cache {
     hipEvent_t ev_plc = nullptr;   // latest placement: after all its kernels but the fill
     hipEvent_t ev_fill[2] = {nullptr, nullptr};  // fill of the latest placement of each parity
     bool fill_rec[2] = {false, false};
+    hipStream_t fill_stream[2] = {nullptr, nullptr};  // stream each parity's latest fill ran on
     int fill_last = -1;  // parity of the latest fill no forward has waited for yet
+    // An error after a call began enqueuing work leaves device and host state
+    // out of step: every later call but destroy is refused.
+    bool broken = false;
     int32_t *fill_src_buf[2] = {nullptr, nullptr}, *fill_slot_buf[2] = {nullptr, nullptr};
     int64_t *fdesc_buf[2] = {nullptr, nullptr};
     int32_t pool_B = -1;
@@ -307,6 +311,20 @@ struct recmg_cache {
 
 namespace {
 
+hipEvent_t take_event(recmg_cache_t *c);
+
+// Timing level 1: an event pair that the kernel's own dispatch records (no
+// stream command is added), kept as a mark of `stage` once the launch is
+// issued.  Both null when not timing at level 1 or out of events.
+struct DispatchTimer {
+    recmg_cache_t *c;
+    int stage;
+    hipEvent_t a = nullptr, b = nullptr;
+    DispatchTimer(recmg_cache_t *c_, int stage_, bool on);
+    void issued();
+    ~DispatchTimer();
+};
+
 hipEvent_t take_event(recmg_cache_t *c) {
     if (c->ev_free.empty()) {
         hipEvent_t e = nullptr;
@@ -316,6 +334,24 @@ hipEvent_t take_event(recmg_cache_t *c) {
     hipEvent_t e = c->ev_free.back();
     c->ev_free.pop_back();
     return e;
+}
+
+DispatchTimer::DispatchTimer(recmg_cache_t *c_, int stage_, bool on) : c(c_), stage(stage_) {
+    if (!on || c->timing != 1) return;
+    a = take_event(c);
+    b = a ? take_event(c) : nullptr;
+    if (a && !b) {
+        c->ev_free.push_back(a);
+        a = nullptr;
+    }
+}
+void DispatchTimer::issued() {
+    if (a) c->marks.push_back({stage, a, b});
+    a = b = nullptr;
+}
+DispatchTimer::~DispatchTimer() {  // not issued: the events go back unused
+    if (a) c->ev_free.push_back(a);
+    if (b) c->ev_free.push_back(b);
 }
 
 // Stage timing (level 2): an event pair per stage per call, resolved in
@@ -346,8 +382,22 @@ struct StageTimer {
 int32_t check_handle(recmg_cache_t *c) {
     if (!c) return fail(RECMG_E_INVALID, "handle is NULL");
     if (c->magic != kMagic) return fail(RECMG_E_STATE, "handle is not live");
+    if (c->broken)
+        return fail(RECMG_E_STATE, "an earlier call failed after enqueuing work; the handle must be destroyed");
     return RECMG_OK;
 }
+
+// Marks the handle broken unless the call reaches its end: errors returned
+// once a call has started enqueuing device work leave the device state ahead
+// of the host bookkeeping.
+struct EnqueueGuard {
+    recmg_cache_t *c;
+    bool done = false;
+    explicit EnqueueGuard(recmg_cache_t *c_) : c(c_) {}
+    ~EnqueueGuard() {
+        if (!done) c->broken = true;
+    }
+};
 
 // Waits for every stream the handle's calls used.
 hipError_t sync_all(recmg_cache_t *c) {
@@ -789,6 +839,9 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (c->cfg.validate && (rc = host_check_ids(prefetch_rows, prefetch_offsets, c->T + 1, 1, num_prefetch, c->geo, s)))
         return rc;
+    const int64_t b = c->placements;
+    if (b + 2 >= (int64_t(1) << 31)) return fail(RECMG_E_STATE, "placement count exhausted");
+    EnqueueGuard guard(c);
     // what this placement reads from calls on other streams: the latest
     // forward's distinct rows, misses and sources; the latest placement's state
     if (c->fwd_ev && c->fwd_stream != s) HIP_TRY(hipStreamWaitEvent(s, c->ev_src, 0));
@@ -803,8 +856,6 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     c->g.fill_slot = c->fill_slot_buf[q];
     int64_t *fdesc = c->fdesc_buf[q];
     const DGlobal &g = c->g;
-    const int64_t b = c->placements;
-    if (b + 2 >= (int64_t(1) << 31)) return fail(RECMG_E_STATE, "placement count exhausted");
     PlcParams p{};
     p.prio = c->cfg.policy == RECMG_PRIORITY;
     p.lfu = c->cfg.policy == RECMG_LFU_BATCH;
@@ -855,15 +906,25 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     hipStream_t fs = c->copy_stream ? c->copy_stream : s;
     if (fs != s) HIP_TRY(hipStreamWaitEvent(fs, c->ev_plc, 0));
     if (c->fwd_ev && c->fwd_stream != fs) HIP_TRY(hipStreamWaitEvent(fs, c->ev_pool, 0));
+    // The previous placement's fill may still write slots this placement has
+    // just freed and handed to other rows.  On one fill stream the two fills
+    // run in order; on different ones (no copy stream, placements on
+    // different streams) this fill waits for it, and so does every forward
+    // that waits for this fill.
+    if (c->fill_rec[q ^ 1] && c->fill_stream[q ^ 1] != fs) HIP_TRY(hipStreamWaitEvent(fs, c->ev_fill[q ^ 1], 0));
     {
         StageTimer tm(c, RECMG_STAGE_PLC_FILL, fs);
         if (c->cfg.miss_mode == RECMG_STAGED && (rc = staged_fill(c, s, fs))) return rc;  // host-staged rows
-        launch_plc_fill(g, fdesc, fs);
+        DispatchTimer dt(c, RECMG_STAGE_PLC_FILL, true);
+        launch_plc_fill(g, fdesc, fs, dt.a, dt.b);
+        dt.issued();
     }
     HIP_TRY(hipEventRecord(c->ev_fill[q], fs));
     c->fill_rec[q] = true;
+    c->fill_stream[q] = fs;
     c->fill_last = q;
     HIP_TRY(hipGetLastError());
+    guard.done = true;
     c->placements++;
     c->calls++;
     c->plc_np = num_prefetch;
@@ -887,6 +948,8 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
     if ((rc = set_device(c))) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (c->cfg.validate && (rc = host_check_ids(indices, offsets, (int64_t)c->T * B + 1, B, n, c->geo, s))) return rc;
+    if (c->forwards + 1 >= (int64_t(1) << 31)) return fail(RECMG_E_STATE, "forward count exhausted");
+    EnqueueGuard guard(c);
     // what this forward needs from calls on other streams: the latest
     // placement's state (its fill is waited for before the pooled kernel) and
     // the end of the latest forward, whose per-index arrays this one rewrites
@@ -912,7 +975,6 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
         c->pool_B = (int32_t)B;
         c->pool_blocks = c->pool_bstart[c->T];
     }
-    if (c->forwards + 1 >= (int64_t(1) << 31)) return fail(RECMG_E_STATE, "forward count exhausted");
     const int32_t stamp = (int32_t)c->forwards;
     c->cur ^= 1;  // the other staging buffer: a pending fill may still read this one
     c->g.staging = c->stage[c->cur];
@@ -933,7 +995,9 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
     if (n > 0) {
         StageTimer tm(c, RECMG_STAGE_FWD_FETCH, s);
         if (c->cfg.miss_mode == RECMG_ZERO_COPY) {
-            launch_fetch(g, s);
+            DispatchTimer dt(c, RECMG_STAGE_FWD_FETCH, true);
+            launch_fetch(g, s, dt.a, dt.b);
+            dt.issued();
         } else if ((rc = staged_fetch(c, s))) {
             return rc;
         }
@@ -963,6 +1027,7 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
     launch_fwd_finalize(g, c->cfg.stats_log_calls ? c->calls % c->cfg.stats_log_calls : -1, s);
     HIP_TRY(hipEventRecord(c->ev_fwd, s));
     HIP_TRY(hipGetLastError());
+    guard.done = true;
     c->forwards++;
     c->calls++;
     c->plc_np = -1;  // coverage counts against the placement just before a forward only

@@ -744,7 +744,10 @@ void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStre
 // (the next placement runs beside it).  Measured on configuration 3 (64-256
 // blocks): 96 is best with 32-way sets (k_sa_place's critical path runs
 // alongside), within 1% of the best without prefetch and on configuration 5.
-void launch_fetch(const DGlobal &g, hipStream_t s) { k_fetch<<<RECMG_FETCH_BLOCKS, kBlock, 0, s>>>(g); }
+void launch_fetch(const DGlobal &g, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    if (ev0 || ev1) hipExtLaunchKernelGGL(k_fetch, dim3(RECMG_FETCH_BLOCKS), dim3(kBlock), 0, s, ev0, ev1, 0, g);
+    else k_fetch<<<RECMG_FETCH_BLOCKS, kBlock, 0, s>>>(g);
+}
 
 int pool_kind(int dtype, int vec, int wlw, int wr) {
     if (wlw == 0) return dtype * 2 + vec;

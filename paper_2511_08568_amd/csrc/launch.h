@@ -17,7 +17,8 @@ void launch_fwd_prep(const DGlobal &g, const int64_t *offsets, int32_t B, int64_
 void launch_fwd_probe(const DGlobal &g, int32_t stamp, int64_t n, hipStream_t s);
 void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStream_t s);
 void launch_fwd_cover(const DGlobal &g, int32_t stamp, int64_t np, hipStream_t s);
-void launch_fetch(const DGlobal &g, hipStream_t s);
+// ev0 / ev1 (may be null): recorded by the dispatch itself around the kernel
+void launch_fetch(const DGlobal &g, hipStream_t s, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // Pooled-sum kernels: kinds [0, kPoolKindsGroup) are the group-per-bag kernel
 // (dtype * 2 + vec), the rest the wave-per-bag kernel per (dtype, wlw, wr).
 constexpr int kPoolKindsGroup = 6, kPoolKinds = kPoolKindsGroup + 15;
@@ -42,7 +43,8 @@ void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, h
 void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,
                       hipStream_t s);
 // fdesc: this placement's fill descriptor, [T][4] int64 (written by finalize, read by fill)
-void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s);
+void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s, hipEvent_t ev0 = nullptr,
+                     hipEvent_t ev1 = nullptr);
 void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, int64_t log_slot, hipStream_t s);
 void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s);
 

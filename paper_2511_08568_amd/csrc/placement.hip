@@ -24,6 +24,8 @@
 // pass 0), k_plc_pick, { k_plc_select (histogram of pass 1..), k_plc_pick }*,
 // k_plc_evict, k_map_clear / k_map_refill (rebuild
 // when deleted entries pile up), k_plc_admit, k_plc_fill, k_plc_finalize.
+#include <hip/hip_ext.h>
+
 #include "launch.h"
 
 namespace recmg {
@@ -663,7 +665,7 @@ void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int
     k_plc_admit<<<dim3(grid_for(cand_bound, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
 }
 
-void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s) {
+void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     // Zero-copy fills read the host: about a hundred blocks of 4-deep 16-byte
     // loads keep the host link full (about 2 MB in flight) when the fill has
     // it to itself.  Host reads hold a CU's L1 miss slots for microseconds, so
@@ -679,7 +681,8 @@ void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s) {
     const int blocks = g.staged_fill ? kStagedFillBlocks
                                      : (RECMG_FILL_BLOCKS > RECMG_FILL_BLOCKS_SHARED ? RECMG_FILL_BLOCKS
                                                                                      : RECMG_FILL_BLOCKS_SHARED);
-    k_plc_fill<<<blocks, kBlock, 0, s>>>(g, fdesc);
+    if (ev0 || ev1) hipExtLaunchKernelGGL(k_plc_fill, dim3(blocks), dim3(kBlock), 0, s, ev0, ev1, 0, g, fdesc);
+    else k_plc_fill<<<blocks, kBlock, 0, s>>>(g, fdesc);
 }
 
 void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, int64_t log_slot, hipStream_t s) {

@@ -81,7 +81,7 @@ class GpuRunner:
     """Drives the HIP path through a workload (test helper; marshalling only)."""
 
     def __init__(self, w, tabs, miss_mode="zero_copy", validate=False, max_indices=None, max_prefetch=None,
-                 nbatches=None, pin=True, pipeline=False, stats_log_calls=0):
+                 nbatches=None, pin=True, pipeline=False, stats_log_calls=0, overlap=True):
         import torch
         from paper_2511_08568_amd import TieredEmbeddingCache
         self.torch = torch
@@ -99,7 +99,7 @@ class GpuRunner:
                                           policy=w.policy, eviction_speed=w.eviction_speed, miss_mode=miss_mode,
                                           max_bags_per_table=w.bags, max_indices=max_indices,
                                           max_prefetch=max_prefetch, validate=validate, ways=w.ways,
-                                          stats_log_calls=stats_log_calls)
+                                          stats_log_calls=stats_log_calls, overlap=overlap)
         # pipelined placement: placements on a stream of their own, whose
         # inputs are copied on that stream too
         self.pstream = torch.cuda.Stream(device=self.dev) if pipeline else None

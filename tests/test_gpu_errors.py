@@ -129,12 +129,45 @@ def test_empty_batches_and_empty_prefetch():
         g.close()
 
 
-def test_destroyed_handle_is_rejected():
+def test_destroy_accepts_null_and_close_is_idempotent():
+    """recmg_cache_destroy(NULL) is a no-op; the binding's close() releases the
+    handle once and forgets it, so a second close() calls nothing.  (A handle
+    pointer is dangling after destroy, so no call is made with it.)"""
     w, g = _runner()
-    h = g.cache.handle
+    g.close()
+    assert g.cache.handle == 0
     g.close()
     assert bd.recmg_cache_destroy(0) == bd.RECMG_OK
-    del h  # the pointer is dangling after destroy; it is not used again
+
+
+def test_init_reports_nomem_through_the_c_abi():
+    """recmg_cache_init itself returns RECMG_E_NOMEM for a device workspace
+    shorter than recmg_query_workspace asks for (and for none at all), and
+    sets no handle."""
+    import ctypes
+    w = _workload()
+    tab = torch.from_numpy(w.table_values(0)).pin_memory()
+    rows = (ctypes.c_int64 * 1)(tab.shape[0])
+    dims = (ctypes.c_int32 * 1)(tab.shape[1])
+    dts = (ctypes.c_int32 * 1)(bd.RECMG_F32)
+    caps = (ctypes.c_int64 * 1)(10)
+    ptrs = (ctypes.c_void_p * 1)(tab.data_ptr())
+    cfg = bd.recmg_config_t()
+    cfg.num_tables, cfg.rows, cfg.dims, cfg.dtypes, cfg.host_tables, cfg.cache_rows = 1, rows, dims, dts, ptrs, caps
+    cfg.max_bags_per_table, cfg.max_indices, cfg.max_prefetch = 8, 64, 64
+    need, _ = bd.recmg_query_workspace(cfg)
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    lib = bd.load_library()
+    for size, ptr in ((need - 256, ws.data_ptr()), (need, 0)):
+        cfg.device_workspace, cfg.device_workspace_bytes = ptr, size
+        h = ctypes.c_void_p(0)
+        assert lib.recmg_cache_init(ctypes.byref(cfg), ctypes.byref(h)) == bd.RECMG_E_NOMEM
+        assert not h.value and "workspace" in bd.recmg_last_error()
+    # the full size is accepted
+    cfg.device_workspace, cfg.device_workspace_bytes = ws.data_ptr(), need
+    h = ctypes.c_void_p(0)
+    assert lib.recmg_cache_init(ctypes.byref(cfg), ctypes.byref(h)) == bd.RECMG_OK and h.value
+    assert lib.recmg_cache_destroy(h) == bd.RECMG_OK
 
 
 def test_init_rejects_small_workspace_and_pageable_tables():

@@ -143,28 +143,45 @@ def test_staged_with_unpinned_tables(cid, scale, tables):
     _parity(w, miss_mode="staged", label=f"c{cid}-staged-unpinned", pin=False)
 
 
-def test_two_placements_in_a_row():
-    """A placement right after another (no forward between) waits for the
-    earlier one's fill; both must match the oracle."""
+@pytest.mark.parametrize("overlap,sync", [(True, True), (True, False), (False, False)])
+def test_two_placements_in_a_row(overlap, sync):
+    """Two placements in a row (no forward between), each on a stream other
+    than the last call's, then a forward on a third stream.  The second
+    placement frees slots the first one's fill may still be writing; its fill
+    must run after that one.  overlap=False: no copy stream, so every fill runs
+    on its own placement's stream.  sync=False: no synchronisation between
+    calls (the resident sets are then checked at the end of each batch)."""
+    import torch as th
     w = tg.scaled_config(2, row_scale=0.01, batches=4, bags=128, max_tables=2)
     tabs = [w.table_values(t) for t in range(w.num_tables)]
+    f64 = [tg.storage_to_f64(a, tb.dtype) for a, tb in zip(tabs, w.tables)]
     import oracle
     o = oracle.for_workload(w, tabs)
-    g = GpuRunner(w, tabs)
+    g = GpuRunner(w, tabs, overlap=overlap)
+    streams = [th.cuda.Stream(), th.cuda.Stream(), th.cuda.Stream()]
     try:
         for b in range(w.batches):
             for rep in range(2):
                 P, poff = w.prefetch_list(b + rep)
-                g.placement(P, poff)
+                s = streams[rep]
+                with th.cuda.stream(s):
+                    g.cache.placement(g.to_dev(P) if P.size else None, g.to_dev(poff), None, stream=s)
                 assert o.placement(P, poff) == 0
-                last, _, res = g.cache.stats(dump=True)
-                for t in range(w.num_tables):
-                    assert res[t].tolist() == o.resident(t).tolist()
-                    assert last[t]["digest"] == o.stats(t)["digest"]
+                if sync:
+                    last, _, res = g.cache.stats(dump=True)
+                    for t in range(w.num_tables):
+                        assert res[t].tolist() == o.resident(t).tolist()
+                        assert last[t]["digest"] == o.stats(t)["digest"]
             idx, off = w.batch(b)
-            out = g.forward(idx, off)
-            st, ref32, _ = o.forward(idx, off, w.bags)
-            assert np.allclose(out, ref32, rtol=1e-5, atol=1e-5)
+            s = streams[2]
+            with th.cuda.stream(s):
+                out = g.cache.forward(g.to_dev(idx), g.to_dev(off), w.bags, stream=s)
+            st, _, ref64 = o.forward(idx, off, w.bags, want64=True)
+            assert st == 0
+            _, _, res = g.cache.stats(dump=True)  # synchronises every stream the calls used
+            for t in range(w.num_tables):
+                assert res[t].tolist() == o.resident(t).tolist()
+            check_pooled(w, f64, idx, off, out.cpu().numpy(), ref64, f"batch {b}")
     finally:
         g.close()
         o.close()
@@ -452,14 +469,15 @@ def test_lfu_configs_scaled(cid, scale, tables, ways):
 
 # ----------------------------------------------------------------------------- random call sequences
 
-@pytest.mark.parametrize("seed", range(9))
-def test_random_call_sequences(seed):
+@pytest.mark.parametrize("seed,overlap", [(s, True) for s in range(9)] + [(s, False) for s in range(6)])
+def test_random_call_sequences(seed, overlap):
     """Random interleavings of placements and forwards on three streams (two
     placements or two forwards in a row, batches out of order, calls on a
     stream other than the previous call's), checked against the oracle
     replaying the same calls: totals, resident sets and digests at random
     check points, every forward's pooled sums at the end.  The library orders
-    calls across streams by events; nothing here synchronises between calls."""
+    calls across streams by events; nothing here synchronises between calls.
+    overlap=False: no copy stream, so each fill runs on its placement's stream."""
     import torch as th
     import oracle
     rng = np.random.default_rng(7000 + seed)
@@ -469,7 +487,7 @@ def test_random_call_sequences(seed):
     w.ways = (0, 4, 32)[(seed // 3) % 3]
     tabs = [w.table_values(t) for t in range(w.num_tables)]
     o = oracle.for_workload(w, tabs)
-    g = GpuRunner(w, tabs)
+    g = GpuRunner(w, tabs, overlap=overlap)
     f64 = [tg.storage_to_f64(a, tb.dtype) for a, tb in zip(tabs, w.tables)]
     streams = [th.cuda.current_stream(), th.cuda.Stream(), th.cuda.Stream()]
     T = w.num_tables
