@@ -229,6 +229,11 @@ def main():
     ap.add_argument("--ways", type=int, default=0,
                     help="W > 0: W-way set-associative caches (Alg. 2 inside each set) instead of fully "
                          "associative ones")
+    ap.add_argument("--start-batch", type=int, default=0,
+                    help="play the trace from this batch on (with --warm-placements: a cache in steady state)")
+    ap.add_argument("--warm-placements", type=int, default=0, metavar="N",
+                    help="before the warmup steps, N placements with no forward between them whose prefetch lists "
+                         "name each table's Cap most popular rows, so the caches start full")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 3 device-to-device copies of MIB MiB (scale for HBM byte counters) and exit")
     args = ap.parse_args()
@@ -267,11 +272,11 @@ def main():
     w.ways = args.ways
     if args.policy is not None:
         w.policy = args.policy
-    W, K = args.warmup, args.steps
-    if W + K > w.batches:
-        raise SystemExit(f"warmup + steps must be at most the workload's {w.batches} batches")
+    W, K, S0, NW = args.warmup, args.steps, args.start_batch, args.warm_placements
+    if S0 < 0 or NW < 0 or S0 + W + K > w.batches:
+        raise SystemExit(f"start + warmup + steps must be at most the workload's {w.batches} batches")
     # after the timed steps, a few more with every stage timed (the breakdown)
-    KB = min(args.breakdown_steps, w.batches - W - K)
+    KB = min(args.breakdown_steps, w.batches - S0 - W - K)
     nb = W + K + KB
     if args.bits == "optgen":
         w.bits = ("optgen", 0.8, nb + 1)  # labels over the batches this run plays
@@ -292,20 +297,24 @@ def main():
 
     # -- traces, staged into HBM before timing ----------------------------------------------------
     t0 = time.time()
+    # step b plays batch S0 + b; the caching bits of its placement come from
+    # the batch before it, if this run played that batch
     batches, prefetch, bits = [], [], []
     for b in range(nb):
-        idx, off = w.batch(b)
-        P, poff = w.prefetch_list(b)
-        cb = w.cache_bits(b - 1) if b > 0 else None
+        idx, off = w.batch(S0 + b)
+        P, poff = w.prefetch_list(S0 + b)
+        cb = w.cache_bits(S0 + b - 1) if b > 0 else None
         batches.append((idx, off))
         prefetch.append((P, poff))
         bits.append(cb)
+    warm_lists = [w.warm_list(k, NW) for k in range(NW)]
+    d_warm = [(torch.from_numpy(P).to(dev), torch.from_numpy(po).to(dev)) for P, po in warm_lists]
     d_batches = [(torch.from_numpy(i).to(dev), torch.from_numpy(o).to(dev)) for i, o in batches]
     d_prefetch = [(torch.from_numpy(P).to(dev) if P.size else None, torch.from_numpy(po).to(dev))
                   for P, po in prefetch]
     d_bits = [None if cb is None else torch.from_numpy(cb).to(dev) for cb in bits]
     max_idx = max(i.size for i, _ in batches)
-    max_pf = max(max(P.size for P, _ in prefetch), 1)
+    max_pf = max(max(P.size for P, _ in prefetch + warm_lists), 1)
     # one output buffer per batch, so that every batch can be checked against the oracle afterwards
     outs = [torch.empty(w.bags * sum(tb.dim for tb in w.tables), dtype=torch.float32, device=dev) for _ in range(nb)]
     torch.cuda.synchronize()
@@ -314,7 +323,7 @@ def main():
     cache = TieredEmbeddingCache(host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables], policy=w.policy,
                                  eviction_speed=w.eviction_speed, miss_mode=args.miss_mode,
                                  max_bags_per_table=w.bags, max_indices=max_idx, max_prefetch=max_pf, timing=1,
-                                 ways=w.ways, stats_log_calls=2 * nb)
+                                 ways=w.ways, stats_log_calls=2 * nb + NW)
     log(f"cache ready: workspace {cache.workspace_bytes / 1e9:.2f} GB")
 
     # Pipelined placement: placements run on a stream of their own, so that
@@ -331,6 +340,13 @@ def main():
         i, o = d_batches[b]
         cache.forward(i, o, w.bags, out=outs[b])
 
+    if NW:
+        t0 = time.time()
+        for P, po in d_warm:
+            cache.placement(P, po, None, stream=pstream)
+        torch.cuda.synchronize()
+        log(f"{NW} warm-up placements in {time.time() - t0:.1f}s: "
+            f"{sum(r['resident'] for r in cache.stats()[0]):,} rows resident")
     for b in range(W):
         step(b)
     torch.cuda.synchronize()
@@ -449,7 +465,8 @@ def main():
         "data": "synthetic (seeded Zipf traces standing in for the paper's Meta embedding-lookup traces)",
         "config": {
             "workload": describe_workload(args.config, w),
-            "batches": f"{W} warmup + {K} timed, each placement + forward",
+            "batches": (f"{NW} warm-up placements filling the caches, then " if NW else "")
+                       + f"batches {S0}.. : {W} warmup + {K} timed, each placement + forward",
             "miss_mode": args.miss_mode,
             "pipelined_placement": bool(args.pipeline),
             "row_scale": args.row_scale,
@@ -561,8 +578,17 @@ def main():
         n_out = w.bags * sum(tb.dim for tb in w.tables)
         o32, o64 = np.zeros(max(n_out, 1), np.float32), np.zeros(max(n_out, 1), np.float64)
         rtol = {"f32": 1e-5, "f16": 2e-2, "bf16": 2e-2}
+        # the warm-up placements (untimed): calls 0 .. NW - 1 of the device log
+        for k, (P, poff) in enumerate(warm_lists):
+            assert o.placement(P, poff, None) == 0
+            for t in range(T):
+                st = o.stats(t)
+                for key in oracle.PLC_FIELDS:
+                    calls_equal &= call_log[k][t][key] == st[key]
+                    sums[t][key] += st[key]
+                digests_equal &= call_log[k][t]["digest"] == st["digest"]
         last_log = time.time()
-        for b in range(w.batches):
+        for b in range(w.batches - S0):
             if time.time() - last_log > 15:
                 log(f"oracle: batch {b}, {secs:.1f}s of oracle time")
                 last_log = time.time()
@@ -571,9 +597,9 @@ def main():
             elif secs > args.cpu_seconds:
                 break
             else:
-                P, poff = w.prefetch_list(b)
-                cb = w.cache_bits(b - 1)
-                idx, off = w.batch(b)
+                P, poff = w.prefetch_list(S0 + b)
+                cb = w.cache_bits(S0 + b - 1)
+                idx, off = w.batch(S0 + b)
             t_start = time.time()
             assert o.placement(P, poff, cb) == 0
             secs += time.time() - t_start
@@ -583,14 +609,14 @@ def main():
             secs += time.time() - t_start
             assert st == 0
             if b < nb:
-                # this batch's two calls against the device log: placement 2b, forward 2b + 1
+                # this batch's two calls against the device log: placement NW + 2b, forward NW + 2b + 1
                 for t in range(T):
                     fw = o.stats(t)
                     for k in oracle.PLC_FIELDS:
-                        calls_equal &= call_log[2 * b][t][k] == plc[t][k]
+                        calls_equal &= call_log[NW + 2 * b][t][k] == plc[t][k]
                     for k in oracle.FWD_FIELDS:
-                        calls_equal &= call_log[2 * b + 1][t][k] == fw[k]
-                    digests_equal &= call_log[2 * b][t]["digest"] == plc[t]["digest"]
+                        calls_equal &= call_log[NW + 2 * b + 1][t][k] == fw[k]
+                    digests_equal &= call_log[NW + 2 * b][t]["digest"] == plc[t]["digest"]
                 if b in gpu_out:
                     mass = o.pooled_abs(idx, off, w.bags)  # the tolerance scale, outside the timed intervals
                     err = np.abs(gpu_out[b].astype(np.float64) - r64)
@@ -626,7 +652,7 @@ def main():
             "unit": "lookups/s",
             "cores": nth,
             "kind": "oracle",
-            "sample": f"batches 0..{done - 1} of the same workload (placement + forward each; the first {min(done, nb)} "
+            "sample": f"batches {S0}..{S0 + done - 1} of the same workload (placement + forward each; the first {min(done, nb)} "
                       f"are the GPU run's), {secs:.1f}s of oracle time, {nth} threads (one per table, at most one per "
                       f"usable core)",
             "cpu_model": cpu_model,

@@ -7,8 +7,8 @@
  * summation) over a two-tier store.  Every table lives whole in pinned host
  * DRAM; a software-managed cache of rows lives in HBM (Sec. I, Sec. VI-B).
  * Residency is decided between batches from two caller-supplied inputs, the
- * per-access caching bits and the prefetch list (Sec. VI-B, VI-C), applied "at
- * the end of each batch" by Alg. 1 (load_embeddings) and Alg. 2
+ * per-access caching bits and the prefetch list (Sec. VI-B, VI-C), applied
+ * once each batch ends by Alg. 1 (load_embeddings) and Alg. 2
  * (gpu_buffer_populate).
  *
  * Cache semantics, per table t (fully associative, one cache per table;

@@ -31,7 +31,10 @@ def _say(msg):
     print(f"[fullsize] {msg}", file=sys.stderr, flush=True)
 
 
-def _run(cid, nb, miss_mode="zero_copy", ways=0, nsample=128):
+def _run(cid, nb, miss_mode="zero_copy", ways=0, nsample=128, start=0, warm=0):
+    """nb steps of configuration cid on batches start .. start + nb - 1, after
+    `warm` warm-up placements (no forward between them) that fill every cache
+    with its Cap most popular rows."""
     import oracle
     from paper_2511_08568_amd import TieredEmbeddingCache
     w = tg.make_config(cid)
@@ -43,9 +46,12 @@ def _run(cid, nb, miss_mode="zero_copy", ways=0, nsample=128):
     for t in range(w.num_tables):
         w.table_values(t, out=host[t].numpy())
     _say(f"config {cid}: tables ready in {time.time() - t0:.1f}s")
-    batches = [w.batch(b) for b in range(nb)]
-    pre = [w.prefetch_list(b) for b in range(nb)]
-    bits = [w.cache_bits(b - 1) if b > 0 else None for b in range(nb)]
+    batches = [w.batch(start + b) for b in range(nb)]
+    pre = [w.prefetch_list(start + b) for b in range(nb)]
+    bits = [w.cache_bits(start + b - 1) if b > 0 else None for b in range(nb)]
+    warm_lists = [w.warm_list(k, warm) for k in range(warm)]
+    _say(f"config {cid}: batches {start}..{start + nb - 1} and {warm} warm-up lists drawn")
+    d_warm = [(torch.from_numpy(P).to(dev), torch.from_numpy(po).to(dev)) for P, po in warm_lists]
     d_in = []
     for b in range(nb):
         (idx, off), (P, po) = batches[b], pre[b]
@@ -55,12 +61,14 @@ def _run(cid, nb, miss_mode="zero_copy", ways=0, nsample=128):
     cache = TieredEmbeddingCache(host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables], policy=w.policy,
                                  eviction_speed=w.eviction_speed, miss_mode=miss_mode, max_bags_per_table=w.bags,
                                  max_indices=max(i.size for i, _ in batches),
-                                 max_prefetch=max(max(P.size for P, _ in pre), 1), ways=ways,
-                                 stats_log_calls=2 * nb)
+                                 max_prefetch=max(max(P.size for P, _ in pre + warm_lists), 1), ways=ways,
+                                 stats_log_calls=2 * nb + warm)
     outs = [torch.empty(w.bags * sum(tb.dim for tb in w.tables), dtype=torch.float32, device=dev) for _ in range(nb)]
     pstream = torch.cuda.Stream(device=dev)
     torch.cuda.synchronize()
     try:
+        for P, po in d_warm:
+            cache.placement(P, po, None, stream=pstream)
         for b in range(nb):
             P, po, cb, idx, off = d_in[b]
             cache.placement(P, po, cb, stream=pstream)
@@ -69,29 +77,40 @@ def _run(cid, nb, miss_mode="zero_copy", ways=0, nsample=128):
         _, _, res = cache.stats(dump=True)
     finally:
         cache.close()
-    del cache, d_in
-    _say(f"config {cid}: {nb} steps on the GPU done")
+    del cache, d_in, d_warm
+    _say(f"config {cid}: {warm} warm-up placements and {nb} steps on the GPU done")
     host_np = [h.numpy() for h in host]
     nth = max(1, min(16, len(os.sched_getaffinity(0)), w.num_tables))
     o = oracle.for_workload(w, host_np, nthreads=nth)
+    evicted = 0
     try:
+        for k, (P, po) in enumerate(warm_lists):
+            assert o.placement(P, po, None) == 0
+            for t in range(w.num_tables):
+                st = o.stats(t)
+                for key in oracle.PLC_FIELDS + ("digest",):
+                    assert log[k][t][key] == st[key], f"config {cid} warm-up placement {k} table {t} {key}"
+            _say(f"config {cid}: warm-up placement {k} equal")
         for b in range(nb):
             (idx, off), (P, po) = batches[b], pre[b]
             assert o.placement(P, po, bits[b]) == 0
             for t in range(w.num_tables):
                 st = o.stats(t)
+                evicted += st["evicted"]
                 for k in oracle.PLC_FIELDS + ("digest",):
-                    assert log[2 * b][t][k] == st[k], f"config {cid} placement {b} table {t} {k}"
+                    assert log[warm + 2 * b][t][k] == st[k], f"config {cid} placement {start + b} table {t} {k}"
             assert o.forward(idx, off, w.bags)[0] == 0
             for t in range(w.num_tables):
                 st = o.stats(t)
                 for k in oracle.FWD_FIELDS:
-                    assert log[2 * b + 1][t][k] == st[k], f"config {cid} forward {b} table {t} {k}"
+                    assert log[warm + 2 * b + 1][t][k] == st[k], f"config {cid} forward {start + b} table {t} {k}"
+            if warm:
+                _say(f"config {cid}: batch {start + b} equal")
         for t in range(w.num_tables):
             assert np.array_equal(res[t], o.resident(t)), f"config {cid} table {t}: final resident set"
     finally:
         o.close()
-    _say(f"config {cid}: counters and resident sets equal the oracle's")
+    _say(f"config {cid}: counters and resident sets equal the oracle's ({evicted} evictions)")
     # sampled bags of the first and last batch, each summed in fp64 on the host
     rng = np.random.default_rng(1000 + cid)
     for b in sorted({0, nb - 1}):
@@ -108,6 +127,7 @@ def _run(cid, nb, miss_mode="zero_copy", ways=0, nsample=128):
                 assert np.all(np.abs(g - ref) <= RTOL[tb.dtype] * mass), f"config {cid} batch {b} table {t} bag {j}"
             base += w.bags * tb.dim
     _say(f"config {cid}: sampled pooled sums within tolerance")
+    return evicted
 
 
 def _release():
@@ -143,6 +163,17 @@ def test_config3_fullsize():
 def test_config4_fullsize_staged():
     """4 x 1e8 x 128 bf16 (102 GB, pageable), 20 GB cache, 16,384 bags of 80: 3 steps."""
     _run(4, 3, miss_mode="staged", nsample=64)
+
+
+def test_config4_fullsize_steady_state():
+    """Configuration 4 with its 20 GB cache full: five warm-up placements name
+    each table's 19,531,250 most popular rows (78.1M resident keys), then
+    batches 46-55 with exact prefetch cross the drift at batch 50 (10% of the
+    lookups move to a new hot set).  Every placement evicts and ranks over the
+    full caches; every call's counters and digests, the final resident sets
+    and sampled pooled sums are checked against the oracle."""
+    evicted = _run(4, 10, miss_mode="staged", nsample=32, start=46, warm=5)
+    assert evicted > 0
 
 
 def test_config5_fullsize_staged():

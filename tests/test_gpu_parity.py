@@ -125,6 +125,52 @@ def test_optgen_caching_bits(cid, scale, tables):
     _parity(w, label=f"c{cid}-optgen")
 
 
+@pytest.mark.parametrize("prefetch", ["exact", "none"])
+def test_config4_scaled_steady_state_across_drift(prefetch):
+    """Scaled configuration 4 (2 tables of 50,000 rows, cache 9,766 each)
+    started full by three warm-up placements, then batches 46-55, across the
+    drift at batch 50: every call against the oracle, with evictions in every
+    placement once the cache is full."""
+    import oracle
+    w = tg.scaled_config(4, row_scale=0.0005, batches=200, bags=512, max_tables=2, prefetch=(prefetch,))
+    tabs = [w.table_values(t) for t in range(w.num_tables)]
+    f64 = [tg.storage_to_f64(a, tb.dtype) for a, tb in zip(tabs, w.tables)]
+    o = oracle.for_workload(w, tabs)
+    warm = [w.warm_list(k, 3) for k in range(3)]
+    maxp = max(max(P.size for P, _ in warm), max(w.prefetch_list(b)[0].size for b in range(46, 56)), 1)
+    g = GpuRunner(w, tabs, max_indices=max(w.batch(b)[0].size for b in range(46, 56)), max_prefetch=maxp)
+    evicted = 0
+    try:
+        for P, po in warm:
+            g.placement(P, po)
+            assert o.placement(P, po) == 0
+        last, _ = g.cache.stats()
+        assert all(last[t]["resident"] == w.tables[t].cap for t in range(w.num_tables))
+        for b in range(46, 56):
+            P, po = w.prefetch_list(b)
+            g.placement(P, po)
+            assert o.placement(P, po) == 0
+            last, _, res = g.cache.stats(dump=True)
+            for t in range(w.num_tables):
+                for k in ("evicted", "admitted_miss", "prefetch_fill", "prefetch_resident", "prefetch_dropped",
+                          "miss_dropped", "resident", "prefetch_distinct", "digest"):
+                    assert last[t][k] == o.stats(t)[k], f"batch {b} table {t} placement {k}"
+                assert np.array_equal(res[t], o.resident(t))
+                evicted += last[t]["evicted"]
+            idx, off = w.batch(b)
+            out = g.forward(idx, off)
+            st, _, r64 = o.forward(idx, off, w.bags, want64=True)
+            last, _ = g.cache.stats()
+            for t in range(w.num_tables):
+                for k in ("lookups", "unique", "hits", "hits_prefetch", "misses", "prefetch_covered"):
+                    assert last[t][k] == o.stats(t)[k], f"batch {b} table {t} forward {k}"
+            check_pooled(w, f64, idx, off, out, r64, f"batch {b}")
+    finally:
+        g.close()
+        o.close()
+    assert evicted > 0
+
+
 def test_config4_no_prefetch_scaled():
     w = tg.scaled_config(4, row_scale=0.0005, batches=6, bags=512, max_tables=2, prefetch=("none",))
     _parity(w, label="c4-noprefetch")

@@ -181,3 +181,18 @@ def test_configuration_shapes():
     assert [t.dim for t in w.tables[:8]] == [32, 64, 128, 256] * 2
     assert all((t.rows, t.dtype, t.cap) == (2_000_000, "f32", 200_000) for t in w.tables)
     assert (w.bags, w.batches, w.policy) == (8192, 300, "priority")
+
+
+@pytest.mark.parametrize("n", [1, 3, 7])
+def test_warm_lists_name_the_cap_most_popular_rows(n):
+    """The n warm-up lists together hold each table's Cap rows of lowest Zipf
+    rank (the permutation's images of ranks 0..Cap-1), each exactly once, and
+    the last list holds the most popular row."""
+    w = tg.scaled_config(5, row_scale=0.005, batches=2, bags=16, max_tables=3)
+    lists = [w.warm_list(k, n) for k in range(n)]
+    for t, tb in enumerate(w.tables):
+        got = np.concatenate([P[o[t]:o[t + 1]] for P, o in lists])
+        want = np.sort(w._perm(t)(np.arange(tb.cap)))
+        assert got.size == tb.cap and np.array_equal(np.sort(got), want)
+        P, o = lists[-1]
+        assert int(w._perm(t)(np.zeros(1, np.int64))[0]) in P[o[t]:o[t + 1]]

@@ -383,6 +383,25 @@ class Workload:
         rows = np.concatenate(parts).astype(np.int32) if parts else np.zeros(0, np.int32)
         return rows, offs
 
+    def warm_list(self, k: int, n: int) -> Tuple[np.ndarray, np.ndarray]:
+        """Prefetch list of warm-up placement k of n (placements with no
+        forward between them, played before a run that starts in the middle
+        of the trace): per table, the rows of Zipf ranks in chunk n-1-k of
+        [0, Cap), chunks of ceil(Cap / n) ranks, mapped through the table's
+        permutation.  Together the n lists name each table's Cap most popular
+        rows once, the most popular chunk last, so the caches start full."""
+        T = self.num_tables
+        parts = []
+        for t in range(T):
+            cap = self.tables[t].cap
+            step = -(-cap // n) if n > 0 else 0
+            j = n - 1 - k
+            lo, hi = min(cap, j * step), min(cap, (j + 1) * step)
+            parts.append(self._perm(t)(np.arange(lo, hi, dtype=np.int64)).astype(np.int32))
+        offs = np.zeros(T + 1, dtype=np.int64)
+        offs[1:] = np.cumsum([p.size for p in parts])
+        return np.concatenate(parts).astype(np.int32), offs
+
     # -- caching bits ----------------------------------------------------------------
     def cache_bits(self, b: int) -> Optional[np.ndarray]:
         """One byte per access of batch b: the stand-in for the caching model's
