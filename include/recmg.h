@@ -187,6 +187,23 @@ int32_t recmg_query_workspace(const recmg_config_t *cfg, size_t *device_bytes, s
  * (synchronously).  The cache starts empty.  *out is set only on success. */
 int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): as
+ * recmg_cache_init, but the workspace is a fixed 32 MiB array inside the
+ * library, one per device (held from the library's first use of it on that
+ * device until the process ends); cfg->device_workspace and
+ * device_workspace_bytes are ignored.  Nothing is allocated on the device.
+ * The host staging buffer (STAGED) still comes from the caller.
+ *   RECMG_E_NOMEM   the configuration's workspace (recmg_query_workspace) is
+ *                   larger than 32 MiB;
+ *   RECMG_E_STATE   another live handle of this device holds the array (at
+ *                   most one at a time; recmg_cache_destroy releases it).
+ * The array keeps what the last handle left in it; init clears everything a
+ * handle reads before writing it.  All calls on the handle use the array, so
+ * calls that overlap on one device race only as calls on one handle would
+ * (they are ordered by the handle's events). */
+int32_t recmg_cache_init_static(const recmg_config_t *cfg, recmg_cache_t **out);
+
 /* Placement before the next forward (Alg. 1 + Alg. 2, batched: one ranking
  * per placement).
  *   prefetch_rows     device int32 [num_prefetch], table-major, may repeat ids;

@@ -14,6 +14,7 @@ from .binding import (  # noqa: F401
     recmg_apply_placement,
     recmg_cache_destroy,
     recmg_cache_init,
+    recmg_cache_init_static,
     recmg_config_t,
     recmg_embbag_forward,
     recmg_last_error,

@@ -29,7 +29,8 @@ STAT_FIELDS = ("lookups", "unique", "hits", "hits_prefetch", "misses", "ondemand
                "evicted", "admitted_miss", "prefetch_fill", "prefetch_resident", "prefetch_dropped", "miss_dropped",
                "resident", "prefetch_bytes", "prefetch_distinct")
 
-EXPORTED = ("recmg_query_workspace", "recmg_cache_init", "recmg_apply_placement", "recmg_embbag_forward",
+EXPORTED = ("recmg_query_workspace", "recmg_cache_init", "recmg_cache_init_static", "recmg_apply_placement",
+            "recmg_embbag_forward",
             "recmg_stats", "recmg_stats_log", "recmg_stage_times", "recmg_set_timing", "recmg_cache_destroy",
             "recmg_last_error")
 STAGES = ("fwd_dedup", "fwd_fetch", "fwd_pool", "plc_classify", "plc_rank", "plc_apply", "plc_fill", "host_link")
@@ -87,6 +88,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.recmg_query_workspace.argtypes = [ctypes.POINTER(recmg_config_t), ctypes.POINTER(ctypes.c_size_t),
                                           ctypes.POINTER(ctypes.c_size_t)]
     lib.recmg_cache_init.argtypes = [ctypes.POINTER(recmg_config_t), ctypes.POINTER(P)]
+    lib.recmg_cache_init_static.argtypes = [ctypes.POINTER(recmg_config_t), ctypes.POINTER(P)]
     lib.recmg_apply_placement.argtypes = [P, P, P, ctypes.c_int64, P, P]
     lib.recmg_embbag_forward.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32, P, P]
     lib.recmg_stats.argtypes = [P, ctypes.POINTER(recmg_table_stats_t), ctypes.POINTER(recmg_table_stats_t), P,
@@ -122,6 +124,12 @@ def recmg_query_workspace(cfg: recmg_config_t):
 def recmg_cache_init(cfg: recmg_config_t) -> int:
     h = ctypes.c_void_p(0)
     _check(load_library().recmg_cache_init(ctypes.byref(cfg), ctypes.byref(h)), "recmg_cache_init")
+    return int(h.value)
+
+
+def recmg_cache_init_static(cfg: recmg_config_t) -> int:
+    h = ctypes.c_void_p(0)
+    _check(load_library().recmg_cache_init_static(ctypes.byref(cfg), ctypes.byref(h)), "recmg_cache_init_static")
     return int(h.value)
 
 
@@ -178,7 +186,7 @@ class TieredEmbeddingCache:
                  policy: str = "lru", eviction_speed: int = 4, miss_mode: str = "zero_copy",
                  max_bags_per_table: int, max_indices: int, max_prefetch: int, validate: bool = False,
                  timing: int = 0, overlap: bool = True, workspace=None, device: int = 0, ways: int = 0,
-                 stats_log_calls: int = 0):
+                 stats_log_calls: int = 0, static_workspace: bool = False):
         import torch
         self.torch = torch
         self.device = torch.device("cuda", device)
@@ -212,7 +220,9 @@ class TieredEmbeddingCache:
         cfg.max_prefetch = int(max_prefetch)
         dev_bytes, host_bytes = recmg_query_workspace(cfg)
         with torch.cuda.device(self.device):
-            if workspace is not None:  # caller-provided device memory (any contents)
+            if static_workspace:  # the library's own fixed array (recmg_cache_init_static)
+                self.workspace = None
+            elif workspace is not None:  # caller-provided device memory (any contents)
                 if workspace.numel() * workspace.element_size() < dev_bytes or not workspace.is_cuda:
                     raise ValueError(f"workspace must be a device tensor of >= {dev_bytes} bytes")
                 self.workspace = workspace
@@ -221,8 +231,9 @@ class TieredEmbeddingCache:
             # side stream: staged miss copies and prefetch fills (which then overlap the next forward's dedup)
             self.copy_stream = torch.cuda.Stream(device=self.device) if (overlap or miss_mode == "staged") else None
         self.staging = torch.empty(host_bytes, dtype=torch.uint8, pin_memory=True) if host_bytes else None
-        cfg.device_workspace = self.workspace.data_ptr()
-        cfg.device_workspace_bytes = dev_bytes
+        if self.workspace is not None:
+            cfg.device_workspace = self.workspace.data_ptr()
+            cfg.device_workspace_bytes = dev_bytes
         if self.staging is not None:
             cfg.host_staging = self.staging.data_ptr()
             cfg.host_staging_bytes = host_bytes
@@ -231,7 +242,7 @@ class TieredEmbeddingCache:
         self.cfg = cfg
         self.workspace_bytes = dev_bytes
         with torch.cuda.device(self.device):
-            self.handle = recmg_cache_init(cfg)
+            self.handle = recmg_cache_init_static(cfg) if static_workspace else recmg_cache_init(cfg)
 
     def placement(self, prefetch_rows, prefetch_offsets, cache_bits=None, stream=None):
         """prefetch_rows: cuda int32 [P]; prefetch_offsets: cuda int64 [T+1];

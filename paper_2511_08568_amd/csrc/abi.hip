@@ -6,6 +6,7 @@
 #include <cstddef>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <string>
 #include <thread>
 #include <vector>
@@ -265,6 +266,7 @@ struct recmg_cache {
     // An error after a call began enqueuing work leaves device and host state
     // out of step: every later call but destroy is refused.
     bool broken = false;
+    bool static_ws = false;  // the workspace is the device's static array (recmg_cache_init_static)
     int32_t *fill_src_buf[2] = {nullptr, nullptr}, *fill_slot_buf[2] = {nullptr, nullptr};
     int64_t *fdesc_buf[2] = {nullptr, nullptr};
     int32_t pool_B = -1;
@@ -611,6 +613,21 @@ int32_t host_check_ids(const int32_t *dev_ids, const int64_t *dev_off, int64_t n
     return RECMG_OK;
 }
 
+// Workspace of the handles recmg_cache_init_static makes, for callers that
+// cannot allocate device memory: a fixed array in the library's code object,
+// one copy per device, held until the process ends.  Host code never uses the
+// array's name as an address (it is a host-side stand-in there): the device
+// address comes from hipGetSymbolAddress, once per device.
+constexpr size_t kStaticWorkspaceBytes = size_t(32) << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticWorkspaceBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_static_mu;
+void *g_static_ptr[kMaxDevices];              // device address of `scratch` per device, set on first use
+recmg_cache_t *g_static_owner[kMaxDevices];   // the live handle that holds it, if any
+
+int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out);
+
 }  // namespace
 
 extern "C" {
@@ -628,7 +645,46 @@ int32_t recmg_query_workspace(const recmg_config_t *cfg, size_t *device_bytes, s
     return RECMG_OK;
 }
 
-int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
+int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) { return cache_init(cfg, out); }
+
+int32_t recmg_cache_init_static(const recmg_config_t *cfg, recmg_cache_t **out) {
+    if (!out) return fail(RECMG_E_INVALID, "out is NULL");
+    std::vector<Geom> geo;
+    int32_t rc = check_config(cfg, &geo);
+    if (rc) return rc;
+    Layout L;
+    make_layout(cfg, geo, &L);
+    if (L.total > kStaticWorkspaceBytes)
+        return fail(RECMG_E_NOMEM, "the configuration needs a " + std::to_string(L.total) +
+                                       "-byte workspace; the static workspace holds " +
+                                       std::to_string(kStaticWorkspaceBytes) + " bytes");
+    int dev = -1;
+    HIP_TRY(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return fail(RECMG_E_INVALID, "device id beyond the static workspace table");
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    if (g_static_owner[dev]) return fail(RECMG_E_STATE, "the static workspace of this device is held by a live handle");
+    if (!g_static_ptr[dev]) {
+        void *p = nullptr;
+        HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return fail(RECMG_E_HIP, "hipGetSymbolAddress gave no address for the static workspace");
+        g_static_ptr[dev] = p;
+    }
+    recmg_config_t c2 = *cfg;
+    c2.device_workspace = g_static_ptr[dev];
+    c2.device_workspace_bytes = kStaticWorkspaceBytes;
+    recmg_cache_t *h = nullptr;
+    if ((rc = cache_init(&c2, &h))) return rc;
+    h->static_ws = true;
+    g_static_owner[dev] = h;
+    *out = h;
+    return RECMG_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     if (!out) return fail(RECMG_E_INVALID, "out is NULL");
     std::vector<Geom> geo;
     int32_t rc = check_config(cfg, &geo);
@@ -826,6 +882,10 @@ int32_t recmg_cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g_last_error.clear();
     return RECMG_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, const int64_t *prefetch_offsets,
                               int64_t num_prefetch, const uint8_t *cache_bits, void *stream) {
@@ -1174,6 +1234,10 @@ int32_t recmg_cache_destroy(recmg_cache_t *c) {
     int32_t rc = RECMG_OK;
     if (sync_all(c) != hipSuccess) rc = fail(RECMG_E_HIP, "synchronize failed at destroy");
     c->magic = 0;
+    if (c->static_ws) {
+        std::lock_guard<std::mutex> lock(g_static_mu);
+        if (g_static_owner[c->device] == c) g_static_owner[c->device] = nullptr;
+    }
     delete c;  // destroys the handle's events
     return rc;
 }
