@@ -52,7 +52,7 @@ def measured_traffic(args, kernel):
     """(bytes per launch, source) of `kernel` when the committed counter record
     matches this workload and the current kernel sources, else (None, reason)."""
     default = (args.row_scale == 1.0 and args.prefetch is None and args.miss_mode == "zero_copy" and args.ways == 0
-               and args.bits is None and args.policy is None)
+               and args.bits is None and args.policy is None and args.start_batch == 0 and args.warm_placements == 0)
     if not default:
         return None, "counters recorded for the configurations' own settings only"
     path = TRAFFIC_RECORD.format(args.config)
@@ -207,6 +207,9 @@ def main():
     ap.add_argument("--config", type=int, default=DEFAULT_CONFIG, help="configuration id (1..5)")
     ap.add_argument("--row-scale", type=float, default=1.0, help="<1 shrinks rows and caches (debug only)")
     ap.add_argument("--miss-mode", default="zero_copy", choices=["zero_copy", "staged"])
+    ap.add_argument("--zero-copy-tables", type=int, default=0, metavar="N",
+                    help="with --miss-mode staged: the first N tables pinned and read zero-copy, the rest "
+                         "gathered on the host (for tables that do not all fit the host's pinned-memory limit)")
     ap.add_argument("--prefetch", default=None, choices=["none", "exact"],
                     help="override the configuration's prefetch recipe (configuration 4 is run both ways)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="time budget of the CPU oracle sample")
@@ -285,15 +288,16 @@ def main():
     # -- tables in pinned host memory -------------------------------------------------------------
     t0 = time.time()
     tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.uint16}
-    pin = args.miss_mode == "zero_copy"  # staged mode reads the tables on the host only
-    if pin:
-        host = [torch.empty((tb.rows, tb.dim), dtype=tdt[tb.dtype], pin_memory=True) for tb in w.tables]
-    else:
-        host = [huge_page_tensor((tb.rows, tb.dim), tdt[tb.dtype]) for tb in w.tables]
+    # zero-copy tables are pinned (the GPU reads them); STAGED tables are read
+    # on the host only and stay pageable
+    modes = ["zero_copy" if args.miss_mode == "zero_copy" or t < args.zero_copy_tables else "staged"
+             for t in range(T)]
+    host = [torch.empty((tb.rows, tb.dim), dtype=tdt[tb.dtype], pin_memory=True) if m == "zero_copy"
+            else huge_page_tensor((tb.rows, tb.dim), tdt[tb.dtype]) for tb, m in zip(w.tables, modes)]
     for t in range(T):  # each table's rows are drawn in parallel chunks
         w.table_values(t, out=host[t].numpy())
-    log(f"tables ready ({sum(h.numel() * h.element_size() for h in host) / 1e9:.2f} GB, pinned={pin}) "
-        f"in {time.time() - t0:.1f}s")
+    log(f"tables ready ({sum(h.numel() * h.element_size() for h in host) / 1e9:.2f} GB, "
+        f"{modes.count('zero_copy')} of {T} pinned) in {time.time() - t0:.1f}s")
 
     # -- traces, staged into HBM before timing ----------------------------------------------------
     t0 = time.time()
@@ -321,7 +325,7 @@ def main():
     log(f"{nb} batches staged in {time.time() - t0:.1f}s (max {max_idx} indices)")
 
     cache = TieredEmbeddingCache(host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables], policy=w.policy,
-                                 eviction_speed=w.eviction_speed, miss_mode=args.miss_mode,
+                                 eviction_speed=w.eviction_speed, miss_mode=modes,
                                  max_bags_per_table=w.bags, max_indices=max_idx, max_prefetch=max_pf, timing=1,
                                  ways=w.ways, stats_log_calls=2 * nb + NW)
     log(f"cache ready: workspace {cache.workspace_bytes / 1e9:.2f} GB")
@@ -424,7 +428,7 @@ def main():
     union_ms = timed_stages["host_link"][0]
     host_bytes = {"k_plc_fill": delta["prefetch_bytes"], "k_fetch": delta["ondemand_bytes"]}
     link_times = {"k_plc_fill": (fill_ms, fill_calls), "k_fetch": (fetch_ms, fetch_calls)}
-    zero_copy = args.miss_mode == "zero_copy"
+    zero_copy = all(m == "zero_copy" for m in modes)
     # host link over the breakdown steps: bytes moved there / the union of the
     # miss-fetch and fill intervals (they overlap on two streams)
     bdelta = {k: sum(tot2[t][k] - tot1[t][k] for t in range(T)) for k in tot2[0] if k != "digest"}
@@ -467,7 +471,8 @@ def main():
             "workload": describe_workload(args.config, w),
             "batches": (f"{NW} warm-up placements filling the caches, then " if NW else "")
                        + f"batches {S0}.. : {W} warmup + {K} timed, each placement + forward",
-            "miss_mode": args.miss_mode,
+            "miss_mode": args.miss_mode if len(set(modes)) == 1 else
+                         f"mixed: tables 0..{args.zero_copy_tables - 1} zero_copy, the rest staged",
             "pipelined_placement": bool(args.pipeline),
             "row_scale": args.row_scale,
         },

@@ -129,6 +129,11 @@ typedef struct {
                                            set-associative caches (see below) */
     int32_t stats_log_calls;            /* >= 0: the counters of the latest this many calls
                                            are kept on the device (recmg_stats_log) */
+    const int32_t *miss_modes;          /* NULL: every table in miss_mode.  Else per table
+                                           (recmg_miss_mode_t): ZERO_COPY tables must be pinned
+                                           and are read by the GPU, STAGED tables are gathered on
+                                           the host (e.g. pin the tables the host allows and
+                                           leave the rest pageable); the two run side by side */
 } recmg_config_t;
 
 /* Stages timed at timing level 2 (at level 1: the kernels named in

@@ -59,6 +59,7 @@ class recmg_config_t(ctypes.Structure):
         ("timing", ctypes.c_int32),
         ("ways", ctypes.c_int32),
         ("stats_log_calls", ctypes.c_int32),
+        ("miss_modes", ctypes.POINTER(ctypes.c_int32)),
     ]
 
 
@@ -180,7 +181,8 @@ class TieredEmbeddingCache:
     host_tables: CPU tensors [rows, dim], float32 / float16 / bfloat16 (or
     uint16 holding bfloat16 bits), pinned for miss_mode="zero_copy".  They must
     outlive the cache.  ways = 0: fully associative caches; W in 1..64: W-way
-    set-associative caches (Alg. 2 inside each set)."""
+    set-associative caches (Alg. 2 inside each set).  miss_mode: one mode for
+    every table, or a list with one per table ("zero_copy" tables pinned)."""
 
     def __init__(self, host_tables: Sequence, dtypes: Sequence[str], cache_rows: Sequence[int], *,
                  policy: str = "lru", eviction_speed: int = 4, miss_mode: str = "zero_copy",
@@ -191,8 +193,11 @@ class TieredEmbeddingCache:
         self.torch = torch
         self.device = torch.device("cuda", device)
         self.T = len(host_tables)
-        for t in host_tables:
-            if miss_mode == "zero_copy" and not t.is_pinned():
+        modes = [miss_mode] * self.T if isinstance(miss_mode, str) else list(miss_mode)
+        if len(modes) != self.T:
+            raise ValueError("miss_mode: one mode, or one per table")
+        for t, m in zip(host_tables, modes):
+            if m == "zero_copy" and not t.is_pinned():
                 raise ValueError("zero_copy needs pinned host tables (pin_memory=True); staged takes any")
         self._host = list(host_tables)
         self.dims = [int(t.shape[1]) for t in host_tables]
@@ -210,7 +215,9 @@ class TieredEmbeddingCache:
         cfg.cache_rows = self._caps
         cfg.policy = POLICY_CODES[policy]
         cfg.eviction_speed = int(eviction_speed)
-        cfg.miss_mode = MISS_CODES[miss_mode]
+        cfg.miss_mode = MISS_CODES[modes[0]]
+        self._modes = (ctypes.c_int32 * self.T)(*[MISS_CODES[m] for m in modes])
+        cfg.miss_modes = self._modes
         cfg.validate = int(bool(validate))
         cfg.timing = 2 if timing is True else int(timing)  # 0 off, 1 pooled kernel, 2 every stage
         cfg.ways = int(ways)  # 0 fully associative, W > 0 W-way set-associative
@@ -229,7 +236,7 @@ class TieredEmbeddingCache:
             else:
                 self.workspace = torch.empty(dev_bytes, dtype=torch.uint8, device=self.device)
             # side stream: staged miss copies and prefetch fills (which then overlap the next forward's dedup)
-            self.copy_stream = torch.cuda.Stream(device=self.device) if (overlap or miss_mode == "staged") else None
+            self.copy_stream = torch.cuda.Stream(device=self.device) if (overlap or "staged" in modes) else None
         self.staging = torch.empty(host_bytes, dtype=torch.uint8, pin_memory=True) if host_bytes else None
         if self.workspace is not None:
             cfg.device_workspace = self.workspace.data_ptr()

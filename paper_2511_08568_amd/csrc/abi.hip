@@ -56,6 +56,7 @@ struct Geom {
     int32_t bm_nblk = 0, gsz = 0, nchunk = 0, vec = 0, bpb = 0, copy_unit = 0;
     int32_t wlw = 0, wr = 0, wnch = 0, kind = 0;
     int32_t ways = 0, nsets = 0, qbits = 0;  // set-associative form (ways > 0)
+    bool staged = false;                      // misses and fills gathered on the host
 };
 
 struct Layout {
@@ -103,6 +104,9 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
         if (g.dtype != RECMG_F32 && g.dtype != RECMG_F16 && g.dtype != RECMG_BF16) return fail(RECMG_E_INVALID, "bad dtype");
         if (cfg->cache_rows[t] < 0) return fail(RECMG_E_INVALID, "negative cache_rows");
         if (!cfg->host_tables[t]) return fail(RECMG_E_INVALID, "host table is NULL");
+        const int32_t mode = cfg->miss_modes ? cfg->miss_modes[t] : cfg->miss_mode;
+        if (mode != RECMG_ZERO_COPY && mode != RECMG_STAGED) return fail(RECMG_E_INVALID, "bad miss_modes entry");
+        g.staged = mode == RECMG_STAGED;
         g.esz = g.dtype == RECMG_F32 ? 4 : 2;
         g.row_bytes = g.dim * g.esz;
         g.cap = (int32_t)std::min<int64_t>(cfg->cache_rows[t], g.rows);
@@ -148,6 +152,12 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
     }
 
     return RECMG_OK;
+}
+
+bool any_staged(const std::vector<Geom> &geo) {
+    for (const Geom &g : geo)
+        if (g.staged) return true;
+    return false;
 }
 
 void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout *L) {
@@ -211,7 +221,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->sa_btab = take(4 * T);
     L->staging[0] = take(mi * (size_t)L->stage_stride);
     L->staging[1] = take(mi * (size_t)L->stage_stride);
-    const bool staged = cfg->miss_mode == RECMG_STAGED;
+    const bool staged = any_staged(geo);
     L->fstage = take(staged ? mp * (size_t)L->stage_stride : 0);
     L->total = off;
     if (staged) {
@@ -243,6 +253,7 @@ struct recmg_cache {
     int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1, nsa = 0;
     int64_t sa_blocks = 0;  // blocks of the set-associative placement kernel
     bool has_fa = false, has_sa = false;  // tables of each form present
+    bool has_zc = false, has_staged = false;  // tables of each miss mode present
     std::vector<int32_t> pool_order;  // table ids ordered by pooled-kernel kind
     std::vector<PoolLaunch> pool_launches;
     int64_t max_rows = 0;
@@ -495,7 +506,7 @@ int32_t staged_fill(recmg_cache_t *c, hipStream_t s, hipStream_t cs) {
     int64_t total = 0;
     for (int t = 0; t < T; ++t) {
         base[t] = c->h_ftstart[t] + c->h_pstart[t];
-        nfill[t] = c->h_st[t].popped;
+        nfill[t] = c->geo[t].staged ? c->h_st[t].popped : 0;  // zero-copy tables' fills read the host themselves
         if (base[t] < 0 || nfill[t] < 0 || base[t] + nfill[t] > c->g.fill_cap)
             return fail(RECMG_E_STATE, "fill list outside its buffer");
         if (nfill[t])
@@ -547,9 +558,11 @@ int32_t staged_fill(recmg_cache_t *c, hipStream_t s, hipStream_t cs) {
     return gather_and_copy(nfill, work, copy);
 }
 
-// STAGED miss path: miss ids to the host, a parallel host gather into pinned
-// staging overlapped with the copies on the copy stream; the compute stream
-// waits for the copies.
+// STAGED miss path: miss ids of the STAGED tables to the host, a parallel
+// host gather into pinned staging overlapped with the copies on the copy
+// stream; the compute stream waits for the copies.  The zero-copy tables'
+// misses are fetched by the kernel, launched once the host has read what it
+// needs (so that its waits do not wait for the kernel), beside the gather.
 int32_t staged_fetch(recmg_cache_t *c, hipStream_t s) {
     const int T = c->T;
     HIP_TRY(hipMemcpyAsync(c->h_st.data(), c->g.st, sizeof(TState) * T, hipMemcpyDeviceToHost, s));
@@ -557,17 +570,25 @@ int32_t staged_fetch(recmg_cache_t *c, hipStream_t s) {
     int32_t err = 0;
     HIP_TRY(hipMemcpyAsync(&err, c->g.err, 4, hipMemcpyDeviceToHost, s));
     HIP_TRY(hipStreamSynchronize(s));
-    if (err) return RECMG_OK;  // the device flag already disables the rest
+    auto zero_copy_fetch = [&]() -> int32_t {
+        if (c->has_zc) {
+            DispatchTimer dt(c, RECMG_STAGE_FWD_FETCH, true);
+            launch_fetch(c->g, s, dt.a, dt.b);
+            dt.issued();
+        }
+        return RECMG_OK;
+    };
+    if (err) return zero_copy_fetch();  // the device flag already disables the rest
     std::vector<int64_t> nm(T);
     int64_t total = 0;
     for (int t = 0; t < T; ++t) {
-        nm[t] = c->h_st[t].mcount;
+        nm[t] = c->geo[t].staged ? c->h_st[t].mcount : 0;
         if (nm[t])
             HIP_TRY(hipMemcpyAsync(c->h_mrows + c->h_tstart[t], c->g.M + c->h_tstart[t], 4 * (size_t)nm[t],
                                    hipMemcpyDeviceToHost, s));
         total += nm[t];
     }
-    if (total == 0) return RECMG_OK;
+    if (total == 0) return zero_copy_fetch();
     HIP_TRY(hipStreamSynchronize(s));
     const int64_t stride = c->L.stage_stride;
     hipStream_t cs = c->copy_stream ? c->copy_stream : s;
@@ -575,6 +596,7 @@ int32_t staged_fetch(recmg_cache_t *c, hipStream_t s) {
         HIP_TRY(hipEventRecord(c->ev_ready, s));
         HIP_TRY(hipStreamWaitEvent(cs, c->ev_ready, 0));
     }
+    if ((err = zero_copy_fetch())) return err;
     auto work = [&](int t, int64_t lo, int64_t hi) {
         const int64_t ts = c->h_tstart[t], rb = c->geo[t].row_bytes;
         for (int64_t m = lo; m < hi; ++m) {
@@ -695,7 +717,7 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         return fail(RECMG_E_NOMEM, "device workspace smaller than recmg_query_workspace");
     if (reinterpret_cast<uintptr_t>(cfg->device_workspace) & 255)
         return fail(RECMG_E_INVALID, "device workspace not 256-byte aligned");
-    if (cfg->miss_mode == RECMG_STAGED && (!cfg->host_staging || cfg->host_staging_bytes < L.host_total))
+    if (any_staged(geo) && (!cfg->host_staging || cfg->host_staging_bytes < L.host_total))
         return fail(RECMG_E_NOMEM, "host staging smaller than recmg_query_workspace");
     const int T = cfg->num_tables;
 
@@ -703,6 +725,7 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     HIP_TRY(hipGetDevice(&c->device));
     c->T = T;
     c->cfg = *cfg;
+    c->cfg.miss_modes = nullptr;  // the caller's array is read during init only (modes are in geo)
     c->timing = cfg->timing;
     c->geo = geo;
     c->L = L;
@@ -710,7 +733,9 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     std::vector<const char *> dev_host(T);
     for (int t = 0; t < T; ++t) {
         c->host.push_back(static_cast<const char *>(cfg->host_tables[t]));
-        if (cfg->miss_mode == RECMG_STAGED) {
+        if (geo[t].staged) c->has_staged = true;
+        else c->has_zc = true;
+        if (geo[t].staged) {
             dev_host[t] = nullptr;  // only the host reads the tables: any host memory will do
             continue;
         }
@@ -751,7 +776,7 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.fill_slot = c->fill_slot_buf[0];
     g.fill_cap = cfg->max_indices + cfg->max_prefetch;
     g.fstage = ws + L.fstage;
-    g.staged_fill = cfg->miss_mode == RECMG_STAGED ? 1 : 0;
+    g.staged_fill = c->has_staged ? 1 : 0;
     g.hist = reinterpret_cast<int32_t *>(ws + L.hist);
     g.dump = reinterpret_cast<int32_t *>(ws + L.dump);
     g.dump_count = reinterpret_cast<int32_t *>(ws + L.dump_count);
@@ -805,6 +830,7 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         d.ways = ge.ways;
         d.nsets = ge.ways ? ge.nsets : 0;
         d.qbits = ge.qbits;
+        d.staged = ge.staged ? 1 : 0;
         d.seg = reinterpret_cast<int4 *>(ws + L.seg[t]);
         d.freq = cfg->policy == RECMG_LFU_BATCH ? reinterpret_cast<int32_t *>(ws + L.freq[t]) : nullptr;
         if (ge.ways) c->has_sa = true;
@@ -823,12 +849,14 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     for (int t = 0; t < T; ++t) c->pool_order[t] = t;
     std::stable_sort(c->pool_order.begin(), c->pool_order.end(),
                      [&](int x, int y) { return geo[x].kind < geo[y].kind; });
-    // set-associative placement: tables with the fewest sets first, kSaWaves sets per block
+    // set-associative placement: tables with the fewest sets first, kSaWaves
+    // waves of sa_sets_per_wave(ways) sets each per block
     std::vector<int32_t> sa_tab, sa_bs(1, 0);
     for (int t = 0; t < T; ++t)
         if (geo[t].ways) sa_tab.push_back(t);
     std::stable_sort(sa_tab.begin(), sa_tab.end(), [&](int x, int y) { return geo[x].nsets < geo[y].nsets; });
-    for (int t : sa_tab) sa_bs.push_back(sa_bs.back() + (geo[t].nsets + kSaWaves - 1) / kSaWaves);
+    const int sa_per_block = kSaWaves * sa_sets_per_wave(cfg->ways);
+    for (int t : sa_tab) sa_bs.push_back(sa_bs.back() + (geo[t].nsets + sa_per_block - 1) / sa_per_block);
     c->nsa = (int32_t)sa_tab.size();
     c->sa_blocks = sa_bs.back();
 
@@ -865,7 +893,7 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     c->copy_stream = static_cast<hipStream_t>(cfg->copy_stream);
     for (hipEvent_t *e : {&c->ev_src, &c->ev_pool, &c->ev_fwd, &c->ev_plc, &c->ev_fill[0], &c->ev_fill[1]})
         HIP_TRY(hipEventCreateWithFlags(e, hipEventDisableTiming));
-    if (cfg->miss_mode == RECMG_STAGED) {
+    if (c->has_staged) {
         char *hs = static_cast<char *>(cfg->host_staging);
         c->h_mrows = reinterpret_cast<int32_t *>(hs + L.h_mrows);
         c->h_rows = hs + L.h_rows;
@@ -910,7 +938,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     if (c->fill_rec[q]) HIP_TRY(hipStreamWaitEvent(s, c->ev_fill[q], 0));  // it read this parity's fill list
     // STAGED: the host rewrites its staging of fill sources and rows, which
     // the previous fill's copies may still read
-    if (c->cfg.miss_mode == RECMG_STAGED && c->fill_rec[q ^ 1]) HIP_TRY(hipStreamWaitEvent(s, c->ev_fill[q ^ 1], 0));
+    if (c->has_staged && c->fill_rec[q ^ 1]) HIP_TRY(hipStreamWaitEvent(s, c->ev_fill[q ^ 1], 0));
     c->g.staging = c->stage[c->cur];  // misses of the latest forward
     c->g.fill_src = c->fill_src_buf[q];
     c->g.fill_slot = c->fill_slot_buf[q];
@@ -954,7 +982,8 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     {
         StageTimer tm(c, RECMG_STAGE_PLC_APPLY, s);
         if (c->has_fa) launch_plc_apply(g, p, c->max_cap, c->max_map, cand_grid, s);
-        if (c->has_sa) launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks, s);
+        if (c->has_sa)
+            launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks, c->cfg.ways, s);
     }
     launch_plc_finalize(g, fdesc, c->cfg.stats_log_calls ? c->calls % c->cfg.stats_log_calls : -1, s);
     HIP_TRY(hipEventRecord(c->ev_plc, s));
@@ -974,9 +1003,15 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     if (c->fill_rec[q ^ 1] && c->fill_stream[q ^ 1] != fs) HIP_TRY(hipStreamWaitEvent(fs, c->ev_fill[q ^ 1], 0));
     {
         StageTimer tm(c, RECMG_STAGE_PLC_FILL, fs);
-        if (c->cfg.miss_mode == RECMG_STAGED && (rc = staged_fill(c, s, fs))) return rc;  // host-staged rows
+        // Zero-copy tables' rows are read from the host by the kernel, at
+        // once (beside the host gather of the STAGED tables' rows); STAGED
+        // tables' rows once the host has staged them.
         DispatchTimer dt(c, RECMG_STAGE_PLC_FILL, true);
-        launch_plc_fill(g, fdesc, fs, dt.a, dt.b);
+        if (c->has_zc) launch_plc_fill(g, fdesc, FILL_ZERO_COPY, fs, dt.a, c->has_staged ? nullptr : dt.b);
+        if (c->has_staged) {
+            if ((rc = staged_fill(c, s, fs))) return rc;  // host-staged rows
+            launch_plc_fill(g, fdesc, FILL_STAGED, fs, c->has_zc ? nullptr : dt.a, dt.b);
+        }
         dt.issued();
     }
     HIP_TRY(hipEventRecord(c->ev_fill[q], fs));
@@ -1026,8 +1061,10 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
             const int32_t nb = (int32_t)((B + ge.bpb - 1) / ge.bpb);
             c->pool_bstart[k + 1] = c->pool_bstart[k] + nb;
             if (c->pool_launches.empty() || c->pool_launches.back().kind != ge.kind)
-                c->pool_launches.push_back({ge.kind, c->pool_bstart[k], 0});
-            c->pool_launches.back().nblk += nb;
+                c->pool_launches.push_back({ge.kind, c->pool_bstart[k], 0, k, nb});
+            PoolLaunch &pl = c->pool_launches.back();
+            pl.nblk += nb;
+            if (pl.nbt != nb) pl.nbt = 0;  // blocks per table differ: the kernel searches bstart
         }
         HIP_TRY(hipMemcpyAsync(static_cast<char *>(c->cfg.device_workspace) + c->L.pool_bstart, c->pool_bstart.data(),
                                4 * (c->T + 1), hipMemcpyHostToDevice, s));
@@ -1054,11 +1091,11 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
     HIP_TRY(hipEventRecord(c->ev_src, s));  // a placement on another stream may start here
     if (n > 0) {
         StageTimer tm(c, RECMG_STAGE_FWD_FETCH, s);
-        if (c->cfg.miss_mode == RECMG_ZERO_COPY) {
+        if (!c->has_staged) {
             DispatchTimer dt(c, RECMG_STAGE_FWD_FETCH, true);
             launch_fetch(g, s, dt.a, dt.b);
             dt.issued();
-        } else if ((rc = staged_fetch(c, s))) {
+        } else if ((rc = staged_fetch(c, s))) {  // launches the zero-copy tables' fetch too
             return rc;
         }
     }

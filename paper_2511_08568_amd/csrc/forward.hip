@@ -148,12 +148,13 @@ __global__ void __launch_bounds__(kBlock) k_fwd_src(DGlobal g, const int32_t *__
 
 // ----------------------------------------------------------------- miss fetch
 
-// ZERO_COPY miss fetch: each distinct miss is read once from pinned host
-// memory (device-visible mapping) and written to its staging row.
+// ZERO_COPY miss fetch: each distinct miss of a zero-copy table is read once
+// from pinned host memory (device-visible mapping) and written to its staging
+// row (STAGED tables' misses are staged by the host).
 __global__ void __launch_bounds__(kBlock) k_fetch(DGlobal g) {
     if (*g.err) return;
     __shared__ int32_t s_cnt[RECMG_MAX_TABLES];
-    for (int t = threadIdx.x; t < g.T; t += blockDim.x) s_cnt[t] = g.st[t].mcount;
+    for (int t = threadIdx.x; t < g.T; t += blockDim.x) s_cnt[t] = g.tabs[t].staged ? 0 : g.st[t].mcount;
     __syncthreads();
     copy_flat(
         g, s_cnt, gridDim.x,
@@ -657,21 +658,32 @@ __device__ __forceinline__ void pool_wave_v(const uint64_t *__restrict__ raddr, 
 #endif
 
 // RECMG_WPOOL_OCC: waves per SIMD the register allocation must allow
+// nbt > 0: every table of the launch has nbt blocks, so block lb belongs to
+// table btab[k0 + (lb - boff) / nbt] (no search; one wave's prologue is a
+// chain of dependent loads, and the search would add four to it).
 template <int DT, int LW, int R>
 __global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(RECMG_WPOOL_OCC))) k_pool_w(DGlobal g, const int64_t *__restrict__ offsets,
                                                    const uint64_t *__restrict__ raddr, int32_t B,
                                                    float *__restrict__ out, const int32_t *__restrict__ bstart,
                                                    const int32_t *__restrict__ btab, int32_t nt, int32_t boff,
-                                                   int32_t nblk) {
-    if (*g.err) return;
+                                                   int32_t nblk, int32_t k0, int32_t nbt) {
     const int lb = boff + xcd_block(nblk);
-    const int k = find_seg32(bstart, nt, lb);
+    int k, b0;
+    if (nbt > 0) {
+        k = k0 + (lb - boff) / nbt;
+        b0 = boff + (k - k0) * nbt;
+    } else {
+        k = find_seg32(bstart, nt, lb);
+        b0 = bstart[k];
+    }
     const int t = btab[k];
+    const int err = *g.err;
     const DTable &tb = g.tabs[t];
     const int D = tb.dim;
     const int64_t ooff = (int64_t)B * tb.out_elem_off;
+    if (err) return;
     const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
-    const int j0 = ((lb - bstart[k]) * (kBlock / 64) + wave) * kWaveBags;
+    const int j0 = ((lb - b0) * (kBlock / 64) + wave) * kWaveBags;
     if (j0 >= B) return;
     const int nbags = B - j0 < kWaveBags ? B - j0 : kWaveBags;
     const int64_t *ob = offsets + (int64_t)t * B + j0;
@@ -763,7 +775,7 @@ void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out
     using KG = void (*)(DGlobal, const int64_t *, int32_t, float *, const int32_t *, const int32_t *, int32_t,
                         int32_t, int32_t);
     using KW = void (*)(DGlobal, const int64_t *, const uint64_t *, int32_t, float *, const int32_t *,
-                        const int32_t *, int32_t, int32_t, int32_t);
+                        const int32_t *, int32_t, int32_t, int32_t, int32_t, int32_t);
     static const KG kg[kPoolKindsGroup] = {k_pool<RECMG_F32, false>,  k_pool<RECMG_F32, true>,
                                            k_pool<RECMG_F16, false>,  k_pool<RECMG_F16, true>,
                                            k_pool<RECMG_BF16, false>, k_pool<RECMG_BF16, true>};
@@ -791,8 +803,8 @@ void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out
             const KW k = kw[L.kind - kPoolKindsGroup];
             const uint64_t *ra = g.raddr;
             if (a || b) hipExtLaunchKernelGGL(k, grid, blk, 0, s, a, b, 0, g, offsets, ra, B, out, bstart, btab, nt,
-                                              L.boff, L.nblk);
-            else k<<<grid, blk, 0, s>>>(g, offsets, ra, B, out, bstart, btab, nt, L.boff, L.nblk);
+                                              L.boff, L.nblk, L.k0, L.nbt);
+            else k<<<grid, blk, 0, s>>>(g, offsets, ra, B, out, bstart, btab, nt, L.boff, L.nblk, L.k0, L.nbt);
         }
     }
 }

@@ -24,9 +24,11 @@ void launch_fetch(const DGlobal &g, hipStream_t s, hipEvent_t ev0 = nullptr, hip
 constexpr int kPoolKindsGroup = 6, kPoolKinds = kPoolKindsGroup + 15;
 int pool_kind(int dtype, int vec, int wlw, int wr);
 // one launch per kind present, over the blocks [boff, boff + nblk) of the
-// tables btab[k] ordered by kind; bstart[k] = first block of btab[k]
+// tables btab[k] ordered by kind; bstart[k] = first block of btab[k].  The
+// launch's tables are btab[k0 ..]; wave-per-bag kinds give every table the
+// same number of blocks, nbt.
 struct PoolLaunch {
-    int32_t kind, boff, nblk;
+    int32_t kind, boff, nblk, k0, nbt;
 };
 void launch_pool(const DGlobal &g, const int64_t *offsets, int32_t B, float *out, const int32_t *bstart,
                  const int32_t *btab, int32_t nt, const PoolLaunch *ls, int nl, hipEvent_t ev0, hipEvent_t ev1,
@@ -42,17 +44,21 @@ void launch_plc_classify(const DGlobal &g, int32_t last_stamp, int64_t np, hipSt
 void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s);
 void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,
                       hipStream_t s);
-// fdesc: this placement's fill descriptor, [T][4] int64 (written by finalize, read by fill)
-void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s, hipEvent_t ev0 = nullptr,
+// fdesc: this placement's fill descriptor, [T][4] int64 (written by finalize, read by fill);
+// phase: the tables whose rows this launch copies, by miss mode
+enum { FILL_ZERO_COPY = 1, FILL_STAGED = 2 };
+void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, int phase, hipStream_t s, hipEvent_t ev0 = nullptr,
                      hipEvent_t ev1 = nullptr);
 void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, int64_t log_slot, hipStream_t s);
 void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s);
 
 // setassoc.hip: placement of the set-associative tables (nu: index space of
 // the last forward's distinct rows, np: of this placement's prefetch rows;
-// nsa tables, blocks = sa_bstart[nsa], kSaWaves sets per block)
+// nsa tables, blocks = sa_bstart[nsa], kSaWaves * sa_sets_per_wave(ways)
+// sets per block)
 constexpr int kSaWaves = 16, kSaBlock = 64 * kSaWaves;
+constexpr int sa_sets_per_wave(int ways) { return ways <= 32 ? 2 : 1; }
 void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks,
-                     hipStream_t s);
+                     int32_t ways, hipStream_t s);
 
 }  // namespace recmg

@@ -91,17 +91,19 @@ __global__ void __launch_bounds__(kBlock) k_plc_freq(DGlobal g, int64_t n) {
     }
 }
 
-// Classify every distinct prefetch row (Alg. 1's prefetch loop taken as a
-// set): resident -> flag the slot; missed by the last batch -> flag the miss;
-// otherwise a new candidate, appended to NP.  One thread per slot of the
-// prefetch index space; table t's distinct rows occupy [pstart[t], + pcount).
+// Classify every distinct prefetch row of the fully associative tables (Alg.
+// 1's prefetch loop taken as a set): resident -> flag the slot; missed by the
+// last batch -> flag the miss; otherwise a new candidate, appended to NP.  One
+// thread per slot of the prefetch index space; table t's distinct rows occupy
+// [pstart[t], + pcount).  Set-associative tables play their prefetch rows as
+// events in k_sa_place, which also counts the resident ones.
 __global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last_stamp, int64_t np) {
     if (*g.err) return;
     __shared__ int64_t s_pstart[RECMG_MAX_TABLES + 1];
     __shared__ int32_t s_pc[RECMG_MAX_TABLES];
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         s_pstart[t] = g.pstart[t];
-        if (t < g.T) s_pc[t] = g.st[t].pcount;
+        if (t < g.T) s_pc[t] = g.tabs[t].ways ? 0 : g.st[t].pcount;
     }
     __syncthreads();
     const int stride_st = (int)(sizeof(TState) / 4);
@@ -505,22 +507,27 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
 }
 
 // Copy admitted rows into their slots: misses from HBM staging, prefetch
-// fills from pinned host memory over the host link (ZERO_COPY) or from rows the
-// host staged and copied in (STAGED).  May run on a side stream, concurrently
-// with the next forward and with the next placement: it reads only its own
-// placement's fill list and descriptor (both double-buffered, see
+// fills from pinned host memory over the host link (ZERO_COPY tables) or from
+// rows the host staged and copied in (STAGED tables).  One launch per miss
+// mode present (phase): the zero-copy tables' at once, the STAGED tables'
+// after the host has staged their rows.  May run on a side stream,
+// concurrently with the next forward and with the next placement: it reads
+// only its own placement's fill list and descriptor (both double-buffered, see
 // k_plc_finalize) and the staging buffer of the forward before that placement,
 // which the next forward does not use.
-__global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, const int64_t *__restrict__ fdesc) {
+__global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, const int64_t *__restrict__ fdesc, int phase) {
     if (*g.err) return;
-    // the blocks that copy, chosen by k_plc_finalize (fdesc[3])
-    const int64_t nb = fdesc[3] < 1 ? 1 : fdesc[3] > (int64_t)gridDim.x ? (int64_t)gridDim.x : fdesc[3];
+    // the blocks that copy: zero-copy fills as many as k_plc_finalize chose
+    // (fdesc[3]), HBM-to-HBM copies of STAGED rows the whole grid
+    const int64_t nb = phase == FILL_STAGED ? (int64_t)gridDim.x
+                       : fdesc[3] < 1 ? 1 : fdesc[3] > (int64_t)gridDim.x ? (int64_t)gridDim.x : fdesc[3];
     if ((int64_t)blockIdx.x >= nb) return;  // block-uniform
     __shared__ int32_t s_cnt[RECMG_MAX_TABLES];
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         const int64_t base = fdesc[4 * t], n = fdesc[4 * t + 1];
+        const bool mine = (g.tabs[t].staged != 0) == (phase == FILL_STAGED);
         // admit wrote entries [base, base + n) and checked them against fill_cap
-        s_cnt[t] = (base >= 0 && n >= 0 && base + n <= g.fill_cap) ? (int32_t)n : 0;
+        s_cnt[t] = (mine && base >= 0 && n >= 0 && base + n <= g.fill_cap) ? (int32_t)n : 0;
     }
     __syncthreads();
     // entries were checked where admit and the set-associative placement wrote them
@@ -529,8 +536,8 @@ __global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, const int64_t *_
         [&](int t, const DTable &tb, int64_t j) -> const char * {
             const int32_t src = g.fill_src[fdesc[4 * t] + j];
             if (src >= 0) return g.staging + (fdesc[4 * t + 2] + src) * g.stage_stride;  // admitted miss
-            return g.staged_fill ? g.fstage + (int64_t)(-src - 1) * g.stage_stride  // prefetch row, host-staged
-                                 : tb.host + (int64_t)(-src - 1) * tb.row_bytes;    // prefetch row, zero-copy
+            return tb.staged ? g.fstage + (int64_t)(-src - 1) * g.stage_stride  // prefetch row, host-staged
+                             : tb.host + (int64_t)(-src - 1) * tb.row_bytes;    // prefetch row, zero-copy
         },
         [&](int t, const DTable &tb, int64_t j) { return tb.pool + (int64_t)g.fill_slot[fdesc[4 * t] + j] * tb.row_bytes; });
 }
@@ -567,9 +574,7 @@ __global__ void k_plc_finalize(DGlobal g, int64_t *fdesc, int64_t log_slot) {
         mb += (unsigned long long)(g.st[t].mcount > 0 ? g.st[t].mcount : 0) * (unsigned long long)g.tabs[t].row_bytes;
     if (mb) atomicAdd(&s_mbytes, mb);
     __syncthreads();
-    if (threadIdx.x == 0)
-        fdesc[3] = g.staged_fill ? kStagedFillBlocks
-                                 : s_mbytes >= kSharedFetchBytes ? RECMG_FILL_BLOCKS_SHARED : RECMG_FILL_BLOCKS;
+    if (threadIdx.x == 0) fdesc[3] = s_mbytes >= kSharedFetchBytes ? RECMG_FILL_BLOCKS_SHARED : RECMG_FILL_BLOCKS;
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         TState &st = g.st[t];
         const DTable &tb = g.tabs[t];
@@ -665,7 +670,8 @@ void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int
     k_plc_admit<<<dim3(grid_for(cand_bound, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
 }
 
-void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, int phase, hipStream_t s, hipEvent_t ev0,
+                     hipEvent_t ev1) {
     // Zero-copy fills read the host: about a hundred blocks of 4-deep 16-byte
     // loads keep the host link full (about 2 MB in flight) when the fill has
     // it to itself.  Host reads hold a CU's L1 miss slots for microseconds, so
@@ -678,11 +684,11 @@ void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, hipStream_t s, hipE
     // and 256 blocks gave +4%.  The grid holds the larger count; k_plc_finalize
     // writes how many of its blocks copy.  STAGED fills copy within HBM and
     // take a full grid.
-    const int blocks = g.staged_fill ? kStagedFillBlocks
-                                     : (RECMG_FILL_BLOCKS > RECMG_FILL_BLOCKS_SHARED ? RECMG_FILL_BLOCKS
-                                                                                     : RECMG_FILL_BLOCKS_SHARED);
-    if (ev0 || ev1) hipExtLaunchKernelGGL(k_plc_fill, dim3(blocks), dim3(kBlock), 0, s, ev0, ev1, 0, g, fdesc);
-    else k_plc_fill<<<blocks, kBlock, 0, s>>>(g, fdesc);
+    const int blocks = phase == FILL_STAGED ? kStagedFillBlocks
+                                            : (RECMG_FILL_BLOCKS > RECMG_FILL_BLOCKS_SHARED ? RECMG_FILL_BLOCKS
+                                                                                            : RECMG_FILL_BLOCKS_SHARED);
+    if (ev0 || ev1) hipExtLaunchKernelGGL(k_plc_fill, dim3(blocks), dim3(kBlock), 0, s, ev0, ev1, 0, g, fdesc, phase);
+    else k_plc_fill<<<blocks, kBlock, 0, s>>>(g, fdesc, phase);
 }
 
 void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, int64_t log_slot, hipStream_t s) {

@@ -73,7 +73,8 @@ struct DTable {
     // position (set << qbits) | (r / nsets), so sorted distinct rows come out
     // grouped by set, ascending within a set.  ways == 0: fully associative
     // (the map above), bitmap position = row.
-    int32_t ways, nsets, qbits, pad_sa;
+    int32_t ways, nsets, qbits;
+    int32_t staged;  // 1: misses and prefetch fills of this table are gathered on the host (STAGED)
     int4 *seg;  // [nsets] (U begin, U end, PU begin, PU end) of each set in the
                 // current placement, relative to the table's lists; zero between uses
     int32_t *freq;  // LFU_BATCH: [rows] batches that accessed each row (every row, cached or not)
@@ -131,7 +132,8 @@ struct DGlobal {
                               // current placement: tstart of the last forward, or 0 if none ran
     int64_t fill_cap;         // entries of fill_src / fill_slot (max_indices + max_prefetch)
     char *fstage;             // [max_prefetch][stage_stride] prefetch rows staged by the host (STAGED)
-    int32_t staged_fill;      // 1: a fill source -(k + 1) is fstage row k, not host row k
+    int32_t staged_fill;      // 1: some table is STAGED; there a fill source -(k + 1) is fstage row k,
+                              // not host row k
     int64_t stage_stride;
     int32_t T;
     int32_t total_bm_blocks;

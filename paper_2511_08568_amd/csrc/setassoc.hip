@@ -69,30 +69,43 @@ __global__ void __launch_bounds__(kBlock) k_sa_heads(DGlobal g, int64_t nu, int6
     }
 }
 
-// Minimum of v over the wave, returned as a scalar: DPP within rows of 16
-// lanes, row broadcasts into the last row, one read of lane 63.  Every lane
-// must be active.
-__device__ __forceinline__ int wave_min_dpp(int v) {
+// Minimum of v over each group of HL lanes (HL = 64: the wave, 32: each
+// half), returned per group as a scalar (m0 of lanes 0-31 or the wave, m1 of
+// lanes 32-63): DPP within rows of 16 lanes, row broadcasts across rows, reads
+// of the groups' last lanes.  Every lane must be active.
+template <int HL>
+__device__ __forceinline__ void group_min_dpp(int v, int &m0, int &m1) {
     v = min(v, __builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));   // quad_perm [1,0,3,2]
     v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));   // quad_perm [2,3,0,1]
     v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x141, 0xF, 0xF, false));  // row_half_mirror
     v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x140, 0xF, 0xF, false));  // row_mirror
     v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x142, 0xA, 0xF, false));  // row_bcast:15 into rows 1, 3
-    v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x143, 0xC, 0xF, false));  // row_bcast:31 into rows 2, 3
-    return __builtin_amdgcn_readlane(v, 63);
+    if constexpr (HL == 64) {
+        v = min(v, __builtin_amdgcn_update_dpp(v, v, 0x143, 0xC, 0xF, false));  // row_bcast:31 into rows 2, 3
+        m0 = m1 = __builtin_amdgcn_readlane(v, 63);
+    } else {
+        m0 = __builtin_amdgcn_readlane(v, 31);
+        m1 = __builtin_amdgcn_readlane(v, 63);
+    }
 }
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
 
 static_assert(kSaWaves == 16, "the block's counts are added up over one DPP row of 16 lanes");
 
-// One wave per set (lane w = way w), kSaWaves sets per block.  Blocks run
-// table by table, tables with the fewest sets first: their sets take the most
-// events each, and the longest waves should start first.  The counters and
-// the fill-list space of a block's sets are added up by its first wave and
-// taken with one atomic each per block (a wave per set would queue hundreds of
-// thousands of atomics on the same few words of a table with many sets).
+// SPW sets per wave (2 when W <= 32, lanes 32h .. 32h + 31 taking set h; else
+// 1), lane w of a set holding way w; kSaWaves * SPW sets per block.  The sets
+// of a wave play their events side by side, one event of each per step, so a
+// wave's chain of dependent loads serves two sets when the ways fit in half a
+// wave.  Blocks run table by table, tables with the fewest sets first: their
+// sets take the most events each, and the longest waves should start first.
+// The counters and the fill-list space of a block's sets are added up by its
+// first wave and taken with one atomic each per block (an atomic per set would
+// queue hundreds of thousands of them on the same few words of a table with
+// many sets).
+template <int SPW>
 __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, int32_t nsa) {
+    constexpr int HL = 64 / SPW;  // lanes per set
     __shared__ int s_cnt[kSaWaves][8];
     __shared__ unsigned long long s_dig[kSaWaves];
     __shared__ int s_off[kSaWaves];
@@ -105,23 +118,41 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     TState &st = g.st[t];
     const int W = tb.ways;
     const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int64_t set = (int64_t)(blockIdx.x - g.sa_bstart[kt]) * kSaWaves + wid;
+    const int h = lane / HL, wl = lane % HL;  // this lane's set of the wave, and its way
+    const bool hi = h != 0;
+    // this lane's half of a 64-bit ballot (the whole ballot when SPW == 1)
+    auto half = [&](uint64_t b) -> uint64_t { return SPW == 1 ? b : (hi ? b >> 32 : b & 0xffffffffull); };
+    // value of lane k of this lane's set (k wave-uniform per set: k0 for set 0, k1 for set 1)
+    auto pick = [&](int v, int k0, int k1) -> int {
+        if constexpr (SPW == 1) return __builtin_amdgcn_readlane(v, k0);
+        const int a = __builtin_amdgcn_readlane(v, k0 & 31), b = __builtin_amdgcn_readlane(v, 32 + (k1 & 31));
+        return hi ? b : a;
+    };
+    const int64_t set = ((int64_t)(blockIdx.x - g.sa_bstart[kt]) * kSaWaves + wid) * SPW + h;
     int4 sg = make_int4(0, 0, 0, 0);
     if (!err && set < tb.nsets) sg = tb.seg[set];
-    const bool active = sg.x != sg.y || sg.z != sg.w;  // wave-uniform
-    const bool way = lane < W;
-    const int64_t slot = set * W + lane;
+    const bool active = sg.x != sg.y || sg.z != sg.w;  // uniform over the set's lanes
+    const bool way = wl < W && active;
+    const int64_t slot = set * W + wl;
     const int64_t pb = g.pstart[t];
+    // per-set event counts, as scalars (set 1's are 0 when SPW == 1)
+    auto both = [&](int v, int &v0, int &v1) {
+        v0 = __builtin_amdgcn_readlane(v, 0);
+        v1 = SPW == 1 ? 0 : __builtin_amdgcn_readlane(v, 32);
+    };
+    int nu0, nu1, np0, np1;
+    both(sg.y - sg.x, nu0, nu1);
+    both(sg.w - sg.z, np0, np1);
     // results of this lane's way, and of the wave
     int32_t row = -1, src = -1;
     bool changed = false, from_m = false;
-    int c_ev = 0, c_am = 0, c_fill = 0, c_pd = 0, c_md = 0, c_res = 0;
+    int c_ev = 0, c_am = 0, c_fill = 0, c_pd = 0, c_md = 0, c_res = 0, c_pres = 0;
     unsigned long long dsum = 0;
-    if (active) {
-    if (lane == 0) tb.seg[set] = make_int4(0, 0, 0, 0);
-    // A set's events are played one after another: a set with many of them is
-    // the kernel's critical path, so its wave takes issue slots first.
-    if ((sg.y - sg.x) + (sg.w - sg.z) > 256) __builtin_amdgcn_s_setprio(3);
+    if (ballot(active)) {
+    if (active && wl == 0) tb.seg[set] = make_int4(0, 0, 0, 0);
+    // A set's events are played one after another: a wave with many of them
+    // is the kernel's critical path, so it takes issue slots first.
+    if (max(nu0 + np0, nu1 + np1) > 256) __builtin_amdgcn_s_setprio(3);
 
     // A. this set's ways; rows the last batch touched take the touch score
     int32_t row0 = -1, score = 0;
@@ -140,56 +171,61 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     row = row0;        // src: this lane's last insertion, staging index of a miss or -1 (host)
     bool inp = false;  // this lane's row is named by the prefetch list
 
-    // insert row r with score v (from: its staging index, or -1); returns the
-    // way.  Ways are never freed, so once no way is free the set stays full.
-    bool full = ballot(way && row < 0) == 0;
-    auto insert = [&](int32_t r, int32_t v, int32_t from) -> int {
-        int victim;
-        if (!full) {
-            const uint64_t fr = ballot(way && row < 0);
-            victim = __ffsll((unsigned long long)fr) - 1;
-            full = (fr & (fr - 1)) == 0;
-        } else {
-            const int m = wave_min_dpp(way ? score : INT32_MAX);
-            victim = __ffsll((unsigned long long)ballot(way && score == m)) - 1;
-            if (p.prio && way) score = score > 0 ? score - 1 : 0;
-        }
-        if (lane == victim) {
-            row = r;
-            score = v;
-            src = from;
-            inp = false;
+    // Insert row r with score v (from: its staging index, or -1) into this
+    // lane's set when `act` (uniform over the set): the lowest free way, else
+    // the lowest way holding the set's minimum score, after which, under
+    // PRIORITY, every way of the set ages by one (saturating at 0).  Returns
+    // the way taken.  Every lane of the wave calls.
+    auto insert = [&](bool act, int32_t r, int32_t v, int32_t from) -> int {
+        const uint64_t fr = half(ballot(way && row < 0));
+        int m0, m1;
+        group_min_dpp<HL>(way ? score : INT32_MAX, m0, m1);
+        const int m = hi ? m1 : m0;
+        const uint64_t mins = half(ballot(way && score == m));
+        const int victim = __ffsll((unsigned long long)(fr ? fr : mins)) - 1;
+        if (act) {
+            if (!fr && p.prio && way) score = score > 0 ? score - 1 : 0;
+            if (wl == victim) {
+                row = r;
+                score = v;
+                src = from;
+                inp = false;
+            }
         }
         return victim;
     };
 
-    // B. misses of the last batch, ascending.  Each chunk of 64 distinct rows
-    // is loaded lane-parallel with the misses' touch scores, then played one
-    // miss at a time from registers.
+    // B. misses of the last batch, ascending.  Each chunk of HL distinct rows
+    // of a set is loaded lane-parallel with the misses' touch scores, then
+    // played one miss at a time from registers.
     const int64_t ub = g.tstart[t];
     int nmiss = 0;
-    for (int32_t i0 = sg.x; i0 < sg.y; i0 += 64) {
-        const int32_t i = i0 + lane;
+    for (int32_t i0 = 0; i0 < max(nu0, nu1); i0 += HL) {
+        const int32_t i = sg.x + i0 + wl;
+        const bool in = i < sg.y;
         int32_t r = 0, su = 0, v = 0;
-        if (i < sg.y) {
+        if (in) {
             r = g.U[ub + i];
             su = g.slotU[ub + i];
-            if (su < 0) v = touch_score(p, tb, r, g.mcbit[ub + (-su - 1)]);
+            if (su < 0) v = touch_score(p, tb, r, p.prio ? g.mcbit[ub + (-su - 1)] : 0);
         }
-        uint64_t mm = ballot(i < sg.y && su < 0);
+        const uint64_t mm = ballot(in && su < 0);
         nmiss += __popcll(mm);
-        while (mm) {
-            const int j = __ffsll((unsigned long long)mm) - 1;
-            mm &= mm - 1;
-            insert(__builtin_amdgcn_readlane(r, j), __builtin_amdgcn_readlane(v, j),
-                   -__builtin_amdgcn_readlane(su, j) - 1);
+        uint64_t mm0 = SPW == 1 ? mm : mm & 0xffffffffull, mm1 = SPW == 1 ? 0 : mm >> 32;
+        while (mm0 | mm1) {
+            const int j0 = mm0 ? __ffsll((unsigned long long)mm0) - 1 : 0;
+            const int j1 = mm1 ? __ffsll((unsigned long long)mm1) - 1 : 0;
+            const bool act = hi ? mm1 != 0 : mm0 != 0;
+            insert(act, pick(r, j0, j1), pick(v, j0, j1), -pick(su, j0, j1) - 1);
+            mm0 &= mm0 ? mm0 - 1 : 0;
+            mm1 &= mm1 ? mm1 - 1 : 0;
         }
     }
 
     // C. distinct prefetch rows, ascending.  Each lane first finds whether its
     // row missed in the last batch (then it is still in staging).
-    for (int32_t i0 = sg.z; i0 < sg.w; i0 += 64) {
-        const int32_t i = i0 + lane;
+    for (int32_t i0 = 0; i0 < max(np0, np1); i0 += HL) {
+        const int32_t i = sg.z + i0 + wl;
         int32_t r = -1, from = -1, v = 0;
         if (i < sg.w) {
             r = g.PU[pb + i];
@@ -204,25 +240,25 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
                 }
             }
         }
-        const int cnt = min(64, sg.w - i0);
-        for (int j = 0; j < cnt; ++j) {
-            const int32_t rr = __builtin_amdgcn_readlane(r, j);
-            const uint64_t h = ballot(way && row == rr);
-            if (h) {
-                if (lane == __ffsll((unsigned long long)h) - 1) {
-                    if (score < p.pscore) score = p.pscore;
-                    inp = true;
-                }
-                continue;
+        const int c0 = min(HL, np0 - i0), c1 = min(HL, np1 - i0);
+        for (int j = 0; j < max(c0, c1); ++j) {
+            const bool act = j < (hi ? c1 : c0);
+            const int32_t rr = pick(r, j, j);
+            const uint64_t hit = half(ballot(way && row == rr));
+            if (act && hit && wl == __ffsll((unsigned long long)hit) - 1) {
+                if (score < p.pscore) score = p.pscore;
+                inp = true;
             }
-            const int w = insert(rr, __builtin_amdgcn_readlane(v, j), __builtin_amdgcn_readlane(from, j));
-            if (lane == w) inp = true;
+            const int w = insert(act && !hit, rr, pick(v, j, j), pick(from, j, j));
+            if (act && !hit && wl == w) inp = true;
         }
     }
 
     // counters: compare the set's rows at the start and at the end.  A set's
     // rows are distinct at every point, so a row that left an unchanged way
-    // can only be found in a changed one, and the search runs over those.
+    // can only be found in a changed one, and the search runs over those (a
+    // row of one set never equals a row of another, so the search may run
+    // over the changed ways of the whole wave).
     const uint64_t dm = ballot(way && row != row0);
     bool kept0 = (dm >> lane & 1ull) == 0, was = kept0;
     for (uint64_t m = dm; m; m &= m - 1) {
@@ -239,15 +275,19 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     if (evicted) dig -= mix64(((unsigned long long)t << 40) | (unsigned long long)row0);
     const int d_res = (way && row >= 0 ? 1 : 0) - (way && row0 >= 0 ? 1 : 0);
 
-    // prefetch rows in neither R nor R'
-    int pdrop = 0;
-    for (int32_t i0 = sg.z; i0 < sg.w; i0 += 64) {
-        const int32_t i = i0 + lane;
+    // prefetch rows in R (prefetch_resident) and in neither R nor R'
+    // (prefetch_dropped); R ∪ R' = the rows at the start and the rows of the
+    // changed ways (again the whole wave may be searched)
+    const uint64_t wm = ballot(way);
+    int pdrop = 0, pres = 0;
+    for (int32_t i0 = 0; i0 < max(np0, np1); i0 += HL) {
+        const int32_t i = sg.z + i0 + wl;
         const int32_t r = i < sg.w ? g.PU[pb + i] : -1;
-        bool in = false;  // R ∪ R' = the rows at the start and the rows of the changed ways
-        for (int k = 0; k < W; ++k) in |= __builtin_amdgcn_readlane(row0, k) == r;
+        bool in_r = false, in = false;
+        for (uint64_t m = wm; m; m &= m - 1) in_r |= __builtin_amdgcn_readlane(row0, __ffsll((unsigned long long)m) - 1) == r;
         for (uint64_t m = dm; m; m &= m - 1) in |= __builtin_amdgcn_readlane(row, __ffsll((unsigned long long)m) - 1) == r;
-        pdrop += (i < sg.w && !in) ? 1 : 0;
+        pres += (i < sg.w && in_r) ? 1 : 0;
+        pdrop += (i < sg.w && !in_r && !in) ? 1 : 0;
     }
 
     if (way) {
@@ -260,10 +300,11 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     c_am = wave_sum(from_m ? 1 : 0);
     c_fill = wave_sum(changed && !from_m ? 1 : 0);
     c_pd = wave_sum(pdrop);
+    c_pres = wave_sum(pres);
     c_md = nmiss - c_am;
     c_res = wave_sum(d_res);
     dsum = wave_sum64(dig);
-    }  // active
+    }  // some set of the wave active
 
     // the block's totals: one atomic per counter, one for the fill-list space
     const uint64_t chm = ballot(changed);
@@ -275,6 +316,7 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
         s_cnt[wid][4] = c_pd;
         s_cnt[wid][5] = c_md;
         s_cnt[wid][6] = c_res;
+        s_cnt[wid][7] = c_pres;
         s_dig[wid] = dsum;
     }
     __syncthreads();
@@ -293,10 +335,10 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
         const int c0 = mine ? s_cnt[lane][0] : 0;
         const int sc0 = row_scan(c0);
         const int tot0 = __builtin_amdgcn_readlane(sc0, kSaWaves - 1);
-        int tot[7];
+        int tot[8];
         tot[0] = tot0;
 #pragma unroll
-        for (int k = 1; k < 7; ++k) tot[k] = __builtin_amdgcn_readlane(row_scan(mine ? s_cnt[lane][k] : 0), kSaWaves - 1);
+        for (int k = 1; k < 8; ++k) tot[k] = __builtin_amdgcn_readlane(row_scan(mine ? s_cnt[lane][k] : 0), kSaWaves - 1);
         const unsigned long long d = wave_sum64(mine ? s_dig[lane] : 0ull);
         int base = 0;
         if (lane == 0 && tot0) base = atomicAdd(&st.popped, tot0);
@@ -309,6 +351,7 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
             if (tot[4]) atomicAdd(&st.p_drop, tot[4]);
             if (tot[5]) atomicAdd(&st.m_drop, tot[5]);
             if (tot[6]) atomicAdd(&st.n_res, tot[6]);
+            if (tot[7]) atomicAdd(&st.p_res, tot[7]);
             if (d) atomicAdd(&st.digest_acc, d);
         }
     }
@@ -332,9 +375,11 @@ static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
 }
 
 void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks,
-                     hipStream_t s) {
+                     int32_t ways, hipStream_t s) {
     if (nu + np > 0) k_sa_heads<<<grid_for(nu + np, kBlock, 8192), kBlock, 0, s>>>(g, nu, np, p.have_fwd);
-    if (blocks > 0) k_sa_place<<<(unsigned)blocks, kSaBlock, 0, s>>>(g, p, nsa);
+    if (blocks <= 0) return;
+    if (sa_sets_per_wave(ways) == 2) k_sa_place<2><<<(unsigned)blocks, kSaBlock, 0, s>>>(g, p, nsa);
+    else k_sa_place<1><<<(unsigned)blocks, kSaBlock, 0, s>>>(g, p, nsa);
 }
 
 }  // namespace recmg

@@ -93,8 +93,9 @@ class GpuRunner:
         if max_prefetch is None:
             max_prefetch = max(max(w.prefetch_list(b)[0].size for b in range(nb)), 1)
         self.host = [torch.from_numpy(np.ascontiguousarray(a)) for a in tabs]
-        if pin:
-            self.host = [h.pin_memory() for h in self.host]
+        # miss_mode: one for every table, or one per table (zero-copy tables are always pinned)
+        modes = [miss_mode] * len(tabs) if isinstance(miss_mode, str) else list(miss_mode)
+        self.host = [h.pin_memory() if (pin or m == "zero_copy") else h for h, m in zip(self.host, modes)]
         self.cache = TieredEmbeddingCache(self.host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables],
                                           policy=w.policy, eviction_speed=w.eviction_speed, miss_mode=miss_mode,
                                           max_bags_per_table=w.bags, max_indices=max_indices,

@@ -126,3 +126,21 @@ def test_missing_library_fails_loudly():
     env = dict(os.environ, RECMG_LIBRARY=os.path.join(root, "no_such_librecmg.so"))
     r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120, cwd=root, env=env)
     assert r.returncode == 0 and r.stdout.startswith("raised"), r.stdout + r.stderr
+
+
+def test_per_table_miss_modes():
+    """miss_modes overrides miss_mode per table: one STAGED table is enough for
+    pinned host staging; a bad entry is rejected; NULL keeps miss_mode."""
+    import ctypes
+    base = _cfg(rows=(1000, 2000), dims=(64, 32), dtypes=(0, 0), caps=(100, 100))
+    _, host0 = bd.recmg_query_workspace(base)
+    assert host0 == 0
+    modes = (ctypes.c_int32 * 2)(0, 1)
+    base.miss_modes = modes
+    _, host1 = bd.recmg_query_workspace(base)
+    assert host1 > 0
+    bad = (ctypes.c_int32 * 2)(0, 7)
+    base.miss_modes = bad
+    with pytest.raises(bd.RecmgError) as e:
+        bd.recmg_query_workspace(base)
+    assert e.value.code == bd.RECMG_E_INVALID and "miss_modes" in pk.recmg_last_error()

@@ -13,6 +13,7 @@ pytestmark = [pytest.mark.gpu,
 
 
 def _parity(w, nbatches=None, miss_mode="zero_copy", label="", pin=True):
+    """The HIP path against the oracle on w's batches (miss_mode: one mode or one per table)."""
     nb = nbatches or w.batches
     tabs, ora = run_oracle(w, nbatches=nb)
     g = GpuRunner(w, tabs, miss_mode=miss_mode, nbatches=nb, pin=pin)
@@ -189,6 +190,17 @@ def test_staged_with_unpinned_tables(cid, scale, tables):
     _parity(w, miss_mode="staged", label=f"c{cid}-staged-unpinned", pin=False)
 
 
+@pytest.mark.parametrize("cid,scale,tables,ways", [(4, 0.0005, 4, 0), (3, 0.01, 5, 0), (5, 0.005, 6, 32)])
+def test_mixed_miss_modes(cid, scale, tables, ways):
+    """Per-table miss modes: the first half of the tables pinned and read
+    zero-copy, the rest ordinary memory gathered on the host, in one handle
+    (the configuration-4 setup where only some tables fit the pinned-memory
+    limit), against the oracle."""
+    w = tg.scaled_config(cid, row_scale=scale, batches=5, bags=256, max_tables=tables, ways=ways)
+    modes = ["zero_copy" if t < tables // 2 else "staged" for t in range(tables)]
+    _parity(w, miss_mode=modes, label=f"c{cid}-mixed", pin=False)
+
+
 @pytest.mark.parametrize("overlap,sync", [(True, True), (True, False), (False, False)])
 def test_two_placements_in_a_row(overlap, sync):
     """Two placements in a row (no forward between), each on a stream other
@@ -253,17 +265,24 @@ def test_cap_zero_and_full_give_identical_outputs():
     del base
 
 
-def test_zero_copy_and_staged_bitwise_equal():
-    outs = []
-    for mode in ("zero_copy", "staged"):
-        w = tg.scaled_config(5, row_scale=0.005, batches=4, bags=128, max_tables=4)
+@pytest.mark.parametrize("ways", [0, 32])
+def test_zero_copy_staged_and_mixed_bitwise_equal(ways):
+    """The miss path changes where rows come from, never a result: zero-copy,
+    STAGED and per-table mixes of the two give bit-identical outputs, counters
+    and resident sets."""
+    runs = []
+    for mode in ("zero_copy", "staged", ["zero_copy", "staged", "staged", "zero_copy"],
+                 ["staged", "zero_copy", "zero_copy", "staged"]):
+        w = tg.scaled_config(5, row_scale=0.005, batches=4, bags=128, max_tables=4, ways=ways)
         tabs = [w.table_values(t) for t in range(w.num_tables)]
         g = GpuRunner(w, tabs, miss_mode=mode)
-        outs.append(g.run())
+        runs.append(g.run())
         g.close()
-    for a, b in zip(*outs):
-        assert np.array_equal(a["out"], b["out"])
-        assert a["fwd"] == b["fwd"] and a["place"] == b["place"]
+    for other in runs[1:]:
+        for a, b in zip(runs[0], other):
+            assert np.array_equal(a["out"], b["out"])
+            assert a["fwd"] == b["fwd"] and a["place"] == b["place"]
+            assert all(np.array_equal(x, y) for x, y in zip(a["resident"], b["resident"]))
 
 
 def test_run_twice_is_deterministic():
