@@ -91,6 +91,32 @@ def huge_page_tensor(shape, dtype):
     return torch.from_numpy(arr).view(dtype).view(shape)
 
 
+_PINNED = []
+
+
+def pinned_tensor(shape, dtype):
+    """Page-locked host tensor of exactly its size, from hipHostMalloc in the
+    HIP runtime torch has loaded (torch's pinned allocator rounds a request up
+    to a power of two: a 25.6 GB table would pin 32 GiB, and the host caps
+    pinned memory).  Freed at exit."""
+    import atexit
+    import ctypes
+
+    import numpy as np
+    import torch
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    nbytes = int(np.prod(shape)) * torch.empty((), dtype=dtype).element_size()
+    ptr = ctypes.c_void_p()
+    rc = hip.hipHostMalloc(ctypes.byref(ptr), ctypes.c_size_t(max(nbytes, 1)), ctypes.c_uint(0))
+    if rc != 0 or not ptr.value:
+        raise MemoryError(f"hipHostMalloc of {nbytes} bytes failed with status {rc}")
+    if not _PINNED:
+        atexit.register(lambda: [hip.hipHostFree(p) for p in _PINNED])
+    _PINNED.append(ptr)
+    arr = np.ctypeslib.as_array((ctypes.c_uint8 * max(nbytes, 1)).from_address(ptr.value))[:nbytes]
+    return torch.from_numpy(arr).view(dtype).view(shape)
+
+
 def buffer_sweep(args, dev):
     """Hit rate against buffer size on one configuration's trace (Sec. VII-D's
     sweep, on synthetic traces): every point runs the HIP path and the oracle
@@ -292,7 +318,7 @@ def main():
     # on the host only and stay pageable
     modes = ["zero_copy" if args.miss_mode == "zero_copy" or t < args.zero_copy_tables else "staged"
              for t in range(T)]
-    host = [torch.empty((tb.rows, tb.dim), dtype=tdt[tb.dtype], pin_memory=True) if m == "zero_copy"
+    host = [pinned_tensor((tb.rows, tb.dim), tdt[tb.dtype]) if m == "zero_copy"
             else huge_page_tensor((tb.rows, tb.dim), tdt[tb.dtype]) for tb, m in zip(w.tables, modes)]
     for t in range(T):  # each table's rows are drawn in parallel chunks
         w.table_values(t, out=host[t].numpy())

@@ -69,7 +69,7 @@ struct Layout {
     size_t sa_bstart = 0, sa_btab = 0, fdesc = 0, stat_log = 0;
     size_t fstage = 0;
     // pinned host staging (STAGED): miss ids, miss rows, fill sources, prefetch rows
-    size_t h_mrows = 0, h_rows = 0, h_fsrc = 0, h_frows = 0;
+    size_t h_mrows = 0, h_rows = 0, h_fsrc = 0, h_frows = 0, h_np = 0, h_early = 0;
     size_t staging[2] = {0, 0};
     int64_t stage_stride = 0, sum_cap = 0;
     int32_t total_bm_blocks = 0;
@@ -235,6 +235,8 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
         L->h_rows = htake(mi * (size_t)L->stage_stride);
         L->h_fsrc = htake(4 * (mi + mp));
         L->h_frows = htake(mp * (size_t)L->stage_stride);
+        L->h_np = htake(4 * mp);
+        L->h_early = htake(sizeof(TState) * T + 8 * (T + 1) + 8);
         L->host_total = h;
     }
 }
@@ -290,6 +292,14 @@ struct recmg_cache {
     // STAGED
     hipStream_t copy_stream = nullptr;
     hipEvent_t ev_ready = nullptr, ev_copied = nullptr;
+    hipEvent_t ev_np = nullptr;  // a placement's new prefetch candidates have reached the host
+    int32_t *h_np = nullptr;     // those candidates (NP), for the early gather
+    // pinned copies made with them: table states, prefetch list starts, error word
+    TState *he_st = nullptr;
+    int64_t *he_pstart = nullptr;
+    int32_t *he_err = nullptr;
+    bool has_staged_fa = false;  // STAGED fully associative tables with slots (gathered early)
+    bool has_staged_sa = false;  // STAGED set-associative tables (gathered after their placement)
     int32_t *h_mrows = nullptr;
     char *h_rows = nullptr;
     int32_t *h_fsrc = nullptr;  // fill sources of a placement, rewritten to staged rows
@@ -311,7 +321,7 @@ struct recmg_cache {
     // Every event the handle created, also when init stops half way.  The
     // caller of delete has synchronised (or nothing was enqueued).
     ~recmg_cache() {
-        for (hipEvent_t e : {ev_src, ev_pool, ev_fwd, ev_plc, ev_fill[0], ev_fill[1], ev_ready, ev_copied})
+        for (hipEvent_t e : {ev_src, ev_pool, ev_fwd, ev_plc, ev_fill[0], ev_fill[1], ev_ready, ev_copied, ev_np})
             if (e) (void)hipEventDestroy(e);
         for (const Mark &m : marks) {
             if (m.a) (void)hipEventDestroy(m.a);
@@ -506,7 +516,9 @@ int32_t staged_fill(recmg_cache_t *c, hipStream_t s, hipStream_t cs) {
     int64_t total = 0;
     for (int t = 0; t < T; ++t) {
         base[t] = c->h_ftstart[t] + c->h_pstart[t];
-        nfill[t] = c->geo[t].staged ? c->h_st[t].popped : 0;  // zero-copy tables' fills read the host themselves
+        // zero-copy tables' fills read the host themselves; fully associative
+        // STAGED tables' prefetch rows were gathered early (early_gather)
+        nfill[t] = c->geo[t].staged && c->geo[t].ways ? c->h_st[t].popped : 0;
         if (base[t] < 0 || nfill[t] < 0 || base[t] + nfill[t] > c->g.fill_cap)
             return fail(RECMG_E_STATE, "fill list outside its buffer");
         if (nfill[t])
@@ -556,6 +568,44 @@ int32_t staged_fill(recmg_cache_t *c, hipStream_t s, hipStream_t cs) {
         return RECMG_OK;
     };
     return gather_and_copy(nfill, work, copy);
+}
+
+// Early gather of the prefetch rows of fully associative STAGED tables: the
+// placement's new prefetch candidates (NP, with their counts) came back to
+// the host right after classification (ev_np), so the host gathers their rows
+// into pinned staging and copies them to the device (fstage row pstart[t] + k
+// for NP[pstart[t] + k]) while the GPU ranks and admits; admission points each
+// admitted candidate's fill at that row.  A candidate the ranking drops was
+// gathered for nothing (under LRU a new prefetch candidate is dropped only
+// when the candidates outnumber the cache).
+int32_t early_gather(recmg_cache_t *c, hipStream_t cs) {
+    const int T = c->T;
+    HIP_TRY(hipEventSynchronize(c->ev_np));
+    if (*c->he_err) return RECMG_OK;  // the device flag already disables the rest
+    const int64_t *ps = c->he_pstart;
+    std::vector<int64_t> n(T, 0);
+    for (int t = 0; t < T; ++t) {
+        const Geom &ge = c->geo[t];
+        if (!ge.staged || ge.ways || ge.cap == 0) continue;
+        n[t] = c->he_st[t].npcount;
+        if (n[t] < 0 || ps[t] < 0 || ps[t] + n[t] > ps[t + 1] || ps[t + 1] > c->cfg.max_prefetch)
+            return fail(RECMG_E_STATE, "prefetch candidates outside their list");
+    }
+    const int64_t stride = c->L.stage_stride;
+    auto work = [&](int t, int64_t lo, int64_t hi) {
+        const int64_t p0 = ps[t], rb = c->geo[t].row_bytes;
+        for (int64_t k = lo; k < hi; ++k) {
+            if (k + kAhead < hi) prefetch_row(c->host[t] + (int64_t)c->h_np[p0 + k + kAhead] * rb, rb);
+            std::memcpy(c->h_frows + (p0 + k) * stride, c->host[t] + (int64_t)c->h_np[p0 + k] * rb, (size_t)rb);
+        }
+    };
+    auto copy = [&](int t, int64_t lo, int64_t hi) -> int32_t {
+        const int64_t r0 = ps[t] + lo;
+        HIP_TRY(hipMemcpyAsync(c->g.fstage + r0 * stride, c->h_frows + r0 * stride, (size_t)((hi - lo) * stride),
+                               hipMemcpyHostToDevice, cs));
+        return RECMG_OK;
+    };
+    return gather_and_copy(n, work, copy);
 }
 
 // STAGED miss path: miss ids of the STAGED tables to the host, a parallel
@@ -735,6 +785,8 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         c->host.push_back(static_cast<const char *>(cfg->host_tables[t]));
         if (geo[t].staged) c->has_staged = true;
         else c->has_zc = true;
+        if (geo[t].staged && geo[t].ways) c->has_staged_sa = true;
+        if (geo[t].staged && !geo[t].ways && geo[t].cap > 0) c->has_staged_fa = true;
         if (geo[t].staged) {
             dev_host[t] = nullptr;  // only the host reads the tables: any host memory will do
             continue;
@@ -899,10 +951,15 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         c->h_rows = hs + L.h_rows;
         c->h_fsrc = reinterpret_cast<int32_t *>(hs + L.h_fsrc);
         c->h_frows = hs + L.h_frows;
+        c->h_np = reinterpret_cast<int32_t *>(hs + L.h_np);
+        c->he_st = reinterpret_cast<TState *>(hs + L.h_early);
+        c->he_pstart = reinterpret_cast<int64_t *>(hs + L.h_early + sizeof(TState) * T);
+        c->he_err = reinterpret_cast<int32_t *>(hs + L.h_early + sizeof(TState) * T + 8 * (T + 1));
         c->h_pstart.resize(T + 1);
         c->h_ftstart.resize(T + 1);
         HIP_TRY(hipEventCreateWithFlags(&c->ev_ready, hipEventDisableTiming));
         HIP_TRY(hipEventCreateWithFlags(&c->ev_copied, hipEventDisableTiming));
+        HIP_TRY(hipEventCreateWithFlags(&c->ev_np, hipEventDisableTiming));
     }
     c->h_st.resize(T);
     c->h_tstart.resize(T + 1);
@@ -972,6 +1029,16 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
             launch_plc_classify(g, p.last_stamp, num_prefetch, s);
         }
     }
+    // fully associative STAGED tables: their new prefetch candidates go to the
+    // host now, so that it gathers their rows while the GPU ranks (early_gather)
+    const bool early = c->has_staged_fa && num_prefetch > 0;
+    if (early) {
+        HIP_TRY(hipMemcpyAsync(c->he_st, g.st, sizeof(TState) * c->T, hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(c->he_pstart, g.pstart, 8 * (c->T + 1), hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(c->h_np, g.NP, 4 * (size_t)num_prefetch, hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipMemcpyAsync(c->he_err, g.err, 4, hipMemcpyDeviceToHost, s));
+        HIP_TRY(hipEventRecord(c->ev_np, s));
+    }
     const int64_t cand = (c->have_fwd ? c->last_n : 0) + num_prefetch;
     const int64_t per_table = c->max_cap + (cand + c->T - 1) / c->T;
     const int64_t cand_grid = std::min<int64_t>(std::max<int64_t>(cand / c->T, 1024), cand + 1);
@@ -987,12 +1054,19 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     }
     launch_plc_finalize(g, fdesc, c->cfg.stats_log_calls ? c->calls % c->cfg.stats_log_calls : -1, s);
     HIP_TRY(hipEventRecord(c->ev_plc, s));
+    hipStream_t fs = c->copy_stream ? c->copy_stream : s;
+    if (early) {
+        // the host gathers while the kernels above run; the copies go on the
+        // fill stream ahead of the fill (the last fill to read fstage has
+        // ended: this placement's stream waited for it)
+        StageTimer tm(c, RECMG_STAGE_PLC_FILL, fs);
+        if ((rc = early_gather(c, fs))) return rc;
+    }
     // The fill overwrites the slots of evicted rows: it waits for the latest
     // forward's pooled kernel, which may read them, and for this placement.
     // On the copy stream it overlaps the next forward's dedup and probe (and a
     // placement on a stream of its own overlaps the previous fill); that
     // forward's pooled kernel waits for it.
-    hipStream_t fs = c->copy_stream ? c->copy_stream : s;
     if (fs != s) HIP_TRY(hipStreamWaitEvent(fs, c->ev_plc, 0));
     if (c->fwd_ev && c->fwd_stream != fs) HIP_TRY(hipStreamWaitEvent(fs, c->ev_pool, 0));
     // The previous placement's fill may still write slots this placement has
@@ -1009,7 +1083,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         DispatchTimer dt(c, RECMG_STAGE_PLC_FILL, true);
         if (c->has_zc) launch_plc_fill(g, fdesc, FILL_ZERO_COPY, fs, dt.a, c->has_staged ? nullptr : dt.b);
         if (c->has_staged) {
-            if ((rc = staged_fill(c, s, fs))) return rc;  // host-staged rows
+            if (c->has_staged_sa && (rc = staged_fill(c, s, fs))) return rc;  // host-staged rows
             launch_plc_fill(g, fdesc, FILL_STAGED, fs, c->has_zc ? nullptr : dt.a, dt.b);
         }
         dt.issued();

@@ -259,6 +259,8 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
             row = tb.slot_row[k];
             s = tb.slot_score[k];
             uint32_t f = tb.slot_flags[k];
+            const int32_t s0 = s;
+            const uint32_t f0 = f;
             const int cb = tb.slot_cbit[k];
             if (cb) tb.slot_cbit[k] = 0;
             if (p.prio) s = s > 0 ? s - 1 : 0;
@@ -267,10 +269,9 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
                 s = touch_score(p, tb, row, cb);
             }
             if ((f & F_INP) && s < p.pscore) s = p.pscore;
-            if (row >= 0) {
-                tb.slot_score[k] = s;
-                tb.slot_flags[k] = f & ~F_INP;
-            }
+            // written back only where they change (most slots keep both)
+            if (row >= 0 && s != s0) tb.slot_score[k] = s;
+            if (row >= 0 && (f & ~F_INP) != f0) tb.slot_flags[k] = f & ~F_INP;
         } else if (k < (int64_t)c.cap + c.nm) {
             const int64_t m = ts + (k - c.cap);
             row = g.M[m];
@@ -348,46 +349,74 @@ __device__ __forceinline__ bool block_err(const DGlobal &g) {
     return s_err != 0;
 }
 
+// Slots a block collects in LDS before it reserves free-stack space for
+// them: one atomic on the table's stack top per block in the common case (a
+// few hundred evictions per block), instead of one per 256 slots scanned (a
+// full cache of 19.5 million slots would queue some 76,000 of those on one
+// word per table).  Freed slots enter the stack in no fixed order; slot
+// numbers are not observable.
+constexpr int kEvictBuf = 2048;
+
 __global__ void __launch_bounds__(kBlock) k_plc_evict(DGlobal g, PlcParams p) {
     if (block_err(g)) return;
     __shared__ int tmp[16];
-    __shared__ int s_base;
+    __shared__ int s_base, s_n;
+    __shared__ int32_t s_free[kEvictBuf];
     const int t = blockIdx.y;
     const DTable &tb = g.tabs[t];
     if (tb.ways) return;
     TState &st = g.st[t];
     const int mode = st.sel_mode;
     const uint64_t thr = st.prefix;
+    const int lane = threadIdx.x & 63;
+    if (threadIdx.x == 0) s_n = 0;
+    __syncthreads();
+    // reserve stack space for the collected slots with one atomic and write
+    // them out; every thread calls (s_n is read after a barrier)
+    auto flush = [&]() {
+        const int n = s_n;
+        if (n == 0) return;
+        if (threadIdx.x == 0) s_base = atomicAdd(&st.free_top, n);
+        __syncthreads();
+        for (int i = threadIdx.x; i < n; i += blockDim.x) {
+            const int64_t at = (int64_t)s_base + i;
+            if (at < tb.cap) tb.free_stack[at] = s_free[i];
+            else atomicOr(g.err, ERR_INTERNAL);
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) s_n = 0;
+        __syncthreads();
+    };
     int nev = 0;
     unsigned long long dig = 0;
     for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < tb.cap; base += (int64_t)gridDim.x * blockDim.x) {
         const int64_t k = base + threadIdx.x;
-        int ev = 0;
+        bool ev = false;
         if (k < tb.cap) {
             const int32_t row = tb.slot_row[k];
             if (row >= 0) {
                 if (kept(mode, make_key(tb.slot_score[k], row, p.rowbits), thr)) {
                     dig += mix64(((unsigned long long)t << 40) | (unsigned long long)row);
                 } else {
-                    ev = 1;
+                    ev = true;
                     map_delete(tb, row);
                     tb.slot_row[k] = -1;
                     tb.slot_flags[k] = 0;
                 }
             }
         }
-        int tot;
-        const int ex = block_excl_scan(ev, tmp, &tot);
-        if (threadIdx.x == 0 && tot) s_base = atomicAdd(&st.free_top, tot);
+        // append the wave's freed slots to the block's list (one LDS atomic per wave)
+        const uint64_t m = __ballot(ev);
+        int wb = 0;
+        if (lane == 0 && m) wb = atomicAdd(&s_n, __popcll(m));
+        wb = __shfl(wb, 0);
+        if (ev) s_free[wb + __popcll(m & ((1ull << lane) - 1ull))] = (int32_t)k;
+        nev += ev ? 1 : 0;
         __syncthreads();
-        if (ev) {
-            const int64_t at = (int64_t)s_base + ex;
-            if (at < tb.cap) tb.free_stack[at] = (int32_t)k;
-            else atomicOr(g.err, ERR_INTERNAL);
-        }
-        nev += ev;
-        __syncthreads();
+        if (s_n > kEvictBuf - (int)blockDim.x) flush();  // room for one more pass of the block
     }
+    __syncthreads();
+    flush();
     const int e = block_sum(nev, tmp);
     const unsigned long long d = wave_sum64(dig);
     if ((threadIdx.x & 63) == 0 && d) atomicAdd(&st.digest_acc, d);
@@ -480,8 +509,11 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
                 tb.slot_flags[slot] = inp ? F_PF : 0u;
                 tb.slot_touch[slot] = -1;
                 n_reuse += map_insert(tb, row, slot);
-                // the fill list: admitted row j of this table, its source and slot
-                g.fill_src[fj] = is_miss ? (int32_t)k : -(row + 1);
+                // the fill list: admitted row j of this table, its source and
+                // slot: a miss's staging row; a prefetch row's host row, or for
+                // a STAGED table the staged row of its candidate (the host
+                // gathered NP[ps + i] into row ps + i)
+                g.fill_src[fj] = is_miss ? (int32_t)k : tb.staged ? -(int32_t)(ps + (k - c.nm)) - 1 : -(row + 1);
                 g.fill_slot[fj] = slot;
                 dig += mix64(((unsigned long long)t << 40) | (unsigned long long)row);
                 if (is_miss) ++n_adm_miss;

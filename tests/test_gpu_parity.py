@@ -201,8 +201,9 @@ def test_mixed_miss_modes(cid, scale, tables, ways):
     _parity(w, miss_mode=modes, label=f"c{cid}-mixed", pin=False)
 
 
-@pytest.mark.parametrize("overlap,sync", [(True, True), (True, False), (False, False)])
-def test_two_placements_in_a_row(overlap, sync):
+@pytest.mark.parametrize("overlap,sync,mode", [(True, True, "zero_copy"), (True, False, "zero_copy"),
+                                               (False, False, "zero_copy"), (True, False, "staged")])
+def test_two_placements_in_a_row(overlap, sync, mode):
     """Two placements in a row (no forward between), each on a stream other
     than the last call's, then a forward on a third stream.  The second
     placement frees slots the first one's fill may still be writing; its fill
@@ -215,7 +216,7 @@ def test_two_placements_in_a_row(overlap, sync):
     f64 = [tg.storage_to_f64(a, tb.dtype) for a, tb in zip(tabs, w.tables)]
     import oracle
     o = oracle.for_workload(w, tabs)
-    g = GpuRunner(w, tabs, overlap=overlap)
+    g = GpuRunner(w, tabs, overlap=overlap, miss_mode=mode)
     streams = [th.cuda.Stream(), th.cuda.Stream(), th.cuda.Stream()]
     try:
         for b in range(w.batches):
@@ -534,15 +535,20 @@ def test_lfu_configs_scaled(cid, scale, tables, ways):
 
 # ----------------------------------------------------------------------------- random call sequences
 
-@pytest.mark.parametrize("seed,overlap", [(s, True) for s in range(9)] + [(s, False) for s in range(6)])
-def test_random_call_sequences(seed, overlap):
+@pytest.mark.parametrize("seed,overlap,mode", [(s, True, "zero_copy") for s in range(9)]
+                         + [(s, False, "zero_copy") for s in range(6)]
+                         + [(s, True, "staged") for s in (0, 1, 2, 4)]
+                         + [(s, True, ["zero_copy", "staged", "staged"]) for s in (3, 5)])
+def test_random_call_sequences(seed, overlap, mode):
     """Random interleavings of placements and forwards on three streams (two
     placements or two forwards in a row, batches out of order, calls on a
     stream other than the previous call's), checked against the oracle
     replaying the same calls: totals, resident sets and digests at random
     check points, every forward's pooled sums at the end.  The library orders
     calls across streams by events; nothing here synchronises between calls.
-    overlap=False: no copy stream, so each fill runs on its placement's stream."""
+    overlap=False: no copy stream, so each fill runs on its placement's stream.
+    STAGED and mixed modes: host-gathered rows (prefetch rows gathered while the
+    placement ranks) under the same interleavings."""
     import torch as th
     import oracle
     rng = np.random.default_rng(7000 + seed)
@@ -552,7 +558,9 @@ def test_random_call_sequences(seed, overlap):
     w.ways = (0, 4, 32)[(seed // 3) % 3]
     tabs = [w.table_values(t) for t in range(w.num_tables)]
     o = oracle.for_workload(w, tabs)
-    g = GpuRunner(w, tabs, overlap=overlap)
+    if not isinstance(mode, str):
+        mode = (mode * w.num_tables)[:w.num_tables]
+    g = GpuRunner(w, tabs, overlap=overlap, miss_mode=mode)
     f64 = [tg.storage_to_f64(a, tb.dtype) for a, tb in zip(tabs, w.tables)]
     streams = [th.cuda.current_stream(), th.cuda.Stream(), th.cuda.Stream()]
     T = w.num_tables
