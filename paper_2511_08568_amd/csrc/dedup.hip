@@ -77,7 +77,12 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
             const uint32_t pos = bm_pos(s_ns[t], s_qb[t], r);
             uint32_t *w = s_bm[t] + (pos >> 5);
             const uint32_t bit = 1u << (pos & 31);
-            if (!(__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit)) atomicOr(w, bit);
+            // A plain (cached) read first: bits only go from 0 to 1 during
+            // this kernel and the previous dedup's clears are visible at the
+            // kernel boundary, so a stale read can only show 0, which costs a
+            // redundant (idempotent) atomic; a device-scope read went to the
+            // fabric for every mark.
+            if (!(gload4(w) & bit)) atomicOr(w, bit);
         }
     }
 }

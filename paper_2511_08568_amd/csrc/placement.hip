@@ -228,6 +228,21 @@ __global__ void __launch_bounds__(kBlock) k_plc_pick(DGlobal g, PlcParams p, int
     }
 }
 
+// The scans over every slot (score update, select passes, evict) take four
+// consecutive slots per thread with 16-byte loads issued together: with one
+// slot per thread and a score load that waited for the row load, they were
+// bound by load latency (configuration 4's 78 million slots: about 1 TB/s).
+// Slots [k0, k0 + 4) of a table, absent ones (k >= cap) reading row -1.
+__device__ __forceinline__ void slot_quad(const int32_t *a, int64_t k0, int64_t cap, int32_t fill, int32_t (&v)[4]) {
+    if (k0 + 3 < cap) {
+        const uint4 w = gload16(a + k0);
+        v[0] = (int32_t)w.x, v[1] = (int32_t)w.y, v[2] = (int32_t)w.z, v[3] = (int32_t)w.w;
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = k0 + i < cap ? (int32_t)gload4(a + k0 + i) : fill;
+    }
+}
+
 // Scores of every candidate (written back) and the first select pass.
 __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
     if (*g.err) return;
@@ -248,39 +263,65 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
     const int64_t ts = g.tstart[t], ps = g.pstart[t];
     const int shift = pass_shift(p, 0);
     const uint32_t dmask = (1u << pass_width(p, 0)) - 1u;
-    const int64_t items = (int64_t)c.cap + c.nm + c.nnp;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    // every lane runs the same number of iterations (hist_add is wave-wide)
-    const int64_t items_r = (items + 63) & ~(int64_t)63;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < items_r; k += stride) {
-        int32_t row = -1, s = 0;
-        if (k >= items) {
-        } else if (k < c.cap) {
-            row = tb.slot_row[k];
-            s = tb.slot_score[k];
-            uint32_t f = tb.slot_flags[k];
-            const int32_t s0 = s;
-            const uint32_t f0 = f;
-            const int cb = tb.slot_cbit[k];
-            if (cb) tb.slot_cbit[k] = 0;
-            if (p.prio) s = s > 0 ? s - 1 : 0;
-            if (row >= 0 && tb.slot_touch[k] == p.last_stamp) {
-                f &= ~F_PF;
-                s = touch_score(p, tb, row, cb);
+    const int64_t cap = c.cap;
+    // resident slots, four per thread; every lane runs the same number of
+    // iterations (hist_add is wave-wide)
+    const int64_t ngrp = (cap + 3) / 4, ngrp_r = (ngrp + 63) & ~(int64_t)63;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < ngrp_r; q += stride) {
+        const int64_t k0 = 4 * q;
+        const int64_t lim = q < ngrp ? cap : 0;  // lanes past the last group see no slot
+        int32_t row[4], sc[4], fl[4], tch[4];
+        slot_quad(tb.slot_row, k0, lim, -1, row);
+        slot_quad(tb.slot_score, k0, lim, 0, sc);
+        slot_quad(reinterpret_cast<const int32_t *>(tb.slot_flags), k0, lim, 0, fl);
+        slot_quad(tb.slot_touch, k0, lim, -1, tch);
+        uint32_t cbw = 0;
+        if (k0 + 3 < lim) cbw = gload4(tb.slot_cbit + k0);
+        else
+            for (int i = 0; i < 4; ++i)
+                if (k0 + i < lim) cbw |= (uint32_t)tb.slot_cbit[k0 + i] << (8 * i);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t k = k0 + i;
+            const int32_t r = row[i];
+            int32_t s = sc[i];
+            uint32_t f = (uint32_t)fl[i];
+            const int cb = (int)((cbw >> (8 * i)) & 0xffu);
+            if (k < lim) {
+                if (p.prio) s = s > 0 ? s - 1 : 0;
+                if (r >= 0 && tch[i] == p.last_stamp) {
+                    f &= ~F_PF;
+                    s = touch_score(p, tb, r, cb);
+                }
+                if ((f & F_INP) && s < p.pscore) s = p.pscore;
+                // written back only where they change (most slots keep both)
+                if (r >= 0 && s != sc[i]) tb.slot_score[k] = s;
+                if (r >= 0 && (f & ~F_INP) != (uint32_t)fl[i]) tb.slot_flags[k] = f & ~F_INP;
             }
-            if ((f & F_INP) && s < p.pscore) s = p.pscore;
-            // written back only where they change (most slots keep both)
-            if (row >= 0 && s != s0) tb.slot_score[k] = s;
-            if (row >= 0 && (f & ~F_INP) != f0) tb.slot_flags[k] = f & ~F_INP;
-        } else if (k < (int64_t)c.cap + c.nm) {
-            const int64_t m = ts + (k - c.cap);
+            if (sel) hist_add(s_hist, k < lim && r >= 0, (uint32_t)(make_key(s, r < 0 ? 0 : r, p.rowbits) >> shift) & dmask);
+        }
+        if (cbw) {  // caching bits are zero between placements
+            if (k0 + 3 < lim) *reinterpret_cast<uint32_t *>(tb.slot_cbit + k0) = 0u;
+            else
+                for (int i = 0; i < 4; ++i)
+                    if (k0 + i < lim && ((cbw >> (8 * i)) & 0xffu)) tb.slot_cbit[k0 + i] = 0;
+        }
+    }
+    // candidates: the last batch's misses, then new prefetch rows
+    const int64_t nc = (int64_t)c.nm + c.nnp, nc_r = (nc + 63) & ~(int64_t)63;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < nc_r; k += stride) {
+        int32_t row = -1, s = 0;
+        if (k >= nc) {
+        } else if (k < c.nm) {
+            const int64_t m = ts + k;
             row = g.M[m];
             const uint32_t f = g.mflags[m];
             s = touch_score(p, tb, row, g.mcbit[m]);
             if ((f & F_INP) && s < p.pscore) s = p.pscore;
             g.mscore[m] = s;
         } else {
-            row = g.NP[ps + (k - c.cap - c.nm)];
+            row = g.NP[ps + (k - c.nm)];
             s = new_prefetch_score(p, tb, row);
         }
         if (sel) hist_add(s_hist, row >= 0, (uint32_t)(make_key(s, row < 0 ? 0 : row, p.rowbits) >> shift) & dmask);
@@ -289,23 +330,19 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
     if (sel) hist_merge(g, t, s_hist);
 }
 
-__device__ __forceinline__ bool item_key(const DGlobal &g, const DTable &tb, const Counts &c, const PlcParams &p,
-                                         int64_t ts, int64_t ps, int64_t k, uint64_t *key) {
+// Key of candidate k (k < nm: a miss of the last batch; else a new prefetch row).
+__device__ __forceinline__ uint64_t cand_key(const DGlobal &g, const DTable &tb, const Counts &c, const PlcParams &p,
+                                             int64_t ts, int64_t ps, int64_t k) {
     int32_t row, s;
-    if (k < c.cap) {
-        row = tb.slot_row[k];
-        if (row < 0) return false;
-        s = tb.slot_score[k];
-    } else if (k < (int64_t)c.cap + c.nm) {
-        const int64_t m = ts + (k - c.cap);
+    if (k < c.nm) {
+        const int64_t m = ts + k;
         row = g.M[m];
         s = g.mscore[m];
     } else {
-        row = g.NP[ps + (k - c.cap - c.nm)];
+        row = g.NP[ps + (k - c.nm)];
         s = new_prefetch_score(p, tb, row);
     }
-    *key = make_key(s, row, p.rowbits);
-    return true;
+    return make_key(s, row, p.rowbits);
 }
 
 __global__ void __launch_bounds__(kBlock) k_plc_select(DGlobal g, PlcParams p, int pass) {
@@ -321,12 +358,26 @@ __global__ void __launch_bounds__(kBlock) k_plc_select(DGlobal g, PlcParams p, i
     const int64_t ts = g.tstart[t], ps = g.pstart[t];
     const int shift = pass_shift(p, pass);
     const uint64_t prefix = st.prefix;
-    const int64_t items = (int64_t)c.cap + c.nm + c.nnp;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    const int64_t items_r = (items + 63) & ~(int64_t)63;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < items_r; k += stride) {
-        uint64_t key = 0;
-        const bool in = k < items && item_key(g, tb, c, p, ts, ps, k, &key) && (key >> (shift + kRadixBits)) == prefix;
+    const int64_t cap = c.cap;
+    const int64_t ngrp = (cap + 3) / 4, ngrp_r = (ngrp + 63) & ~(int64_t)63;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < ngrp_r; q += stride) {
+        const int64_t k0 = 4 * q;
+        const int64_t lim = q < ngrp ? cap : 0;
+        int32_t row[4], sc[4];
+        slot_quad(tb.slot_row, k0, lim, -1, row);
+        slot_quad(tb.slot_score, k0, lim, 0, sc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint64_t key = make_key(sc[i], row[i] < 0 ? 0 : row[i], p.rowbits);
+            const bool in = row[i] >= 0 && (key >> (shift + kRadixBits)) == prefix;
+            hist_add(s_hist, in, (uint32_t)(key >> shift) & (kRadix - 1));
+        }
+    }
+    const int64_t nc = (int64_t)c.nm + c.nnp, nc_r = (nc + 63) & ~(int64_t)63;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < nc_r; k += stride) {
+        const uint64_t key = k < nc ? cand_key(g, tb, c, p, ts, ps, k) : 0;
+        const bool in = k < nc && (key >> (shift + kRadixBits)) == prefix;
         hist_add(s_hist, in, (uint32_t)(key >> shift) & (kRadix - 1));
     }
     __syncthreads();
@@ -389,31 +440,40 @@ __global__ void __launch_bounds__(kBlock) k_plc_evict(DGlobal g, PlcParams p) {
     };
     int nev = 0;
     unsigned long long dig = 0;
-    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < tb.cap; base += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t k = base + threadIdx.x;
-        bool ev = false;
-        if (k < tb.cap) {
-            const int32_t row = tb.slot_row[k];
-            if (row >= 0) {
-                if (kept(mode, make_key(tb.slot_score[k], row, p.rowbits), thr)) {
-                    dig += mix64(((unsigned long long)t << 40) | (unsigned long long)row);
+    const int64_t cap = tb.cap;
+    // four slots per thread; a block's iterations are uniform (its barriers)
+    const int64_t ngrp = (cap + 3) / 4, stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < ngrp; base += stride) {
+        const int64_t q = base + threadIdx.x;
+        const int64_t k0 = 4 * q;
+        const int64_t lim = q < ngrp ? cap : 0;
+        int32_t row[4], sc[4];
+        slot_quad(tb.slot_row, k0, lim, -1, row);
+        slot_quad(tb.slot_score, k0, lim, 0, sc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t k = k0 + i;
+            bool ev = false;
+            if (row[i] >= 0) {
+                if (kept(mode, make_key(sc[i], row[i], p.rowbits), thr)) {
+                    dig += mix64(((unsigned long long)t << 40) | (unsigned long long)row[i]);
                 } else {
                     ev = true;
-                    map_delete(tb, row);
+                    map_delete(tb, row[i]);
                     tb.slot_row[k] = -1;
                     tb.slot_flags[k] = 0;
                 }
             }
+            // append the wave's freed slots to the block's list (one LDS atomic per wave)
+            const uint64_t m = __ballot(ev);
+            int wb = 0;
+            if (lane == 0 && m) wb = atomicAdd(&s_n, __popcll(m));
+            wb = __shfl(wb, 0);
+            if (ev) s_free[wb + __popcll(m & ((1ull << lane) - 1ull))] = (int32_t)k;
+            nev += ev ? 1 : 0;
         }
-        // append the wave's freed slots to the block's list (one LDS atomic per wave)
-        const uint64_t m = __ballot(ev);
-        int wb = 0;
-        if (lane == 0 && m) wb = atomicAdd(&s_n, __popcll(m));
-        wb = __shfl(wb, 0);
-        if (ev) s_free[wb + __popcll(m & ((1ull << lane) - 1ull))] = (int32_t)k;
-        nev += ev ? 1 : 0;
         __syncthreads();
-        if (s_n > kEvictBuf - (int)blockDim.x) flush();  // room for one more pass of the block
+        if (s_n > kEvictBuf - 4 * (int)blockDim.x) flush();  // room for one more pass of the block
     }
     __syncthreads();
     flush();
