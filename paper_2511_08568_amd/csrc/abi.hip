@@ -66,7 +66,7 @@ struct Layout {
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, raddr = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
     size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, pool_btab = 0, ftstart = 0;
-    size_t sa_bstart = 0, sa_btab = 0, fdesc = 0, stat_log = 0;
+    size_t sa_bstart = 0, sa_btab = 0, fdesc = 0, stat_log = 0, pfrom = 0;
     size_t fstage = 0;
     // pinned host staging (STAGED): miss ids, miss rows, fill sources, prefetch rows
     size_t h_mrows = 0, h_rows = 0, h_fsrc = 0, h_frows = 0, h_np = 0, h_early = 0;
@@ -219,6 +219,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->stat_log = take((size_t)cfg->stats_log_calls * T * sizeof(recmg_table_stats_t));
     L->sa_bstart = take(4 * (T + 1));
     L->sa_btab = take(4 * T);
+    L->pfrom = take(cfg->ways > 0 ? 4 * mp : 0);
     L->staging[0] = take(mi * (size_t)L->stage_stride);
     L->staging[1] = take(mi * (size_t)L->stage_stride);
     const bool staged = any_staged(geo);
@@ -252,7 +253,7 @@ struct recmg_cache {
     Layout L;
     DGlobal g{};
     std::vector<const char *> host;  // host tables (host pointers)
-    int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1, nsa = 0;
+    int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1, nsa = 0, max_nblk = 0;
     int64_t sa_blocks = 0;  // blocks of the set-associative placement kernel
     bool has_fa = false, has_sa = false;  // tables of each form present
     bool has_zc = false, has_staged = false;  // tables of each miss mode present
@@ -841,6 +842,7 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.stat_log = reinterpret_cast<int64_t *>(ws + L.stat_log);
     g.sa_bstart = reinterpret_cast<int32_t *>(ws + L.sa_bstart);
     g.sa_btab = reinterpret_cast<int32_t *>(ws + L.sa_btab);
+    g.pfrom = reinterpret_cast<int32_t *>(ws + L.pfrom);
 
     std::vector<DTable> tabs(T);
     std::vector<int32_t> bstart(T + 1, 0);
@@ -895,6 +897,7 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         c->max_map = (int32_t)std::max<int64_t>(c->max_map, ge.map_cap);
         c->max_units = std::max(c->max_units, ge.row_bytes / ge.copy_unit);
         c->max_rows = std::max(c->max_rows, ge.rows);
+        c->max_nblk = std::max(c->max_nblk, ge.bm_nblk);
     }
     c->rowbits = std::max(1, bitlen((uint64_t)(c->max_rows - 1)));
     c->pool_order.resize(T);
@@ -1025,7 +1028,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
             launch_mark(g, prefetch_rows, g.pstart, num_prefetch, s);
             launch_dedup(g, EMIT_PREFETCH,
                          reinterpret_cast<int32_t *>(reinterpret_cast<char *>(g.st) + offsetof(TState, pcount)),
-                         (int)(sizeof(TState) / 4), 0, s);
+                         (int)(sizeof(TState) / 4), 0, c->max_nblk, s);
             launch_plc_classify(g, p.last_stamp, num_prefetch, s);
         }
     }
@@ -1156,7 +1159,7 @@ int32_t recmg_embbag_forward(recmg_cache_t *c, const int32_t *indices, const int
             launch_mark(g, indices, g.tstart, n, s);
             launch_dedup(g, EMIT_FORWARD,
                          reinterpret_cast<int32_t *>(reinterpret_cast<char *>(g.st) + offsetof(TState, ucount)),
-                         (int)(sizeof(TState) / 4), stamp, s);
+                         (int)(sizeof(TState) / 4), stamp, c->max_nblk, s);
             launch_fwd_probe(g, stamp, n, s);
             launch_fwd_src(g, indices, n, s);
             if (c->plc_np >= 0) launch_fwd_cover(g, stamp, c->plc_np, s);
@@ -1241,7 +1244,7 @@ int32_t recmg_stats(recmg_cache_t *c, recmg_table_stats_t *last, recmg_table_sta
         for (int t = 0; t < T; ++t) need += st[t].n_res;
         if (resident_dump && dump_capacity < need) return fail(RECMG_E_INVALID, "dump_capacity too small");
         launch_mark_resident(c->g, c->max_cap, s);
-        launch_dedup(c->g, EMIT_DUMP, c->g.dump_count, 1, 0, s);
+        launch_dedup(c->g, EMIT_DUMP, c->g.dump_count, 1, 0, c->max_nblk, s);
         HIP_TRY(hipGetLastError());
         std::vector<int32_t> cnt(T);
         HIP_TRY(hipMemcpyAsync(cnt.data(), c->g.dump_count, 4 * T, hipMemcpyDeviceToHost, s));

@@ -77,12 +77,7 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
             const uint32_t pos = bm_pos(s_ns[t], s_qb[t], r);
             uint32_t *w = s_bm[t] + (pos >> 5);
             const uint32_t bit = 1u << (pos & 31);
-            // A plain (cached) read first: bits only go from 0 to 1 during
-            // this kernel and the previous dedup's clears are visible at the
-            // kernel boundary, so a stale read can only show 0, which costs a
-            // redundant (idempotent) atomic; a device-scope read went to the
-            // fabric for every mark.
-            if (!(gload4(w) & bit)) atomicOr(w, bit);
+            if (!(__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit)) atomicOr(w, bit);
         }
     }
 }
@@ -173,6 +168,53 @@ __global__ void __launch_bounds__(kBlock) k_bm_emit(DGlobal g, int32_t stamp) {
     }
 }
 
+// Small tables: count, scan and emit in one kernel, one block of 1024 threads
+// per table walking its bitmap 4096 words at a time (the three-kernel form
+// costs two more launches, which dominate when a table's bitmap is a few
+// blocks: configuration 1 has four).
+constexpr int kFusedThreads = 1024, kFusedWords = kFusedThreads * kWordsPerThread;
+
+template <int MODE>
+__global__ void __launch_bounds__(kFusedThreads) k_bm_fused(DGlobal g, int32_t *counts, int count_stride,
+                                                           int32_t stamp) {
+    if (*g.err) return;
+    __shared__ int tmp[16];
+    const int t = blockIdx.x;
+    const DTable &tb = g.tabs[t];
+    int32_t *out;
+    if (MODE == EMIT_FORWARD) out = g.U + g.tstart[t];
+    else if (MODE == EMIT_PREFETCH) out = g.PU + g.pstart[t];
+    else out = g.dump + tb.cap_off;
+    int base = 0;  // distinct ids of the words before this pass
+    for (int64_t w0 = 0; w0 < tb.bm_words; w0 += kFusedWords) {
+        const int64_t wbase = w0 + threadIdx.x * kWordsPerThread;
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+        if (wbase < tb.bm_words) {  // bm_words is a multiple of kWordsPerBlock, so four words are present
+            const uint4 w4 = *reinterpret_cast<const uint4 *>(tb.bitmap + wbase);
+            w[0] = w4.x, w[1] = w4.y, w[2] = w4.z, w[3] = w4.w;
+        }
+        const int cnt = __popc(w[0]) + __popc(w[1]) + __popc(w[2]) + __popc(w[3]);
+        int tot;
+        int u = base + block_excl_scan(cnt, tmp, &tot);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            uint32_t bits = w[q];
+            if (!bits) continue;
+            const int64_t word = wbase + q;
+            if (MODE == EMIT_FORWARD) tb.rank[word] = make_uint4((uint32_t)u, bits, (uint32_t)stamp, 0u);
+            tb.bitmap[word] = 0;
+            while (bits) {
+                const int b = __ffs(bits) - 1;
+                bits &= bits - 1;
+                const uint32_t pos = (uint32_t)(word * 32 + b);
+                out[u++] = MODE == EMIT_DUMP ? (int32_t)pos : bm_row(tb, pos);
+            }
+        }
+        base += tot;
+    }
+    if (threadIdx.x == 0) counts[(int64_t)t * count_stride] = base;
+}
+
 // ------------------------------------------------------------------- launchers
 
 static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
@@ -193,7 +235,14 @@ void launch_mark_resident(const DGlobal &g, int32_t max_cap, hipStream_t s) {
     k_mark_resident<<<grid, kBlock, 0, s>>>(g);
 }
 
-void launch_dedup(const DGlobal &g, int mode, int32_t *counts, int count_stride, int32_t stamp, hipStream_t s) {
+void launch_dedup(const DGlobal &g, int mode, int32_t *counts, int count_stride, int32_t stamp, int32_t max_nblk,
+                  hipStream_t s) {
+    if (max_nblk <= kFusedMaxBlocks) {
+        if (mode == EMIT_FORWARD) k_bm_fused<EMIT_FORWARD><<<g.T, kFusedThreads, 0, s>>>(g, counts, count_stride, stamp);
+        else if (mode == EMIT_PREFETCH) k_bm_fused<EMIT_PREFETCH><<<g.T, kFusedThreads, 0, s>>>(g, counts, count_stride, stamp);
+        else k_bm_fused<EMIT_DUMP><<<g.T, kFusedThreads, 0, s>>>(g, counts, count_stride, stamp);
+        return;
+    }
     k_bm_count<<<g.total_bm_blocks, kBlock, 0, s>>>(g);
     k_bm_scan<<<g.T, 1024, 0, s>>>(g, counts, count_stride);
     if (mode == EMIT_FORWARD) k_bm_emit<EMIT_FORWARD><<<g.total_bm_blocks, kBlock, 0, s>>>(g, stamp);

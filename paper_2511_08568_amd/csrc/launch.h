@@ -9,8 +9,11 @@ namespace recmg {
 void launch_mark(const DGlobal &g, const int32_t *keys, const int64_t *starts, int64_t n, hipStream_t s);
 void launch_mark_resident(const DGlobal &g, int32_t max_cap, hipStream_t s);
 enum { EMIT_FORWARD = 0, EMIT_PREFETCH = 1, EMIT_DUMP = 2 };
-// mode: where the sorted distinct ids go (U of a forward, PU of a placement, the resident dump)
-void launch_dedup(const DGlobal &g, int mode, int32_t *counts, int count_stride, int32_t stamp, hipStream_t s);
+// mode: where the sorted distinct ids go (U of a forward, PU of a placement, the resident dump);
+// max_nblk: the most bitmap blocks of any table (at most kFusedMaxBlocks: one kernel does it all)
+constexpr int kFusedMaxBlocks = 8;
+void launch_dedup(const DGlobal &g, int mode, int32_t *counts, int count_stride, int32_t stamp, int32_t max_nblk,
+                  hipStream_t s);
 
 // forward.hip
 void launch_fwd_prep(const DGlobal &g, const int64_t *offsets, int32_t B, int64_t n, hipStream_t s);

@@ -139,6 +139,8 @@ struct DGlobal {
     int32_t total_bm_blocks;
     int32_t *sa_bstart;  // [nsa + 1] first placement block of each set-associative table
     int32_t *sa_btab;    // [nsa] those tables, fewest sets first
+    int32_t *pfrom;      // [max_prefetch] set-associative tables: per distinct prefetch row (PU), its
+                         // staging row if the last batch missed it, else -1
     int64_t *stat_log;   // [log calls][T][kNumStats + 1]: the counters of each call (see recmg_stats_log)
 };
 
@@ -199,23 +201,10 @@ __device__ __forceinline__ uint32_t hash_row(int32_t r) {
     return h;
 }
 
-// Home entry of `row` in a map of mask + 1 entries (a power of two): the row's
-// own position, its aligned 64-entry window moved by a mix of the row's bits
-// above the map's size.  Rows below the map's size keep their own entries (no
-// collisions when the table is no larger than the map), and sorted queries
-// (the dedup lists are ascending) read the map in address order, a page at a
-// time; rows above it are spread over windows like a random hash.
-__device__ __forceinline__ uint32_t map_home(int32_t row, int32_t mask) {
-    const uint32_t r = (uint32_t)row, m = (uint32_t)mask;
-    const int bits = 32 - __clz((int)m);  // log2 of the map size
-    const uint32_t hi = bits >= 31 ? 0u : r >> bits;
-    return (r ^ (hash_row((int32_t)hi) << 6)) & m;
-}
-
 // Slot of `row` or -1.  Linear probing; deleted entries are skipped.
 __device__ __forceinline__ int32_t map_find(const DTable &tb, int32_t row) {
     const int32_t mask = tb.map_mask;
-    uint32_t i = map_home(row, mask);
+    uint32_t i = hash_row(row) & (uint32_t)mask;
     for (int32_t n = 0; n <= mask; ++n) {
         const int2 e = gload_int2(tb.map + i);
         if (e.x == row) return e.y;
@@ -232,7 +221,7 @@ __device__ __forceinline__ int32_t map_find(const DTable &tb, int32_t row) {
 // safe; no lookup may run concurrently.  Returns 1 if a deleted entry was reused.
 __device__ __forceinline__ int map_insert(const DTable &tb, int32_t row, int32_t slot) {
     const int32_t mask = tb.map_mask;
-    uint32_t i = map_home(row, mask);
+    uint32_t i = hash_row(row) & (uint32_t)mask;
     for (int32_t n = 0; n <= mask; ++n) {
         int32_t k = tb.map[i].x;  // may be stale (L1); the CAS result is not
         while (k == kEmpty || k == kTomb) {
@@ -251,7 +240,7 @@ __device__ __forceinline__ int map_insert(const DTable &tb, int32_t row, int32_t
 // Delete a present row (distinct rows may be deleted concurrently).
 __device__ __forceinline__ void map_delete(const DTable &tb, int32_t row) {
     const int32_t mask = tb.map_mask;
-    uint32_t i = map_home(row, mask);
+    uint32_t i = hash_row(row) & (uint32_t)mask;
     for (int32_t n = 0; n <= mask; ++n) {
         int32_t k = tb.map[i].x;
         if (k == row) {

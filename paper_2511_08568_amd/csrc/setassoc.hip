@@ -36,8 +36,11 @@ namespace recmg {
 // Segment bounds of every set that has events.  Index space: the last
 // forward's distinct rows (all tables, nu), then this placement's distinct
 // prefetch rows (np).  A first element of its set in its table's list writes
-// the begin, a last element the end.
-__global__ void __launch_bounds__(kBlock) k_sa_heads(DGlobal g, int64_t nu, int64_t np, int32_t have_fwd) {
+// the begin, a last element the end.  A prefetch row also gets its staging
+// row if the last batch missed it (pfrom): found here, where every row is
+// looked up in parallel, its two dependent loads stay off the sets' chains.
+__global__ void __launch_bounds__(kBlock) k_sa_heads(DGlobal g, int64_t nu, int64_t np, int32_t have_fwd,
+                                                     int32_t last_stamp) {
     if (*g.err) return;
     __shared__ int64_t s_ts[RECMG_MAX_TABLES + 1], s_ps[RECMG_MAX_TABLES + 1];
     __shared__ int32_t s_uc[RECMG_MAX_TABLES], s_pc[RECMG_MAX_TABLES];
@@ -63,6 +66,20 @@ __global__ void __launch_bounds__(kBlock) k_sa_heads(DGlobal g, int64_t nu, int6
         const int32_t *list = (is_u ? g.U : g.PU) + starts[t];
         const uint32_t ns = (uint32_t)tb.nsets;
         const uint32_t set = (uint32_t)list[loc] % ns;
+        if (!is_u) {
+            int32_t from = -1;
+            if (have_fwd) {
+                const int32_t r = list[loc];
+                const uint32_t pos = bm_pos(tb, r);
+                const uint4 rk = tb.rank[pos >> 5];
+                const uint32_t bit = 1u << (pos & 31);
+                if ((int32_t)rk.z == last_stamp && (rk.y & bit)) {
+                    const int32_t su = g.slotU[s_ts[t] + (int32_t)rk.x + __popc(rk.y & (bit - 1u))];
+                    if (su < 0) from = -su - 1;
+                }
+            }
+            g.pfrom[starts[t] + loc] = from;
+        }
         int *sg = reinterpret_cast<int *>(tb.seg + set);
         if (loc == 0 || (uint32_t)list[loc - 1] % ns != set) sg[is_u ? 0 : 2] = (int)loc;
         if (loc + 1 == cnt || (uint32_t)list[loc + 1] % ns != set) sg[is_u ? 1 : 3] = (int)(loc + 1);
@@ -154,6 +171,19 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     // is the kernel's critical path, so it takes issue slots first.
     if (max(nu0 + np0, nu1 + np1) > 256) __builtin_amdgcn_s_setprio(3);
 
+    // The first chunk of each event list is loaded with the ways (one round
+    // trip for all of them; most sets have fewer than HL events of each kind).
+    const int64_t ub = g.tstart[t];
+    int32_t u0_r = 0, u0_su = 0, p0_r = -1, p0_from = -1;
+    if (sg.x + wl < sg.y) {
+        u0_r = g.U[ub + sg.x + wl];
+        u0_su = g.slotU[ub + sg.x + wl];
+    }
+    if (sg.z + wl < sg.w) {
+        p0_r = g.PU[pb + sg.z + wl];
+        p0_from = g.pfrom[pb + sg.z + wl];
+    }
+
     // A. this set's ways; rows the last batch touched take the touch score
     int32_t row0 = -1, score = 0;
     uint32_t flags = 0;
@@ -198,15 +228,16 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     // B. misses of the last batch, ascending.  Each chunk of HL distinct rows
     // of a set is loaded lane-parallel with the misses' touch scores, then
     // played one miss at a time from registers.
-    const int64_t ub = g.tstart[t];
     int nmiss = 0;
     for (int32_t i0 = 0; i0 < max(nu0, nu1); i0 += HL) {
         const int32_t i = sg.x + i0 + wl;
         const bool in = i < sg.y;
-        int32_t r = 0, su = 0, v = 0;
+        int32_t r = u0_r, su = u0_su, v = 0;
         if (in) {
-            r = g.U[ub + i];
-            su = g.slotU[ub + i];
+            if (i0 > 0) {
+                r = g.U[ub + i];
+                su = g.slotU[ub + i];
+            }
             if (su < 0) v = touch_score(p, tb, r, p.prio ? g.mcbit[ub + (-su - 1)] : 0);
         }
         const uint64_t mm = ballot(in && su < 0);
@@ -228,17 +259,9 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
         const int32_t i = sg.z + i0 + wl;
         int32_t r = -1, from = -1, v = 0;
         if (i < sg.w) {
-            r = g.PU[pb + i];
+            r = i0 > 0 ? g.PU[pb + i] : p0_r;
+            from = i0 > 0 ? g.pfrom[pb + i] : p0_from;  // staging row of a row the last batch missed (k_sa_heads)
             v = new_prefetch_score(p, tb, r);
-            if (p.have_fwd) {
-                const uint32_t pos = bm_pos(tb, r);
-                const uint4 rk = tb.rank[pos >> 5];
-                const uint32_t bit = 1u << (pos & 31);
-                if ((int32_t)rk.z == p.last_stamp && (rk.y & bit)) {
-                    const int32_t su = g.slotU[ub + (int32_t)rk.x + __popc(rk.y & (bit - 1u))];
-                    if (su < 0) from = -su - 1;
-                }
-            }
         }
         const int c0 = min(HL, np0 - i0), c1 = min(HL, np1 - i0);
         for (int j = 0; j < max(c0, c1); ++j) {
@@ -376,7 +399,7 @@ static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
 
 void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks,
                      int32_t ways, hipStream_t s) {
-    if (nu + np > 0) k_sa_heads<<<grid_for(nu + np, kBlock, 8192), kBlock, 0, s>>>(g, nu, np, p.have_fwd);
+    if (nu + np > 0) k_sa_heads<<<grid_for(nu + np, kBlock, 8192), kBlock, 0, s>>>(g, nu, np, p.have_fwd, p.last_stamp);
     if (blocks <= 0) return;
     if (sa_sets_per_wave(ways) == 2) k_sa_place<2><<<(unsigned)blocks, kSaBlock, 0, s>>>(g, p, nsa);
     else k_sa_place<1><<<(unsigned)blocks, kSaBlock, 0, s>>>(g, p, nsa);
