@@ -10,7 +10,7 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "librecmg.so")
-SOURCES = ("dedup.hip", "forward.hip", "placement.hip", "setassoc.hip", "abi.hip")
+SOURCES = ("dedup.hip", "forward.hip", "placement.hip", "ring.hip", "setassoc.hip", "abi.hip")
 ARCH = os.environ.get("RECMG_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

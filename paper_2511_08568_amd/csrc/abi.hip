@@ -57,17 +57,19 @@ struct Geom {
     int32_t wlw = 0, wr = 0, wnch = 0, kind = 0;
     int32_t ways = 0, nsets = 0, qbits = 0;  // set-associative form (ways > 0)
     bool staged = false;                      // misses and fills gathered on the host
+    int32_t ring_cap = 0;                     // entries per resident-ring buffer (0: radix select)
 };
 
 struct Layout {
     size_t total = 0, host_total = 0;
     std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, slot_cbit, free_stack, map, bitmap, rank,
-        seg, freq;
+        seg, freq, slot_pos, ring0, ring1, rcnt, roff;
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, raddr = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
     size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, pool_btab = 0, ftstart = 0;
     size_t sa_bstart = 0, sa_btab = 0, fdesc = 0, stat_log = 0, pfrom = 0;
     size_t fstage = 0;
+    size_t puref = 0, zone = 0, mslot = 0, npslot = 0, pend_row[2] = {0, 0}, pend_slot[2] = {0, 0};
     // pinned host staging (STAGED): miss ids, miss rows, fill sources, prefetch rows
     size_t h_mrows = 0, h_rows = 0, h_fsrc = 0, h_frows = 0, h_np = 0, h_early = 0;
     size_t staging[2] = {0, 0};
@@ -149,6 +151,15 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
         if (g.wlw) g.bpb = (kBlock / 64) * kWaveBags;
         g.kind = pool_kind(g.dtype, g.vec, g.wlw, g.wr);
         g.copy_unit = g.row_bytes % 16 == 0 ? 16 : (g.row_bytes % 4 == 0 ? 4 : 2);
+        // LRU_BATCH fully associative tables keep their residents in key order
+        // (ring.hip).  A placement appends at most max_prefetch + max_indices
+        // entries; after a compaction at most Cap are live, and the rest of the
+        // buffer takes the appends of the placements until the next one.
+        const int64_t per_plc = cfg->max_indices + cfg->max_prefetch;
+        const int64_t rc = ((int64_t)g.cap + 3 * per_plc + 2 * kRingChunk) / kRingChunk * kRingChunk;
+        if (cfg->policy == RECMG_LRU_BATCH && !g.ways && g.cap > 0 && cfg->max_indices < (1 << 30) - 1 &&
+            cfg->max_prefetch < (1 << 30) - 1 && rc < (int64_t(1) << 31) - kRingChunk)
+            g.ring_cap = (int32_t)rc;
     }
 
     return RECMG_OK;
@@ -169,6 +180,7 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
         return at;
     };
     int32_t maxrb = 0;
+    bool any_ring = false;
     for (const Geom &g : geo) maxrb = std::max(maxrb, g.row_bytes);
     L->stage_stride = ((int64_t)maxrb + 15) / 16 * 16;
     for (int t = 0; t < T; ++t) {
@@ -185,6 +197,13 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
         L->rank.push_back(take((size_t)g.bm_words * 16));
         L->seg.push_back(take((size_t)g.nsets * 16));
         L->freq.push_back(take(cfg->policy == RECMG_LFU_BATCH ? (size_t)g.rows * 4 : 0));
+        const size_t rc = (size_t)g.ring_cap;
+        L->slot_pos.push_back(take(rc ? (size_t)g.cap * 4 : 0));
+        L->ring0.push_back(take(rc * 4));
+        L->ring1.push_back(take(rc * 4));
+        L->rcnt.push_back(take(rc / kRingChunk * 4));
+        L->roff.push_back(take(rc / kRingChunk * 4));
+        if (rc) any_ring = true;
         L->total_bm_blocks += g.bm_nblk;
         L->sum_cap += g.cap;
     }
@@ -220,6 +239,14 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->sa_bstart = take(4 * (T + 1));
     L->sa_btab = take(4 * T);
     L->pfrom = take(cfg->ways > 0 ? 4 * mp : 0);
+    L->puref = take(4 * mp);
+    L->zone = take(any_ring ? 8 * (mi + mp) : 0);
+    L->mslot = take(any_ring ? 4 * mi : 0);
+    L->npslot = take(any_ring ? 4 * mp : 0);
+    for (int k = 0; k < 2; ++k) {
+        L->pend_row[k] = take(any_ring ? 4 * mp : 0);
+        L->pend_slot[k] = take(any_ring ? 4 * mp : 0);
+    }
     L->staging[0] = take(mi * (size_t)L->stage_stride);
     L->staging[1] = take(mi * (size_t)L->stage_stride);
     const bool staged = any_staged(geo);
@@ -256,6 +283,8 @@ struct recmg_cache {
     int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1, nsa = 0, max_nblk = 0;
     int64_t sa_blocks = 0;  // blocks of the set-associative placement kernel
     bool has_fa = false, has_sa = false;  // tables of each form present
+    bool has_ring = false, has_scan_fa = false;  // fully associative tables with and without a resident ring
+    int32_t max_ring_chunks = 0;
     bool has_zc = false, has_staged = false;  // tables of each miss mode present
     std::vector<int32_t> pool_order;  // table ids ordered by pooled-kernel kind
     std::vector<PoolLaunch> pool_launches;
@@ -285,6 +314,7 @@ struct recmg_cache {
     int64_t *fdesc_buf[2] = {nullptr, nullptr};
     int32_t pool_B = -1;
     int64_t plc_np = -1;  // prefetch ids of the placement since the last forward (-1: none)
+    int64_t plc_np_last = 0;  // prefetch ids of the latest placement
     char *stage[2] = {nullptr, nullptr};  // staging buffers, alternating between forwards
     int cur = 0;                          // buffer of the latest forward
 
@@ -843,6 +873,14 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.sa_bstart = reinterpret_cast<int32_t *>(ws + L.sa_bstart);
     g.sa_btab = reinterpret_cast<int32_t *>(ws + L.sa_btab);
     g.pfrom = reinterpret_cast<int32_t *>(ws + L.pfrom);
+    g.puref = reinterpret_cast<int32_t *>(ws + L.puref);
+    g.zone = reinterpret_cast<int2 *>(ws + L.zone);
+    g.mslot = reinterpret_cast<int32_t *>(ws + L.mslot);
+    g.npslot = reinterpret_cast<int32_t *>(ws + L.npslot);
+    for (int k = 0; k < 2; ++k) {
+        g.pend_row[k] = reinterpret_cast<int32_t *>(ws + L.pend_row[k]);
+        g.pend_slot[k] = reinterpret_cast<int32_t *>(ws + L.pend_slot[k]);
+    }
 
     std::vector<DTable> tabs(T);
     std::vector<int32_t> bstart(T + 1, 0);
@@ -887,6 +925,18 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         d.staged = ge.staged ? 1 : 0;
         d.seg = reinterpret_cast<int4 *>(ws + L.seg[t]);
         d.freq = cfg->policy == RECMG_LFU_BATCH ? reinterpret_cast<int32_t *>(ws + L.freq[t]) : nullptr;
+        if (ge.ring_cap) {
+            d.slot_pos = reinterpret_cast<int32_t *>(ws + L.slot_pos[t]);
+            d.ring[0] = reinterpret_cast<int32_t *>(ws + L.ring0[t]);
+            d.ring[1] = reinterpret_cast<int32_t *>(ws + L.ring1[t]);
+            d.rcnt = reinterpret_cast<int32_t *>(ws + L.rcnt[t]);
+            d.roff = reinterpret_cast<int32_t *>(ws + L.roff[t]);
+            d.ring_cap = ge.ring_cap;
+            c->has_ring = true;
+            c->max_ring_chunks = std::max(c->max_ring_chunks, ge.ring_cap / kRingChunk);
+        } else if (!ge.ways) {
+            c->has_scan_fa = true;
+        }
         if (ge.ways) c->has_sa = true;
         else c->has_fa = true;
 
@@ -929,6 +979,12 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         HIP_TRY(hipMemsetAsync(ws + L.rank[t], 0xff, (size_t)ge.bm_words * 16, s0));  // stamp -1
         HIP_TRY(hipMemsetAsync(ws + L.seg[t], 0, (size_t)ge.nsets * 16, s0));
         if (cfg->policy == RECMG_LFU_BATCH) HIP_TRY(hipMemsetAsync(ws + L.freq[t], 0, (size_t)ge.rows * 4, s0));
+        if (ge.ring_cap) {  // empty rings: no slot has an entry, no chunk a live one
+            HIP_TRY(hipMemsetAsync(ws + L.slot_pos[t], 0xff, (size_t)ge.cap * 4, s0));
+            HIP_TRY(hipMemsetAsync(ws + L.ring0[t], 0xff, (size_t)ge.ring_cap * 4, s0));
+            HIP_TRY(hipMemsetAsync(ws + L.ring1[t], 0xff, (size_t)ge.ring_cap * 4, s0));
+            HIP_TRY(hipMemsetAsync(ws + L.rcnt[t], 0, (size_t)ge.ring_cap / kRingChunk * 4, s0));
+        }
     }
     HIP_TRY(hipMemsetAsync(ws + L.st, 0, sizeof(TState) * T, s0));
     HIP_TRY(hipMemsetAsync(ws + L.tstart, 0, 8 * (T + 1), s0));
@@ -1045,13 +1101,20 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     const int64_t cand = (c->have_fwd ? c->last_n : 0) + num_prefetch;
     const int64_t per_table = c->max_cap + (cand + c->T - 1) / c->T;
     const int64_t cand_grid = std::min<int64_t>(std::max<int64_t>(cand / c->T, 1024), cand + 1);
+    // resident rings: a table's zones hold its pending rows (at most the last
+    // placement's prefetch rows) and the last batch's distinct rows
+    const int64_t ring_items = ((c->have_fwd ? c->last_n : 0) + c->plc_np_last + num_prefetch + c->T - 1) / c->T;
     if (c->has_fa) {
         StageTimer tm(c, RECMG_STAGE_PLC_RANK, s);
-        launch_plc_rank(g, p, per_table, s);
+        if (c->has_scan_fa) launch_plc_rank(g, p, per_table, s);
+        if (c->has_ring) launch_ring_rank(g, p, ring_items, s);
     }
     {
         StageTimer tm(c, RECMG_STAGE_PLC_APPLY, s);
-        if (c->has_fa) launch_plc_apply(g, p, c->max_cap, c->max_map, cand_grid, s);
+        if (c->has_scan_fa) launch_plc_evict(g, p, c->max_cap, s);
+        if (c->has_ring) launch_ring_evict(g, p, ring_items, c->max_ring_chunks, s);
+        if (c->has_fa) launch_plc_admit(g, p, c->max_cap, c->max_map, cand_grid, s);
+        if (c->has_ring) launch_ring_store(g, p, ring_items, c->max_ring_chunks, c->max_cap, q, s);
         if (c->has_sa)
             launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks, c->cfg.ways, s);
     }
@@ -1100,6 +1163,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
     c->placements++;
     c->calls++;
     c->plc_np = num_prefetch;
+    c->plc_np_last = num_prefetch;
     c->have_fwd = false;
     c->last_stream = s;
     c->plc_stream = s;

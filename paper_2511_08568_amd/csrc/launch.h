@@ -44,8 +44,14 @@ void launch_plc_prep(const DGlobal &g, const int64_t *poff, int64_t np, int32_t 
 void launch_plc_bits(const DGlobal &g, const uint8_t *bits, int64_t n_last, hipStream_t s);
 void launch_plc_freq(const DGlobal &g, int64_t n_last, hipStream_t s);
 void launch_plc_classify(const DGlobal &g, int32_t last_stamp, int64_t np, hipStream_t s);
+// item_bound: the most slots + candidates of any table; up to kRankSmallItems one
+// block per table ranks it whole
+constexpr int64_t kRankSmallItems = 1 << 16;
 void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s);
-void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,
+// evict (tables ranked by radix select), then map upkeep and admission (every
+// fully associative table)
+void launch_plc_evict(const DGlobal &g, const PlcParams &p, int32_t max_cap, hipStream_t s);
+void launch_plc_admit(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,
                       hipStream_t s);
 // fdesc: this placement's fill descriptor, [T][4] int64 (written by finalize, read by fill);
 // phase: the tables whose rows this launch copies, by miss mode
@@ -54,6 +60,16 @@ void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, int phase, hipStrea
                      hipEvent_t ev1 = nullptr);
 void launch_plc_finalize(const DGlobal &g, int64_t *fdesc, int64_t log_slot, hipStream_t s);
 void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s);
+
+// ring.hip: LRU_BATCH placement of tables with a resident ring (ring_cap > 0).
+// item_bound: entries of a table's zones and prefetch list (last forward's
+// distinct rows + pending rows + prefetch rows, per table); ring_chunks: the
+// most kRingChunk chunks of any ring; wr: the pending buffer this placement
+// writes (the next one reads it).
+void launch_ring_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s);
+void launch_ring_evict(const DGlobal &g, const PlcParams &p, int64_t item_bound, int32_t ring_chunks, hipStream_t s);
+void launch_ring_store(const DGlobal &g, const PlcParams &p, int64_t item_bound, int32_t ring_chunks, int32_t max_cap,
+                       int wr, hipStream_t s);
 
 // setassoc.hip: placement of the set-associative tables (nu: index space of
 // the last forward's distinct rows, np: of this placement's prefetch rows;

@@ -50,8 +50,11 @@ __global__ void k_plc_prep(DGlobal g, const int64_t *__restrict__ poff, int64_t 
             st.p_fill = 0;
             st.p_drop = 0;
             st.m_drop = 0;
-            // set-associative tables update the digest by the rows that come and go
-            st.digest_acc = g.tabs[t].ways ? st.digest : 0ull;
+            st.z1_keys = 0;
+            st.pend_keep = 0;
+            // set-associative tables and resident rings update the digest by
+            // the rows that come and go
+            st.digest_acc = (g.tabs[t].ways || g.tabs[t].ring_cap) ? st.digest : 0ull;
         }
     }
 }
@@ -123,6 +126,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last
             if (slot >= 0) {
                 atomicOr(&tb.slot_flags[slot], F_INP);
                 resident = true;
+                g.puref[i] = slot;
             } else {
                 // distinct rows of the last batch carry its stamp in the rank word
                 const uint32_t pos = bm_pos(tb, row);
@@ -133,6 +137,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last
                     const int32_t u = (int32_t)rk.x + __popc(rk.y & (bit - 1u));
                     const int64_t m = -(int64_t)g.slotU[ts + u] - 1;
                     atomicOr(&g.mflags[ts + m], F_INP);
+                    g.puref[i] = ring_ref_miss((int32_t)m);
                 } else {
                     isnew = true;
                 }
@@ -140,26 +145,14 @@ __global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last
         }
         (void)wave_append(resident, t, &g.st[0].p_res, stride_st);  // counts only
         const int32_t k = wave_append(isnew, t, &g.st[0].npcount, stride_st);
-        if (isnew) g.NP[s_pstart[t] + k] = row;
+        if (isnew) {
+            g.NP[s_pstart[t] + k] = row;
+            g.puref[i] = ring_ref_new(k);
+        }
     }
 }
 
 // ----------------------------------------------------------------- ranking
-
-struct Counts {
-    int32_t cap, nm, nnp, mode, keep;
-};
-
-__device__ __forceinline__ Counts table_counts(const DTable &tb, const TState &st, const PlcParams &p) {
-    Counts c;
-    c.cap = tb.cap;
-    c.nm = p.have_fwd ? st.mcount : 0;
-    c.nnp = st.npcount;
-    const int64_t nk = (int64_t)st.n_res + c.nm + c.nnp;
-    c.keep = (int32_t)(nk < c.cap ? nk : c.cap);
-    c.mode = nk <= c.cap ? SEL_ALL : (c.keep == 0 ? SEL_NONE : SEL_SELECT);
-    return c;
-}
 
 __device__ __forceinline__ int pass_shift(const PlcParams &p, int pass) { return kRadixBits * (p.passes - 1 - pass); }
 __device__ __forceinline__ int pass_width(const PlcParams &p, int pass) {
@@ -189,17 +182,51 @@ __device__ __forceinline__ void hist_merge(const DGlobal &g, int t, const int *s
         if (s_hist[b]) atomicAdd(&gh[b], s_hist[b]);
 }
 
-// One block per table: the digit of this pass.  Bins are taken from the top
-// until `need` keys are covered; the bin reached extends the threshold prefix
-// and the keys still needed inside it carry over to the next pass.  Clears the
-// histogram for the next pass.
+// The digit of one pass from a table's histogram in LDS: bins are taken from
+// the top until `need` keys are covered; the bin reached (*digit) extends the
+// threshold prefix and the keys still needed inside it (*rest) carry over to
+// the next pass.  Every thread of the block calls; blockDim.x divides kRadix;
+// the results are valid in every thread.
+__device__ __forceinline__ void pick_digit(const int *s_hist, int need, int *tmp, int *digit, int *rest) {
+    __shared__ int s_digit, s_rest;
+    // thread k owns bin group (groups - 1 - k), so an exclusive scan gives the
+    // keys in the groups above
+    if (threadIdx.x == 0) {  // a histogram short of `need` (never, when the counts hold) keeps digit 0
+        s_digit = 0;
+        s_rest = need;
+    }
+    const int per = kRadix / (int)blockDim.x;
+    const int grp = (int)blockDim.x - 1 - (int)threadIdx.x;
+    int cs = 0;
+    for (int b = 0; b < per; ++b) cs += s_hist[grp * per + b];
+    int tot;
+    const int above = block_excl_scan(cs, tmp, &tot);
+    if (above < need && above + cs >= need) {
+        int cum = above;
+        for (int b = grp * per + per - 1; b >= grp * per; --b) {
+            if (cum + s_hist[b] >= need) {
+                s_digit = b;
+                s_rest = need - cum;
+                break;
+            }
+            cum += s_hist[b];
+        }
+    }
+    __syncthreads();
+    *digit = s_digit;
+    *rest = s_rest;
+    __syncthreads();
+}
+
+// One block per table: the digit of this pass from the table's global
+// histogram (clearing it for the next pass).
 __global__ void __launch_bounds__(kBlock) k_plc_pick(DGlobal g, PlcParams p, int pass) {
     if (*g.err) return;
     __shared__ int s_hist[kRadix];
     __shared__ int tmp[16];
     const int t = blockIdx.x;
     TState &st = g.st[t];
-    if (st.sel_mode != SEL_SELECT) return;  // uniform over the block
+    if (g.tabs[t].ring_cap || st.sel_mode != SEL_SELECT) return;  // uniform over the block
     int *gh = g.hist + (int64_t)t * kRadix;
     for (int b = threadIdx.x; b < kRadix; b += blockDim.x) {
         s_hist[b] = gh[b];
@@ -207,24 +234,11 @@ __global__ void __launch_bounds__(kBlock) k_plc_pick(DGlobal g, PlcParams p, int
     }
     __syncthreads();
     const int need = pass == 0 ? table_counts(g.tabs[t], st, p).keep : st.need;
-    // thread k owns bin group 255-k, so an inclusive scan gives suffix sums
-    constexpr int per = kRadix / kBlock;
-    const int grp = kBlock - 1 - (int)threadIdx.x;
-    int cs = 0;
-#pragma unroll
-    for (int b = 0; b < per; ++b) cs += s_hist[grp * per + b];
-    int tot;
-    const int above = block_excl_scan(cs, tmp, &tot);  // keys in groups above grp
-    if (above < need && above + cs >= need) {
-        int cum = above;
-        for (int b = grp * per + per - 1; b >= grp * per; --b) {
-            if (cum + s_hist[b] >= need) {
-                st.prefix = pass == 0 ? (uint64_t)b : ((st.prefix << kRadixBits) | (uint64_t)b);
-                st.need = need - cum;
-                break;
-            }
-            cum += s_hist[b];
-        }
+    int digit, rest;
+    pick_digit(s_hist, need, tmp, &digit, &rest);
+    if (threadIdx.x == 0) {
+        st.prefix = pass == 0 ? (uint64_t)digit : ((st.prefix << kRadixBits) | (uint64_t)digit);
+        st.need = rest;
     }
 }
 
@@ -243,32 +257,19 @@ __device__ __forceinline__ void slot_quad(const int32_t *a, int64_t k0, int64_t 
     }
 }
 
-// Scores of every candidate (written back) and the first select pass.
-__global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
-    if (*g.err) return;
-    __shared__ int s_hist[kRadix];
-    const int t = blockIdx.y;
-    const DTable &tb = g.tabs[t];
-    TState &st = g.st[t];
-    const Counts c = table_counts(tb, st, p);
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        st.sel_mode = tb.ways ? SEL_NONE : c.mode;  // set-associative tables place in setassoc.hip
-        st.plc_nm = c.nm;
-    }
-    if (tb.ways) return;
-    const bool sel = c.mode == SEL_SELECT;
-    if (sel)
-        for (int b = threadIdx.x; b < kRadix; b += blockDim.x) s_hist[b] = 0;
-    __syncthreads();
+// Scores of every candidate of table t (written back) and, when `sel`, the
+// histogram of the first select pass, over items tid, tid + stride, ...
+// (stride a multiple of 64: hist_add is wave-wide).
+__device__ __forceinline__ void update_items(const DGlobal &g, const PlcParams &p, const DTable &tb, const Counts &c,
+                                             int t, int *s_hist, bool sel, int64_t tid, int64_t stride) {
     const int64_t ts = g.tstart[t], ps = g.pstart[t];
     const int shift = pass_shift(p, 0);
     const uint32_t dmask = (1u << pass_width(p, 0)) - 1u;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t cap = c.cap;
     // resident slots, four per thread; every lane runs the same number of
     // iterations (hist_add is wave-wide)
     const int64_t ngrp = (cap + 3) / 4, ngrp_r = (ngrp + 63) & ~(int64_t)63;
-    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < ngrp_r; q += stride) {
+    for (int64_t q = tid; q < ngrp_r; q += stride) {
         const int64_t k0 = 4 * q;
         const int64_t lim = q < ngrp ? cap : 0;  // lanes past the last group see no slot
         int32_t row[4], sc[4], fl[4], tch[4];
@@ -310,7 +311,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
     }
     // candidates: the last batch's misses, then new prefetch rows
     const int64_t nc = (int64_t)c.nm + c.nnp, nc_r = (nc + 63) & ~(int64_t)63;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < nc_r; k += stride) {
+    for (int64_t k = tid; k < nc_r; k += stride) {
         int32_t row = -1, s = 0;
         if (k >= nc) {
         } else if (k < c.nm) {
@@ -326,6 +327,28 @@ __global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
         }
         if (sel) hist_add(s_hist, row >= 0, (uint32_t)(make_key(s, row < 0 ? 0 : row, p.rowbits) >> shift) & dmask);
     }
+}
+
+// Scores of every candidate (written back) and the first select pass.
+__global__ void __launch_bounds__(kBlock) k_plc_update(DGlobal g, PlcParams p) {
+    if (*g.err) return;
+    __shared__ int s_hist[kRadix];
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    if (tb.ring_cap) return;  // ranked in ring.hip
+    const Counts c = table_counts(tb, st, p);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        st.sel_mode = tb.ways ? SEL_NONE : c.mode;  // set-associative tables place in setassoc.hip
+        st.plc_nm = c.nm;
+    }
+    if (tb.ways) return;
+    const bool sel = c.mode == SEL_SELECT;
+    if (sel)
+        for (int b = threadIdx.x; b < kRadix; b += blockDim.x) s_hist[b] = 0;
+    __syncthreads();
+    update_items(g, p, tb, c, t, s_hist, sel, (int64_t)blockIdx.x * blockDim.x + threadIdx.x,
+                 (int64_t)gridDim.x * blockDim.x);
     __syncthreads();
     if (sel) hist_merge(g, t, s_hist);
 }
@@ -345,23 +368,16 @@ __device__ __forceinline__ uint64_t cand_key(const DGlobal &g, const DTable &tb,
     return make_key(s, row, p.rowbits);
 }
 
-__global__ void __launch_bounds__(kBlock) k_plc_select(DGlobal g, PlcParams p, int pass) {
-    if (*g.err) return;
-    __shared__ int s_hist[kRadix];
-    const int t = blockIdx.y;
-    const DTable &tb = g.tabs[t];
-    TState &st = g.st[t];
-    if (st.sel_mode != SEL_SELECT) return;  // uniform over the table's blocks
-    const Counts c = table_counts(tb, st, p);
-    for (int b = threadIdx.x; b < kRadix; b += blockDim.x) s_hist[b] = 0;
-    __syncthreads();
+// Histogram of pass `pass` over the keys of table t whose higher digits equal
+// `prefix`, over items tid, tid + stride, ... (stride a multiple of 64).
+__device__ __forceinline__ void select_items(const DGlobal &g, const PlcParams &p, const DTable &tb, const Counts &c,
+                                             int t, int *s_hist, int pass, uint64_t prefix, int64_t tid,
+                                             int64_t stride) {
     const int64_t ts = g.tstart[t], ps = g.pstart[t];
     const int shift = pass_shift(p, pass);
-    const uint64_t prefix = st.prefix;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     const int64_t cap = c.cap;
     const int64_t ngrp = (cap + 3) / 4, ngrp_r = (ngrp + 63) & ~(int64_t)63;
-    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < ngrp_r; q += stride) {
+    for (int64_t q = tid; q < ngrp_r; q += stride) {
         const int64_t k0 = 4 * q;
         const int64_t lim = q < ngrp ? cap : 0;
         int32_t row[4], sc[4];
@@ -375,30 +391,73 @@ __global__ void __launch_bounds__(kBlock) k_plc_select(DGlobal g, PlcParams p, i
         }
     }
     const int64_t nc = (int64_t)c.nm + c.nnp, nc_r = (nc + 63) & ~(int64_t)63;
-    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < nc_r; k += stride) {
+    for (int64_t k = tid; k < nc_r; k += stride) {
         const uint64_t key = k < nc ? cand_key(g, tb, c, p, ts, ps, k) : 0;
         const bool in = k < nc && (key >> (shift + kRadixBits)) == prefix;
         hist_add(s_hist, in, (uint32_t)(key >> shift) & (kRadix - 1));
     }
+}
+
+__global__ void __launch_bounds__(kBlock) k_plc_select(DGlobal g, PlcParams p, int pass) {
+    if (*g.err) return;
+    __shared__ int s_hist[kRadix];
+    const int t = blockIdx.y;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    if (tb.ring_cap || st.sel_mode != SEL_SELECT) return;  // uniform over the table's blocks
+    const Counts c = table_counts(tb, st, p);
+    for (int b = threadIdx.x; b < kRadix; b += blockDim.x) s_hist[b] = 0;
+    __syncthreads();
+    select_items(g, p, tb, c, t, s_hist, pass, st.prefix, (int64_t)blockIdx.x * blockDim.x + threadIdx.x,
+                 (int64_t)gridDim.x * blockDim.x);
     __syncthreads();
     hist_merge(g, t, s_hist);
 }
 
-__device__ __forceinline__ bool kept(int mode, uint64_t key, uint64_t thr) {
-    return mode == SEL_ALL || (mode == SEL_SELECT && key >= thr);
+// Small tables: the whole ranking of a table in one block (scores, then every
+// pass's histogram in LDS and its digit), one launch instead of 2 per pass.
+constexpr int kRankSmallThreads = 1024;
+__global__ void __launch_bounds__(kRankSmallThreads) k_plc_rank_small(DGlobal g, PlcParams p) {
+    if (*g.err) return;
+    __shared__ int s_hist[kRadix];
+    __shared__ int tmp[16];
+    const int t = blockIdx.x;
+    const DTable &tb = g.tabs[t];
+    TState &st = g.st[t];
+    if (tb.ring_cap) return;
+    const Counts c = table_counts(tb, st, p);
+    if (threadIdx.x == 0) {
+        st.sel_mode = tb.ways ? SEL_NONE : c.mode;
+        st.plc_nm = c.nm;
+    }
+    if (tb.ways) return;
+    const bool sel = c.mode == SEL_SELECT;
+    for (int b = threadIdx.x; b < kRadix; b += blockDim.x) s_hist[b] = 0;
+    __syncthreads();
+    update_items(g, p, tb, c, t, s_hist, sel, threadIdx.x, blockDim.x);
+    __syncthreads();  // also makes the scores written above visible to the block
+    if (!sel) return;
+    uint64_t prefix = 0;
+    int need = c.keep;
+    for (int pass = 0; pass < p.passes; ++pass) {
+        if (pass > 0) {
+            for (int b = threadIdx.x; b < kRadix; b += blockDim.x) s_hist[b] = 0;
+            __syncthreads();
+            select_items(g, p, tb, c, t, s_hist, pass, prefix, threadIdx.x, blockDim.x);
+            __syncthreads();
+        }
+        int digit, rest;
+        pick_digit(s_hist, need, tmp, &digit, &rest);
+        prefix = pass == 0 ? (uint64_t)digit : ((prefix << kRadixBits) | (uint64_t)digit);
+        need = rest;
+    }
+    if (threadIdx.x == 0) {
+        st.prefix = prefix;
+        st.need = need;
+    }
 }
 
 // ----------------------------------------------------------------- evict / admit
-
-// The error word read once per block.  Evict and admit may set it (a broken
-// invariant) while other blocks of the same kernel start, and the waves of a
-// block must agree before the block's barriers.
-__device__ __forceinline__ bool block_err(const DGlobal &g) {
-    __shared__ int s_err;
-    if (threadIdx.x == 0) s_err = *g.err;
-    __syncthreads();
-    return s_err != 0;
-}
 
 // Slots a block collects in LDS before it reserves free-stack space for
 // them: one atomic on the table's stack top per block in the common case (a
@@ -415,7 +474,7 @@ __global__ void __launch_bounds__(kBlock) k_plc_evict(DGlobal g, PlcParams p) {
     __shared__ int32_t s_free[kEvictBuf];
     const int t = blockIdx.y;
     const DTable &tb = g.tabs[t];
-    if (tb.ways) return;
+    if (tb.ways || tb.ring_cap) return;
     TState &st = g.st[t];
     const int mode = st.sel_mode;
     const uint64_t thr = st.prefix;
@@ -575,6 +634,10 @@ __global__ void __launch_bounds__(kBlock) k_plc_admit(DGlobal g, PlcParams p) {
                 // gathered NP[ps + i] into row ps + i)
                 g.fill_src[fj] = is_miss ? (int32_t)k : tb.staged ? -(int32_t)(ps + (k - c.nm)) - 1 : -(row + 1);
                 g.fill_slot[fj] = slot;
+                if (tb.ring_cap) {  // where ring.hip finds the admitted rows' slots
+                    if (is_miss) g.mslot[ts + k] = slot;
+                    else g.npslot[ps + (k - c.nm)] = slot;
+                }
                 dig += mix64(((unsigned long long)t << 40) | (unsigned long long)row);
                 if (is_miss) ++n_adm_miss;
                 else ++n_fill;
@@ -677,6 +740,13 @@ __global__ void k_plc_finalize(DGlobal g, int64_t *fdesc, int64_t log_slot) {
             st.free_top -= st.popped;  // popped stays: the fill may still read it
             st.n_res = tb.cap - st.free_top;
         }
+        if (tb.ring_cap) {  // the ring's new front and back, the new pending list
+            st.r_tail = st.r_cut;
+            st.r_head += st.z1_len;
+            st.pend_n = st.pcount;
+            st.pend_off = g.pstart[t];
+            if (st.r_valid + st.pend_keep != st.n_res || st.r_head > tb.ring_cap) atomicOr(g.err, ERR_INTERNAL);
+        }
         st.rebuild = 0;
         int64_t v[kPlcStats];
         v[0] = st.evicted;
@@ -739,6 +809,10 @@ void launch_plc_classify(const DGlobal &g, int32_t last_stamp, int64_t np, hipSt
 }
 
 void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s) {
+    if (item_bound <= kRankSmallItems) {  // a table's slots and candidates fit one block's loop
+        k_plc_rank_small<<<g.T, kRankSmallThreads, 0, s>>>(g, p);
+        return;
+    }
     // few blocks per table: each block merges its non-zero histogram bins
     // into global memory
 #ifndef RECMG_RANK_IPT
@@ -753,12 +827,14 @@ void launch_plc_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, h
     }
 }
 
-void launch_plc_apply(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,
+void launch_plc_evict(const DGlobal &g, const PlcParams &p, int32_t max_cap, hipStream_t s) {
+    k_plc_evict<<<dim3(grid_for(max_cap, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
+}
+
+void launch_plc_admit(const DGlobal &g, const PlcParams &p, int32_t max_cap, int32_t max_map, int64_t cand_bound,
                       hipStream_t s) {
-    const dim3 gcap(grid_for(max_cap, kBlock * 4, 2048), g.T);
-    k_plc_evict<<<gcap, kBlock, 0, s>>>(g, p);
     k_map_clear<<<dim3(grid_for(max_map, kBlock * 8, 2048), g.T), kBlock, 0, s>>>(g);
-    k_map_refill<<<gcap, kBlock, 0, s>>>(g);
+    k_map_refill<<<dim3(grid_for(max_cap, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g);
     k_plc_admit<<<dim3(grid_for(cand_bound, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
 }
 

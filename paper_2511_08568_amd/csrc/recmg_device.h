@@ -31,9 +31,17 @@ constexpr int32_t ERR_OFFSETS = 2;
 #endif
 constexpr int kWaveBags = RECMG_WPOOL_BAGS;  // consecutive bags per wave in the wave-per-bag pooled kernel
 constexpr int kRaddrPad = 64;  // entries past the batch in the per-index row-address array (read, never used)
-constexpr int32_t ERR_INTERNAL = 4;
+constexpr int32_t ERR_INTERNAL = 4;  // a slot-accounting invariant failed (never expected)
 // int64 counters of recmg_table_stats_t: kFwdStats of a forward, then the placement's
-constexpr int kFwdStats = 7, kPlcStats = 9, kNumStats = kFwdStats + kPlcStats;  // a slot-accounting invariant failed (never expected)
+constexpr int kFwdStats = 7, kPlcStats = 9, kNumStats = kFwdStats + kPlcStats;
+
+// Resident rings: chunks of the buffer whose live entries are counted, and
+// the references a zone entry holds besides a slot id.
+constexpr int kRingChunk = 1024;
+constexpr int32_t kRingHole = INT32_MIN;
+constexpr int32_t kRingNewBase = -(1 << 30) - 1;
+__host__ __device__ constexpr int32_t ring_ref_miss(int32_t m) { return -1 - m; }            // m < 2^30
+__host__ __device__ constexpr int32_t ring_ref_new(int32_t k) { return kRingNewBase - k; }  // k < 2^30 - 1
 
 // outcome of the top-Cap ranking of one table
 constexpr int32_t SEL_SELECT = 0;  // keep keys >= threshold
@@ -78,6 +86,15 @@ struct DTable {
     int4 *seg;  // [nsets] (U begin, U end, PU begin, PU end) of each set in the
                 // current placement, relative to the table's lists; zero between uses
     int32_t *freq;  // LFU_BATCH: [rows] batches that accessed each row (every row, cached or not)
+    // LRU_BATCH, fully associative, Cap > 0 (ring_cap > 0): the residents in
+    // ascending key order, so that a placement evicts from the front instead
+    // of ranking every slot (ring.hip)
+    int32_t *slot_pos;  // [cap] index of the slot's entry in the current ring buffer, -1 if none
+    int32_t *ring[2];   // [ring_cap] each: slot ids in key order, kRingHole where none; one buffer is
+                        // current, the other receives the compacted entries
+    int32_t *rcnt;      // [ring_cap / kRingChunk] live entries per chunk of the current buffer
+    int32_t *roff;      // [ring_cap / kRingChunk] compaction: first new index of each chunk's entries
+    int32_t ring_cap;   // entries per buffer (a multiple of kRingChunk); 0: ranked by radix select
 };
 
 // Mutable per-table state and counters, resident in the workspace.
@@ -94,6 +111,15 @@ struct TState {
     // accumulators of the call in flight
     int32_t hits, hits_pf, p_res, evicted, adm_miss, p_fill, p_drop, m_drop;
     unsigned long long digest_acc;
+    // resident ring (ring_cap > 0): live entries lie in [r_tail, r_head) of
+    // buffer r_buf; r_valid of them are live; this placement evicts the live
+    // ones in [r_tail, r_cut).  The rows the last placement's prefetch named
+    // (score = this placement's LRU touch) wait in the pending list, entries
+    // [pend_off, + pend_n) of pend_row / pend_slot[pend_buf], until a placement
+    // merges them into the ring with the rows the last batch touched.
+    int32_t r_head, r_tail, r_cut, r_valid, r_buf, r_compact, r_zevict;
+    int32_t z1_len, z1_keys, pend_n, pend_buf, pend_keep;
+    int64_t pend_off;
     // published counters, in recmg_table_stats_t order
     int64_t last[kNumStats];
     unsigned long long digest;
@@ -142,6 +168,15 @@ struct DGlobal {
     int32_t *pfrom;      // [max_prefetch] set-associative tables: per distinct prefetch row (PU), its
                          // staging row if the last batch missed it, else -1
     int64_t *stat_log;   // [log calls][T][kNumStats + 1]: the counters of each call (see recmg_stats_log)
+    // resident rings (ring.hip)
+    int32_t *puref;         // [max_prefetch] per distinct prefetch row (PU) of a fully associative
+                            // table: its slot, or ring_ref_miss(m), or ring_ref_new(NP index)
+    int2 *zone;             // [max_indices + max_prefetch] (ref, row) of the rows that take the LRU
+                            // touch score, in row order; table t at pend_off + tstart[t]
+    int32_t *mslot;         // [max_indices] slot admitted for miss m (table t at tstart[t])
+    int32_t *npslot;        // [max_prefetch] slot admitted for new candidate k (table t at pstart[t])
+    int32_t *pend_row[2];   // [max_prefetch] pending lists (see TState), written by alternate placements
+    int32_t *pend_slot[2];  // [max_prefetch] their slots, -1 where the row was not kept
 };
 
 // Parameters of one placement.
@@ -401,6 +436,37 @@ __device__ __forceinline__ int32_t wave_append(bool want, int t, int32_t *counte
 
 __device__ __forceinline__ uint64_t make_key(int32_t score, int32_t row, int rowbits) {
     return ((uint64_t)(uint32_t)score << rowbits) | (uint64_t)(uint32_t)row;
+}
+
+// The error word read once per block.  Evict and admit may set it (a broken
+// invariant) while other blocks of the same kernel start, and the waves of a
+// block must agree before the block's barriers.
+__device__ __forceinline__ bool block_err(const DGlobal &g) {
+    __shared__ int s_err;
+    if (threadIdx.x == 0) s_err = *g.err;
+    __syncthreads();
+    return s_err != 0;
+}
+
+// A placement's candidate counts for table t: |K| = residents + the last
+// batch's misses + new prefetch rows, of which min(Cap, |K|) stay.
+struct Counts {
+    int32_t cap, nm, nnp, mode, keep;
+};
+
+__device__ __forceinline__ Counts table_counts(const DTable &tb, const TState &st, const PlcParams &p) {
+    Counts c;
+    c.cap = tb.cap;
+    c.nm = p.have_fwd ? st.mcount : 0;
+    c.nnp = st.npcount;
+    const int64_t nk = (int64_t)st.n_res + c.nm + c.nnp;
+    c.keep = (int32_t)(nk < c.cap ? nk : c.cap);
+    c.mode = nk <= c.cap ? SEL_ALL : (c.keep == 0 ? SEL_NONE : SEL_SELECT);
+    return c;
+}
+
+__device__ __forceinline__ bool kept(int mode, uint64_t key, uint64_t thr) {
+    return mode == SEL_ALL || (mode == SEL_SELECT && key >= thr);
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {

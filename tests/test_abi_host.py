@@ -65,10 +65,28 @@ def test_query_workspace_sizes():
 
 
 def test_lfu_keeps_a_counter_per_row():
-    """LFU_BATCH counts batches for every row: 4 bytes per row more workspace."""
-    lru, _ = bd.recmg_query_workspace(_cfg(rows=(100000,)))
+    """LFU_BATCH counts batches for every row: 4 bytes per row more workspace
+    than PRIORITY, which keeps no per-row state."""
+    prio, _ = bd.recmg_query_workspace(_cfg(rows=(100000,), policy=1))
     lfu, _ = bd.recmg_query_workspace(_cfg(rows=(100000,), policy=2))
-    assert lfu - lru >= 4 * 100000 - 1024  # up to a few 256-byte alignments
+    assert lfu - prio >= 4 * 100000 - 1024  # up to a few 256-byte alignments
+
+
+def test_lru_keeps_a_resident_ring():
+    """LRU_BATCH fully associative tables keep their residents in key order:
+    two ring buffers of at least Cap + 3 x (max_indices + max_prefetch)
+    entries, a slot -> entry index, the zones and the pending lists.  Tables
+    with Cap 0 and set-associative tables keep none."""
+    lru, _ = bd.recmg_query_workspace(_cfg(caps=(100,)))
+    prio, _ = bd.recmg_query_workspace(_cfg(caps=(100,), policy=1))
+    ring = 2 * 4 * (100 + 3 * (5000 + 5000))
+    assert lru - prio >= ring + 8 * (5000 + 5000)
+    lru0, _ = bd.recmg_query_workspace(_cfg(caps=(0,)))
+    prio0, _ = bd.recmg_query_workspace(_cfg(caps=(0,), policy=1))
+    assert lru0 - prio0 < 4096
+    lru_sa, _ = bd.recmg_query_workspace(_cfg(caps=(128,), ways=32))
+    prio_sa, _ = bd.recmg_query_workspace(_cfg(caps=(128,), ways=32, policy=1))
+    assert lru_sa - prio_sa < 4096
 
 
 def test_query_scales_with_capacity():
