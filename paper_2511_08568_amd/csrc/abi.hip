@@ -49,6 +49,10 @@ int64_t pow2ceil(int64_t x) {
     return p;
 }
 
+#ifndef RECMG_RING_SLACK
+#define RECMG_RING_SLACK 3  // resident-ring buffers hold Cap + this many placements' appends (>= 1)
+#endif
+
 struct Geom {
     int64_t rows = 0;
     int32_t dim = 0, dtype = 0, esz = 0, row_bytes = 0, cap = 0;
@@ -63,7 +67,7 @@ struct Geom {
 struct Layout {
     size_t total = 0, host_total = 0;
     std::vector<size_t> pool, slot_row, slot_score, slot_flags, slot_touch, slot_cbit, free_stack, map, bitmap, rank,
-        seg, freq, slot_pos, ring0, ring1, rcnt, roff;
+        seg, freq, slot_pos, ring0, ring1, rcnt0, rcnt1, roff;
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, raddr = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
     size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, pool_btab = 0, ftstart = 0;
@@ -156,9 +160,10 @@ int32_t check_config(const recmg_config_t *cfg, std::vector<Geom> *geo) {
         // entries; after a compaction at most Cap are live, and the rest of the
         // buffer takes the appends of the placements until the next one.
         const int64_t per_plc = cfg->max_indices + cfg->max_prefetch;
-        const int64_t rc = ((int64_t)g.cap + 3 * per_plc + 2 * kRingChunk) / kRingChunk * kRingChunk;
+        const int64_t rc = ((int64_t)g.cap + RECMG_RING_SLACK * per_plc + 2 * kRingChunk) / kRingChunk * kRingChunk;
         if (cfg->policy == RECMG_LRU_BATCH && !g.ways && g.cap > 0 && cfg->max_indices < (1 << 30) - 1 &&
-            cfg->max_prefetch < (1 << 30) - 1 && rc < (int64_t(1) << 31) - kRingChunk)
+            cfg->max_prefetch < (1 << 30) - 1 && cfg->max_indices + 2 * cfg->max_prefetch < (int64_t(1) << 31) &&
+            rc < (int64_t(1) << 31) - kRingChunk)
             g.ring_cap = (int32_t)rc;
     }
 
@@ -201,7 +206,8 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
         L->slot_pos.push_back(take(rc ? (size_t)g.cap * 4 : 0));
         L->ring0.push_back(take(rc * 4));
         L->ring1.push_back(take(rc * 4));
-        L->rcnt.push_back(take(rc / kRingChunk * 4));
+        L->rcnt0.push_back(take(rc / kRingChunk * 4));
+        L->rcnt1.push_back(take(rc / kRingChunk * 4));
         L->roff.push_back(take(rc / kRingChunk * 4));
         if (rc) any_ring = true;
         L->total_bm_blocks += g.bm_nblk;
@@ -929,7 +935,8 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
             d.slot_pos = reinterpret_cast<int32_t *>(ws + L.slot_pos[t]);
             d.ring[0] = reinterpret_cast<int32_t *>(ws + L.ring0[t]);
             d.ring[1] = reinterpret_cast<int32_t *>(ws + L.ring1[t]);
-            d.rcnt = reinterpret_cast<int32_t *>(ws + L.rcnt[t]);
+            d.rcnt[0] = reinterpret_cast<int32_t *>(ws + L.rcnt0[t]);
+            d.rcnt[1] = reinterpret_cast<int32_t *>(ws + L.rcnt1[t]);
             d.roff = reinterpret_cast<int32_t *>(ws + L.roff[t]);
             d.ring_cap = ge.ring_cap;
             c->has_ring = true;
@@ -983,7 +990,8 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
             HIP_TRY(hipMemsetAsync(ws + L.slot_pos[t], 0xff, (size_t)ge.cap * 4, s0));
             HIP_TRY(hipMemsetAsync(ws + L.ring0[t], 0xff, (size_t)ge.ring_cap * 4, s0));
             HIP_TRY(hipMemsetAsync(ws + L.ring1[t], 0xff, (size_t)ge.ring_cap * 4, s0));
-            HIP_TRY(hipMemsetAsync(ws + L.rcnt[t], 0, (size_t)ge.ring_cap / kRingChunk * 4, s0));
+            HIP_TRY(hipMemsetAsync(ws + L.rcnt0[t], 0, (size_t)ge.ring_cap / kRingChunk * 4, s0));
+            HIP_TRY(hipMemsetAsync(ws + L.rcnt1[t], 0, (size_t)ge.ring_cap / kRingChunk * 4, s0));
         }
     }
     HIP_TRY(hipMemsetAsync(ws + L.st, 0, sizeof(TState) * T, s0));
@@ -1114,7 +1122,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         if (c->has_scan_fa) launch_plc_evict(g, p, c->max_cap, s);
         if (c->has_ring) launch_ring_evict(g, p, ring_items, c->max_ring_chunks, s);
         if (c->has_fa) launch_plc_admit(g, p, c->max_cap, c->max_map, cand_grid, s);
-        if (c->has_ring) launch_ring_store(g, p, ring_items, c->max_ring_chunks, c->max_cap, q, s);
+        if (c->has_ring) launch_ring_store(g, p, ring_items, c->max_cap, q, s);
         if (c->has_sa)
             launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks, c->cfg.ways, s);
     }

@@ -68,8 +68,8 @@ void launch_init_state(const DGlobal &g, int32_t max_cap, hipStream_t s);
 // writes (the next one reads it).
 void launch_ring_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s);
 void launch_ring_evict(const DGlobal &g, const PlcParams &p, int64_t item_bound, int32_t ring_chunks, hipStream_t s);
-void launch_ring_store(const DGlobal &g, const PlcParams &p, int64_t item_bound, int32_t ring_chunks, int32_t max_cap,
-                       int wr, hipStream_t s);
+void launch_ring_store(const DGlobal &g, const PlcParams &p, int64_t item_bound, int32_t max_cap, int wr,
+                       hipStream_t s);
 
 // setassoc.hip: placement of the set-associative tables (nu: index space of
 // the last forward's distinct rows, np: of this placement's prefetch rows;

@@ -741,8 +741,15 @@ __global__ void k_plc_finalize(DGlobal g, int64_t *fdesc, int64_t log_slot) {
             st.n_res = tb.cap - st.free_top;
         }
         if (tb.ring_cap) {  // the ring's new front and back, the new pending list
-            st.r_tail = st.r_cut;
-            st.r_head += st.z1_len;
+            if (st.r_compact) {  // the live entries moved to the front of the other buffer
+                st.r_buf ^= 1;
+                st.r_tail = 0;
+                st.r_head = st.r_moved + st.z1_len;
+                st.r_compact = 0;
+            } else {
+                st.r_tail = st.r_cut;
+                st.r_head += st.z1_len;
+            }
             st.pend_n = st.pcount;
             st.pend_off = g.pstart[t];
             if (st.r_valid + st.pend_keep != st.n_res || st.r_head > tb.ring_cap) atomicOr(g.err, ERR_INTERNAL);

@@ -92,7 +92,7 @@ struct DTable {
     int32_t *slot_pos;  // [cap] index of the slot's entry in the current ring buffer, -1 if none
     int32_t *ring[2];   // [ring_cap] each: slot ids in key order, kRingHole where none; one buffer is
                         // current, the other receives the compacted entries
-    int32_t *rcnt;      // [ring_cap / kRingChunk] live entries per chunk of the current buffer
+    int32_t *rcnt[2];   // [ring_cap / kRingChunk] each: live entries per chunk of each buffer
     int32_t *roff;      // [ring_cap / kRingChunk] compaction: first new index of each chunk's entries
     int32_t ring_cap;   // entries per buffer (a multiple of kRingChunk); 0: ranked by radix select
 };
@@ -117,7 +117,7 @@ struct TState {
     // (score = this placement's LRU touch) wait in the pending list, entries
     // [pend_off, + pend_n) of pend_row / pend_slot[pend_buf], until a placement
     // merges them into the ring with the rows the last batch touched.
-    int32_t r_head, r_tail, r_cut, r_valid, r_buf, r_compact, r_zevict;
+    int32_t r_head, r_tail, r_cut, r_valid, r_buf, r_compact, r_zevict, r_moved;
     int32_t z1_len, z1_keys, pend_n, pend_buf, pend_keep;
     int64_t pend_off;
     // published counters, in recmg_table_stats_t order

@@ -68,8 +68,20 @@ __device__ __forceinline__ int2 *ring_zone(const DGlobal &g, const TState &st, i
     return g.zone + st.pend_off + g.tstart[t];
 }
 
-// New scores of the last batch's hits (touch score, or pscore if the list
-// names them; they lose F_PF) and of the list's untouched residents (pscore).
+// One pass over the pending rows, the last batch's distinct rows and the
+// prefetch list:
+//  * Z1 by merging two ascending lists: pending entry i lands at i + (U rows
+//    below it), U entry u at u + (pending rows at or below it), so a row in
+//    both (a pending row the batch touched) takes two places, the pending one
+//    a hole.  A key is a pending row neither touched nor named again, a hit or
+//    miss the list does not name (F_INP, set by classification).
+//  * new scores: hits take the touch score, or pscore if the list names them
+//    (and lose F_PF); the list's untouched residents take pscore.  Their ring
+//    entries go stale (slot_pos = -1).  F_INP stays until the append.
+//  * the misses' scores, which admission reads.
+// A thread reads a pending row's flags only if the batch did not touch it,
+// and only hit threads write flags (of touched slots), so the reads see
+// settled values.
 __global__ void __launch_bounds__(kBlock) k_ring_touch(DGlobal g, PlcParams p) {
     if (*g.err) return;
     __shared__ int tmp[16];
@@ -78,90 +90,75 @@ __global__ void __launch_bounds__(kBlock) k_ring_touch(DGlobal g, PlcParams p) {
     if (!tb.ring_cap) return;
     TState &st = g.st[t];
     const int64_t ts = g.tstart[t], ps = g.pstart[t];
-    const int32_t nu = p.have_fwd ? st.ucount : 0;
-    const int64_t n = (int64_t)nu + st.pcount;
-    int stale = 0;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-        int32_t sl, s;
-        if (i < nu) {
-            sl = g.slotU[ts + i];  // a slot for a hit
-            if (sl < 0) continue;
-            const uint32_t f = tb.slot_flags[sl];
-            s = (f & F_INP) ? p.pscore : p.lru_touch;
-            tb.slot_flags[sl] = f & ~(F_PF | F_INP);
-        } else {
-            sl = g.puref[ps + (i - nu)];
-            // not resident, or touched (the hit above gave it its score)
-            if (sl < 0 || tb.slot_touch[sl] == p.last_stamp) continue;
-            s = p.pscore;
-            tb.slot_flags[sl] &= ~F_INP;
-        }
-        tb.slot_score[sl] = s;
-        const int32_t e = tb.slot_pos[sl];
-        if (e >= 0) {  // its ring entry goes stale (pending rows have none)
-            tb.slot_pos[sl] = -1;
-            atomicSub(&tb.rcnt[e / kRingChunk], 1);
-            ++stale;
-        }
-    }
-    const int ns = block_sum(stale, tmp);
-    if (threadIdx.x == 0 && ns) atomicSub(&st.r_valid, ns);
-}
-
-// Z1 by merging two ascending lists: pending entry i lands at i + (U rows
-// below it), U entry u at u + (pending rows at or below it), so a row in both
-// (a pending row the batch touched) takes two places, the pending one a hole.
-// Also the misses' scores, which admission reads.
-__global__ void __launch_bounds__(kBlock) k_ring_zones(DGlobal g, PlcParams p) {
-    if (*g.err) return;
-    __shared__ int tmp[16];
-    const int t = blockIdx.y;
-    const DTable &tb = g.tabs[t];
-    if (!tb.ring_cap) return;
-    TState &st = g.st[t];
-    const int64_t ts = g.tstart[t];
     const int32_t nu = p.have_fwd ? st.ucount : 0, pn = st.pend_n;
     const int32_t *prow = g.pend_row[st.pend_buf] + st.pend_off;
     const int32_t *pslot = g.pend_slot[st.pend_buf] + st.pend_off;
     const int32_t *urow = g.U + ts;
+    int32_t *rcnt = tb.rcnt[st.r_buf];
     int2 *z = ring_zone(g, st, t);
-    const int32_t n = pn + nu;
-    if (blockIdx.x == 0 && threadIdx.x == 0) st.z1_len = n;
-    int keys = 0;
+    const int32_t n1 = pn + nu, n = n1 + st.pcount;
+    if (blockIdx.x == 0 && threadIdx.x == 0) st.z1_len = n1;
+    int keys = 0, stale = 0;
     for (int32_t j = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x); j < n; j += (int32_t)(gridDim.x * blockDim.x)) {
-        int32_t row, at, ref = kRingHole;
-        if (j < pn) {
-            row = prow[j];
-            const int32_t sl = pslot[j];
-            at = j + ring_bound(urow, nu, row, false);
-            // still score b: neither touched by the batch nor named again
-            if (sl >= 0 && sl < tb.cap && tb.slot_score[sl] == p.lru_touch && tb.slot_touch[sl] != p.last_stamp)
-                ref = sl;
-        } else {
-            const int32_t u = j - pn;
-            row = urow[u];
-            const int32_t sl = g.slotU[ts + u];
-            at = u + ring_bound(prow, pn, row, true);
-            if (sl >= 0) {
-                if (tb.slot_score[sl] == p.lru_touch) ref = sl;  // a hit the list does not name
+        int32_t sl = -1, s = 0;  // a resident whose score changes, and its new score
+        if (j < n1) {
+            int32_t row, at, ref = kRingHole;
+            if (j < pn) {
+                row = prow[j];
+                const int32_t q = pslot[j];
+                at = j + ring_bound(urow, nu, row, false);
+                if (q >= 0 && q < tb.cap && tb.slot_touch[q] != p.last_stamp && !(tb.slot_flags[q] & F_INP)) ref = q;
             } else {
-                const int32_t m = -sl - 1;
-                const bool inp = (g.mflags[ts + m] & F_INP) != 0;
-                g.mscore[ts + m] = inp ? p.pscore : p.lru_touch;
-                if (!inp) ref = ring_ref_miss(m);
+                const int32_t u = j - pn;
+                row = urow[u];
+                const int32_t h = g.slotU[ts + u];
+                at = u + ring_bound(prow, pn, row, true);
+                if (h >= 0) {
+                    const uint32_t f = tb.slot_flags[h];
+                    const bool inp = (f & F_INP) != 0;
+                    if (!inp) ref = h;
+                    sl = h;
+                    s = inp ? p.pscore : p.lru_touch;
+                    if (f & F_PF) tb.slot_flags[h] = f & ~F_PF;
+                } else {
+                    const int32_t m = -h - 1;
+                    const bool inp = (g.mflags[ts + m] & F_INP) != 0;
+                    g.mscore[ts + m] = inp ? p.pscore : p.lru_touch;
+                    if (!inp) ref = ring_ref_miss(m);
+                }
+            }
+            z[at] = make_int2(ref, row);
+            keys += ref != kRingHole ? 1 : 0;
+        } else {
+            const int32_t v = g.puref[ps + (j - n1)];
+            if (v >= 0 && tb.slot_touch[v] != p.last_stamp) {  // touched: its hit entry scored it
+                sl = v;
+                s = p.pscore;
             }
         }
-        z[at] = make_int2(ref, row);
-        keys += ref != kRingHole ? 1 : 0;
+        if (sl >= 0) {
+            tb.slot_score[sl] = s;
+            const int32_t e = tb.slot_pos[sl];
+            if (e >= 0) {  // pending rows have no ring entry
+                tb.slot_pos[sl] = -1;
+                atomicSub(&rcnt[e / kRingChunk], 1);
+                ++stale;
+            }
+        }
     }
-    const int k = block_sum(keys, tmp);
-    if (threadIdx.x == 0 && k) atomicAdd(&st.z1_keys, k);
+    const int k = block_sum(keys, tmp), ns = block_sum(stale, tmp);
+    if (threadIdx.x == 0) {
+        if (k) atomicAdd(&st.z1_keys, k);
+        if (ns) atomicSub(&st.r_valid, ns);
+    }
 }
 
 // One block per table: where the D keys to drop end.  Sets sel_mode and the
 // threshold key (st.prefix) that admission applies to the candidates, the
-// ring's cut, whether Z1/Z2 residents are evicted, whether the ring is
-// compacted before this placement's run is appended.
+// ring's cut, whether Z1/Z2 residents are evicted, and whether the live
+// entries after the cut move to the front of the other buffer (when this
+// placement's run would not fit behind them), with each chunk's first new
+// index.
 __global__ void __launch_bounds__(kRingThreads) k_ring_cut(DGlobal g, PlcParams p) {
     if (*g.err) return;
     __shared__ int tmp[16];
@@ -176,18 +173,19 @@ __global__ void __launch_bounds__(kRingThreads) k_ring_cut(DGlobal g, PlcParams 
     const int32_t nold = st.r_valid, z1 = st.z1_keys, z2 = st.pcount;
     const int32_t head = st.r_head, tail = st.r_tail;
     const int32_t *ring = tb.ring[st.r_buf];
+    const int32_t *rcnt = tb.rcnt[st.r_buf];
+    const int32_t nch = (int32_t)(((int64_t)head + kRingChunk - 1) / kRingChunk);
     bool bad = nold < 0 || (int64_t)nold + z1 + z2 != nk;  // every key sits in the ring, Z1 or Z2
-    int32_t mode = c.mode, cut = tail, zev = 0;
+    int32_t mode = c.mode, cut = tail, zev = 0, cut_live = 0;  // cut_live: live entries of cut's chunk before it
     uint64_t thr = make_key(p.lru_touch, 0, p.rowbits);  // below every key of Z1 and Z2
     if (!bad && drop > 0 && drop <= nold) {
         // the drop-th live entry from the front: whole chunks by their counts,
         // then the entries of the chunk that reaches it
         mode = SEL_SELECT;
         int32_t need = (int32_t)drop, cc = -1;
-        const int32_t nch = (int32_t)(((int64_t)head + kRingChunk - 1) / kRingChunk);
         for (int32_t base = tail / kRingChunk; base < nch; base += kRingThreads) {
             const int32_t ch = base + (int32_t)threadIdx.x;
-            const int v = ch < nch ? tb.rcnt[ch] : 0;
+            const int v = ch < nch ? rcnt[ch] : 0;
             int tot;
             const int ex = block_excl_scan(v, tmp, &tot);
             if (need <= tot) {  // block-uniform
@@ -215,6 +213,7 @@ __global__ void __launch_bounds__(kRingThreads) k_ring_cut(DGlobal g, PlcParams 
             __syncthreads();
             cut = s_at;
             if (cut < 0) bad = true;
+            else if (cut / kRingChunk == cc) cut_live = need;
         }
     } else if (!bad && drop > nold) {
         // the whole ring goes; the threshold is the key of rank r of Z1, or of
@@ -253,6 +252,22 @@ __global__ void __launch_bounds__(kRingThreads) k_ring_cut(DGlobal g, PlcParams 
     } else if (!bad) {
         mode = SEL_ALL;  // nothing to drop
     }
+    const int32_t moved = bad ? 0 : (int32_t)(drop <= 0 ? nold : drop <= nold ? nold - drop : 0);
+    const bool compact = (int64_t)head + st.z1_len > tb.ring_cap;
+    if (compact && moved > 0) {
+        // first new index of each chunk from cut's on: its live entries at or after the cut
+        int32_t run = 0;
+        const int32_t c0 = cut / kRingChunk;
+        for (int32_t base = c0; base < nch; base += kRingThreads) {
+            const int32_t ch = base + (int32_t)threadIdx.x;
+            const int v = ch < nch ? rcnt[ch] - (ch == c0 ? cut_live : 0) : 0;
+            int tot;
+            const int ex = block_excl_scan(v, tmp, &tot);
+            if (ch < nch) tb.roff[ch] = run + ex;
+            run += tot;
+        }
+        if (run != moved) bad = true;
+    }
     if (threadIdx.x == 0) {
         if (bad) atomicOr(g.err, ERR_INTERNAL);
         st.sel_mode = mode;
@@ -260,14 +275,18 @@ __global__ void __launch_bounds__(kRingThreads) k_ring_cut(DGlobal g, PlcParams 
         st.plc_nm = c.nm;
         st.r_cut = cut;
         st.r_zevict = zev;
-        st.r_compact = (int64_t)head + st.z1_len > tb.ring_cap ? 1 : 0;
+        st.r_compact = compact ? 1 : 0;
+        st.r_moved = moved;
     }
 }
 
-// Evict the live ring entries in [r_tail, r_cut), a chunk per block
-// iteration (one count update per chunk), and, when the cut passed the whole
-// ring, the Z1 and Z2 residents below the threshold.  Freed slots gather in
-// LDS and reach the free stack with one atomic per flush.
+// Evict the live ring entries in [r_tail, r_cut) and, when the cut passed
+// the whole ring, the Z1 and Z2 residents below the threshold.  When
+// compacting, the live entries after the cut go, in order, to the front of
+// the other buffer (whose chunk counts are set here; their slots learn their
+// new index in the append, after every move has read the old ones).  A
+// chunk per block iteration, one count update per chunk; freed slots gather
+// in LDS and reach the free stack with one atomic per flush.
 __global__ void __launch_bounds__(kBlock) k_ring_evict(DGlobal g, PlcParams p) {
     if (block_err(g)) return;
     __shared__ int tmp[16];
@@ -313,27 +332,53 @@ __global__ void __launch_bounds__(kBlock) k_ring_evict(DGlobal g, PlcParams p) {
         wb = __shfl(wb, 0);
         if (ev) s_free[wb + __popcll(m & ((1ull << lane) - 1ull))] = sl;
     };
-    const int32_t tail = st.r_tail, cut = st.r_cut;
-    const int32_t *ring = tb.ring[st.r_buf];
-    if (cut > tail) {
-        const int32_t c1 = (cut - 1) / kRingChunk;
-        for (int32_t ch = tail / kRingChunk + (int32_t)blockIdx.x; ch <= c1; ch += (int32_t)gridDim.x) {
-            const int32_t e0 = ch * kRingChunk + 4 * (int32_t)threadIdx.x;
-            const uint4 v = gload16(ring + e0);
-            const int32_t sl[4] = {(int32_t)v.x, (int32_t)v.y, (int32_t)v.z, (int32_t)v.w};
-            int here = 0;
+    const int32_t tail = st.r_tail, cut = st.r_cut, head = st.r_head, moved = st.r_moved;
+    const bool compact = st.r_compact != 0;
+    const int cur = st.r_buf;
+    const int32_t *ring = tb.ring[cur];
+    int32_t *dst = tb.ring[cur ^ 1];
+    // chunks [tail's, hi): up to the cut's, or to the last live one when moving
+    const int32_t hi = compact && moved > 0 ? (int32_t)(((int64_t)head + kRingChunk - 1) / kRingChunk)
+                       : cut > tail          ? (cut - 1) / kRingChunk + 1
+                                             : 0;
+    for (int32_t ch = tail / kRingChunk + (int32_t)blockIdx.x; ch < hi; ch += (int32_t)gridDim.x) {
+        const int32_t e0 = ch * kRingChunk + 4 * (int32_t)threadIdx.x;
+        const uint4 v = gload16(ring + e0);
+        const int32_t sl[4] = {(int32_t)v.x, (int32_t)v.y, (int32_t)v.z, (int32_t)v.w};
+        bool mv[4];
+        int here = 0, nmv = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int32_t e = e0 + i;
+            const bool live = e >= tail && e < head && ring_live(tb, sl[i], e);
+            const bool ev = live && e < cut;
+            mv[i] = live && !ev && compact;
+            evict(ev, sl[i]);
+            here += ev ? 1 : 0;
+            nmv += mv[i] ? 1 : 0;
+        }
+        int tot;
+        const int ex = block_excl_scan(nmv, tmp, &tot);
+        if (tot) {  // block-uniform; chunks with movers lie at or after the cut's
+            int32_t at = tb.roff[ch] + ex;
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int32_t e = e0 + i;
-                const bool ev = e >= tail && e < cut && ring_live(tb, sl[i], e);
-                evict(ev, sl[i]);
-                here += ev ? 1 : 0;
+                if (!mv[i]) continue;
+                if (at < moved) dst[at++] = sl[i];
+                else atomicOr(g.err, ERR_INTERNAL);  // counts and entries disagree (never expected)
             }
-            const int hn = block_sum(here, tmp);
-            if (threadIdx.x == 0 && hn) atomicSub(&tb.rcnt[ch], hn);
-            nring += here;
-            __syncthreads();
-            if (s_n > kRingEvictBuf - 4 * (int)blockDim.x) flush();
+        }
+        const int hn = block_sum(here, tmp);
+        if (threadIdx.x == 0 && hn) atomicSub(&tb.rcnt[cur][ch], hn);
+        nring += here;
+        __syncthreads();
+        if (s_n > kRingEvictBuf - 4 * (int)blockDim.x) flush();
+    }
+    if (compact) {  // the other buffer's chunk counts: [0, moved) live
+        const int32_t nchunks = tb.ring_cap / kRingChunk;
+        for (int32_t ch = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x); ch < nchunks; ch += (int32_t)(gridDim.x * blockDim.x)) {
+            const int64_t left = (int64_t)moved - (int64_t)ch * kRingChunk;
+            tb.rcnt[cur ^ 1][ch] = left <= 0 ? 0 : left >= kRingChunk ? kRingChunk : (int32_t)left;
         }
     }
     if (st.r_zevict) {
@@ -371,107 +416,11 @@ __global__ void __launch_bounds__(kBlock) k_ring_evict(DGlobal g, PlcParams p) {
     }
 }
 
-// Compaction (when r_compact): the live entries of [r_cut, r_head), in
-// order, to the front of the other buffer.  First each chunk's new offset.
-__global__ void __launch_bounds__(kRingThreads) k_ring_cscan(DGlobal g) {
-    if (*g.err) return;
-    __shared__ int tmp[16];
-    const int t = blockIdx.x;
-    const DTable &tb = g.tabs[t];
-    if (!tb.ring_cap) return;
-    TState &st = g.st[t];
-    if (!st.r_compact) return;
-    const int32_t nch = (int32_t)(((int64_t)st.r_head + kRingChunk - 1) / kRingChunk);
-    int32_t run = 0;
-    for (int32_t base = st.r_cut / kRingChunk; base < nch; base += kRingThreads) {
-        const int32_t ch = base + (int32_t)threadIdx.x;
-        const int v = ch < nch ? tb.rcnt[ch] : 0;
-        int tot;
-        const int ex = block_excl_scan(v, tmp, &tot);
-        if (ch < nch) tb.roff[ch] = run + ex;
-        run += tot;
-    }
-    if (threadIdx.x == 0 && run != st.r_valid) atomicOr(g.err, ERR_INTERNAL);
-}
-
-// ... then each chunk's live entries at their offsets (four per thread, in order).
-__global__ void __launch_bounds__(kBlock) k_ring_cmove(DGlobal g) {
-    if (*g.err) return;
-    __shared__ int tmp[16];
-    const int t = blockIdx.y;
-    const DTable &tb = g.tabs[t];
-    if (!tb.ring_cap) return;
-    const TState &st = g.st[t];
-    if (!st.r_compact) return;
-    const int32_t *src = tb.ring[st.r_buf];
-    int32_t *dst = tb.ring[st.r_buf ^ 1];
-    const int32_t cut = st.r_cut, head = st.r_head;
-    const int32_t nch = (int32_t)(((int64_t)head + kRingChunk - 1) / kRingChunk);
-    for (int32_t ch = cut / kRingChunk + (int32_t)blockIdx.x; ch < nch; ch += (int32_t)gridDim.x) {
-        const int32_t e0 = ch * kRingChunk + 4 * (int32_t)threadIdx.x;
-        const uint4 v = gload16(src + e0);
-        const int32_t sl[4] = {(int32_t)v.x, (int32_t)v.y, (int32_t)v.z, (int32_t)v.w};
-        bool lv[4];
-        int cnt = 0;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int32_t e = e0 + i;
-            lv[i] = e >= cut && e < head && ring_live(tb, sl[i], e);
-            cnt += lv[i] ? 1 : 0;
-        }
-        int tot;
-        int32_t at = tb.roff[ch] + block_excl_scan(cnt, tmp, &tot);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if (!lv[i]) continue;
-            if (at < st.r_valid) dst[at++] = sl[i];
-            else atomicOr(g.err, ERR_INTERNAL);  // counts and entries disagree (never expected)
-        }
-    }
-}
-
-// ... then the moved slots' new positions (after every move has read the old ones).
-__global__ void __launch_bounds__(kBlock) k_ring_cfix(DGlobal g) {
-    if (*g.err) return;
-    const int t = blockIdx.y;
-    const DTable &tb = g.tabs[t];
-    if (!tb.ring_cap) return;
-    const TState &st = g.st[t];
-    if (!st.r_compact) return;
-    const int32_t *dst = tb.ring[st.r_buf ^ 1];
-    for (int32_t k = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x); k < st.r_valid; k += (int32_t)(gridDim.x * blockDim.x)) {
-        const int32_t sl = dst[k];
-        if (sl >= 0 && sl < tb.cap) tb.slot_pos[sl] = k;
-        else atomicOr(g.err, ERR_INTERNAL);
-    }
-}
-
-// ... then the other buffer becomes current: entries [0, r_valid) all live.
-__global__ void __launch_bounds__(kRingThreads) k_ring_cfin(DGlobal g) {
-    if (*g.err) return;
-    const int t = blockIdx.x;
-    const DTable &tb = g.tabs[t];
-    if (!tb.ring_cap) return;
-    TState &st = g.st[t];
-    if (!st.r_compact) return;
-    const int32_t n = st.r_valid, nch = tb.ring_cap / kRingChunk;
-    for (int32_t ch = threadIdx.x; ch < nch; ch += blockDim.x) {
-        const int64_t left = (int64_t)n - (int64_t)ch * kRingChunk;
-        tb.rcnt[ch] = left <= 0 ? 0 : left >= kRingChunk ? kRingChunk : (int32_t)left;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        st.r_buf ^= 1;
-        st.r_tail = 0;
-        st.r_cut = 0;
-        st.r_head = n;
-        st.r_compact = 0;
-    }
-}
-
-// Z1's kept keys to ring entries [r_head, + z1_len) (a chunk per block
-// iteration); Z2's rows and their slots (-1 where not kept) to the pending
-// list of buffer wr.  Admitted candidates' slots come from admission.
+// After admission: when compacting, the moved slots' new indices (every move
+// has read the old ones); Z1's kept keys to ring entries [head, + z1_len) of
+// the buffer that stays current (a chunk per block iteration); Z2's rows and
+// their slots (-1 where not kept) to the pending list of buffer wr, the kept
+// residents losing F_INP.  Admitted candidates' slots come from admission.
 __global__ void __launch_bounds__(kBlock) k_ring_append(DGlobal g, PlcParams p, int wr) {
     if (*g.err) return;
     __shared__ int tmp[16];
@@ -482,12 +431,21 @@ __global__ void __launch_bounds__(kBlock) k_ring_append(DGlobal g, PlcParams p, 
     const int mode = st.sel_mode;
     const uint64_t thr = st.prefix;
     const int64_t ts = g.tstart[t], ps = g.pstart[t];
-    const int32_t n1 = st.z1_len, head = st.r_head;
+    const bool compact = st.r_compact != 0;
+    const int buf = compact ? st.r_buf ^ 1 : st.r_buf;
+    const int32_t n1 = st.z1_len, head = compact ? st.r_moved : st.r_head;
     if ((int64_t)head + n1 > tb.ring_cap) {  // compaction made room; never expected
         if (threadIdx.x == 0) atomicOr(g.err, ERR_INTERNAL);
         return;
     }
-    int32_t *ring = tb.ring[st.r_buf];
+    int32_t *ring = tb.ring[buf];
+    if (compact) {
+        for (int32_t k = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x); k < head; k += (int32_t)(gridDim.x * blockDim.x)) {
+            const int32_t sl = ring[k];
+            if (sl >= 0 && sl < tb.cap) tb.slot_pos[sl] = k;
+            else atomicOr(g.err, ERR_INTERNAL);
+        }
+    }
     const int2 *z = ring_zone(g, st, t);
     if (n1 > 0) {
         const int32_t c1 = (head + n1 - 1) / kRingChunk;
@@ -513,7 +471,7 @@ __global__ void __launch_bounds__(kBlock) k_ring_append(DGlobal g, PlcParams p, 
             }
             const int an = block_sum(add, tmp);
             if (threadIdx.x == 0 && an) {
-                atomicAdd(&tb.rcnt[ch], an);
+                atomicAdd(&tb.rcnt[buf][ch], an);
                 atomicAdd(&st.r_valid, an);
             }
         }
@@ -523,8 +481,14 @@ __global__ void __launch_bounds__(kBlock) k_ring_append(DGlobal g, PlcParams p, 
     for (int32_t i = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x); i < st.pcount; i += (int32_t)(gridDim.x * blockDim.x)) {
         const int32_t row = g.PU[ps + i], v = g.puref[ps + i];
         int32_t sl = -1;
-        if (kept(mode, make_key(p.pscore, row, p.rowbits), thr))
-            sl = v >= 0 ? v : v > kRingNewBase ? g.mslot[ts + (-1 - v)] : g.npslot[ps + (kRingNewBase - v)];
+        if (kept(mode, make_key(p.pscore, row, p.rowbits), thr)) {
+            if (v >= 0) {
+                sl = v;
+                tb.slot_flags[v] &= ~F_INP;
+            } else {
+                sl = v > kRingNewBase ? g.mslot[ts + (-1 - v)] : g.npslot[ps + (kRingNewBase - v)];
+            }
+        }
         prow[i] = row;
         pslot[i] = sl;
         keepn += sl >= 0 ? 1 : 0;
@@ -544,25 +508,21 @@ static inline unsigned ring_grid(int64_t n, int per_block, unsigned cap) {
 }
 
 void launch_ring_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s) {
-    const dim3 grid(ring_grid(item_bound, kBlock * 4, 1024), g.T);
-    k_ring_touch<<<grid, kBlock, 0, s>>>(g, p);
-    k_ring_zones<<<grid, kBlock, 0, s>>>(g, p);
+    k_ring_touch<<<dim3(ring_grid(item_bound, kBlock * 4, 1024), g.T), kBlock, 0, s>>>(g, p);
     k_ring_cut<<<g.T, kRingThreads, 0, s>>>(g, p);
 }
 
 void launch_ring_evict(const DGlobal &g, const PlcParams &p, int64_t item_bound, int32_t ring_chunks, hipStream_t s) {
-    // the cut is typically a few chunks past the front; blocks loop over more
+    // the cut is typically a few chunks past the front; a compaction walks
+    // every chunk, so blocks loop
     const unsigned gx = std::max(ring_grid(item_bound, kBlock * 4, 256), ring_grid(ring_chunks, 64, 256));
     k_ring_evict<<<dim3(gx, g.T), kBlock, 0, s>>>(g, p);
 }
 
-void launch_ring_store(const DGlobal &g, const PlcParams &p, int64_t item_bound, int32_t ring_chunks, int32_t max_cap,
-                       int wr, hipStream_t s) {
-    k_ring_cscan<<<g.T, kRingThreads, 0, s>>>(g);
-    k_ring_cmove<<<dim3(ring_grid(ring_chunks, 8, 1024), g.T), kBlock, 0, s>>>(g);
-    k_ring_cfix<<<dim3(ring_grid(max_cap, kBlock * 8, 1024), g.T), kBlock, 0, s>>>(g);
-    k_ring_cfin<<<g.T, kRingThreads, 0, s>>>(g);
-    k_ring_append<<<dim3(ring_grid(item_bound, kBlock * 4, 1024), g.T), kBlock, 0, s>>>(g, p, wr);
+void launch_ring_store(const DGlobal &g, const PlcParams &p, int64_t item_bound, int32_t max_cap, int wr,
+                       hipStream_t s) {
+    const unsigned gx = std::max(ring_grid(item_bound, kBlock * 4, 1024), ring_grid(max_cap, kBlock * 16, 1024));
+    k_ring_append<<<dim3(gx, g.T), kBlock, 0, s>>>(g, p, wr);
 }
 
 }  // namespace recmg
