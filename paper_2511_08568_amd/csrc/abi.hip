@@ -287,7 +287,8 @@ struct recmg_cache {
     DGlobal g{};
     std::vector<const char *> host;  // host tables (host pointers)
     int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1, nsa = 0, max_nblk = 0;
-    int64_t sa_blocks = 0;  // blocks of the set-associative placement kernel
+    int64_t sa_blocks = 0;   // blocks of the set-associative placement kernel
+    int64_t sa_blocks1 = 0;  // the first of them, over the tables of one set per wave
     bool has_fa = false, has_sa = false;  // tables of each form present
     bool has_ring = false, has_scan_fa = false;  // fully associative tables with and without a resident ring
     int32_t max_ring_chunks = 0;
@@ -962,13 +963,17 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     std::stable_sort(c->pool_order.begin(), c->pool_order.end(),
                      [&](int x, int y) { return geo[x].kind < geo[y].kind; });
     // set-associative placement: tables with the fewest sets first, kSaWaves
-    // waves of sa_sets_per_wave(ways) sets each per block
+    // waves of sa_sets_per_wave(ways, nsets) sets each per block
     std::vector<int32_t> sa_tab, sa_bs(1, 0);
     for (int t = 0; t < T; ++t)
         if (geo[t].ways) sa_tab.push_back(t);
     std::stable_sort(sa_tab.begin(), sa_tab.end(), [&](int x, int y) { return geo[x].nsets < geo[y].nsets; });
-    const int sa_per_block = kSaWaves * sa_sets_per_wave(cfg->ways);
-    for (int t : sa_tab) sa_bs.push_back(sa_bs.back() + (geo[t].nsets + sa_per_block - 1) / sa_per_block);
+    for (int t : sa_tab) {
+        const int spw = sa_sets_per_wave(geo[t].ways, geo[t].nsets);
+        const int per_block = kSaWaves * spw;
+        sa_bs.push_back(sa_bs.back() + (geo[t].nsets + per_block - 1) / per_block);
+        if (spw == 1) c->sa_blocks1 = sa_bs.back();  // a prefix: one set per wave only below kSaPairMinSets
+    }
     c->nsa = (int32_t)sa_tab.size();
     c->sa_blocks = sa_bs.back();
 
@@ -1124,7 +1129,7 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         if (c->has_fa) launch_plc_admit(g, p, c->max_cap, c->max_map, cand_grid, s);
         if (c->has_ring) launch_ring_store(g, p, ring_items, c->max_cap, q, s);
         if (c->has_sa)
-            launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks, c->cfg.ways, s);
+            launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks1, c->sa_blocks, s);
     }
     launch_plc_finalize(g, fdesc, c->cfg.stats_log_calls ? c->calls % c->cfg.stats_log_calls : -1, s);
     HIP_TRY(hipEventRecord(c->ev_plc, s));

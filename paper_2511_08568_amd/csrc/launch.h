@@ -73,11 +73,15 @@ void launch_ring_store(const DGlobal &g, const PlcParams &p, int64_t item_bound,
 
 // setassoc.hip: placement of the set-associative tables (nu: index space of
 // the last forward's distinct rows, np: of this placement's prefetch rows;
-// nsa tables, blocks = sa_bstart[nsa], kSaWaves * sa_sets_per_wave(ways)
-// sets per block)
+// nsa tables, fewest sets first; blocks = sa_bstart[nsa], the first blocks1 of
+// them over tables of one set per wave), kSaWaves * sa_sets_per_wave(ways,
+// nsets) sets per block of a table
 constexpr int kSaWaves = 16, kSaBlock = 64 * kSaWaves;
-constexpr int sa_sets_per_wave(int ways) { return ways <= 32 ? 2 : 1; }
-void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks,
-                     int32_t ways, hipStream_t s);
+// sets per wave of a table: two (32 lanes each) when the ways fit in half a
+// wave and the sets are many (few events each); one where sets take many events
+constexpr int64_t kSaPairMinSets = 16384;
+constexpr int sa_sets_per_wave(int ways, int64_t nsets) { return ways <= 32 && nsets >= kSaPairMinSets ? 2 : 1; }
+void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks1,
+                     int64_t blocks, hipStream_t s);
 
 }  // namespace recmg

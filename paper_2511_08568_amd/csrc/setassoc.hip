@@ -110,18 +110,20 @@ __device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_bal
 
 static_assert(kSaWaves == 16, "the block's counts are added up over one DPP row of 16 lanes");
 
-// SPW sets per wave (2 when W <= 32, lanes 32h .. 32h + 31 taking set h; else
-// 1), lane w of a set holding way w; kSaWaves * SPW sets per block.  The sets
-// of a wave play their events side by side, one event of each per step, so a
-// wave's chain of dependent loads serves two sets when the ways fit in half a
-// wave.  Blocks run table by table, tables with the fewest sets first: their
-// sets take the most events each, and the longest waves should start first.
-// The counters and the fill-list space of a block's sets are added up by its
-// first wave and taken with one atomic each per block (an atomic per set would
-// queue hundreds of thousands of them on the same few words of a table with
-// many sets).
+// SPW sets per wave (2 for tables with many sets of W <= 32 ways, lanes
+// 32h .. 32h + 31 taking set h; else 1), lane w of a set holding way w;
+// kSaWaves * SPW sets per block.  The sets of a wave play their events side
+// by side, one event of each per step, so a wave's chain of dependent loads
+// serves two sets when the ways fit in half a wave; a step then costs more
+// instructions, so tables with few sets (many events each, played one after
+// another) keep one set per wave.  Blocks run table by table, tables with the
+// fewest sets first: their sets take the most events each, and the longest
+// waves should start first.  The counters and the fill-list space of a
+// block's sets are added up by its first wave and taken with one atomic each
+// per block (an atomic per set would queue hundreds of thousands of them on
+// the same few words of a table with many sets).
 template <int SPW>
-__global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, int32_t nsa) {
+__global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, int32_t nsa, int32_t boff) {
     constexpr int HL = 64 / SPW;  // lanes per set
     __shared__ int s_cnt[kSaWaves][8];
     __shared__ unsigned long long s_dig[kSaWaves];
@@ -129,7 +131,8 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     // No early return: every wave reaches the block's barriers.  A wave that
     // finds the error word set (another block may set it meanwhile) does no work.
     const bool err = *g.err != 0;
-    const int kt = find_seg32(g.sa_bstart, nsa, (int32_t)blockIdx.x);
+    const int32_t bid = (int32_t)blockIdx.x + boff;  // block of the whole set-associative placement
+    const int kt = find_seg32(g.sa_bstart, nsa, bid);
     const int t = g.sa_btab[kt];
     const DTable &tb = g.tabs[t];
     TState &st = g.st[t];
@@ -145,9 +148,26 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
         const int a = __builtin_amdgcn_readlane(v, k0 & 31), b = __builtin_amdgcn_readlane(v, 32 + (k1 & 31));
         return hi ? b : a;
     };
-    const int64_t set = ((int64_t)(blockIdx.x - g.sa_bstart[kt]) * kSaWaves + wid) * SPW + h;
+    const int64_t set = ((int64_t)(bid - g.sa_bstart[kt]) * kSaWaves + wid) * SPW + h;
     int4 sg = make_int4(0, 0, 0, 0);
-    if (!err && set < tb.nsets) sg = tb.seg[set];
+    // the ways are read beside the segment bounds, before it is known whether
+    // the set has events (about half of a large cache's sets have none in a
+    // placement): one round trip less on every set's chain
+    int32_t w_row = -1, w_score = 0, w_touch = -1, w_cbit = 0;
+    uint32_t w_flags = 0;
+    if (!err && set < tb.nsets) {
+        const uint4 sv = gload16(tb.seg + set);
+        sg = make_int4((int)sv.x, (int)sv.y, (int)sv.z, (int)sv.w);
+        if (wl < W) {
+            const int64_t sl = set * W + wl;
+            w_row = (int32_t)gload4(tb.slot_row + sl);
+            w_score = (int32_t)gload4(tb.slot_score + sl);
+            w_flags = gload4(tb.slot_flags + sl);
+            w_touch = (int32_t)gload4(tb.slot_touch + sl);
+            // caching bits are set only under PRIORITY (zero otherwise)
+            if (p.prio) w_cbit = RECMG_GLOBAL(uint8_t, tb.slot_cbit + sl);
+        }
+    }
     const bool active = sg.x != sg.y || sg.z != sg.w;  // uniform over the set's lanes
     const bool way = wl < W && active;
     const int64_t slot = set * W + wl;
@@ -188,11 +208,11 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     int32_t row0 = -1, score = 0;
     uint32_t flags = 0;
     if (way) {
-        row0 = tb.slot_row[slot];
-        score = tb.slot_score[slot];
-        flags = tb.slot_flags[slot] & F_PF;
-        if (row0 >= 0 && tb.slot_touch[slot] == p.last_stamp) {
-            const int cb = tb.slot_cbit[slot];
+        row0 = w_row;
+        score = w_score;
+        flags = w_flags & F_PF;
+        if (row0 >= 0 && w_touch == p.last_stamp) {
+            const int cb = w_cbit;
             if (cb) tb.slot_cbit[slot] = 0;
             flags = 0;
             score = touch_score(p, tb, row0, cb);
@@ -305,7 +325,7 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     int pdrop = 0, pres = 0;
     for (int32_t i0 = 0; i0 < max(np0, np1); i0 += HL) {
         const int32_t i = sg.z + i0 + wl;
-        const int32_t r = i < sg.w ? g.PU[pb + i] : -1;
+        const int32_t r = i < sg.w ? (i0 == 0 ? p0_r : g.PU[pb + i]) : -1;  // the first chunk is in registers
         bool in_r = false, in = false;
         for (uint64_t m = wm; m; m &= m - 1) in_r |= __builtin_amdgcn_readlane(row0, __ffsll((unsigned long long)m) - 1) == r;
         for (uint64_t m = dm; m; m &= m - 1) in |= __builtin_amdgcn_readlane(row, __ffsll((unsigned long long)m) - 1) == r;
@@ -397,12 +417,12 @@ static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
     return (unsigned)b;
 }
 
-void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks,
-                     int32_t ways, hipStream_t s) {
+void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks1,
+                     int64_t blocks, hipStream_t s) {
     if (nu + np > 0) k_sa_heads<<<grid_for(nu + np, kBlock, 8192), kBlock, 0, s>>>(g, nu, np, p.have_fwd, p.last_stamp);
-    if (blocks <= 0) return;
-    if (sa_sets_per_wave(ways) == 2) k_sa_place<2><<<(unsigned)blocks, kSaBlock, 0, s>>>(g, p, nsa);
-    else k_sa_place<1><<<(unsigned)blocks, kSaBlock, 0, s>>>(g, p, nsa);
+    // tables of one set per wave come first (fewest sets), then those of two
+    if (blocks1 > 0) k_sa_place<1><<<(unsigned)blocks1, kSaBlock, 0, s>>>(g, p, nsa, 0);
+    if (blocks > blocks1) k_sa_place<2><<<(unsigned)(blocks - blocks1), kSaBlock, 0, s>>>(g, p, nsa, (int32_t)blocks1);
 }
 
 }  // namespace recmg
