@@ -143,7 +143,9 @@ typedef enum {
     RECMG_STAGE_FWD_FETCH = 1,  /* on-demand miss fetch (zero-copy kernel or staged copy) */
     RECMG_STAGE_FWD_POOL = 2,   /* pooled gather + sum */
     RECMG_STAGE_PLC_CLASSIFY = 3, /* caching bits, prefetch dedup + classification */
-    RECMG_STAGE_PLC_RANK = 4,   /* scoring + radix select of the kept keys */
+    RECMG_STAGE_PLC_RANK = 4,   /* scoring + radix select of the kept keys (LRU_BATCH fully
+                                   associative tables: new scores, zones and the cut of the
+                                   resident ring) */
     RECMG_STAGE_PLC_APPLY = 5,  /* evict, map maintenance, admit, counters */
     RECMG_STAGE_PLC_FILL = 6,   /* copy of admitted rows into slots (host link for prefetch) */
     RECMG_STAGE_HOST_LINK = 7,  /* union of the FWD_FETCH and PLC_FILL intervals: the time the host
