@@ -62,6 +62,20 @@ def test_tiny_random(seed):
 
 
 @pytest.mark.parametrize("seed", range(6))
+def test_lru_ring_long_runs(seed):
+    """LRU_BATCH fully associative tables keep their residents in a key-ordered
+    ring: 60 placements on caches of at most 300 rows with prefetch lists of
+    every kind, so that the ring compacts (its buffers hold Cap plus three
+    placements' worth of appends) and some placements drop more keys than the
+    ring holds live (the threshold then falls among this placement's own
+    keys); every placement's counters, digest and resident set against the
+    oracle."""
+    w = tg.random_tiny(800 + seed, max_rows=3000, max_cap=300, max_dim=17, batches=60, bags=40,
+                       integer_values=False, policy="lru")
+    _parity(w, label=f"ring{seed}")
+
+
+@pytest.mark.parametrize("seed", range(6))
 def test_small_random_real_values(seed):
     w = tg.random_tiny(100 + seed, max_rows=3000, max_cap=600, max_dim=70, batches=5, bags=40,
                        integer_values=False)
@@ -439,7 +453,8 @@ def test_pipelined_placement_matches_oracle(cid, scale, tables, ways):
 
 
 @pytest.mark.parametrize("pipeline", [False, True])
-@pytest.mark.parametrize("ways,policy", [(0, "priority"), (16, "priority"), (0, "lfu"), (16, "lfu")])
+@pytest.mark.parametrize("ways,policy", [(0, "priority"), (16, "priority"), (0, "lfu"), (16, "lfu"), (0, "lru"),
+                                         (16, "lru")])
 def test_skipped_placements(pipeline, ways, policy):
     """Placements the caller skips (the models were late, Sec. VI-C): the
     next placement sees only the most recent forward's rows and misses, and
