@@ -71,7 +71,7 @@ struct Layout {
     size_t tabs = 0, st = 0, err = 0, bm_block_start = 0, blocksum = 0, blockoff = 0, tstart = 0, pstart = 0;
     size_t src = 0, raddr = 0, U = 0, slotU = 0, M = 0, mflags = 0, mcbit = 0, mscore = 0, fill_src = 0, fill_slot = 0;
     size_t NP = 0, PU = 0, hist = 0, dump = 0, dump_count = 0, pool_bstart = 0, pool_btab = 0, ftstart = 0;
-    size_t sa_bstart = 0, sa_btab = 0, fdesc = 0, stat_log = 0, pfrom = 0;
+    size_t sa_bstart = 0, sa_btab = 0, fdesc = 0, stat_log = 0, pfrom = 0, sa_part = 0;
     size_t fstage = 0;
     size_t puref = 0, zone = 0, mslot = 0, npslot = 0, pend_row[2] = {0, 0}, pend_slot[2] = {0, 0};
     // pinned host staging (STAGED): miss ids, miss rows, fill sources, prefetch rows
@@ -245,6 +245,11 @@ void make_layout(const recmg_config_t *cfg, const std::vector<Geom> &geo, Layout
     L->sa_bstart = take(4 * (T + 1));
     L->sa_btab = take(4 * T);
     L->pfrom = take(cfg->ways > 0 ? 4 * mp : 0);
+    int64_t sa_blocks = 0;  // blocks of the set-associative placement (as cache_init counts them)
+    for (const Geom &g : geo)
+        if (g.ways) sa_blocks += (g.nsets + kSaWaves * sa_sets_per_wave(g.ways, g.nsets) - 1) /
+                                 (kSaWaves * sa_sets_per_wave(g.ways, g.nsets));
+    L->sa_part = take(8 * 8 * (size_t)sa_blocks);
     L->puref = take(4 * mp);
     L->zone = take(any_ring ? 8 * (mi + mp) : 0);
     L->mslot = take(any_ring ? 4 * mi : 0);
@@ -289,6 +294,7 @@ struct recmg_cache {
     int32_t max_cap = 0, max_map = 0, max_units = 0, rowbits = 1, nsa = 0, max_nblk = 0;
     int64_t sa_blocks = 0;   // blocks of the set-associative placement kernel
     int64_t sa_blocks1 = 0;  // the first of them, over the tables of one set per wave
+    int64_t sa_max_blocks = 0;  // the most blocks of one table
     bool has_fa = false, has_sa = false;  // tables of each form present
     bool has_ring = false, has_scan_fa = false;  // fully associative tables with and without a resident ring
     int32_t max_ring_chunks = 0;
@@ -879,6 +885,7 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.stat_log = reinterpret_cast<int64_t *>(ws + L.stat_log);
     g.sa_bstart = reinterpret_cast<int32_t *>(ws + L.sa_bstart);
     g.sa_btab = reinterpret_cast<int32_t *>(ws + L.sa_btab);
+    g.sa_part = reinterpret_cast<int64_t *>(ws + L.sa_part);
     g.pfrom = reinterpret_cast<int32_t *>(ws + L.pfrom);
     g.puref = reinterpret_cast<int32_t *>(ws + L.puref);
     g.zone = reinterpret_cast<int2 *>(ws + L.zone);
@@ -973,6 +980,7 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         const int per_block = kSaWaves * spw;
         sa_bs.push_back(sa_bs.back() + (geo[t].nsets + per_block - 1) / per_block);
         if (spw == 1) c->sa_blocks1 = sa_bs.back();  // a prefix: one set per wave only below kSaPairMinSets
+        c->sa_max_blocks = std::max<int64_t>(c->sa_max_blocks, (geo[t].nsets + per_block - 1) / per_block);
     }
     c->nsa = (int32_t)sa_tab.size();
     c->sa_blocks = sa_bs.back();
@@ -1129,7 +1137,8 @@ int32_t recmg_apply_placement(recmg_cache_t *c, const int32_t *prefetch_rows, co
         if (c->has_fa) launch_plc_admit(g, p, c->max_cap, c->max_map, cand_grid, s);
         if (c->has_ring) launch_ring_store(g, p, ring_items, c->max_cap, q, s);
         if (c->has_sa)
-            launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks1, c->sa_blocks, s);
+            launch_sa_place(g, p, c->have_fwd ? c->last_n : 0, num_prefetch, c->nsa, c->sa_blocks1, c->sa_blocks,
+                            c->sa_max_blocks, s);
     }
     launch_plc_finalize(g, fdesc, c->cfg.stats_log_calls ? c->calls % c->cfg.stats_log_calls : -1, s);
     HIP_TRY(hipEventRecord(c->ev_plc, s));

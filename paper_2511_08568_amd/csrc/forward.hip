@@ -42,12 +42,15 @@ __global__ void __launch_bounds__(kBlock) k_fwd_cover(DGlobal g, int32_t stamp, 
     if (*g.err) return;
     __shared__ int64_t s_pstart[RECMG_MAX_TABLES + 1];
     __shared__ int32_t s_pc[RECMG_MAX_TABLES];
+    __shared__ int s_cov[RECMG_MAX_TABLES];
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         s_pstart[t] = g.pstart[t];
-        if (t < g.T) s_pc[t] = g.st[t].pcount;
+        if (t < g.T) {
+            s_pc[t] = g.st[t].pcount;
+            s_cov[t] = 0;
+        }
     }
     __syncthreads();
-    const int stride_st = (int)(sizeof(TState) / 4);
     for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < np; base += (int64_t)gridDim.x * blockDim.x) {
         const int64_t i = base + threadIdx.x;
         int t = 0;
@@ -61,8 +64,11 @@ __global__ void __launch_bounds__(kBlock) k_fwd_cover(DGlobal g, int32_t stamp, 
                 hit = (int32_t)rk.z == stamp && (rk.y & (1u << (pos & 31)));
             }
         }
-        (void)wave_append(hit, t, &g.st[0].covered, stride_st);  // counts only
+        wave_count_lds(hit, t, s_cov);  // counts only
     }
+    __syncthreads();
+    for (int t = threadIdx.x; t < g.T; t += blockDim.x)
+        if (s_cov[t]) atomicAdd(&g.st[t].covered, s_cov[t]);
 }
 
 // Cache probe of every distinct row (row -> slot map, or a scan of the row's
@@ -73,9 +79,14 @@ __global__ void __launch_bounds__(kBlock) k_fwd_probe(DGlobal g, int32_t stamp, 
     if (*g.err) return;
     __shared__ int64_t s_start[RECMG_MAX_TABLES + 1];
     __shared__ int32_t s_uc[RECMG_MAX_TABLES];
+    __shared__ int s_hits[RECMG_MAX_TABLES], s_hits_pf[RECMG_MAX_TABLES];
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         s_start[t] = g.tstart[t];
-        if (t < g.T) s_uc[t] = g.st[t].ucount;
+        if (t < g.T) {
+            s_uc[t] = g.st[t].ucount;
+            s_hits[t] = 0;
+            s_hits_pf[t] = 0;
+        }
     }
     __syncthreads();
     int32_t *mcount0 = &g.st[0].mcount;
@@ -102,8 +113,8 @@ __global__ void __launch_bounds__(kBlock) k_fwd_probe(DGlobal g, int32_t stamp, 
                 miss = true;
             }
         }
-        (void)wave_append(hit, t, &g.st[0].hits, stride_st);  // counts only
-        (void)wave_append(hit_pf, t, &g.st[0].hits_pf, stride_st);
+        wave_count_lds(hit, t, s_hits);  // counts only
+        wave_count_lds(hit_pf, t, s_hits_pf);
         const int32_t m = wave_append(miss, t, mcount0, stride_st);
         if (miss) {
             const int64_t at = s_start[t] + m;
@@ -112,6 +123,11 @@ __global__ void __launch_bounds__(kBlock) k_fwd_probe(DGlobal g, int32_t stamp, 
             g.mflags[at] = 0;
             g.mcbit[at] = 0;
         }
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
+        if (s_hits[t]) atomicAdd(&g.st[t].hits, s_hits[t]);
+        if (s_hits_pf[t]) atomicAdd(&g.st[t].hits_pf, s_hits_pf[t]);
     }
 }
 

@@ -81,7 +81,8 @@ constexpr int kSaWaves = 16, kSaBlock = 64 * kSaWaves;
 // wave and the sets are many (few events each); one where sets take many events
 constexpr int64_t kSaPairMinSets = 16384;
 constexpr int sa_sets_per_wave(int ways, int64_t nsets) { return ways <= 32 && nsets >= kSaPairMinSets ? 2 : 1; }
+// max_blocks: the most blocks of one table (sizes the per-table sum of the blocks' counts)
 void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks1,
-                     int64_t blocks, hipStream_t s);
+                     int64_t blocks, int64_t max_blocks, hipStream_t s);
 
 }  // namespace recmg

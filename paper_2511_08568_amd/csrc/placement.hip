@@ -104,9 +104,13 @@ __global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last
     if (*g.err) return;
     __shared__ int64_t s_pstart[RECMG_MAX_TABLES + 1];
     __shared__ int32_t s_pc[RECMG_MAX_TABLES];
+    __shared__ int s_res[RECMG_MAX_TABLES];
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         s_pstart[t] = g.pstart[t];
-        if (t < g.T) s_pc[t] = g.tabs[t].ways ? 0 : g.st[t].pcount;
+        if (t < g.T) {
+            s_pc[t] = g.tabs[t].ways ? 0 : g.st[t].pcount;
+            s_res[t] = 0;
+        }
     }
     __syncthreads();
     const int stride_st = (int)(sizeof(TState) / 4);
@@ -124,7 +128,8 @@ __global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last
             row = g.PU[i];
             const int32_t slot = find_slot(tb, row);
             if (slot >= 0) {
-                atomicOr(&tb.slot_flags[slot], F_INP);
+                // distinct prefetch rows name distinct slots: plain read-modify-write
+                tb.slot_flags[slot] |= F_INP;
                 resident = true;
                 g.puref[i] = slot;
             } else {
@@ -136,20 +141,23 @@ __global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last
                     const int64_t ts = g.tstart[t];
                     const int32_t u = (int32_t)rk.x + __popc(rk.y & (bit - 1u));
                     const int64_t m = -(int64_t)g.slotU[ts + u] - 1;
-                    atomicOr(&g.mflags[ts + m], F_INP);
+                    g.mflags[ts + m] |= F_INP;  // distinct rows, distinct misses
                     g.puref[i] = ring_ref_miss((int32_t)m);
                 } else {
                     isnew = true;
                 }
             }
         }
-        (void)wave_append(resident, t, &g.st[0].p_res, stride_st);  // counts only
+        wave_count_lds(resident, t, s_res);  // counts only
         const int32_t k = wave_append(isnew, t, &g.st[0].npcount, stride_st);
         if (isnew) {
             g.NP[s_pstart[t] + k] = row;
             g.puref[i] = ring_ref_new(k);
         }
     }
+    __syncthreads();
+    for (int t = threadIdx.x; t < g.T; t += blockDim.x)
+        if (s_res[t]) atomicAdd(&g.st[t].p_res, s_res[t]);
 }
 
 // ----------------------------------------------------------------- ranking

@@ -165,6 +165,7 @@ struct DGlobal {
     int32_t total_bm_blocks;
     int32_t *sa_bstart;  // [nsa + 1] first placement block of each set-associative table
     int32_t *sa_btab;    // [nsa] those tables, fewest sets first
+    int64_t *sa_part;    // [sa blocks][8] each set-associative placement block's counts (added up per table after)
     int32_t *pfrom;      // [max_prefetch] set-associative tables: per distinct prefetch row (PU), its
                          // staging row if the last batch missed it, else -1
     int64_t *stat_log;   // [log calls][T][kNumStats + 1]: the counters of each call (see recmg_stats_log)
@@ -432,6 +433,23 @@ __device__ __forceinline__ int32_t wave_append(bool want, int t, int32_t *counte
         pending &= ~grp;
     }
     return mine;
+}
+
+// Count the lanes with `want` into their own table's LDS counter, one LDS
+// atomic per table present in the wave.  Counts that only add up go through
+// LDS and reach the table's state once per block: a global atomic from every
+// wave would queue on the few lines of the table's state.  Every lane of the
+// wave must call.
+__device__ __forceinline__ void wave_count_lds(bool want, int t, int *s_cnt) {
+    const int lane = threadIdx.x & 63;
+    unsigned long long pending = __ballot(want);
+    while (pending) {
+        const int leader = __ffsll((long long)pending) - 1;
+        const int lt = __shfl(t, leader, 64);
+        const unsigned long long grp = __ballot(want && t == lt);
+        if (lane == leader) atomicAdd(&s_cnt[lt], (int)__popcll(grp));
+        pending &= ~grp;
+    }
 }
 
 __device__ __forceinline__ uint64_t make_key(int32_t score, int32_t row, int rowbits) {

@@ -29,6 +29,8 @@
 // |(R' \ R) ∩ M|, prefetch_fill = rows read from the host (new rows and rows
 // moved to another way), prefetch_dropped |P \ (R ∪ R')|, miss_dropped
 // |M \ R'|; the digest and the resident count change by what came and went.
+#include <algorithm>
+
 #include "launch.h"
 
 namespace recmg {
@@ -107,6 +109,14 @@ __device__ __forceinline__ void group_min_dpp(int v, int &m0, int &m1) {
 }
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+
+// tot[k] for a lane-dependent k in [1, 7] (a select chain: no dynamic register indexing)
+__device__ __forceinline__ int64_t pick_lane_tot(const int (&tot)[8], int k) {
+    int v = tot[1];
+#pragma unroll
+    for (int i = 2; i < 8; ++i) v = k == i ? tot[i] : v;
+    return v;
+}
 
 static_assert(kSaWaves == 16, "the block's counts are added up over one DPP row of 16 lanes");
 
@@ -387,16 +397,11 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
         if (lane == 0 && tot0) base = atomicAdd(&st.popped, tot0);
         base = __builtin_amdgcn_readfirstlane(base);
         if (mine) s_off[lane] = base + sc0 - c0;
-        if (lane == 0) {
-            if (tot[1]) atomicAdd(&st.evicted, tot[1]);
-            if (tot[2]) atomicAdd(&st.adm_miss, tot[2]);
-            if (tot[3]) atomicAdd(&st.p_fill, tot[3]);
-            if (tot[4]) atomicAdd(&st.p_drop, tot[4]);
-            if (tot[5]) atomicAdd(&st.m_drop, tot[5]);
-            if (tot[6]) atomicAdd(&st.n_res, tot[6]);
-            if (tot[7]) atomicAdd(&st.p_res, tot[7]);
-            if (d) atomicAdd(&st.digest_acc, d);
-        }
+        // the other counts go to this block's record (plain stores: atomics from
+        // every block would queue on the table state's few lines), added up per
+        // table by k_sa_sum
+        if (lane < 7) g.sa_part[(int64_t)bid * 8 + lane] = pick_lane_tot(tot, lane + 1);
+        if (lane == 7) g.sa_part[(int64_t)bid * 8 + 7] = (int64_t)d;  // the digest's bits
     }
     __syncthreads();
     if (changed) {
@@ -410,6 +415,44 @@ __global__ void __launch_bounds__(kSaBlock) k_sa_place(DGlobal g, PlcParams p, i
     }
 }
 
+// The placement blocks' records added to their tables' counters: blockIdx.x
+// is the table (in sa_btab order), blockIdx.y one of gridDim.y slices of its
+// blocks; one atomic per counter per slice.
+__global__ void __launch_bounds__(1024) k_sa_sum(DGlobal g, int32_t nsa) {
+    if (*g.err) return;
+    __shared__ long long tmp[16];
+    __shared__ unsigned long long s_dig[16];
+    const int kt = blockIdx.x;
+    TState &st = g.st[g.sa_btab[kt]];
+    const int32_t b0 = g.sa_bstart[kt], b1 = g.sa_bstart[kt + 1];
+    long long v[7] = {0, 0, 0, 0, 0, 0, 0};
+    unsigned long long dg = 0;  // digests add modulo 2^64
+    for (int32_t b = b0 + (int32_t)(blockIdx.y * blockDim.x + threadIdx.x); b < b1;
+         b += (int32_t)(gridDim.y * blockDim.x)) {
+#pragma unroll
+        for (int k = 0; k < 7; ++k) v[k] += g.sa_part[(int64_t)b * 8 + k];
+        dg += (unsigned long long)g.sa_part[(int64_t)b * 8 + 7];
+    }
+    long long tot[7];
+#pragma unroll
+    for (int k = 0; k < 7; ++k) (void)block_excl_scan64(v[k], tmp, &tot[k]);
+    dg = wave_sum64(dg);
+    if ((threadIdx.x & 63) == 0) s_dig[threadIdx.x >> 6] = dg;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long d = 0;
+        for (int w = 0; w < (int)(blockDim.x >> 6); ++w) d += s_dig[w];
+        if (tot[0]) atomicAdd(&st.evicted, (int32_t)tot[0]);
+        if (tot[1]) atomicAdd(&st.adm_miss, (int32_t)tot[1]);
+        if (tot[2]) atomicAdd(&st.p_fill, (int32_t)tot[2]);
+        if (tot[3]) atomicAdd(&st.p_drop, (int32_t)tot[3]);
+        if (tot[4]) atomicAdd(&st.m_drop, (int32_t)tot[4]);
+        if (tot[5]) atomicAdd(&st.n_res, (int32_t)tot[5]);
+        if (tot[6]) atomicAdd(&st.p_res, (int32_t)tot[6]);
+        if (d) atomicAdd(&st.digest_acc, d);
+    }
+}
+
 static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
     int64_t b = (n + per_block - 1) / per_block;
     if (b < 1) b = 1;
@@ -418,11 +461,14 @@ static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
 }
 
 void launch_sa_place(const DGlobal &g, const PlcParams &p, int64_t nu, int64_t np, int32_t nsa, int64_t blocks1,
-                     int64_t blocks, hipStream_t s) {
+                     int64_t blocks, int64_t max_blocks, hipStream_t s) {
     if (nu + np > 0) k_sa_heads<<<grid_for(nu + np, kBlock, 8192), kBlock, 0, s>>>(g, nu, np, p.have_fwd, p.last_stamp);
     // tables of one set per wave come first (fewest sets), then those of two
     if (blocks1 > 0) k_sa_place<1><<<(unsigned)blocks1, kSaBlock, 0, s>>>(g, p, nsa, 0);
     if (blocks > blocks1) k_sa_place<2><<<(unsigned)(blocks - blocks1), kSaBlock, 0, s>>>(g, p, nsa, (int32_t)blocks1);
+    // slices: about 4,096 records each for the table with the most blocks
+    const unsigned slices = (unsigned)std::min<int64_t>(32, std::max<int64_t>(1, (max_blocks + 4095) / 4096));
+    k_sa_sum<<<dim3(nsa, slices), 1024, 0, s>>>(g, nsa);
 }
 
 }  // namespace recmg
