@@ -51,11 +51,13 @@ __global__ void __launch_bounds__(kBlock) k_fwd_cover(DGlobal g, int32_t stamp, 
         }
     }
     __syncthreads();
-    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < np; base += (int64_t)gridDim.x * blockDim.x) {
+    int64_t lo, hi;
+    block_share(np, &lo, &hi);
+    for (int64_t base = lo; base < hi; base += blockDim.x) {  // block-uniform
         const int64_t i = base + threadIdx.x;
         int t = 0;
         bool hit = false;
-        if (i < np) {
+        if (i < hi) {
             t = find_seg(s_pstart, g.T, i);
             if (i - s_pstart[t] < s_pc[t]) {
                 const DTable &tb = g.tabs[t];
@@ -91,12 +93,14 @@ __global__ void __launch_bounds__(kBlock) k_fwd_probe(DGlobal g, int32_t stamp, 
     __syncthreads();
     int32_t *mcount0 = &g.st[0].mcount;
     const int stride_st = (int)(sizeof(TState) / 4);
-    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < n; base += (int64_t)gridDim.x * blockDim.x) {
+    int64_t lo, hi;
+    block_share(n, &lo, &hi);
+    for (int64_t base = lo; base < hi; base += blockDim.x) {  // block-uniform
         const int64_t i = base + threadIdx.x;
         int t = 0;
         bool miss = false, valid = false, hit = false, hit_pf = false;
         int32_t row = 0;
-        if (i < n) {
+        if (i < hi) {
             t = find_seg(s_start, g.T, i);
             valid = i - s_start[t] < s_uc[t];
         }

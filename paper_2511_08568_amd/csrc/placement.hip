@@ -114,12 +114,14 @@ __global__ void __launch_bounds__(kBlock) k_plc_classify(DGlobal g, int32_t last
     }
     __syncthreads();
     const int stride_st = (int)(sizeof(TState) / 4);
-    for (int64_t base = (int64_t)blockIdx.x * blockDim.x; base < np; base += (int64_t)gridDim.x * blockDim.x) {
+    int64_t lo, hi;
+    block_share(np, &lo, &hi);
+    for (int64_t base = lo; base < hi; base += blockDim.x) {  // block-uniform
         const int64_t i = base + threadIdx.x;
         int t = 0;
         bool valid = false, isnew = false, resident = false;
         int32_t row = 0;
-        if (i < np) {
+        if (i < hi) {
             t = find_seg(s_pstart, g.T, i);
             valid = i - s_pstart[t] < s_pc[t];
         }

@@ -435,6 +435,15 @@ __device__ __forceinline__ int32_t wave_append(bool want, int t, int32_t *counte
     return mine;
 }
 
+// This block's contiguous share [*lo, *hi) of an index space of n, in whole
+// blocks of blockDim.x: a block then meets one or two tables, and its LDS
+// counters reach the table states with one or two atomics.
+__device__ __forceinline__ void block_share(int64_t n, int64_t *lo, int64_t *hi) {
+    const int64_t per = ((n + gridDim.x - 1) / gridDim.x + blockDim.x - 1) / blockDim.x * blockDim.x;
+    *lo = (int64_t)blockIdx.x * per;
+    *hi = *lo + per < n ? *lo + per : n;
+}
+
 // Count the lanes with `want` into their own table's LDS counter, one LDS
 // atomic per table present in the wave.  Counts that only add up go through
 // LDS and reach the table's state once per block: a global atomic from every
