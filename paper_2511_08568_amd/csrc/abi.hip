@@ -882,6 +882,8 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
     g.stage_stride = L.stage_stride;
     g.T = T;
     g.total_bm_blocks = L.total_bm_blocks;
+    g.own_tables = 0;
+    g.own_slices = 0;
     g.stat_log = reinterpret_cast<int64_t *>(ws + L.stat_log);
     g.sa_bstart = reinterpret_cast<int32_t *>(ws + L.sa_bstart);
     g.sa_btab = reinterpret_cast<int32_t *>(ws + L.sa_btab);
@@ -963,6 +965,10 @@ int32_t cache_init(const recmg_config_t *cfg, recmg_cache_t **out) {
         c->max_units = std::max(c->max_units, ge.row_bytes / ge.copy_unit);
         c->max_rows = std::max(c->max_rows, ge.rows);
         c->max_nblk = std::max(c->max_nblk, ge.bm_nblk);
+        if (owns_bitmap(ge.bm_nblk)) {
+            g.own_tables += 1;
+            g.own_slices = std::max(g.own_slices, (ge.bm_nblk + kOwnSliceBlocks - 1) / kOwnSliceBlocks);
+        }
     }
     c->rowbits = std::max(1, bitlen((uint64_t)(c->max_rows - 1)));
     c->pool_order.resize(T);

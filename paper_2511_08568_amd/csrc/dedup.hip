@@ -16,9 +16,17 @@
 // set (the order in which a set takes its events); the resident dump keeps
 // plain row positions.
 //
-// Marking: Zipf-popular rows make many threads set the same bit.  Each block
-// first deduplicates its ids in a small LDS hash set, so a popular row costs
-// one global atomic per block instead of one per occurrence.
+// Marking.  A table whose bitmap spans at most kOwnMaxSlices slices of
+// kOwnSliceWords words is marked in LDS: one block per slice reads all of the
+// table's ids, sets the bits that fall in its slice with LDS atomics, then
+// stores the slice's non-zero words and the popcount of each of its bitmap
+// blocks (so the count pass is not needed).  Its ids cost one 4-byte read per
+// slice and the bitmap one write.  Larger tables are marked in HBM: Zipf-popular
+// rows make many threads set the same bit, so each block first deduplicates its
+// ids in a small LDS hash set and a popular row costs one device atomic per
+// block instead of one per occurrence.  A bitmap word there is shared by blocks
+// on every XCD, so that atomic (and the load before it) is served past the
+// XCD's L2, a cache line per distinct id and block.
 #include "launch.h"
 
 namespace recmg {
@@ -36,6 +44,7 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
     __shared__ int64_t s_rows[RECMG_MAX_TABLES];
     __shared__ uint32_t *s_bm[RECMG_MAX_TABLES];
     __shared__ int32_t s_ns[RECMG_MAX_TABLES], s_qb[RECMG_MAX_TABLES];
+    __shared__ bool s_own[RECMG_MAX_TABLES];
     __shared__ unsigned long long s_set[kLdsSet];
     for (int t = threadIdx.x; t <= g.T; t += blockDim.x) {
         s_start[t] = starts[t];
@@ -44,6 +53,7 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
             s_bm[t] = g.tabs[t].bitmap;
             s_ns[t] = g.tabs[t].nsets;
             s_qb[t] = g.tabs[t].qbits;
+            s_own[t] = owns_bitmap(g.tabs[t].bm_nblk);
         }
     }
     for (int k = threadIdx.x; k < kLdsSet; k += blockDim.x) s_set[k] = ~0ull;
@@ -55,6 +65,7 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
     const int64_t hi = lo + chunk < n ? lo + chunk : n;
     for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
         const int t = find_seg(s_start, g.T, i);
+        if (s_own[t]) continue;  // marked by k_mark_own
         const int32_t r = keys[i];
         if (r < 0 || (int64_t)r >= s_rows[t]) {
             atomicOr(g.err, ERR_RANGE);
@@ -80,6 +91,69 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
             if (!(__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit)) atomicOr(w, bit);
         }
     }
+}
+
+constexpr int kOwnThreads = 1024, kOwnUnroll = 8;
+
+// Block (slice, table) of the LDS marking: grid (g.own_slices, T); blocks of
+// tables that are not owned, and slices past a table's bitmap, exit at once.
+// Writes the slice's non-zero words into the (all-zero) bitmap and blocksum of
+// each of its bitmap blocks.  Range errors are raised by slice 0 only.
+__global__ void __launch_bounds__(kOwnThreads) k_mark_own(DGlobal g, const int32_t *__restrict__ keys,
+                                                          const int64_t *__restrict__ starts) {
+    __shared__ uint4 s_bm[kOwnSliceWords / 4];
+    __shared__ int s_cnt[kOwnSliceBlocks];
+    __shared__ int s_err;
+    const int t = blockIdx.y, sl = blockIdx.x;
+    const DTable &tb = g.tabs[t];
+    const int nblk = tb.bm_nblk;
+    if (!owns_bitmap(nblk) || sl * kOwnSliceBlocks >= nblk) return;  // block-uniform
+    // the error word is read once: slice 0 of another table may set it meanwhile,
+    // and the waves of the block must agree before its barriers
+    if (threadIdx.x == 0) s_err = *g.err;
+    const int sblk = nblk - sl * kOwnSliceBlocks < kOwnSliceBlocks ? nblk - sl * kOwnSliceBlocks : kOwnSliceBlocks;
+    const int nq = sblk * (kWordsPerBlock / 4);  // uint4 words of the slice
+    for (int k = threadIdx.x; k < nq; k += kOwnThreads) s_bm[k] = make_uint4(0u, 0u, 0u, 0u);
+    if (threadIdx.x < kOwnSliceBlocks) s_cnt[threadIdx.x] = 0;
+    __syncthreads();
+    if (s_err) return;  // block-uniform
+    uint32_t *bm = reinterpret_cast<uint32_t *>(s_bm);
+    const int64_t lo = starts[t], hi = starts[t + 1];
+    const int64_t rows = tb.rows;
+    const int32_t ns = tb.nsets, qb = tb.qbits;
+    for (int64_t i0 = lo + threadIdx.x; i0 < hi; i0 += (int64_t)kOwnThreads * kOwnUnroll) {
+        int32_t r[kOwnUnroll];
+#pragma unroll
+        for (int u = 0; u < kOwnUnroll; ++u) {
+            const int64_t i = i0 + (int64_t)u * kOwnThreads;
+            r[u] = i < hi ? keys[i] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < kOwnUnroll; ++u) {
+            if (i0 + (int64_t)u * kOwnThreads >= hi) continue;
+            if (r[u] < 0 || (int64_t)r[u] >= rows) {
+                if (sl == 0) atomicOr(g.err, ERR_RANGE);
+                continue;
+            }
+            const uint32_t pos = bm_pos(ns, qb, r[u]);
+            if ((int)(pos >> 20) != sl) continue;  // 2^20 positions per slice
+            const uint32_t w = (pos >> 5) & (kOwnSliceWords - 1), bit = 1u << (pos & 31);
+            if (!(bm[w] & bit)) atomicOr(&bm[w], bit);
+        }
+    }
+    __syncthreads();
+    uint4 *gbm = reinterpret_cast<uint4 *>(tb.bitmap + (int64_t)sl * kOwnSliceWords);
+    for (int k = threadIdx.x; k < nq; k += kOwnThreads) {
+        const uint4 v = s_bm[k];
+        if (v.x | v.y | v.z | v.w) gbm[k] = v;
+        int c = __popc(v.x) + __popc(v.y) + __popc(v.z) + __popc(v.w);
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) c += __shfl_xor(c, m);
+        // a wave's 64 uint4 words lie in one bitmap block of 256 uint4 words
+        if ((threadIdx.x & 63) == 0 && c) atomicAdd(&s_cnt[k / (kWordsPerBlock / 4)], c);
+    }
+    __syncthreads();
+    if (threadIdx.x < sblk) g.blocksum[tb.bm_block0 + sl * kOwnSliceBlocks + threadIdx.x] = s_cnt[threadIdx.x];
 }
 
 // Mark the resident rows of every table (for the sorted dump).
@@ -226,7 +300,8 @@ static inline unsigned grid_for(int64_t n, int per_block, unsigned cap) {
 
 void launch_mark(const DGlobal &g, const int32_t *keys, const int64_t *starts, int64_t n, hipStream_t s) {
     if (n <= 0) return;
-    k_mark<<<grid_for(n, kBlock * 8, 4096), kBlock, 0, s>>>(g, keys, starts, n);
+    if (g.own_tables > 0) k_mark_own<<<dim3((unsigned)g.own_slices, (unsigned)g.T), kOwnThreads, 0, s>>>(g, keys, starts);
+    if (g.own_tables < g.T) k_mark<<<grid_for(n, kBlock * 8, 4096), kBlock, 0, s>>>(g, keys, starts, n);
 }
 
 void launch_mark_resident(const DGlobal &g, int32_t max_cap, hipStream_t s) {
@@ -243,7 +318,8 @@ void launch_dedup(const DGlobal &g, int mode, int32_t *counts, int count_stride,
         else k_bm_fused<EMIT_DUMP><<<g.T, kFusedThreads, 0, s>>>(g, counts, count_stride, stamp);
         return;
     }
-    k_bm_count<<<g.total_bm_blocks, kBlock, 0, s>>>(g);
+    // k_mark_own has counted the owned tables' blocks (not those of the resident dump)
+    if (mode == EMIT_DUMP || g.own_tables < g.T) k_bm_count<<<g.total_bm_blocks, kBlock, 0, s>>>(g);
     k_bm_scan<<<g.T, 1024, 0, s>>>(g, counts, count_stride);
     if (mode == EMIT_FORWARD) k_bm_emit<EMIT_FORWARD><<<g.total_bm_blocks, kBlock, 0, s>>>(g, stamp);
     else if (mode == EMIT_PREFETCH) k_bm_emit<EMIT_PREFETCH><<<g.total_bm_blocks, kBlock, 0, s>>>(g, stamp);

@@ -13,6 +13,16 @@ namespace recmg {
 constexpr int kBlock = 256;                         // threads per block (4 waves)
 constexpr int kWordsPerThread = 4;                  // presence-bitmap words per thread
 constexpr int kWordsPerBlock = kBlock * kWordsPerThread;  // 1024 words = 32768 rows
+// Tables whose bitmap spans at most kOwnMaxSlices slices of kOwnSliceWords words
+// are marked slice by slice in LDS (one block per slice reads the table's ids);
+// larger ones with a device atomic per distinct id and block.
+constexpr int kOwnSliceWords = 32768;  // 128 KiB of LDS, 2^20 rows
+constexpr int kOwnSliceBlocks = kOwnSliceWords / kWordsPerBlock;
+#ifndef RECMG_OWN_MAX_SLICES
+#define RECMG_OWN_MAX_SLICES 8
+#endif
+constexpr int kOwnMaxSlices = RECMG_OWN_MAX_SLICES;
+__host__ __device__ constexpr bool owns_bitmap(int32_t bm_nblk) { return bm_nblk <= kOwnMaxSlices * kOwnSliceBlocks; }
 constexpr int kRadixBits = 11;                      // radix-select digit
 constexpr int kRadix = 1 << kRadixBits;
 constexpr int32_t kEmpty = -1;                      // map key of a never-used entry
@@ -163,6 +173,8 @@ struct DGlobal {
     int64_t stage_stride;
     int32_t T;
     int32_t total_bm_blocks;
+    int32_t own_tables;  // tables with owns_bitmap(bm_nblk)
+    int32_t own_slices;  // the most LDS slices of such a table
     int32_t *sa_bstart;  // [nsa + 1] first placement block of each set-associative table
     int32_t *sa_btab;    // [nsa] those tables, fewest sets first
     int64_t *sa_part;    // [sa blocks][8] each set-associative placement block's counts (added up per table after)

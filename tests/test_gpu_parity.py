@@ -97,6 +97,20 @@ def test_configs_scaled(cid, scale, bags, tables):
     _parity(w, label=f"c{cid}-scaled")
 
 
+@pytest.mark.parametrize("ways,policy", [(0, "priority"), (0, "lru"), (16, "priority")])
+def test_dedup_bitmap_slices(ways, policy):
+    """Row counts on both sides of the dedup's limits: a bitmap of exactly one
+    LDS slice (2^20 rows), one row more (a second, nearly empty slice), exactly
+    the most slices marked in LDS (2^23 rows) and one row more (marked with
+    device atomics, beside the others in the same call), and a small table."""
+    rows = [1 << 20, (1 << 20) + 1, 1 << 23, (1 << 23) + 1, 3000]
+    tabs = [tg.Table(n, 4, "f32", 1500 if ways == 0 else 1024, a, ("poisson", 20.0, 1, 60))
+            for n, a in zip(rows, (0.9, 1.1, 1.0, 1.2, 1.05))]
+    w = tg.Workload(0, f"dedup-slices-w{ways}-{policy}", tabs, batches=6, bags=512, policy=policy,
+                    prefetch=("mix", 0.7), ways=ways)
+    _parity(w)
+
+
 # Row sizes that pick each pooled-kernel shape: 64 and 128 bytes (4 or 2 rows
 # per load instruction), 256 / 512 / 1024 bytes (one row per instruction, 4, 8
 # or 16 bytes per lane), 2048 bytes (two chunks per row), and sizes the
