@@ -764,7 +764,7 @@ void launch_fwd_cover(const DGlobal &g, int32_t stamp, int64_t np, hipStream_t s
 
 void launch_fwd_src(const DGlobal &g, const int32_t *indices, int64_t n, hipStream_t s) {
     if (n <= 0) return;
-    k_fwd_src<<<grid_for(n, kBlock * 4, 16384), kBlock, 0, s>>>(g, indices, n);
+    k_fwd_src<<<grid_for(n, kBlock * items_per_thread(n, 4), 16384), kBlock, 0, s>>>(g, indices, n);
 }
 
 #ifndef RECMG_FETCH_BLOCKS

@@ -5,6 +5,12 @@
 
 namespace recmg {
 
+// Up to this many items, a grid-stride launch gives each thread one item (a
+// short batch is latency-bound: its threads' dependent load chains run side
+// by side instead of one after another); above, `big` items per thread.
+constexpr int64_t kTinyItems = 16384;
+static inline int items_per_thread(int64_t n, int big) { return n <= kTinyItems ? 1 : big; }
+
 // dedup.hip
 void launch_mark(const DGlobal &g, const int32_t *keys, const int64_t *starts, int64_t n, hipStream_t s);
 void launch_mark_resident(const DGlobal &g, int32_t max_cap, hipStream_t s);

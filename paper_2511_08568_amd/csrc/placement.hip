@@ -852,7 +852,7 @@ void launch_plc_admit(const DGlobal &g, const PlcParams &p, int32_t max_cap, int
                       hipStream_t s) {
     k_map_clear<<<dim3(grid_for(max_map, kBlock * 8, 2048), g.T), kBlock, 0, s>>>(g);
     k_map_refill<<<dim3(grid_for(max_cap, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g);
-    k_plc_admit<<<dim3(grid_for(cand_bound, kBlock * 4, 2048), g.T), kBlock, 0, s>>>(g, p);
+    k_plc_admit<<<dim3(grid_for(cand_bound, kBlock * items_per_thread(cand_bound, 4), 2048), g.T), kBlock, 0, s>>>(g, p);
 }
 
 void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, int phase, hipStream_t s, hipEvent_t ev0,

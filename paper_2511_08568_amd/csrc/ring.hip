@@ -508,7 +508,7 @@ static inline unsigned ring_grid(int64_t n, int per_block, unsigned cap) {
 }
 
 void launch_ring_rank(const DGlobal &g, const PlcParams &p, int64_t item_bound, hipStream_t s) {
-    k_ring_touch<<<dim3(ring_grid(item_bound, kBlock * 4, 1024), g.T), kBlock, 0, s>>>(g, p);
+    k_ring_touch<<<dim3(ring_grid(item_bound, kBlock * items_per_thread(item_bound, 4), 1024), g.T), kBlock, 0, s>>>(g, p);
     k_ring_cut<<<g.T, kRingThreads, 0, s>>>(g, p);
 }
 
