@@ -19,7 +19,7 @@ constexpr int kWordsPerBlock = kBlock * kWordsPerThread;  // 1024 words = 32768 
 constexpr int kOwnSliceWords = 32768;  // 128 KiB of LDS, 2^20 rows
 constexpr int kOwnSliceBlocks = kOwnSliceWords / kWordsPerBlock;
 #ifndef RECMG_OWN_MAX_SLICES
-#define RECMG_OWN_MAX_SLICES 8
+#define RECMG_OWN_MAX_SLICES 32
 #endif
 constexpr int kOwnMaxSlices = RECMG_OWN_MAX_SLICES;
 __host__ __device__ constexpr bool owns_bitmap(int32_t bm_nblk) { return bm_nblk <= kOwnMaxSlices * kOwnSliceBlocks; }

@@ -101,9 +101,9 @@ def test_configs_scaled(cid, scale, bags, tables):
 def test_dedup_bitmap_slices(ways, policy):
     """Row counts on both sides of the dedup's limits: a bitmap of exactly one
     LDS slice (2^20 rows), one row more (a second, nearly empty slice), exactly
-    the most slices marked in LDS (2^23 rows) and one row more (marked with
+    the most slices marked in LDS (2^25 rows) and one row more (marked with
     device atomics, beside the others in the same call), and a small table."""
-    rows = [1 << 20, (1 << 20) + 1, 1 << 23, (1 << 23) + 1, 3000]
+    rows = [1 << 20, (1 << 20) + 1, 1 << 25, (1 << 25) + 1, 3000]
     tabs = [tg.Table(n, 4, "f32", 1500 if ways == 0 else 1024, a, ("poisson", 20.0, 1, 60))
             for n, a in zip(rows, (0.9, 1.1, 1.0, 1.2, 1.05))]
     w = tg.Workload(0, f"dedup-slices-w{ways}-{policy}", tabs, batches=6, bags=512, policy=policy,
