@@ -253,6 +253,10 @@ def main():
     ap.add_argument("--sweep-batches", type=int, default=60)
     ap.add_argument("--no-pipeline", dest="pipeline", action="store_false",
                     help="run placements on the forward's stream (no overlap of placement b+1 with forward b)")
+    ap.add_argument("--no-copy-stream", dest="copy_stream", action="store_false",
+                    help="ZERO_COPY: run the prefetch fill on the placement's stream, not a copy stream of its "
+                         "own (with --no-pipeline every kernel of a step is on one stream: no cross-stream waits, "
+                         "which a launch-bound small batch feels)")
     ap.add_argument("--policy", default=None, choices=["lru", "priority", "lfu"],
                     help="override the configuration's placement policy")
     ap.add_argument("--ways", type=int, default=0,
@@ -353,7 +357,7 @@ def main():
     cache = TieredEmbeddingCache(host, [tb.dtype for tb in w.tables], [tb.cap for tb in w.tables], policy=w.policy,
                                  eviction_speed=w.eviction_speed, miss_mode=modes,
                                  max_bags_per_table=w.bags, max_indices=max_idx, max_prefetch=max_pf, timing=1,
-                                 ways=w.ways, stats_log_calls=2 * nb + NW)
+                                 ways=w.ways, stats_log_calls=2 * nb + NW, overlap=args.copy_stream)
     log(f"cache ready: workspace {cache.workspace_bytes / 1e9:.2f} GB")
 
     # Pipelined placement: placements run on a stream of their own, so that
@@ -500,6 +504,7 @@ def main():
             "miss_mode": args.miss_mode if len(set(modes)) == 1 else
                          f"mixed: tables 0..{args.zero_copy_tables - 1} zero_copy, the rest staged",
             "pipelined_placement": bool(args.pipeline),
+            "copy_stream": bool(args.copy_stream or args.miss_mode == "staged"),
             "row_scale": args.row_scale,
         },
         "hit_path_roofline": {
