@@ -94,6 +94,8 @@ __global__ void __launch_bounds__(kBlock) k_mark(DGlobal g, const int32_t *__res
 }
 
 constexpr int kOwnThreads = 1024, kOwnUnroll = 8;
+static_assert(kOwnSliceWords * 32 == 1 << 20, "a slice holds 2^20 bitmap positions");
+static_assert(kOwnSliceBlocks <= kOwnThreads && kOwnSliceWords % kWordsPerBlock == 0, "slice = whole bitmap blocks");
 
 // Block (slice, table) of the LDS marking: grid (g.own_slices, T); blocks of
 // tables that are not owned, and slices past a table's bitmap, exit at once.
@@ -136,7 +138,7 @@ __global__ void __launch_bounds__(kOwnThreads) k_mark_own(DGlobal g, const int32
                 continue;
             }
             const uint32_t pos = bm_pos(ns, qb, r[u]);
-            if ((int)(pos >> 20) != sl) continue;  // 2^20 positions per slice
+            if ((int)(pos >> 20) != sl) continue;  // the position's slice
             const uint32_t w = (pos >> 5) & (kOwnSliceWords - 1), bit = 1u << (pos & 31);
             if (!(bm[w] & bit)) atomicOr(&bm[w], bit);
         }
