@@ -713,10 +713,19 @@ __global__ void __launch_bounds__(kBlock) k_plc_fill(DGlobal g, const int64_t *_
 #ifndef RECMG_FILL_BLOCKS_SHARED
 #define RECMG_FILL_BLOCKS_SHARED 256  // zero-copy fill beside the next forward's on-demand fetch
 #endif
+#ifndef RECMG_FILL_BLOCKS_BIG
+#define RECMG_FILL_BLOCKS_BIG 512  // zero-copy fill beside a fetch of hundreds of MB
+#endif
 constexpr int kStagedFillBlocks = 1024;
 // on-demand fetch bytes above which the next fetch is taken to share the link
 // with the fill (below it, the fetch takes a few microseconds of link time)
 constexpr unsigned long long kSharedFetchBytes = 1ull << 20;
+// ... and above which the two hold the link together for tens of milliseconds
+constexpr unsigned long long kBigFetchBytes = 1ull << 28;
+constexpr int kFillGridBlocks = RECMG_FILL_BLOCKS > RECMG_FILL_BLOCKS_SHARED
+                                    ? (RECMG_FILL_BLOCKS > RECMG_FILL_BLOCKS_BIG ? RECMG_FILL_BLOCKS : RECMG_FILL_BLOCKS_BIG)
+                                    : (RECMG_FILL_BLOCKS_SHARED > RECMG_FILL_BLOCKS_BIG ? RECMG_FILL_BLOCKS_SHARED
+                                                                                       : RECMG_FILL_BLOCKS_BIG);
 
 // Publishes the counters and writes the fill descriptor of this placement
 // (per table: first fill-list entry, entry count, base of its admitted misses
@@ -724,9 +733,11 @@ constexpr unsigned long long kSharedFetchBytes = 1ull << 20;
 // fdesc[3] (a spare word of table 0's entry) is the number of blocks the fill
 // copies with: zero-copy fills take more when the last forward fetched at
 // least 1 MB on demand, since the next forward's fetch will then share the
-// host link (with fewer waves of its own the fill gets less of it), and fewer
-// when the fill has the link to itself, so that it takes no more CUs than it
-// needs from the kernels beside it.
+// host link (with fewer waves of its own the fill gets less of it), more
+// still when it fetched at least 256 MB (the two then hold the link for tens
+// of milliseconds, and the kernels beside them are a small part of the step),
+// and fewer when the fill has the link to itself, so that it takes no more
+// CUs than it needs from the kernels beside it.
 // log_slot >= 0: the counters also go to that call's record of the stats log
 // (the forward group of the record stays zero).
 __global__ void k_plc_finalize(DGlobal g, int64_t *fdesc, int64_t log_slot) {
@@ -739,7 +750,10 @@ __global__ void k_plc_finalize(DGlobal g, int64_t *fdesc, int64_t log_slot) {
         mb += (unsigned long long)(g.st[t].mcount > 0 ? g.st[t].mcount : 0) * (unsigned long long)g.tabs[t].row_bytes;
     if (mb) atomicAdd(&s_mbytes, mb);
     __syncthreads();
-    if (threadIdx.x == 0) fdesc[3] = s_mbytes >= kSharedFetchBytes ? RECMG_FILL_BLOCKS_SHARED : RECMG_FILL_BLOCKS;
+    if (threadIdx.x == 0)
+        fdesc[3] = s_mbytes >= kBigFetchBytes      ? RECMG_FILL_BLOCKS_BIG
+                   : s_mbytes >= kSharedFetchBytes ? RECMG_FILL_BLOCKS_SHARED
+                                                   : RECMG_FILL_BLOCKS;
     for (int t = threadIdx.x; t < g.T; t += blockDim.x) {
         TState &st = g.st[t];
         const DTable &tb = g.tabs[t];
@@ -865,13 +879,13 @@ void launch_plc_fill(const DGlobal &g, const int64_t *fdesc, int phase, hipStrea
     // instead of 0.28 ms.  Measured on configuration 2 (no on-demand misses):
     // 80-96 blocks leave the link short, 160 and more slow the placement that
     // runs beside the fill (192: -8% lookups/s).  On configuration 3 the fill
-    // shares the link with the next forward's fetch of about 330,000 misses,
-    // and 256 blocks gave +4%.  The grid holds the larger count; k_plc_finalize
-    // writes how many of its blocks copy.  STAGED fills copy within HBM and
-    // take a full grid.
-    const int blocks = phase == FILL_STAGED ? kStagedFillBlocks
-                                            : (RECMG_FILL_BLOCKS > RECMG_FILL_BLOCKS_SHARED ? RECMG_FILL_BLOCKS
-                                                                                            : RECMG_FILL_BLOCKS_SHARED);
+    // shares the link with the next forward's fetch of about 330,000 misses
+    // (85 MB), and 256 blocks gave +4% (512: -6%).  On configuration 5 the
+    // fetch moves about 750 MB per batch beside a 3.8 GB fill, and 512 blocks
+    // gave +2.7% against 256 (768 and 1024: the same as 512).  The grid holds
+    // the largest count; k_plc_finalize writes how many of its blocks copy.
+    // STAGED fills copy within HBM and take a full grid.
+    const int blocks = phase == FILL_STAGED ? kStagedFillBlocks : kFillGridBlocks;
     if (ev0 || ev1) hipExtLaunchKernelGGL(k_plc_fill, dim3(blocks), dim3(kBlock), 0, s, ev0, ev1, 0, g, fdesc, phase);
     else k_plc_fill<<<blocks, kBlock, 0, s>>>(g, fdesc, phase);
 }
